@@ -1,0 +1,238 @@
+/*
+ * rlx.h -- C ABI of the MI355X (gfx950) MiniLM-L6-shaped encoder forward.
+ *
+ * The library computes the forward pass of a BERT-style sentence-embedding
+ * encoder (all-MiniLM-L6-v2 shape: hidden 384, 12 heads of 32, FFN 1536,
+ * 6 post-LN layers), the workload of the paper's inference evaluation
+ * (RLX, arxiv 2609.37916, Section VIII-B), with hand-written HIP kernels.
+ *
+ * Conventions shared by every entry point
+ *  - All tensor pointers are DEVICE pointers unless marked "host".  The
+ *    caller owns every buffer it passes; the library never frees or keeps
+ *    them beyond the call, except the weights bound by rlx_encoder_create,
+ *    which must outlive the encoder handle.
+ *  - Tensors are dense and row-major unless a row stride is given; strides
+ *    are in elements.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Work is enqueued asynchronously on it; results are ready when the
+ *    stream is synchronised.
+ *  - Every argument is validated before any GPU work is enqueued.  A call
+ *    that cannot be executed exactly as asked returns an error and does
+ *    nothing: there is no fallback to another algorithm or to the CPU
+ *    (the paper's dispatch fails with a diagnostic rather than degrading,
+ *    Section IV).  rlx_last_error() then describes the problem.
+ *  - bf16 is bfloat16 (upper 16 bits of an IEEE binary32); conversions to
+ *    bf16 round to nearest, ties to even.  f16 is IEEE binary16.
+ *  - Thread safety: entry points may be called from several host threads;
+ *    one encoder handle must not be used by two threads at once.
+ */
+#ifndef RLX_H_
+#define RLX_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RLX_OK = 0,
+  RLX_ERR_INVALID_ARG = 1,  /* null pointer, negative size, inconsistent shapes     */
+  RLX_ERR_UNSUPPORTED = 2,  /* well-formed request outside what the kernels implement */
+  RLX_ERR_HIP = 3,          /* a HIP runtime call or kernel launch failed          */
+  RLX_ERR_OOM = 4           /* device allocation failed (encoder workspace)        */
+} rlx_status;
+
+typedef enum {
+  RLX_F32 = 0, RLX_BF16 = 1, RLX_F16 = 2, RLX_I8 = 3, RLX_U4X2 = 4, RLX_I32 = 5, RLX_U8 = 6
+} rlx_dtype;
+
+/* The masked-attention primitive's MaskKind (Section III-A): None, Causal,
+ * SlidingWindow(w), Custom (an explicit mask). */
+typedef enum {
+  RLX_MASK_NONE = 0,
+  RLX_MASK_CAUSAL = 1,          /* key j visible to query i iff j <= i                */
+  RLX_MASK_SLIDING_WINDOW = 2,  /* iff i - window < j <= i                            */
+  RLX_MASK_CUSTOM = 3           /* iff key_mask[b][j] != 0 (key_mask required)        */
+} rlx_mask_kind;
+
+/* Weight-only quantisation schemes of Op::DequantMatMul (Sections III-A, VI). */
+typedef enum {
+  RLX_Q_NONE = 0,              /* w has the activation dtype (f32 or bf16), [N,K]      */
+  RLX_Q_INT8_PER_CHANNEL = 1,  /* w int8 [N,K]; scales f16 [N]; W = q * s[n]          */
+  RLX_Q_INT4_GROUP_ZP = 2      /* w u8 [N,K/2], two codes per byte (k = 2j in the low
+                                  nibble, 2j+1 in the high nibble); scales and zeros
+                                  f16 [N, K/group]; W = (q - z[n,g]) * s[n,g],
+                                  g = k / group                                       */
+} rlx_quant;
+
+typedef enum {
+  RLX_EPI_NONE = 0,           /* y = acc                                   */
+  RLX_EPI_BIAS = 1,           /* y = acc + bias[n]                         */
+  RLX_EPI_BIAS_GELU = 2,      /* y = GELU(acc + bias[n]), erf form         */
+  RLX_EPI_BIAS_RESIDUAL = 3   /* y = acc + bias[n] + residual[m][n]        */
+} rlx_epilogue;
+
+/* ------------------------------------------------------------------------ */
+/* Masked multi-head attention (Section III-A: attention with an explicit
+ * MaskKind; Section III-B: Q, K and V read as strided narrows of one buffer).
+ *
+ * For every sequence b < B, head h < num_heads, query i < S:
+ *   out[b,i,h,:] = sum_j P_ij v[b,j,h,:],  P_i = softmax over visible j of
+ *                  scale * <q[b,i,h,:], k[b,j,h,:]>
+ * with visibility given by `kind` (see rlx_mask_kind) and, when key_mask is
+ * non-NULL, additionally key_mask[b*S + j] != 0.  A query with no visible key
+ * gets an all-zero output row.
+ *
+ * Layout: element (b, s, h, d) of q, k and v is at
+ *   ptr[(b*S + s) * qkv_row_stride + h*head_dim + d]
+ * so q, k, v may be column offsets into one fused [B*S, 3*H] projection
+ * (stride 3*H) or separate [B*S, H] tensors (stride H); out is
+ *   out[(b*S + s) * out_row_stride + h*head_dim + d].
+ * dt: RLX_BF16 (fp32 softmax and accumulation, output rounded to bf16) or
+ * RLX_F32.  key_mask: u8 [B,S] or NULL (required for RLX_MASK_CUSTOM).
+ * window >= 1 for RLX_MASK_SLIDING_WINDOW, ignored otherwise.
+ * Supported: head_dim == 32; 1 <= S <= 512; qkv_row_stride and
+ * out_row_stride multiples of 8 and >= num_heads*head_dim; q, k, v, out
+ * 16-byte aligned.  Otherwise RLX_ERR_UNSUPPORTED.
+ */
+rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int64_t qkv_row_stride,
+                                void* out, int64_t out_row_stride, int B, int S, int num_heads, int head_dim,
+                                rlx_dtype dt, rlx_mask_kind kind, const uint8_t* key_mask, int window,
+                                float scale, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Matrix multiply with weights dequantised on the fly and a fused epilogue
+ * (Op::DequantMatMul, Sections III-A and VI; Linear block, Section III-A):
+ *
+ *   y[m,n] = epi( sum_k x[m,k] * W[n,k] )      0 <= m < M, 0 <= n < N
+ *
+ * x: [M,K] row-major, dtype x_dt (RLX_BF16 or RLX_F32; quantised schemes
+ * need RLX_BF16).  W: [N,K] in the layout of `scheme` (nn.Linear
+ * convention: one row per output feature).  bias: f32 [N] (needed by every
+ * epilogue except RLX_EPI_NONE).  residual: [M,N] of dtype x_dt (only for
+ * RLX_EPI_BIAS_RESIDUAL).  y: [M,N] of dtype x_dt.  Accumulation is fp32;
+ * bf16 outputs are rounded once at the end.
+ * int8: the integer codes enter the bf16 matrix cores exactly and the
+ * per-channel scale is applied to the fp32 sum.  int4: each weight
+ * (q - z) * s is formed in fp32 and rounded to bf16 before the product.
+ * Supported: M >= 0 (M == 0 is a no-op), N and K positive multiples of 64,
+ * group_size == 32 for RLX_Q_INT4_GROUP_ZP (ignored otherwise), 16-byte
+ * aligned x, w, residual and y.  Otherwise RLX_ERR_UNSUPPORTED.
+ */
+rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const void* w, rlx_quant scheme,
+                              const void* scales, const void* zeros, int group_size, int N,
+                              const float* bias, const void* residual, rlx_epilogue epi, void* y,
+                              void* stream);
+
+/* Test support for the dequantisation step alone: writes the dequantised
+ * weights W[n,k] as f32 [N,K] (exact: both products are representable in
+ * fp32).  Same weight layouts and limits as rlx_dequant_matmul;
+ * scheme must not be RLX_Q_NONE.
+ */
+rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scales, const void* zeros,
+                              int group_size, int N, int K, float* w_out, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Encoder: compile once (bind weights, plan the workspace), run many times
+ * (the paper's Session::compile -> CompiledGraph executed with bound inputs,
+ * Section III-C).
+ */
+typedef enum { RLX_INPUT_IDS = 0, RLX_INPUT_HIDDEN = 1 } rlx_input_kind;
+typedef enum { RLX_OUTPUT_POOLED = 0, RLX_OUTPUT_HIDDEN = 1 } rlx_output_kind;
+
+typedef struct {
+  int hidden;        /* H = heads * head_dim (384)                        */
+  int heads;         /* 12                                               */
+  int head_dim;      /* 32 (only supported value)                        */
+  int ffn;           /* F (1536)                                         */
+  int layers;        /* >= 1                                             */
+  int vocab;         /* word-embedding rows (IDS input)                  */
+  int max_pos;       /* position-embedding rows; >= max_seq (IDS input)  */
+  int type_vocab;    /* token-type rows (>= 1, row 0 is used)            */
+  float ln_eps;      /* LayerNorm epsilon (1e-12)                        */
+  rlx_dtype dtype;   /* RLX_F32 or RLX_BF16: activations, tables, unquantised weights */
+  rlx_quant quant;   /* linear-weight scheme; quantised needs RLX_BF16   */
+  int group_size;    /* 32 for RLX_Q_INT4_GROUP_ZP                       */
+  rlx_input_kind input_kind;
+  rlx_output_kind output_kind;
+  int max_batch;     /* <= 8192; workspace is planned for max_batch * max_seq tokens */
+  int max_seq;       /* <= 512                                           */
+  int use_graph;     /* 1: record each (B,S,buffers) forward once as a HIP graph and replay it */
+} rlx_encoder_config;
+
+/* One layer's weights.  Linear weights follow the nn.Linear convention
+ * ([out,in]); their dtype is the config's dtype when quant is RLX_Q_NONE,
+ * otherwise the scheme's layout (see rlx_quant), with *_scales / *_zeros
+ * pointing at the f16 scale / zero-point arrays (NULL when unused).
+ * wqkv stacks the Q, K and V projections: rows [0,H) Q, [H,2H) K, [2H,3H) V;
+ * head h owns rows h*head_dim .. h*head_dim+head_dim-1 of each block.
+ * Biases and LayerNorm parameters are f32.
+ */
+typedef struct {
+  const void* wqkv; const void* wqkv_scales; const void* wqkv_zeros; const float* bqkv;  /* [3H,H], [3H] */
+  const void* wo;   const void* wo_scales;   const void* wo_zeros;   const float* bo;    /* [H,H],  [H]  */
+  const float* ln1_gamma; const float* ln1_beta;                                         /* [H]          */
+  const void* w1;   const void* w1_scales;   const void* w1_zeros;   const float* b1;    /* [F,H],  [F]  */
+  const void* w2;   const void* w2_scales;   const void* w2_zeros;   const float* b2;    /* [H,F],  [H]  */
+  const float* ln2_gamma; const float* ln2_beta;                                         /* [H]          */
+} rlx_layer_weights;
+
+typedef struct {
+  const void* word_emb;  /* [vocab, H] dtype (IDS input only) */
+  const void* pos_emb;   /* [max_pos, H] dtype                 */
+  const void* type_emb;  /* [type_vocab, H] dtype              */
+  const float* emb_ln_gamma;  /* [H] */
+  const float* emb_ln_beta;   /* [H] */
+  const rlx_layer_weights* layers;  /* host array of cfg->layers entries; copied by create */
+} rlx_encoder_weights;
+
+typedef struct rlx_encoder rlx_encoder;
+
+/* Validates cfg and the weight pointers, allocates the workspace for
+ * max_batch * max_seq tokens on the current HIP device, and returns a handle
+ * in *out.  `cfg` and `w` are host pointers; they are copied.
+ * Errors: RLX_ERR_INVALID_ARG (nulls, non-positive sizes, H != heads*head_dim),
+ * RLX_ERR_UNSUPPORTED (head_dim != 32, H or F not a multiple of 64,
+ * max_seq > 512 or > max_pos, quantised weights with f32 activations,
+ * group_size != 32), RLX_ERR_OOM, RLX_ERR_HIP. */
+rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_weights* w, rlx_encoder** out);
+
+/* One forward pass.
+ * input: IDS -> int32 ids [B,S] in [0, vocab); HIDDEN -> [B,S,H] of cfg.dtype.
+ * attention_mask: u8 [B,S], 1 = real token.  Masked tokens are excluded as
+ * attention keys, from pooling, and produce zero rows in hidden output.
+ * Token (b,s) uses position embedding row s and token-type row 0.
+ * output: f32, [B,H] L2-normalised masked-mean embeddings (POOLED) or
+ * [B,S,H] final hidden states with zero rows at masked tokens (HIDDEN).
+ * Requires 1 <= B <= max_batch, 1 <= S <= max_seq; ids outside the vocabulary
+ * are clamped to row vocab-1 rather than read out of bounds.
+ * The handle's workspace is reused: do not run two forwards of one handle
+ * concurrently on different streams. */
+rlx_status rlx_encoder_forward(rlx_encoder* enc, const void* input, const uint8_t* attention_mask, int B, int S,
+                               void* output, void* stream);
+
+/* Frees the workspace and cached graphs (waits for the device first).  NULL is ignored. */
+void rlx_encoder_destroy(rlx_encoder* enc);
+
+/* Per-kernel timing of forward passes (a native counterpart of a per-operator
+ * dispatch report).  While enabled, forwards run kernel by kernel (never from
+ * a graph) with a HIP event pair around every launch; rlx_encoder_profile_read
+ * returns, per kernel class, the number of launches and the summed event time
+ * in milliseconds.  Names are static strings owned by the library. */
+rlx_status rlx_encoder_set_profiling(rlx_encoder* enc, int enable);
+rlx_status rlx_encoder_profile_read(rlx_encoder* enc, int max_entries, const char** names, int* launches,
+                                    double* total_ms, int* n_entries);
+
+/* Message describing the last error on the calling thread ("" if none).
+ * Valid until the next rlx_* call on this thread. */
+const char* rlx_last_error(void);
+
+/* Library version string, e.g. "rlx-mi355x 0.1.0 (gfx950)". */
+const char* rlx_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RLX_H_ */

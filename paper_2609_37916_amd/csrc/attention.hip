@@ -1,0 +1,314 @@
+// Fused masked multi-head attention for gfx950.
+//
+// The paper's IR carries attention as one primitive parameterised by an
+// explicit MaskKind in {None, Causal, SlidingWindow(w), Custom} (Section
+// III-A), and its optimizer fuses the attention block and reads Q, K and V as
+// strided narrows of one buffer (Section III-B).  Here that is one kernel that
+// reads Q/K/V by row stride straight out of the fused QKV projection.
+//
+// bf16 kernel -- one block per (query block of 128, head, sequence), four
+// waves of 32 queries each:
+//  * K rows and V (transposed) for the block's key range are staged once in
+//    LDS; key tiles of 32 whose keys are all masked are skipped.
+//  * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16
+//    (d = 32 is two k-steps), so each lane holds 16 keys of a single query:
+//    the softmax max / sum over keys is 15 in-lane steps plus one exchange
+//    with the partner lane 32 away.
+//  * Online softmax in fp32 in base 2 (scale * log2 e folded into one
+//    multiply), then P is rounded to bf16 and multiplied into ctx^T = V^T P^T,
+//    again on the matrix cores.  The probabilities stay in registers: their
+//    C-layout is used directly as the B operand, with the V^T operand read in
+//    the matching (permuted) key order.
+//  * Two layouts: padded (rows b*S .. b*S+S-1, optional u8 key mask) and
+//    variable-length (rows cu[b] .. cu[b+1]-1, every row a real token), which
+//    the encoder uses after compacting away padded tokens.
+// fp32 kernel -- one thread per query, K/V staged in LDS, scalar online softmax.
+#include <math.h>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace rlx {
+namespace {
+
+constexpr int kQBlock = 128;
+constexpr int kKRow = 80;  // bytes per staged K row (64 + 16 pad)
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct SeqRange {
+  int row0, n;
+};
+
+__device__ __forceinline__ SeqRange seq_range(const AttnParams& p, int b) {
+  if (p.cu_seqlens) {
+    int r0 = p.cu_seqlens[b];
+    return {r0, p.cu_seqlens[b + 1] - r0};
+  }
+  return {b * p.S, p.S};
+}
+
+// Key range [lo, hi) that queries [q_begin, q_end) may see, before the key mask.
+__device__ __forceinline__ void key_bounds(const AttnParams& p, int n, int q_begin, int q_end, int& lo, int& hi) {
+  lo = 0;
+  hi = n;
+  if (p.kind == 1 || p.kind == 2) hi = min(n, q_end);
+  if (p.kind == 2) lo = max(0, q_begin - p.window + 1);
+}
+
+__device__ __forceinline__ bool visible(int kind, int window, int qi, int key) {
+  if (kind == 1) return key <= qi;
+  if (kind == 2) return key <= qi && key > qi - window;
+  return true;
+}
+
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnParams p, int vt_stride) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int b = blockIdx.z, h = blockIdx.y;
+  const SeqRange sr = seq_range(p, b);
+  const int n = sr.n;
+  const int q_begin = blockIdx.x * kQBlock;
+  if (q_begin >= n) return;
+  const int q_end = min(n, q_begin + kQBlock);
+
+  int klo, khi;
+  key_bounds(p, n, q_begin, q_end, klo, khi);
+  klo &= ~31;                                  // stage whole 32-key tiles
+  const int nk = ((khi - klo) + 31) & ~31;     // staged keys (>= 0)
+  const int ntiles = nk >> 5;
+
+  uint8_t* k_lds = smem;                                               // [nk][80 B]
+  bf16_t* vt_lds = reinterpret_cast<bf16_t*>(smem + (size_t)nk * kKRow);  // [32][vt_stride]
+  uint32_t* kbits = reinterpret_cast<uint32_t*>(smem + (size_t)nk * kKRow + 32 * vt_stride * 2);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const bf16_t* kg = reinterpret_cast<const bf16_t*>(p.k);
+  const bf16_t* vg = reinterpret_cast<const bf16_t*>(p.v);
+  const bf16_t* qg = reinterpret_cast<const bf16_t*>(p.q);
+  const size_t ld = (size_t)p.ld_qkv;
+  const int col = h * 32;
+
+  // Stage K (row-major) and V (transposed); keys past the sequence are zero.
+  for (int idx = tid; idx < nk * 4; idx += 256) {
+    const int kr = idx >> 2, c = idx & 3;
+    const int key = klo + kr;
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (key < n) {
+      const size_t off = (size_t)(sr.row0 + key) * ld + col + c * 8;
+      kv = *reinterpret_cast<const uint4*>(kg + off);
+      vv = *reinterpret_cast<const uint4*>(vg + off);
+    }
+    *reinterpret_cast<uint4*>(k_lds + kr * kKRow + c * 16) = kv;
+    const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      vt_lds[(c * 8 + 2 * e) * vt_stride + kr] = (bf16_t)(w4[e] & 0xffffu);
+      vt_lds[(c * 8 + 2 * e + 1) * vt_stride + kr] = (bf16_t)(w4[e] >> 16);
+    }
+  }
+  // Per-tile validity bits (key inside the sequence and allowed by the key mask).
+  for (int t = wave; t < ntiles; t += 4) {
+    const int key = klo + t * 32 + (lane & 31);
+    bool ok = key < n;
+    if (ok && p.key_mask) ok = p.key_mask[(size_t)b * p.S + key] != 0;
+    const uint64_t bal = __ballot(ok && lane < 32);
+    if (lane == 0) kbits[t] = (uint32_t)bal;
+  }
+  __syncthreads();
+
+  const int q0 = q_begin + wave * 32;
+  if (q0 >= n) return;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int qi = q0 + l32;
+  const int qrow = sr.row0 + min(qi, n - 1);
+
+  const bf16x8_t qf0 = as_bf16x8(*reinterpret_cast<const uint4*>(qg + (size_t)qrow * ld + col + half * 8));
+  const bf16x8_t qf1 = as_bf16x8(*reinterpret_cast<const uint4*>(qg + (size_t)qrow * ld + col + 16 + half * 8));
+
+  // Tiles this wave needs.
+  int wlo, whi;
+  key_bounds(p, n, q0, min(n, q0 + 32), wlo, whi);
+  const int t_begin = max(0, (wlo - klo) >> 5);
+  const int t_end = min(ntiles, (whi - klo + 31) >> 5);
+
+  const float sl2 = p.scale * kLog2e;
+  float m_run = -INFINITY, l_run = 0.0f;
+  f32x16_t acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+
+  for (int t = t_begin; t < t_end; ++t) {
+    const uint32_t bits = kbits[t];
+    if (bits == 0u) continue;
+    const int kb = t * 32;
+    const uint8_t* krow = k_lds + (kb + l32) * kKRow + half * 16;
+    f32x16_t s;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[v] = 0.0f;
+    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(*reinterpret_cast<const uint4*>(krow)), qf0, s, 0, 0, 0);
+    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(*reinterpret_cast<const uint4*>(krow + 32)), qf1, s, 0, 0,
+                                                0);
+    // Register v holds key kb + 8*(v/4) + 4*half + (v%4) for query qi.
+    float tv[16];
+    float tmax = -INFINITY;
+    const bool need_pos = p.kind == 1 || p.kind == 2;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int kk = 8 * (v >> 2) + 4 * half + (v & 3);
+      bool ok = (bits >> kk) & 1u;
+      if (need_pos) ok = ok && visible(p.kind, p.window, qi, klo + kb + kk);
+      tv[v] = ok ? s[v] * sl2 : -INFINITY;
+      tmax = fmaxf(tmax, tv[v]);
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float m_new = fmaxf(m_run, tmax);
+    float alpha, psum = 0.0f;
+    float pv[16];
+    if (m_new == -INFINITY) {
+      alpha = 1.0f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) pv[v] = 0.0f;
+    } else {
+      alpha = exp2f(m_run - m_new);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        pv[v] = exp2f(tv[v] - m_new);
+        psum += pv[v];
+      }
+    }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] *= alpha;
+
+    const uint4 pb0 = make_uint4(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]), pack_bf16x2(pv[4], pv[5]),
+                                 pack_bf16x2(pv[6], pv[7]));
+    const uint4 pb1 = make_uint4(pack_bf16x2(pv[8], pv[9]), pack_bf16x2(pv[10], pv[11]),
+                                 pack_bf16x2(pv[12], pv[13]), pack_bf16x2(pv[14], pv[15]));
+    // V^T operand: row d = l32, keys kb + 4*half + {0..3} and kb + 8 + 4*half + {0..3} (+16 for step 2).
+    const bf16_t* vrow = vt_lds + (size_t)l32 * vt_stride + kb + 4 * half;
+    const uint2 v00 = *reinterpret_cast<const uint2*>(vrow);
+    const uint2 v01 = *reinterpret_cast<const uint2*>(vrow + 8);
+    const uint2 v10 = *reinterpret_cast<const uint2*>(vrow + 16);
+    const uint2 v11 = *reinterpret_cast<const uint2*>(vrow + 24);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(make_uint4(v00.x, v00.y, v01.x, v01.y)),
+                                                  as_bf16x8(pb0), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(make_uint4(v10.x, v10.y, v11.x, v11.y)),
+                                                  as_bf16x8(pb1), acc, 0, 0, 0);
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  if (qi >= n) return;
+  const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+  bf16_t* og = reinterpret_cast<bf16_t*>(p.out) + (size_t)(sr.row0 + qi) * p.ld_out + col;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int d = 8 * i + 4 * half;
+    *reinterpret_cast<uint2*>(og + d) =
+        make_uint2(pack_bf16x2(acc[4 * i] * inv, acc[4 * i + 1] * inv),
+                   pack_bf16x2(acc[4 * i + 2] * inv, acc[4 * i + 3] * inv));
+  }
+}
+
+__global__ __launch_bounds__(128) void attn_f32_kernel(AttnParams p) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int b = blockIdx.z, h = blockIdx.y;
+  const SeqRange sr = seq_range(p, b);
+  const int n = sr.n;
+  const int q_begin = blockIdx.x * kQBlock;
+  if (q_begin >= n) return;
+  const int q_end = min(n, q_begin + kQBlock);
+  int klo, khi;
+  key_bounds(p, n, q_begin, q_end, klo, khi);
+  const int nk = khi - klo;
+
+  float* k_lds = reinterpret_cast<float*>(smem);   // [nk][32]
+  float* v_lds = k_lds + (size_t)nk * 32;           // [nk][32]
+  uint8_t* ok_lds = reinterpret_cast<uint8_t*>(v_lds + (size_t)nk * 32);
+  const float* kg = reinterpret_cast<const float*>(p.k);
+  const float* vg = reinterpret_cast<const float*>(p.v);
+  const float* qg = reinterpret_cast<const float*>(p.q);
+  const size_t ld = (size_t)p.ld_qkv;
+  const int col = h * 32;
+  for (int idx = threadIdx.x; idx < nk * 8; idx += blockDim.x) {
+    const int kr = idx >> 3, c = idx & 7;
+    const size_t off = (size_t)(sr.row0 + klo + kr) * ld + col + c * 4;
+    *reinterpret_cast<float4*>(k_lds + kr * 32 + c * 4) = *reinterpret_cast<const float4*>(kg + off);
+    *reinterpret_cast<float4*>(v_lds + kr * 32 + c * 4) = *reinterpret_cast<const float4*>(vg + off);
+  }
+  for (int kr = threadIdx.x; kr < nk; kr += blockDim.x)
+    ok_lds[kr] = p.key_mask ? (p.key_mask[(size_t)b * p.S + klo + kr] != 0) : 1;
+  __syncthreads();
+
+  const int qi = q_begin + threadIdx.x;
+  if (qi >= n) return;
+  const float sl2 = p.scale * kLog2e;
+  float qv[32], acc[32];
+  const float* qrow = qg + (size_t)(sr.row0 + qi) * ld + col;
+#pragma unroll
+  for (int d = 0; d < 32; ++d) {
+    qv[d] = qrow[d] * sl2;
+    acc[d] = 0.0f;
+  }
+  float m_run = -INFINITY, l_run = 0.0f;
+  for (int kr = 0; kr < nk; ++kr) {
+    const int key = klo + kr;
+    if (!ok_lds[kr] || !visible(p.kind, p.window, qi, key)) continue;
+    const float* kk = k_lds + kr * 32;
+    float s = 0.0f;
+#pragma unroll
+    for (int d = 0; d < 32; ++d) s = fmaf(qv[d], kk[d], s);
+    if (s > m_run) {
+      const float alpha = exp2f(m_run - s);
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < 32; ++d) acc[d] *= alpha;
+      m_run = s;
+    }
+    const float pr = exp2f(s - m_run);
+    l_run += pr;
+    const float* vv = v_lds + kr * 32;
+#pragma unroll
+    for (int d = 0; d < 32; ++d) acc[d] = fmaf(pr, vv[d], acc[d]);
+  }
+  const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+  float* og = reinterpret_cast<float*>(p.out) + (size_t)(sr.row0 + qi) * p.ld_out + col;
+#pragma unroll
+  for (int d = 0; d < 32; d += 4)
+    *reinterpret_cast<float4*>(og + d) = make_float4(acc[d] * inv, acc[d + 1] * inv, acc[d + 2] * inv, acc[d + 3] * inv);
+}
+
+}  // namespace
+
+// Raise the dynamic-LDS limit of both kernels once (S = 512 needs ~74 KB for
+// bf16 and ~128 KB for f32; gfx950 has 160 KB per workgroup).
+hipError_t set_lds_limits() {
+  static const hipError_t once = [] {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(attn_bf16_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(attn_f32_kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  }();
+  return once;
+}
+
+hipError_t init_kernel_attributes() { return set_lds_limits(); }
+
+hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
+  if (p.B <= 0 || p.S <= 0) return hipSuccess;
+  const hipError_t le = set_lds_limits();
+  if (le != hipSuccess) return le;
+  const dim3 grid((p.S + kQBlock - 1) / kQBlock, p.heads, p.B);
+  if (p.dtype == DType::BF16) {
+    const int nk_max = (p.S + 31) & ~31;  // staged keys never exceed the padded length
+    const int vt_stride = ((nk_max + 127) & ~127) + 4;
+    const size_t lds = (size_t)nk_max * kKRow + 32 * (size_t)vt_stride * 2 + (size_t)(nk_max / 32) * 4;
+    hipLaunchKernelGGL(attn_bf16_kernel, grid, dim3(256), lds, s, p, vt_stride);
+  } else {
+    const size_t lds = (size_t)p.S * 32 * 4 * 2 + (size_t)p.S;
+    hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(128), lds, s, p);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace rlx

@@ -1,0 +1,563 @@
+// C ABI: argument validation, the encoder handle (bound weights + planned
+// workspace + cached HIP graphs), per-kernel profiling and error reporting.
+//
+// The paper's runtime compiles a graph once for a device and executes the
+// cached schedule with bound inputs (Section III-C), and its dispatch fails
+// with a diagnostic instead of silently degrading (Section IV).  Here:
+// rlx_encoder_create binds the weights and allocates one workspace for
+// max_batch * max_seq tokens; rlx_encoder_forward validates everything
+// before enqueueing anything, then replays a HIP graph recorded for the same
+// (B, S, buffers) or records one.  Unsupported requests return
+// RLX_ERR_UNSUPPORTED with a message; no other code path is ever taken.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/rlx.h"
+#include "kernels.hpp"
+
+using namespace rlx;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+rlx_status fail(rlx_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+rlx_status ok() {
+  g_last_error.clear();
+  return RLX_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+rlx_status hip_fail(hipError_t e, const char* what) {
+  return fail(RLX_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define RLX_HIP(call, what)                        \
+  do {                                             \
+    hipError_t e_ = (call);                        \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+const char* dtype_name(rlx_dtype d) {
+  switch (d) {
+    case RLX_F32: return "f32";
+    case RLX_BF16: return "bf16";
+    case RLX_F16: return "f16";
+    case RLX_I8: return "i8";
+    case RLX_U4X2: return "u4x2";
+    case RLX_I32: return "i32";
+    case RLX_U8: return "u8";
+  }
+  return "?";
+}
+
+rlx_status check_attention_args(const void* q, const void* k, const void* v, int64_t ld, const void* out,
+                                int64_t ld_out, int B, int S, int heads, int head_dim, rlx_dtype dt,
+                                rlx_mask_kind kind, const uint8_t* key_mask, int window, float scale) {
+  if (B < 0 || S < 0) return fail(RLX_ERR_INVALID_ARG, "attention: B=%d and S=%d must be >= 0", B, S);
+  if (heads <= 0 || head_dim <= 0)
+    return fail(RLX_ERR_INVALID_ARG, "attention: num_heads=%d and head_dim=%d must be positive", heads, head_dim);
+  if (!q || !k || !v || !out) return fail(RLX_ERR_INVALID_ARG, "attention: q, k, v and out must be non-null");
+  if (kind < RLX_MASK_NONE || kind > RLX_MASK_CUSTOM)
+    return fail(RLX_ERR_INVALID_ARG, "attention: unknown mask kind %d", (int)kind);
+  if (kind == RLX_MASK_CUSTOM && !key_mask)
+    return fail(RLX_ERR_INVALID_ARG, "attention: RLX_MASK_CUSTOM needs a key mask");
+  if (kind == RLX_MASK_SLIDING_WINDOW && window < 1)
+    return fail(RLX_ERR_INVALID_ARG, "attention: sliding window %d must be >= 1", window);
+  if (!std::isfinite(scale)) return fail(RLX_ERR_INVALID_ARG, "attention: scale must be finite");
+  if (dt != RLX_BF16 && dt != RLX_F32)
+    return fail(RLX_ERR_UNSUPPORTED, "attention: dtype %s not supported (bf16, f32)", dtype_name(dt));
+  if (head_dim != 32) return fail(RLX_ERR_UNSUPPORTED, "attention: head_dim %d not supported (32)", head_dim);
+  if (S > 512) return fail(RLX_ERR_UNSUPPORTED, "attention: S=%d exceeds 512", S);
+  const int64_t hw = (int64_t)heads * head_dim;
+  if (ld < hw || ld_out < hw)
+    return fail(RLX_ERR_INVALID_ARG, "attention: row strides (%lld, %lld) smaller than heads*head_dim=%lld",
+                (long long)ld, (long long)ld_out, (long long)hw);
+  if (ld % 8 || ld_out % 8)
+    return fail(RLX_ERR_UNSUPPORTED, "attention: row strides must be multiples of 8 elements");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(RLX_ERR_UNSUPPORTED, "attention: q, k, v and out must be 16-byte aligned");
+  return RLX_OK;
+}
+
+rlx_status check_quant_weights(const char* who, rlx_quant scheme, const void* w, const void* scales,
+                               const void* zeros, int group_size, int N, int K) {
+  if (!w) return fail(RLX_ERR_INVALID_ARG, "%s: weight pointer is null", who);
+  if (scheme < RLX_Q_NONE || scheme > RLX_Q_INT4_GROUP_ZP)
+    return fail(RLX_ERR_INVALID_ARG, "%s: unknown quantisation scheme %d", who, (int)scheme);
+  if (N % 64 || K % 64)
+    return fail(RLX_ERR_UNSUPPORTED, "%s: N=%d and K=%d must be multiples of 64", who, N, K);
+  if (!aligned16(w)) return fail(RLX_ERR_UNSUPPORTED, "%s: weights must be 16-byte aligned", who);
+  if (scheme == RLX_Q_INT8_PER_CHANNEL && !scales)
+    return fail(RLX_ERR_INVALID_ARG, "%s: int8 weights need scales", who);
+  if (scheme == RLX_Q_INT4_GROUP_ZP) {
+    if (!scales || !zeros) return fail(RLX_ERR_INVALID_ARG, "%s: int4 weights need scales and zeros", who);
+    if (group_size != 32)
+      return fail(RLX_ERR_UNSUPPORTED, "%s: int4 group size %d not supported (32)", who, group_size);
+  }
+  return RLX_OK;
+}
+
+Quant to_quant(rlx_quant q) {
+  return q == RLX_Q_INT8_PER_CHANNEL ? Quant::Int8 : (q == RLX_Q_INT4_GROUP_ZP ? Quant::Int4 : Quant::None);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// encoder handle
+// ---------------------------------------------------------------------------
+
+namespace {
+
+enum KernelClass {
+  K_MASK_SCAN = 0, K_EMBED_LN, K_GATHER_ROWS, K_GEMM_QKV, K_ATTENTION, K_GEMM_ATTN_OUT, K_LN1, K_GEMM_FFN_UP,
+  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_NUM_CLASSES
+};
+const char* kClassNames[K_NUM_CLASSES] = {"mask_scan",     "embed_ln",    "gather_rows", "gemm_qkv",
+                                          "attention",     "gemm_attn_out", "layer_norm_1", "gemm_ffn_up",
+                                          "gemm_ffn_down", "layer_norm_2", "pool_l2",     "scatter_hidden"};
+
+struct GraphEntry {
+  int B, S;
+  const void* input;
+  const uint8_t* mask;
+  void* output;
+  hipGraphExec_t exec;
+  uint64_t last_use;
+};
+
+struct ProfRec {
+  int cls;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct rlx_encoder {
+  rlx_encoder_config cfg;
+  rlx_encoder_weights w;
+  std::vector<rlx_layer_weights> layers;
+  int device = 0;
+  DType dt = DType::BF16;
+  void* ws = nullptr;
+  int* cu = nullptr;
+  int* tok_src = nullptr;
+  int* tok_dst = nullptr;
+  void *X = nullptr, *X1 = nullptr, *A = nullptr, *CTX = nullptr, *QKV = nullptr, *G = nullptr;
+  hipStream_t cap_stream = nullptr;
+  std::vector<GraphEntry> graphs;
+  uint64_t use_clock = 0;
+  bool profiling = false;
+  std::vector<ProfRec> prof;
+};
+
+namespace {
+
+constexpr size_t kMaxGraphs = 16;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+rlx_status check_config(const rlx_encoder_config* c) {
+  if (c->hidden <= 0 || c->heads <= 0 || c->head_dim <= 0 || c->ffn <= 0 || c->layers <= 0)
+    return fail(RLX_ERR_INVALID_ARG, "encoder: hidden, heads, head_dim, ffn and layers must be positive");
+  if (c->hidden != c->heads * c->head_dim)
+    return fail(RLX_ERR_INVALID_ARG, "encoder: hidden %d != heads %d * head_dim %d", c->hidden, c->heads,
+                c->head_dim);
+  if (c->max_batch <= 0 || c->max_seq <= 0)
+    return fail(RLX_ERR_INVALID_ARG, "encoder: max_batch and max_seq must be positive");
+  if (c->input_kind != RLX_INPUT_IDS && c->input_kind != RLX_INPUT_HIDDEN)
+    return fail(RLX_ERR_INVALID_ARG, "encoder: unknown input kind %d", (int)c->input_kind);
+  if (c->output_kind != RLX_OUTPUT_POOLED && c->output_kind != RLX_OUTPUT_HIDDEN)
+    return fail(RLX_ERR_INVALID_ARG, "encoder: unknown output kind %d", (int)c->output_kind);
+  if (!(c->ln_eps >= 0.0f) || !std::isfinite(c->ln_eps))
+    return fail(RLX_ERR_INVALID_ARG, "encoder: ln_eps must be finite and >= 0");
+  if (c->input_kind == RLX_INPUT_IDS && (c->vocab <= 0 || c->max_pos <= 0 || c->type_vocab <= 0))
+    return fail(RLX_ERR_INVALID_ARG, "encoder: vocab, max_pos and type_vocab must be positive for id input");
+  if (c->dtype != RLX_F32 && c->dtype != RLX_BF16)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder: dtype %s not supported (f32, bf16)", dtype_name(c->dtype));
+  if (c->quant < RLX_Q_NONE || c->quant > RLX_Q_INT4_GROUP_ZP)
+    return fail(RLX_ERR_INVALID_ARG, "encoder: unknown quantisation scheme %d", (int)c->quant);
+  if (c->quant != RLX_Q_NONE && c->dtype != RLX_BF16)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder: quantised weights need bf16 activations");
+  if (c->quant == RLX_Q_INT4_GROUP_ZP && c->group_size != 32)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder: int4 group size %d not supported (32)", c->group_size);
+  if (c->head_dim != 32) return fail(RLX_ERR_UNSUPPORTED, "encoder: head_dim %d not supported (32)", c->head_dim);
+  if (c->hidden % 64 || c->ffn % 64 || c->hidden > 1024)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder: hidden %d and ffn %d must be multiples of 64, hidden <= 1024",
+                c->hidden, c->ffn);
+  if (c->max_seq > 512) return fail(RLX_ERR_UNSUPPORTED, "encoder: max_seq %d exceeds 512", c->max_seq);
+  if (c->input_kind == RLX_INPUT_IDS && c->max_seq > c->max_pos)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder: max_seq %d exceeds max_pos %d", c->max_seq, c->max_pos);
+  if (c->max_batch > 8192) return fail(RLX_ERR_UNSUPPORTED, "encoder: max_batch %d exceeds 8192", c->max_batch);
+  if ((int64_t)c->max_batch * c->max_seq > (int64_t)1 << 24)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder: max_batch * max_seq exceeds 2^24 tokens");
+  return RLX_OK;
+}
+
+rlx_status check_weights(const rlx_encoder_config* c, const rlx_encoder_weights* w) {
+  if (!w->layers) return fail(RLX_ERR_INVALID_ARG, "encoder: weights->layers is null");
+  if (c->input_kind == RLX_INPUT_IDS) {
+    if (!w->word_emb || !w->pos_emb || !w->type_emb || !w->emb_ln_gamma || !w->emb_ln_beta)
+      return fail(RLX_ERR_INVALID_ARG, "encoder: embedding tables and embedding LayerNorm parameters are required");
+  }
+  const int H = c->hidden, F = c->ffn;
+  for (int l = 0; l < c->layers; ++l) {
+    const rlx_layer_weights& L = w->layers[l];
+    if (!L.bqkv || !L.bo || !L.b1 || !L.b2 || !L.ln1_gamma || !L.ln1_beta || !L.ln2_gamma || !L.ln2_beta)
+      return fail(RLX_ERR_INVALID_ARG, "encoder: layer %d has a null bias or LayerNorm parameter", l);
+    struct { const char* nm; const void *w, *s, *z; int N, K; const float* b; } lin[4] = {
+        {"wqkv", L.wqkv, L.wqkv_scales, L.wqkv_zeros, 3 * H, H, L.bqkv},
+        {"wo", L.wo, L.wo_scales, L.wo_zeros, H, H, L.bo},
+        {"w1", L.w1, L.w1_scales, L.w1_zeros, F, H, L.b1},
+        {"w2", L.w2, L.w2_scales, L.w2_zeros, H, F, L.b2}};
+    for (auto& x : lin) {
+      char who[64];
+      snprintf(who, sizeof who, "encoder layer %d %s", l, x.nm);
+      rlx_status st = check_quant_weights(who, c->quant, x.w, x.s, x.z, c->group_size, x.N, x.K);
+      if (st != RLX_OK) return st;
+      if (!aligned16(x.b)) return fail(RLX_ERR_UNSUPPORTED, "%s: bias must be 16-byte aligned", who);
+    }
+  }
+  return RLX_OK;
+}
+
+// Enqueue one forward on `s`.  `prof` records an event pair around every launch.
+rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
+                           hipStream_t s, bool prof) {
+  const rlx_encoder_config& c = e->cfg;
+  const int H = c.hidden, F = c.ffn, T = B * S;
+  const int* n_dev = e->cu + B;  // number of real tokens, written by the mask scan
+  auto step = [&](int cls, auto&& fn) -> rlx_status {
+    hipEvent_t a = nullptr, b = nullptr;
+    if (prof) {
+      RLX_HIP(hipEventCreate(&a), "hipEventCreate");
+      RLX_HIP(hipEventCreate(&b), "hipEventCreate");
+      RLX_HIP(hipEventRecord(a, s), "hipEventRecord");
+    }
+    hipError_t err = fn();
+    if (err != hipSuccess) return hip_fail(err, kClassNames[cls]);
+    if (prof) {
+      RLX_HIP(hipEventRecord(b, s), "hipEventRecord");
+      e->prof.push_back({cls, a, b});
+    }
+    return RLX_OK;
+  };
+#define STEP(cls, expr)                                                   \
+  do {                                                                    \
+    rlx_status st_ = step(cls, [&]() -> hipError_t { return (expr); }); \
+    if (st_ != RLX_OK) return st_;                                        \
+  } while (0)
+
+  STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, e->cu, e->tok_src, e->tok_dst, s));
+  if (c.input_kind == RLX_INPUT_IDS) {
+    STEP(K_EMBED_LN, launch_embed_ln(static_cast<const int*>(input), e->w.word_emb, e->w.pos_emb, e->w.type_emb,
+                                     e->w.emb_ln_gamma, e->w.emb_ln_beta, c.ln_eps, c.vocab, S, H, e->tok_src, n_dev,
+                                     T, e->X, e->dt, s));
+  } else {
+    STEP(K_GATHER_ROWS, launch_gather_rows(input, H, e->tok_src, n_dev, T, e->X, e->dt, s));
+  }
+  const Quant q = to_quant(c.quant);
+  for (int l = 0; l < c.layers; ++l) {
+    const rlx_layer_weights& L = e->layers[l];
+    GemmParams g{};
+    g.m_dev = n_dev;
+    g.M = T;
+    g.dtype = e->dt;
+    g.quant = q;
+
+    g.x = e->X; g.w = L.wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = L.bqkv;
+    g.residual = nullptr; g.y = e->QKV; g.N = 3 * H; g.K = H; g.epi = Epi::Bias;
+    STEP(K_GEMM_QKV, launch_gemm(g, s));
+
+    AttnParams a{};
+    const size_t es = e->dt == DType::BF16 ? 2 : 4;
+    a.q = e->QKV;
+    a.k = static_cast<const uint8_t*>(e->QKV) + (size_t)H * es;
+    a.v = static_cast<const uint8_t*>(e->QKV) + (size_t)2 * H * es;
+    a.ld_qkv = 3 * H;
+    a.out = e->CTX; a.ld_out = H;
+    a.B = B; a.S = S; a.heads = c.heads; a.kind = 0; a.key_mask = nullptr; a.window = 0;
+    a.scale = 1.0f / std::sqrt((float)c.head_dim);
+    a.cu_seqlens = e->cu;
+    a.dtype = e->dt;
+    STEP(K_ATTENTION, launch_attention(a, s));
+
+    g.x = e->CTX; g.w = L.wo; g.scales = L.wo_scales; g.zeros = L.wo_zeros; g.bias = L.bo;
+    g.residual = e->X; g.y = e->A; g.N = H; g.K = H; g.epi = Epi::BiasResidual;
+    STEP(K_GEMM_ATTN_OUT, launch_gemm(g, s));
+    STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, s));
+
+    g.x = e->X1; g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;
+    g.residual = nullptr; g.y = e->G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
+    STEP(K_GEMM_FFN_UP, launch_gemm(g, s));
+
+    g.x = e->G; g.w = L.w2; g.scales = L.w2_scales; g.zeros = L.w2_zeros; g.bias = L.b2;
+    g.residual = e->X1; g.y = e->A; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
+    STEP(K_GEMM_FFN_DOWN, launch_gemm(g, s));
+    STEP(K_LN2, launch_layer_norm(e->A, L.ln2_gamma, L.ln2_beta, c.ln_eps, H, n_dev, T, e->X, e->dt, s));
+  }
+  if (c.output_kind == RLX_OUTPUT_POOLED) {
+    STEP(K_POOL, launch_pool_l2(e->X, H, e->cu, B, static_cast<float*>(output), e->dt, s));
+  } else {
+    STEP(K_SCATTER, launch_scatter_hidden(e->X, H, e->tok_dst, T, static_cast<float*>(output), e->dt, s));
+  }
+#undef STEP
+  return RLX_OK;
+}
+
+void destroy_graphs(rlx_encoder* e) {
+  for (auto& g : e->graphs) (void)hipGraphExecDestroy(g.exec);
+  e->graphs.clear();
+}
+
+void clear_profile(rlx_encoder* e) {
+  for (auto& r : e->prof) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  e->prof.clear();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rlx_last_error(void) { return g_last_error.c_str(); }
+
+const char* rlx_version(void) { return "rlx-mi355x 0.1.0 (gfx950)"; }
+
+rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int64_t qkv_row_stride, void* out,
+                                int64_t out_row_stride, int B, int S, int num_heads, int head_dim, rlx_dtype dt,
+                                rlx_mask_kind kind, const uint8_t* key_mask, int window, float scale,
+                                void* stream) {
+  rlx_status st = check_attention_args(q, k, v, qkv_row_stride, out, out_row_stride, B, S, num_heads, head_dim, dt,
+                                       kind, key_mask, window, scale);
+  if (st != RLX_OK) return st;
+  if (B == 0 || S == 0) return ok();
+  AttnParams a{};
+  a.q = q; a.k = k; a.v = v; a.ld_qkv = qkv_row_stride;
+  a.out = out; a.ld_out = out_row_stride;
+  a.B = B; a.S = S; a.heads = num_heads; a.kind = (int)kind; a.key_mask = key_mask; a.window = window;
+  a.scale = scale; a.cu_seqlens = nullptr;
+  a.dtype = dt == RLX_BF16 ? DType::BF16 : DType::F32;
+  RLX_HIP(launch_attention(a, static_cast<hipStream_t>(stream)), "attention launch");
+  return ok();
+}
+
+rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const void* w, rlx_quant scheme,
+                              const void* scales, const void* zeros, int group_size, int N, const float* bias,
+                              const void* residual, rlx_epilogue epi, void* y, void* stream) {
+  if (M < 0 || N <= 0 || K <= 0)
+    return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: M=%d must be >= 0, N=%d and K=%d positive", M, N, K);
+  if (!x || !y) return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: x and y must be non-null");
+  if (epi < RLX_EPI_NONE || epi > RLX_EPI_BIAS_RESIDUAL)
+    return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: unknown epilogue %d", (int)epi);
+  if (epi != RLX_EPI_NONE && !bias) return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: epilogue needs a bias");
+  if (epi == RLX_EPI_BIAS_RESIDUAL && !residual)
+    return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: residual epilogue needs a residual");
+  if (x_dt != RLX_BF16 && x_dt != RLX_F32)
+    return fail(RLX_ERR_UNSUPPORTED, "dequant_matmul: activation dtype %s not supported (bf16, f32)",
+                dtype_name(x_dt));
+  rlx_status st = check_quant_weights("dequant_matmul", scheme, w, scales, zeros, group_size, N, K);
+  if (st != RLX_OK) return st;
+  if (scheme != RLX_Q_NONE && x_dt != RLX_BF16)
+    return fail(RLX_ERR_UNSUPPORTED, "dequant_matmul: quantised weights need bf16 activations");
+  if (!aligned16(x) || !aligned16(y) || (residual && !aligned16(residual)) || (bias && !aligned16(bias)))
+    return fail(RLX_ERR_UNSUPPORTED, "dequant_matmul: x, y, bias and residual must be 16-byte aligned");
+  if (M == 0) return ok();
+  GemmParams g{};
+  g.x = x; g.w = w; g.scales = scales; g.zeros = zeros; g.bias = bias; g.residual = residual; g.y = y;
+  g.M = M; g.N = N; g.K = K; g.m_dev = nullptr;
+  g.dtype = x_dt == RLX_BF16 ? DType::BF16 : DType::F32;
+  g.quant = to_quant(scheme);
+  g.epi = static_cast<Epi>(epi);
+  RLX_HIP(launch_gemm(g, static_cast<hipStream_t>(stream)), "gemm launch");
+  return ok();
+}
+
+rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scales, const void* zeros, int group_size,
+                              int N, int K, float* w_out, void* stream) {
+  if (N <= 0 || K <= 0) return fail(RLX_ERR_INVALID_ARG, "dequant_unpack: N=%d and K=%d must be positive", N, K);
+  if (!w_out) return fail(RLX_ERR_INVALID_ARG, "dequant_unpack: w_out must be non-null");
+  if (scheme == RLX_Q_NONE) return fail(RLX_ERR_INVALID_ARG, "dequant_unpack: scheme must be int8 or int4");
+  rlx_status st = check_quant_weights("dequant_unpack", scheme, w, scales, zeros, group_size, N, K);
+  if (st != RLX_OK) return st;
+  RLX_HIP(launch_dequant_unpack(w, to_quant(scheme), scales, zeros, N, K, w_out, static_cast<hipStream_t>(stream)),
+          "dequant unpack launch");
+  return ok();
+}
+
+rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_weights* w, rlx_encoder** out) {
+  if (!cfg || !w || !out) return fail(RLX_ERR_INVALID_ARG, "encoder_create: cfg, weights and out must be non-null");
+  *out = nullptr;
+  rlx_status st = check_config(cfg);
+  if (st != RLX_OK) return st;
+  st = check_weights(cfg, w);
+  if (st != RLX_OK) return st;
+
+  rlx_encoder* e = new rlx_encoder();
+  e->cfg = *cfg;
+  e->w = *w;
+  e->layers.assign(w->layers, w->layers + cfg->layers);
+  e->w.layers = e->layers.data();
+  e->dt = cfg->dtype == RLX_BF16 ? DType::BF16 : DType::F32;
+  hipError_t he = hipGetDevice(&e->device);
+  if (he == hipSuccess) he = init_kernel_attributes();  // outside any graph capture
+  if (he != hipSuccess) {
+    delete e;
+    return hip_fail(he, "encoder_create: device setup");
+  }
+
+  // Workspace plan: token maps, then six activation buffers for T_max tokens.
+  const size_t T = (size_t)cfg->max_batch * cfg->max_seq;
+  const size_t es = e->dt == DType::BF16 ? 2 : 4;
+  const size_t H = cfg->hidden, F = cfg->ffn;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+  const size_t o_cu = take((cfg->max_batch + 1) * sizeof(int));
+  const size_t o_src = take(T * sizeof(int));
+  const size_t o_dst = take(T * sizeof(int));
+  const size_t o_X = take(T * H * es), o_X1 = take(T * H * es), o_A = take(T * H * es), o_C = take(T * H * es);
+  const size_t o_Q = take(T * 3 * H * es), o_G = take(T * F * es);
+  he = hipMalloc(&e->ws, off);
+  if (he != hipSuccess) {
+    delete e;
+    return fail(RLX_ERR_OOM, "encoder_create: workspace of %zu bytes: %s", off, hipGetErrorString(he));
+  }
+  uint8_t* base = static_cast<uint8_t*>(e->ws);
+  e->cu = reinterpret_cast<int*>(base + o_cu);
+  e->tok_src = reinterpret_cast<int*>(base + o_src);
+  e->tok_dst = reinterpret_cast<int*>(base + o_dst);
+  e->X = base + o_X; e->X1 = base + o_X1; e->A = base + o_A; e->CTX = base + o_C; e->QKV = base + o_Q;
+  e->G = base + o_G;
+  he = hipStreamCreateWithFlags(&e->cap_stream, hipStreamNonBlocking);
+  if (he != hipSuccess) {
+    (void)hipFree(e->ws);
+    delete e;
+    return hip_fail(he, "hipStreamCreateWithFlags");
+  }
+  *out = e;
+  return ok();
+}
+
+rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t* attention_mask, int B, int S,
+                               void* output, void* stream) {
+  if (!e) return fail(RLX_ERR_INVALID_ARG, "encoder_forward: null handle");
+  if (!input || !attention_mask || !output)
+    return fail(RLX_ERR_INVALID_ARG, "encoder_forward: input, attention_mask and output must be non-null");
+  if (B < 1 || S < 1) return fail(RLX_ERR_INVALID_ARG, "encoder_forward: B=%d and S=%d must be >= 1", B, S);
+  if (B > e->cfg.max_batch || S > e->cfg.max_seq)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder_forward: B=%d, S=%d exceed the planned max_batch=%d, max_seq=%d", B,
+                S, e->cfg.max_batch, e->cfg.max_seq);
+  int dev = -1;
+  RLX_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev != e->device)
+    return fail(RLX_ERR_INVALID_ARG, "encoder_forward: current device %d differs from the handle's device %d", dev,
+                e->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (e->profiling) {
+    rlx_status st = enqueue_forward(e, input, attention_mask, B, S, output, s, true);
+    return st == RLX_OK ? ok() : st;
+  }
+  if (!e->cfg.use_graph) {
+    rlx_status st = enqueue_forward(e, input, attention_mask, B, S, output, s, false);
+    return st == RLX_OK ? ok() : st;
+  }
+  GraphEntry* hit = nullptr;
+  for (auto& g : e->graphs)
+    if (g.B == B && g.S == S && g.input == input && g.mask == attention_mask && g.output == output) hit = &g;
+  if (!hit) {
+    if (e->graphs.size() >= kMaxGraphs) {
+      auto lru = std::min_element(e->graphs.begin(), e->graphs.end(),
+                                  [](const GraphEntry& a, const GraphEntry& b) { return a.last_use < b.last_use; });
+      RLX_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
+      (void)hipGraphExecDestroy(lru->exec);
+      e->graphs.erase(lru);
+    }
+    RLX_HIP(hipStreamBeginCapture(e->cap_stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+    rlx_status st = enqueue_forward(e, input, attention_mask, B, S, output, e->cap_stream, false);
+    hipGraph_t graph = nullptr;
+    hipError_t he = hipStreamEndCapture(e->cap_stream, &graph);
+    if (st != RLX_OK) {
+      if (graph) (void)hipGraphDestroy(graph);
+      return st;
+    }
+    if (he != hipSuccess) return hip_fail(he, "hipStreamEndCapture");
+    hipGraphExec_t exec = nullptr;
+    he = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (he != hipSuccess) return hip_fail(he, "hipGraphInstantiate");
+    e->graphs.push_back({B, S, input, attention_mask, output, exec, 0});
+    hit = &e->graphs.back();
+  }
+  hit->last_use = ++e->use_clock;
+  RLX_HIP(hipGraphLaunch(hit->exec, s), "hipGraphLaunch");
+  return ok();
+}
+
+void rlx_encoder_destroy(rlx_encoder* e) {
+  if (!e) return;
+  (void)hipDeviceSynchronize();
+  destroy_graphs(e);
+  clear_profile(e);
+  if (e->cap_stream) (void)hipStreamDestroy(e->cap_stream);
+  if (e->ws) (void)hipFree(e->ws);
+  delete e;
+}
+
+rlx_status rlx_encoder_set_profiling(rlx_encoder* e, int enable) {
+  if (!e) return fail(RLX_ERR_INVALID_ARG, "encoder_set_profiling: null handle");
+  e->profiling = enable != 0;
+  if (!e->profiling) {
+    (void)hipDeviceSynchronize();
+    clear_profile(e);
+  }
+  return ok();
+}
+
+rlx_status rlx_encoder_profile_read(rlx_encoder* e, int max_entries, const char** names, int* launches,
+                                    double* total_ms, int* n_entries) {
+  if (!e || !n_entries) return fail(RLX_ERR_INVALID_ARG, "encoder_profile_read: null handle or n_entries");
+  if (max_entries < 0 || (max_entries > 0 && (!names || !launches || !total_ms)))
+    return fail(RLX_ERR_INVALID_ARG, "encoder_profile_read: output arrays required for max_entries > 0");
+  int cnt[K_NUM_CLASSES] = {0};
+  double ms[K_NUM_CLASSES] = {0};
+  for (auto& r : e->prof) {
+    RLX_HIP(hipEventSynchronize(r.b), "hipEventSynchronize");
+    float t = 0.0f;
+    RLX_HIP(hipEventElapsedTime(&t, r.a, r.b), "hipEventElapsedTime");
+    cnt[r.cls] += 1;
+    ms[r.cls] += t;
+  }
+  int n = 0;
+  for (int c = 0; c < K_NUM_CLASSES; ++c) {
+    if (!cnt[c]) continue;
+    if (n < max_entries) {
+      names[n] = kClassNames[c];
+      launches[n] = cnt[c];
+      total_ms[n] = ms[c];
+    }
+    ++n;
+  }
+  *n_entries = n;
+  clear_profile(e);
+  return ok();
+}
+
+}  // extern "C"

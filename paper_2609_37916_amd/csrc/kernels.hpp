@@ -1,0 +1,75 @@
+// Internal launch interface between the C ABI (capi.hip) and the kernels.
+// Launchers assume their arguments were validated by the caller; they only
+// enqueue work and return the launch status.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rlx {
+
+enum class DType : int { F32 = 0, BF16 = 1 };
+enum class Quant : int { None = 0, Int8 = 1, Int4 = 2 };
+enum class Epi : int { None = 0, Bias = 1, BiasGelu = 2, BiasResidual = 3 };
+
+struct GemmParams {
+  const void* x;         // [M,K] activations (dtype)
+  const void* w;         // weights in the layout of `quant`
+  const void* scales;    // f16 (int8: [N]; int4: [N,K/32])
+  const void* zeros;     // f16 [N,K/32] (int4)
+  const float* bias;     // f32 [N]
+  const void* residual;  // [M,N] (dtype)
+  void* y;               // [M,N] (dtype)
+  int M, N, K;           // M is an upper bound when m_dev is set
+  const int* m_dev;      // optional device-side row count (rows >= *m_dev are skipped)
+  DType dtype;
+  Quant quant;
+  Epi epi;
+};
+hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
+
+hipError_t launch_dequant_unpack(const void* w, Quant q, const void* scales, const void* zeros, int N, int K,
+                                 float* out, hipStream_t s);
+
+struct AttnParams {
+  const void* q; const void* k; const void* v; int64_t ld_qkv;
+  void* out; int64_t ld_out;
+  int B, S, heads;            // S: padded length (max rows per sequence)
+  int kind;                   // 0 none, 1 causal, 2 sliding window, 3 custom
+  const uint8_t* key_mask;    // [B,S] or null (padded layout only)
+  int window;
+  float scale;
+  const int* cu_seqlens;      // varlen layout: rows of sequence b are [cu[b], cu[b+1]); null = padded layout
+  DType dtype;
+};
+hipError_t launch_attention(const AttnParams& p, hipStream_t s);
+
+// Raises per-kernel dynamic-LDS limits once per process (idempotent).
+hipError_t init_kernel_attributes();
+
+// Mask scan: per-sequence valid counts, offsets and the token compaction maps.
+//   cu[0..B]    exclusive prefix of valid counts (cu[B] = valid tokens)
+//   tok_src[t]  = b*S + s of compact token t            (t < cu[B])
+//   tok_dst[i]  = compact index of padded token i, or -1 (i < B*S)
+hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, hipStream_t s);
+
+// x[t] = LN(word[id] + pos[s] + type[0]) for compact tokens t < cu[B].
+hipError_t launch_embed_ln(const int* ids, const void* word, const void* pos, const void* type, const float* gamma,
+                           const float* beta, float eps, int vocab, int S, int H, const int* tok_src,
+                           const int* n_dev, int n_max, void* x, DType dt, hipStream_t s);
+
+// x[t] = hidden[tok_src[t]] (row copy) for t < *n_dev.
+hipError_t launch_gather_rows(const void* hidden, int H, const int* tok_src, const int* n_dev, int n_max, void* x,
+                              DType dt, hipStream_t s);
+
+// y[t] = LN(a[t]) * gamma + beta for t < *n_dev; optional f32 copy of the result.
+hipError_t launch_layer_norm(const void* a, const float* gamma, const float* beta, float eps, int H,
+                             const int* n_dev, int n_max, void* y, DType dt, hipStream_t s);
+
+// out[b] = normalize(mean over the sequence's compact rows) (f32 [B,H]).
+hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s);
+
+// out[b,s,:] = x[tok_dst[b*S+s]] or 0 (f32 [B,S,H]).
+hipError_t launch_scatter_hidden(const void* x, int H, const int* tok_dst, int n_tok, float* out, DType dt,
+                                 hipStream_t s);
+
+}  // namespace rlx

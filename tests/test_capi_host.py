@@ -1,0 +1,146 @@
+"""Host-only checks of the C ABI: the library loads, exports every function
+that include/rlx.h declares, and rejects bad arguments before touching the
+GPU (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_37916_amd as rlx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(rlx.LIB_PATH):
+        from paper_2609_37916_amd import _build
+        _build.build_library()
+    return rlx.lib()
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "rlx.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rlx_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported(L):
+    declared = header_functions()
+    assert set(declared) == set(rlx.EXPORTS), declared
+    for name in declared:
+        assert getattr(L, name) is not None
+
+
+def test_version_string(L):
+    assert "gfx950" in rlx.version()
+
+
+def test_attention_argument_errors(L):
+    f = L.rlx_masked_attention
+    P = 4096  # an aligned stand-in address: validation rejects before any use
+    assert f(None, P, P, 96, P, 32, 1, 8, 1, 32, rlx.BF16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.ERR_INVALID_ARG
+    assert b"non-null" in L.rlx_last_error()
+    assert f(P, P, P, 96, P, 32, 1, 8, 1, 32, rlx.BF16, rlx.MASK_CUSTOM, None, 0, 1.0, None) == rlx.ERR_INVALID_ARG
+    assert b"key mask" in L.rlx_last_error()
+    assert f(P, P, P, 96, P, 32, 1, 8, 1, 32, rlx.BF16, rlx.MASK_SLIDING_WINDOW, None, 0, 1.0, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, P, P, 192, P, 64, 1, 8, 1, 64, rlx.BF16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.ERR_UNSUPPORTED
+    assert b"head_dim" in L.rlx_last_error()
+    assert f(P, P, P, 96, P, 32, 1, 513, 1, 32, rlx.BF16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, P, P, 96, P, 32, 1, 8, 1, 32, rlx.F16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, P, P, 20, P, 32, 1, 8, 1, 32, rlx.BF16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.ERR_INVALID_ARG
+    assert f(P + 2, P, P, 96, P, 32, 1, 8, 1, 32, rlx.BF16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, P, P, 96, P, 32, -1, 8, 1, 32, rlx.BF16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.ERR_INVALID_ARG
+    assert f(P, P, P, 96, P, 32, 1, 8, 1, 32, rlx.BF16, rlx.MASK_NONE, None, 0, float("nan"), None) == \
+        rlx.ERR_INVALID_ARG
+    # empty batch / sequence: a no-op that succeeds without touching the device
+    assert f(P, P, P, 96, P, 32, 0, 8, 1, 32, rlx.BF16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.OK
+    assert f(P, P, P, 96, P, 32, 3, 0, 1, 32, rlx.BF16, rlx.MASK_NONE, None, 0, 1.0, None) == rlx.OK
+    assert L.rlx_last_error() == b""
+
+
+def test_dequant_matmul_argument_errors(L):
+    f = L.rlx_dequant_matmul
+    P = 4096
+    # (x, x_dt, M, K, w, scheme, scales, zeros, group, N, bias, residual, epi, y, stream)
+    assert f(P, rlx.BF16, 8, 96, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, rlx.EPI_BIAS, P, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, P, None, rlx.EPI_BIAS_RESIDUAL, P, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, rlx.F32, 8, 64, P, rlx.Q_INT8_PER_CHANNEL, P, None, 32, 64, None, None, 0, P, None) == \
+        rlx.ERR_UNSUPPORTED
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT8_PER_CHANNEL, None, None, 32, 64, None, None, 0, P, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT4_GROUP_ZP, P, P, 64, 64, None, None, 0, P, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT4_GROUP_ZP, P, None, 32, 64, None, None, 0, P, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, rlx.F16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.ERR_UNSUPPORTED
+    assert f(None, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.ERR_INVALID_ARG
+    assert f(P, rlx.BF16, -1, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.ERR_INVALID_ARG
+    assert f(P, rlx.BF16, 0, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.OK
+    assert L.rlx_dequant_unpack(P, rlx.Q_NONE, P, None, 32, 64, 64, P, None) == rlx.ERR_INVALID_ARG
+
+
+def _cfg(**kw):
+    base = dict(hidden=384, heads=12, head_dim=32, ffn=1536, layers=6, vocab=30522, max_pos=512, type_vocab=2,
+                ln_eps=1e-12, dtype=rlx.BF16, quant=rlx.Q_NONE, group_size=32, input_kind=rlx.INPUT_IDS,
+                output_kind=rlx.OUTPUT_POOLED, max_batch=32, max_seq=128, use_graph=1)
+    base.update(kw)
+    return rlx.EncoderConfig(**base)
+
+
+def _weights(layers=6, **null):
+    P = 4096
+    arr = (rlx.LayerWeights * layers)()
+    for L_ in arr:
+        for f, _ in rlx.LayerWeights._fields_:
+            if not f.endswith("_scales") and not f.endswith("_zeros"):
+                setattr(L_, f, P)
+    w = rlx.EncoderWeights(P, P, P, P, P, ctypes.cast(arr, ctypes.POINTER(rlx.LayerWeights)))
+    for k, v in null.items():
+        setattr(w, k, v)
+    return w, arr
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(head_dim=64, heads=6), rlx.ERR_UNSUPPORTED, b"head_dim"),
+    (dict(hidden=380), rlx.ERR_INVALID_ARG, b"hidden"),
+    (dict(max_seq=1024), rlx.ERR_UNSUPPORTED, b"max_seq"),
+    (dict(max_pos=64), rlx.ERR_UNSUPPORTED, b"max_pos"),
+    (dict(dtype=rlx.F32, quant=rlx.Q_INT8_PER_CHANNEL), rlx.ERR_UNSUPPORTED, b"bf16"),
+    (dict(quant=rlx.Q_INT4_GROUP_ZP, group_size=128), rlx.ERR_UNSUPPORTED, b"group"),
+    (dict(dtype=rlx.F16), rlx.ERR_UNSUPPORTED, b"dtype"),
+    (dict(layers=0), rlx.ERR_INVALID_ARG, b"positive"),
+    (dict(max_batch=0), rlx.ERR_INVALID_ARG, b"max_batch"),
+    (dict(ffn=1500), rlx.ERR_UNSUPPORTED, b"multiples of 64"),
+])
+def test_encoder_create_config_errors(L, kw, status, needle):
+    w, _arr = _weights()
+    h = ctypes.c_void_p()
+    st = L.rlx_encoder_create(ctypes.byref(_cfg(**kw)), ctypes.byref(w), ctypes.byref(h))
+    assert st == status
+    assert needle in L.rlx_last_error()
+    assert not h.value
+
+
+def test_encoder_create_weight_errors(L):
+    h = ctypes.c_void_p()
+    w, _arr = _weights(word_emb=None)
+    assert L.rlx_encoder_create(ctypes.byref(_cfg()), ctypes.byref(w), ctypes.byref(h)) == rlx.ERR_INVALID_ARG
+    w, arr = _weights()
+    arr[3].b1 = None
+    assert L.rlx_encoder_create(ctypes.byref(_cfg()), ctypes.byref(w), ctypes.byref(h)) == rlx.ERR_INVALID_ARG
+    assert b"layer 3" in L.rlx_last_error()
+    w, arr = _weights()
+    assert L.rlx_encoder_create(ctypes.byref(_cfg(quant=rlx.Q_INT8_PER_CHANNEL)), ctypes.byref(w),
+                                ctypes.byref(h)) == rlx.ERR_INVALID_ARG
+    assert b"scales" in L.rlx_last_error()
+    assert L.rlx_encoder_create(None, ctypes.byref(w), ctypes.byref(h)) == rlx.ERR_INVALID_ARG
+
+
+def test_encoder_forward_null_handle(L):
+    assert L.rlx_encoder_forward(None, 4096, 4096, 1, 1, 4096, None) == rlx.ERR_INVALID_ARG
+    L.rlx_encoder_destroy(None)

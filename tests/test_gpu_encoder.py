@@ -1,0 +1,180 @@
+"""GPU parity of rlx_encoder_forward against the CPU oracle on every workload
+family (one fp32 layer; the batch-32 x 128 bf16 forward; the batch sweep in
+fp32 and bf16; batch 8 x 512; int8 and int4 weights), plus invariants of the
+compiled forward (padding extension, graph replay, repeat stability, errors).
+
+Tolerances (max-abs on the final output): fp32 1e-4, bf16 2e-2, int8/int4
+5e-2 against the oracle run on the same dequantised weights.  For the two
+largest sweep batches the oracle is run on a sample of sequences (they are
+independent), at the full launch configuration on the GPU.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from workloads.device import encoder_kwargs, to_device
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+TOL = {"f32": 1e-4, "bf16": 2e-2, "int8": 5e-2, "int4": 5e-2}
+
+
+@pytest.fixture(scope="module")
+def rlx():
+    import paper_2609_37916_amd as m
+    m.lib()
+    return m
+
+
+def _tol(sp):
+    return TOL[sp.quant] if sp.quant != "none" else TOL[sp.dtype]
+
+
+def _run(rlx, wl, use_graph=True, max_batch=None, max_seq=None):
+    weights, inputs = to_device(wl)
+    enc = rlx.Encoder(**encoder_kwargs(wl.spec, max_batch, max_seq, use_graph), weights=weights)
+    out = enc.forward(inputs["input"], inputs["mask"])
+    torch.cuda.synchronize()
+    res = out.cpu().numpy()
+    enc.close()
+    return res
+
+
+def _compare(got, ref, wl, tol, what):
+    sp = wl.spec
+    assert np.all(np.isfinite(got)), what
+    if sp.output_kind == "hidden":
+        err = max(np.abs(got[b, :L] - ref[b, :L]).max() for b, L in enumerate(wl.lengths) if L > 0)
+        for b, L in enumerate(wl.lengths):
+            assert np.all(got[b, L:] == 0), f"{what}: padded rows must be zero"
+    else:
+        err = np.abs(got - ref).max()
+    print(f"{what}: max-abs error {err:.3g} (tolerance {tol})", flush=True)
+    assert err <= tol, f"{what}: max-abs error {err} > {tol}"
+
+
+SAMPLED = {"minilm_b64_s128_f32": 24, "minilm_b64_s128_bf16": 24, "minilm_b256_s128_f32": 16,
+           "minilm_b256_s128_bf16": 16}
+
+
+@pytest.mark.parametrize("name", workloads.PARITY_CONFIGS)
+def test_encoder_parity(rlx, name):
+    wl = workloads.make(name)
+    got = _run(rlx, wl)
+    if name in SAMPLED:
+        rows = np.random.default_rng(7).choice(wl.spec.batch, SAMPLED[name], replace=False)
+        rows.sort()
+        sub = workloads.select_rows(wl, rows)
+        ref = oracle.encoder_forward(sub)
+        _compare(got[rows], ref, sub, _tol(wl.spec), name + " (sampled rows)")
+        # every row, sampled or not, is a unit vector
+        assert np.max(np.abs(np.linalg.norm(got, axis=1) - 1)) < 1e-3
+    else:
+        ref = oracle.encoder_forward(wl)
+        _compare(got, ref, wl, _tol(wl.spec), name)
+
+
+@pytest.mark.parametrize("name", ["layer_f32_b2_s16", "minilm_b4_s128_bf16", "minilm_b4_s128_f32"])
+def test_encoder_parity_affine(rlx, name):
+    """Non-zero biases and LayerNorm affine parameters exercise every epilogue."""
+    wl = workloads.make(name, affine=True)
+    _compare(_run(rlx, wl), oracle.encoder_forward(wl), wl, _tol(wl.spec), name + " affine")
+
+
+@pytest.mark.parametrize("quant", ["int8", "int4"])
+def test_encoder_parity_quant_affine(rlx, quant):
+    sp = workloads.spec(f"minilm_b32_s128_{quant}", batch=6)
+    wl = workloads.make(sp, affine=True)
+    _compare(_run(rlx, wl), oracle.encoder_forward(wl), wl, _tol(sp), sp.name + " affine")
+
+
+def test_encoder_mask_with_holes_and_empty_row(rlx):
+    """A custom key mask that is not right-padded, and a sequence with no token."""
+    sp = workloads.spec("minilm_b4_s128_bf16", batch=5, seq=64, len_lo=30, len_hi=64)
+    wl = workloads.make(sp, affine=True)
+    rng = np.random.default_rng(8)
+    wl.mask = (wl.mask & (rng.random(wl.mask.shape) < 0.6)).astype(np.uint8)
+    wl.mask[3] = 0
+    wl.lengths = wl.mask.sum(axis=1)
+    got = _run(rlx, wl)
+    ref = oracle.encoder_forward(wl)
+    assert np.all(got[3] == 0)
+    _compare(got, ref, wl, TOL["bf16"], "mask with holes")
+
+
+def test_encoder_hidden_output_f32(rlx):
+    sp = workloads.spec("minilm_b4_s128_f32", batch=3, seq=40, layers=2, output_kind="hidden", len_lo=1, len_hi=40)
+    wl = workloads.make(sp, affine=True)
+    _compare(_run(rlx, wl), oracle.encoder_forward(wl), wl, TOL["f32"], "hidden output f32")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_encoder_padding_extension_bit_identical(rlx, dtype):
+    sp = workloads.spec(f"minilm_b16_s128_{dtype}", batch=6)
+    wl = workloads.make(sp)
+    a = _run(rlx, wl)
+    b = _run(rlx, workloads.with_padding_extended(wl, 77), max_seq=205)
+    assert np.array_equal(a, b)
+
+
+def test_encoder_graph_replay_eager_and_repeat_are_bit_identical(rlx):
+    wl = workloads.make("minilm_b32_s128_bf16")
+    weights, inputs = to_device(wl)
+    enc_g = rlx.Encoder(**encoder_kwargs(wl.spec, use_graph=True), weights=weights)
+    enc_e = rlx.Encoder(**encoder_kwargs(wl.spec, use_graph=False), weights=weights)
+    ref = enc_e.forward(inputs["input"], inputs["mask"]).cpu().numpy()
+    out = torch.empty((32, 384), dtype=torch.float32, device="cuda")
+    for i in range(5):
+        out.zero_()
+        enc_g.forward(inputs["input"], inputs["mask"], out=out)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), ref), f"replay {i}"
+        enc_e.forward(inputs["input"], inputs["mask"], out=out)  # eager work between replays
+    enc_g.close()
+    enc_e.close()
+
+
+def test_encoder_smaller_call_after_larger(rlx):
+    """One handle serves a smaller (B, S) after a larger one."""
+    wl = workloads.make("minilm_b16_s128_bf16")
+    weights, inputs = to_device(wl)
+    enc = rlx.Encoder(**encoder_kwargs(wl.spec), weights=weights)
+    full = enc.forward(inputs["input"], inputs["mask"]).cpu().numpy()
+    sub = enc.forward(inputs["input"][:5, :100].contiguous(), inputs["mask"][:5, :100].contiguous()).cpu().numpy()
+    keep = [b for b in range(5) if wl.lengths[b] <= 100]
+    assert np.array_equal(full[keep], sub[keep])
+    enc.close()
+
+
+def test_encoder_profile_mode(rlx):
+    wl = workloads.make("minilm_b4_s128_bf16")
+    weights, inputs = to_device(wl)
+    enc = rlx.Encoder(**encoder_kwargs(wl.spec), weights=weights)
+    enc.set_profiling(True)
+    enc.forward(inputs["input"], inputs["mask"])
+    enc.forward(inputs["input"], inputs["mask"])
+    prof = enc.profile_read()
+    assert prof["gemm_ffn_up"][0] == 12 and prof["attention"][0] == 12 and prof["mask_scan"][0] == 2
+    assert all(ms >= 0 for _, ms in prof.values())
+    enc.set_profiling(False)
+    enc.close()
+
+
+def test_encoder_forward_errors(rlx):
+    wl = workloads.make("minilm_b4_s128_bf16")
+    weights, inputs = to_device(wl)
+    enc = rlx.Encoder(**encoder_kwargs(wl.spec), weights=weights)
+    big = torch.zeros((5, 128), dtype=torch.int32, device="cuda")
+    with pytest.raises(rlx.RlxError) as e:
+        enc.forward(big, torch.ones((5, 128), dtype=torch.uint8, device="cuda"))
+    assert e.value.status == rlx.ERR_UNSUPPORTED
+    with pytest.raises(rlx.RlxError) as e:
+        enc.forward(torch.zeros((4, 129), dtype=torch.int32, device="cuda"),
+                    torch.ones((4, 129), dtype=torch.uint8, device="cuda"))
+    assert e.value.status == rlx.ERR_UNSUPPORTED
+    with pytest.raises(ValueError):
+        enc.forward(inputs["input"].cpu(), inputs["mask"])
+    enc.close()

@@ -294,3 +294,14 @@ def with_padding_extended(wl: Workload, extra: int) -> Workload:
         hidden_in = np.zeros((B, S + extra, wl.hidden_in.shape[2]), np.float32)
         hidden_in[:, :S] = wl.hidden_in
     return Workload(sp, wl.lengths.copy(), mask, ids, hidden_in, wl.emb, wl.layers, wl.quant)
+
+
+def select_rows(wl: Workload, rows) -> Workload:
+    """The sub-workload of the given sequences (same weights).  Sequences are
+    independent in the encoder, so this is how a large batch is checked on a
+    sample of its rows."""
+    rows = np.asarray(rows)
+    sp = Spec(**{**wl.spec.__dict__, "batch": len(rows), "full_rows": 0, "name": wl.spec.name + f"[{len(rows)} rows]"})
+    return Workload(sp, wl.lengths[rows].copy(), wl.mask[rows].copy(),
+                    None if wl.ids is None else wl.ids[rows].copy(),
+                    None if wl.hidden_in is None else wl.hidden_in[rows].copy(), wl.emb, wl.layers, wl.quant)
