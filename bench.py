@@ -1,0 +1,207 @@
+#!/usr/bin/env python3
+"""Encoder-forward benchmark on one MI355X.
+
+Workload: the MiniLM-L6-shaped encoder (hidden 384, 12 heads x 32, FFN 1536,
+6 post-LN layers), batch 32 x sequence 128, bf16 storage with fp32
+accumulation, seeded synthetic ids and N(0, 0.02) weights, valid lengths
+U[16, 128] -- the paper's inference measurement (p50 of the encoder forward
+at seq 128, batch up to 32) restated on this GPU.  One step is one whole
+forward (embedding, 6 layers, pooling) with the inputs resident in HBM,
+replayed from the encoder's recorded HIP graph.
+
+Prints one JSON line: sequences/s, p50 ms, the roofline of the dominant
+kernel (algorithmic flops per launch / its event-timed average duration) and
+the CPU oracle timed on this host as a reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def gemm_flops_per_token(sp):
+    H, F = sp.hidden, sp.ffn
+    return {"gemm_qkv": 2 * H * 3 * H, "gemm_attn_out": 2 * H * H, "gemm_ffn_up": 2 * H * F, "gemm_ffn_down": 2 * F * H}
+
+
+def attention_flops(sp, lengths):
+    # QK^T and PV over real queries x real keys, per layer: 2 * 2 * d * L^2 per head
+    return sum(4 * sp.head_dim * sp.heads * int(L) ** 2 for L in lengths)
+
+
+def kernel_source_digest():
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "common.hpp", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2609_37916_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(kernel_class, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when no summary exists or the GEMM sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel_class}_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_b = re.search(r"^hbm_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
+    m_h = re.search(r"^kernel_source_digest:\s*([0-9a-f]+)", text, re.M)
+    if not m_b or not m_h or m_h.group(1) != kernel_source_digest():
+        return None
+    return float(m_b.group(1))
+
+
+def cpu_baseline(workload_name, target_s):
+    """The float64 oracle on this host's cores, on a bounded sample of the workload."""
+    import numpy as np
+
+    import oracle
+    import workloads
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    wl = workloads.make(workload_name)
+    B = wl.spec.batch
+    probe = workloads.select_rows(wl, np.arange(min(2, B)))
+    t0 = time.perf_counter()
+    oracle.encoder_forward(probe)
+    per_seq = (time.perf_counter() - t0) / probe.spec.batch
+    n = int(max(1, min(B, round(target_s / max(per_seq, 1e-6)))))
+    sample = workloads.select_rows(wl, np.arange(n))
+    t0 = time.perf_counter()
+    oracle.encoder_forward(sample)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "sequences/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {n} of {B} sequences of {workload_name}, float64 NumPy oracle, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="minilm_b32_s128_bf16")
+    ap.add_argument("--profile-steps", type=int, default=20, help="forwards timed kernel by kernel")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: --gpus {args.gpus} (WORLD_SIZE {world}) is not supported; the encoder "
+              f"forward is data-parallel over sequences and this build runs on a single MI355X.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_37916_amd as rlx
+    import workloads
+    from workloads.device import encoder_kwargs, to_device
+
+    if not os.path.exists(rlx.LIB_PATH):
+        from paper_2609_37916_amd import _build
+        _build.build_library()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+
+    sp = workloads.spec(args.workload)
+    wl = workloads.make(sp)
+    weights, inputs = to_device(wl)
+    enc = rlx.Encoder(**encoder_kwargs(sp), weights=weights)
+    out = torch.empty((sp.batch, sp.hidden), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        enc.forward(inputs["input"], inputs["mask"], out=out)
+    torch.cuda.synchronize()
+
+    # timed region: K back-to-back forwards, an event before each and after the last
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    t_host = time.perf_counter()
+    evs[0].record(stream)
+    for i in range(args.steps):
+        enc.forward(inputs["input"], inputs["mask"], out=out)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    t_host = time.perf_counter() - t_host
+    total_ms = evs[0].elapsed_time(evs[-1])
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms_per_step = total_ms / args.steps
+    p50 = statistics.median(step_ms)
+    p10, p90 = np.percentile(step_ms, [10, 90]).tolist()
+    seq_per_s = sp.batch * args.steps / (total_ms / 1e3)
+
+    # per-kernel times: the same forward launched kernel by kernel, an event pair around every launch
+    enc.set_profiling(True)
+    for _ in range(args.profile_steps):
+        enc.forward(inputs["input"], inputs["mask"], out=out)
+    prof = enc.profile_read()
+    enc.set_profiling(False)
+    per_launch_us = {k: 1e3 * ms / n for k, (n, ms) in prof.items()}
+    per_fwd_us = {k: 1e3 * ms / args.profile_steps for k, (n, ms) in prof.items()}
+
+    tokens = int(wl.mask.sum())  # real tokens: every row-local step runs on these after compaction
+    fpt = gemm_flops_per_token(sp)
+    flops_launch = {k: v * tokens for k, v in fpt.items()}
+    flops_launch["attention"] = attention_flops(sp, wl.mask.sum(axis=1))
+    matrix_classes = list(flops_launch)
+    dominant = max(matrix_classes, key=lambda k: per_fwd_us.get(k, 0.0))
+    achieved = flops_launch[dominant] / (per_launch_us[dominant] * 1e-6) / 1e12
+    traffic = committed_traffic(dominant, args.workload)
+    mm_flops = sum(flops_launch[k] * sp.layers for k in matrix_classes)
+    mm_us = sum(per_fwd_us.get(k, 0.0) for k in matrix_classes)
+    mfma_util = mm_flops / (mm_us * 1e-6) / (PEAK_BF16_TFLOPS * 1e12)
+
+    rec = {
+        "metric": "encoder fwd sequences/sec (b32, s128, bf16, 1 MI355X)",
+        "value": round(seq_per_s, 1),
+        "unit": "sequences/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "p50_ms": round(p50, 5),
+        "p10_ms": round(p10, 5),
+        "p90_ms": round(p90, 5),
+        "host_wall_ms_per_step": round(1e3 * t_host / args.steps, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if sp.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded ids, N(0,0.02) weights, lengths U[%d,%d])" % (sp.len_lo, sp.len_hi),
+        "config": {"workload": sp.name, "batch": sp.batch, "seq_len": sp.seq, "layers": sp.layers,
+                   "hidden": sp.hidden, "heads": sp.heads, "ffn": sp.ffn, "real_tokens": tokens,
+                   "quant": sp.quant, "parallelism": "single GPU", "graph_replay": True},
+        "mfma_util_pct": round(100 * mfma_util, 2),
+        "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic, "flops_per_launch": flops_launch[dominant],
+                     "avg_launch_us": round(per_launch_us[dominant], 3)},
+        "kernel_us_per_forward": {k: round(v, 2) for k, v in sorted(per_fwd_us.items(), key=lambda kv: -kv[1])},
+    }
+    enc.close()
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

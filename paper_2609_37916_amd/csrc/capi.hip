@@ -127,11 +127,12 @@ namespace {
 
 enum KernelClass {
   K_MASK_SCAN = 0, K_EMBED_LN, K_GATHER_ROWS, K_GEMM_QKV, K_ATTENTION, K_GEMM_ATTN_OUT, K_LN1, K_GEMM_FFN_UP,
-  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_NUM_CLASSES
+  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_NUM_CLASSES
 };
 const char* kClassNames[K_NUM_CLASSES] = {"mask_scan",     "embed_ln",    "gather_rows", "gemm_qkv",
                                           "attention",     "gemm_attn_out", "layer_norm_1", "gemm_ffn_up",
-                                          "gemm_ffn_down", "layer_norm_2", "pool_l2",     "scatter_hidden"};
+                                          "gemm_ffn_down", "layer_norm_2", "pool_l2",     "scatter_hidden",
+                                          "qkv_attention"};
 
 struct GraphEntry {
   int B, S;
@@ -281,26 +282,36 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
     g.dtype = e->dt;
     g.quant = q;
 
-    g.x = e->X; g.w = L.wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = L.bqkv;
-    g.residual = nullptr; g.y = e->QKV; g.N = 3 * H; g.K = H; g.epi = Epi::Bias;
-    STEP(K_GEMM_QKV, launch_gemm(g, s));
+    const bool fused_attn = e->dt == DType::BF16 && q == Quant::None && S <= 128;
+    if (fused_attn) {
+      FusedAttnParams fa{};
+      fa.x = e->X; fa.wqkv = L.wqkv; fa.bqkv = L.bqkv; fa.cu_seqlens = e->cu; fa.out = e->CTX; fa.out_rows = T;
+      fa.B = B; fa.H = H; fa.heads = c.heads; fa.scale = 1.0f / std::sqrt((float)c.head_dim);
+      STEP(K_QKV_ATTENTION, launch_qkv_attention(fa, s));
+    } else {
+      g.x = e->X; g.w = L.wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = L.bqkv;
+      g.residual = nullptr; g.y = e->QKV; g.N = 3 * H; g.K = H; g.epi = Epi::Bias;
+      STEP(K_GEMM_QKV, launch_gemm(g, s));
 
-    AttnParams a{};
-    const size_t es = e->dt == DType::BF16 ? 2 : 4;
-    a.q = e->QKV;
-    a.k = static_cast<const uint8_t*>(e->QKV) + (size_t)H * es;
-    a.v = static_cast<const uint8_t*>(e->QKV) + (size_t)2 * H * es;
-    a.ld_qkv = 3 * H;
-    a.out = e->CTX; a.ld_out = H;
-    a.B = B; a.S = S; a.heads = c.heads; a.kind = 0; a.key_mask = nullptr; a.window = 0;
-    a.scale = 1.0f / std::sqrt((float)c.head_dim);
-    a.cu_seqlens = e->cu;
-    a.dtype = e->dt;
-    STEP(K_ATTENTION, launch_attention(a, s));
+      AttnParams a{};
+      const size_t es = e->dt == DType::BF16 ? 2 : 4;
+      a.q = e->QKV;
+      a.k = static_cast<const uint8_t*>(e->QKV) + (size_t)H * es;
+      a.v = static_cast<const uint8_t*>(e->QKV) + (size_t)2 * H * es;
+      a.ld_qkv = 3 * H;
+      a.out = e->CTX; a.ld_out = H;
+      a.B = B; a.S = S; a.heads = c.heads; a.kind = 0; a.key_mask = nullptr; a.window = 0;
+      a.scale = 1.0f / std::sqrt((float)c.head_dim);
+      a.cu_seqlens = e->cu;
+      a.dtype = e->dt;
+      STEP(K_ATTENTION, launch_attention(a, s));
+    }
 
     g.x = e->CTX; g.w = L.wo; g.scales = L.wo_scales; g.zeros = L.wo_zeros; g.bias = L.bo;
     g.residual = e->X; g.y = e->A; g.N = H; g.K = H; g.epi = Epi::BiasResidual;
+    g.x_head_rows = fused_attn ? T : 0;  // the fused attention writes the context head-major
     STEP(K_GEMM_ATTN_OUT, launch_gemm(g, s));
+    g.x_head_rows = 0;
     STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, s));
 
     g.x = e->X1; g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;

@@ -10,8 +10,20 @@
 // Design (256 threads = 4 waves in a 2x2 grid, block tile BM x BN):
 //  * Both operands are K-contiguous, so every global load is a 16-byte vector
 //    of one row and every stage row is 128 bytes (64 bf16 or 32 f32 of K).
-//    Stages are double-buffered in LDS with 16 bytes of padding per row so
-//    that the 16-byte fragment reads of 16 consecutive rows hit distinct banks.
+//  * Dense weights (bf16 / f32): operands go global -> LDS directly
+//    (global_load_lds_dwordx4, no register staging) into a ring of STAGES
+//    buffers, so several K-steps are in flight at once.  At the encoder's
+//    sizes a K-step holds ~0.1-0.2 us of matrix work while a memory round
+//    trip costs ~0.5 us; with a single buffer in flight the kernel is
+//    latency-bound.  Rows are stored unpadded with the 16-byte chunk index
+//    XOR-swizzled by (row / 2) mod 8, which keeps both the DMA writes (1 KB
+//    contiguous per wave) and the 16-row fragment reads conflict-free.
+//  * Tiles are ordered XCD-aware: the device-side row count gives the live
+//    tile count, the live tiles are spread over all 8 XCDs (workgroups are
+//    dispatched round-robin over XCDs) and each XCD gets a contiguous run of
+//    row tiles, so an XCD's L2 holds its own activation rows plus the weights.
+//  * Quantised weights keep a register-staged double buffer (the codes are
+//    converted to bf16 on their way into LDS), with 16 bytes of row padding.
 //  * The MFMA computes the transposed tile: the weight rows are the A operand
 //    and the activation rows the B operand, so each lane ends up owning one
 //    output row m and four consecutive output columns n per register quad --
@@ -26,6 +38,8 @@
 //    (q - z) * s is formed in fp32 and rounded to bf16 on its way into LDS.
 //  * Rows at or beyond M (or the device-side row count) are clamped on load
 //    and skipped on store; whole blocks past the row count exit at once.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -73,6 +87,35 @@ __device__ __forceinline__ void int4x32_to_bf16(uint4 src, float s, float z, uin
   }
 }
 
+// 16 bytes of output: 8 bf16 or 4 f32, converted to / from fp32.
+template <typename T> struct Vec16;
+template <> struct Vec16<bf16_t> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void load(const bf16_t* p, float v[8]) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+  static __device__ __forceinline__ void store(bf16_t* p, const float v[8]) {
+    *reinterpret_cast<uint4*>(p) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                              pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+  }
+};
+template <> struct Vec16<float> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void load(const float* p, float v[4]) {
+    const float4 u = *reinterpret_cast<const float4*>(p);
+    v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float v[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+};
+
 template <typename T> struct OutVec;
 template <> struct OutVec<bf16_t> {
   static __device__ __forceinline__ void load4(const bf16_t* p, float v[4]) {
@@ -94,6 +137,80 @@ template <> struct OutVec<float> {
   }
 };
 
+
+// Epilogue through LDS: the fp32 accumulators are written to LDS in their MFMA
+// layout, then every thread takes whole 16-byte output chunks of a row, so bias,
+// residual and output all move as coalesced 16-byte vectors.  (Storing straight
+// from the MFMA layout spreads each wave's store over 32 rows, 16 bytes per
+// row, and runs several times slower.)
+template <int BM, int BN, typename T, Quant Q, Epi E, int TM, int TN, int NRB>
+__device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_t* lds, const GemmParams& p, int m0,
+                                           int n0, int M) {
+  static_assert(NRB == 1 || NRB == 2, "row blocks follow the 2 wave rows");
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int PITCH = BN * 4 + 16;  // bytes; 16 rows of a column land on distinct banks
+  constexpr int EPC = 16 / (int)sizeof(T);
+  constexpr int CPR = BN / EPC;
+  constexpr int RB = BM / NRB;        // rows staged at a time
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, half = lane >> 5;
+  const int N = p.N;
+  T* y = reinterpret_cast<T*>(p.y);
+  const T* res = reinterpret_cast<const T*>(p.residual);
+  const uint16_t* qs = reinterpret_cast<const uint16_t*>(p.scales);
+#pragma unroll
+  for (int rb = 0; rb < NRB; ++rb) {
+    __syncthreads();  // the operand stages (or the previous row block) are no longer read
+    if (NRB == 1 || wm == rb) {
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int r = wm * WM + tm * 32 + l32 - rb * RB;
+            const int c = wn * WN + tn * 32 + 8 * i + 4 * half;
+            *reinterpret_cast<float4*>(lds + r * PITCH + c * 4) = make_float4(
+                acc[tm][tn][4 * i], acc[tm][tn][4 * i + 1], acc[tm][tn][4 * i + 2], acc[tm][tn][4 * i + 3]);
+          }
+    }
+    __syncthreads();
+    for (int idx = tid; idx < RB * CPR; idx += kThreads) {
+      const int r = idx / CPR, cc = idx % CPR;
+      const int m = m0 + rb * RB + r;
+      if (m >= M) continue;
+      const int n = n0 + cc * EPC;
+      float v[EPC];
+#pragma unroll
+      for (int e = 0; e < EPC; e += 4) {
+        const float4 a = *reinterpret_cast<const float4*>(lds + r * PITCH + (cc * EPC + e) * 4);
+        v[e] = a.x; v[e + 1] = a.y; v[e + 2] = a.z; v[e + 3] = a.w;
+      }
+      if constexpr (Q == Quant::Int8) {
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) v[e] *= f16_bits_to_f32(qs[n + e]);
+      }
+      if constexpr (E != Epi::None) {
+#pragma unroll
+        for (int e = 0; e < EPC; e += 4) {
+          const float4 bb = *reinterpret_cast<const float4*>(p.bias + n + e);
+          v[e] += bb.x; v[e + 1] += bb.y; v[e + 2] += bb.z; v[e + 3] += bb.w;
+        }
+      }
+      if constexpr (E == Epi::BiasGelu) {
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) v[e] = gelu_erf(v[e]);
+      }
+      if constexpr (E == Epi::BiasResidual) {
+        float rr[EPC];
+        Vec16<T>::load(res + (size_t)m * N + n, rr);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) v[e] += rr[e];
+      }
+      Vec16<T>::store(y + (size_t)m * N + n, v);
+    }
+  }
+}
 template <int BM, int BN, typename T, Quant Q, Epi E>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
@@ -256,45 +373,240 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
     __syncthreads();
   }
 
-  // Epilogue: lane owns row m = l32 of each m-tile and columns
-  // n = 8*i + 4*half + j (j = 0..3) of each n-tile, register 4*i + j.
-  const int N = p.N;
-  T* y = reinterpret_cast<T*>(p.y);
-  const T* res = reinterpret_cast<const T*>(p.residual);
-  const uint16_t* qs = reinterpret_cast<const uint16_t*>(p.scales);
+  static_assert(BM * (BN * 4 + 16) <= (int)sizeof(smem), "epilogue tile fits the stage memory");
+  store_tile<BM, BN, T, Q, E, TM, TN, 1>(acc, smem, p, m0, n0, M);
+}
+
+// ---------------------------------------------------------------------------
+// LDS-DMA kernel for dense weights
+// ---------------------------------------------------------------------------
+
+// 16 bytes per lane from global memory straight into LDS at m0 + lane * 16.
+// Inline assembly keeps the compiler from inserting a full vmcnt wait before
+// every later LDS read (it cannot tell which LDS bytes the DMA writes); the
+// kernel places its own waits.  M0 is used by nothing else in these kernels.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <int LPS, int MAXA>
+__device__ __forceinline__ void wait_stage(int ahead) {
+  // ahead stages (LPS loads each) may stay in flight
+  if constexpr (MAXA >= 4) { if (ahead >= 4) { wait_vmcnt<4 * LPS>(); return; } }
+  if constexpr (MAXA >= 3) { if (ahead == 3) { wait_vmcnt<3 * LPS>(); return; } }
+  if constexpr (MAXA >= 2) { if (ahead == 2) { wait_vmcnt<2 * LPS>(); return; } }
+  if constexpr (MAXA >= 1) { if (ahead == 1) { wait_vmcnt<LPS>(); return; } }
+  wait_vmcnt<0>();
+}
+
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+template <int BM, int BN, int STAGES, typename T, Epi E>
+__global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
+  static_assert(BM % 64 == 0 && BN % 64 == 0 && STAGES >= 2 && STAGES <= 6, "tile");
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int ES = sizeof(T);
+  constexpr int BK = kRowBytes / ES;
+  constexpr int CH = BK / 16;
+  constexpr int kStage = (BM + BN) * kRowBytes;
+  constexpr int LPS = (BM + BN) / 32;   // DMA instructions per thread per stage (8 rows each per wave)
+  static_assert((STAGES - 2) * LPS < 64, "vmcnt range");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * kStage];
+
+  int M = p.M;
+  if (p.m_dev) M = min(M, *p.m_dev);
+  const int n_tiles = p.N / BN;
+  const int live = n_tiles * ((M + BM - 1) / BM);
+  const int bid = blockIdx.x;
+  if (bid >= live) return;
+  // XCD-aware order: bid % 8 is the XCD; give XCD x a contiguous range of tiles.
+  const int q8 = live >> 3, r8 = live & 7, xcd = bid & 7;
+  const int tile = xcd * q8 + min(xcd, r8) + (bid >> 3);
+  const int m0 = (tile / n_tiles) * BM;
+  const int n0 = (tile % n_tiles) * BN;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int K = p.K;
+  const int KT = K / BK;
+  const size_t pitch = (size_t)K * ES;
+
+  // Per-lane source rows of the DMA: instruction i of this wave fills tile rows
+  // wave*8 + i*32 .. +7 (rows < BM are activations, the rest weights); lane
+  // lands at row (lane >> 3), physical chunk (lane & 7).
+  // Activations are row-major, or head-major ([K/32][x_head_rows][32], 64-byte
+  // rows per head) when they come from the fused attention; a 64-k stage then
+  // spans two heads, and logical chunk c sits in head c/4 at dims (c%4)*8.
+  const bool head_major = ES == 2 && p.x_head_rows > 0;
+  const size_t x_stage = head_major ? (size_t)2 * p.x_head_rows * 64 : kRowBytes;
+  const uint8_t* src[LPS];
+  bool is_x[LPS];
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm) {
-    const int m = m0 + wm * WM + tm * 32 + l32;
-    if (m >= M) continue;
+  for (int i = 0; i < LPS; ++i) {
+    const int row = wave * 8 + i * 32 + (lane >> 3);
+    const int c = swz(row, lane & 7);
+    is_x[i] = row < BM;
+    if (row < BM) {
+      const int m = min(m0 + row, M - 1);
+      src[i] = head_major ? reinterpret_cast<const uint8_t*>(p.x) + ((size_t)(c >> 2) * p.x_head_rows + m) * 64 + (c & 3) * 16
+                          : reinterpret_cast<const uint8_t*>(p.x) + (size_t)m * pitch + c * 16;
+    } else {
+      src[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row - BM) * pitch + c * 16;
+    }
+  }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)smem;
+
+  auto issue = [&](int kt, int buf) {
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
+    for (int i = 0; i < LPS; ++i) {
+      const uint32_t la = lds0 + buf * kStage + (wave * 8 + i * 32) * kRowBytes;
+      lds_dma16(src[i] + (size_t)kt * (is_x[i] ? x_stage : (size_t)kRowBytes), __builtin_amdgcn_readfirstlane(la));
+    }
+  };
+
+  f32x16_t acc[TM][TN];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int n = n0 + wn * WN + tn * 32 + i * 8 + half * 4;
-        float v[4];
+  for (int a = 0; a < TM; ++a)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = acc[tm][tn][4 * i + j];
-        if constexpr (Q == Quant::Int8) {
+    for (int b = 0; b < TN; ++b)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] *= f16_bits_to_f32(qs[n + j]);
+      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
+
+#pragma unroll
+  for (int st = 0; st < STAGES - 1; ++st)
+    if (st < KT) issue(st, st);
+
+  for (int kt0 = 0; kt0 < KT; kt0 += STAGES) {
+#pragma unroll
+    for (int u = 0; u < STAGES; ++u) {
+      const int kt = kt0 + u;
+      if (kt < KT) {
+        wait_stage<LPS, STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
+        __syncthreads();  // stage kt visible to all waves; buffer of stage kt-1 is free
+        if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, (u + STAGES - 1) % STAGES);
+        const uint8_t* xs = smem + u * kStage;
+        const uint8_t* ws = xs + BM * kRowBytes;
+        if constexpr (ES == 2) {
+          // fragments of chunk q+1 are read while chunk q is on the matrix cores
+          bf16x8_t af[2][TN], bfr[2][TM];
+          auto load_frags = [&](int q, int slot) {
+#pragma unroll
+            for (int tn = 0; tn < TN; ++tn) {
+              const int r = wn * WN + tn * 32 + l32;
+              af[slot][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
+            }
+#pragma unroll
+            for (int tm = 0; tm < TM; ++tm) {
+              const int r = wm * WM + tm * 32 + l32;
+              bfr[slot][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
+            }
+          };
+          load_frags(0, 0);
+#pragma unroll
+          for (int q = 0; q < CH; ++q) {
+            if (q + 1 < CH) load_frags(q + 1, (q + 1) & 1);
+#pragma unroll
+            for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+              for (int tn = 0; tn < TN; ++tn)
+                acc[tm][tn] =
+                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][tn], bfr[q & 1][tm], acc[tm][tn], 0, 0, 0);
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < CH; ++q) {
+            float af[TN][8], bfr[TM][8];
+#pragma unroll
+            for (int tn = 0; tn < TN; ++tn) {
+              const int r = wn * WN + tn * 32 + l32;
+              const uint4 u0 = ld16(ws + r * kRowBytes + swz(r, 4 * q + 2 * half) * 16);
+              const uint4 u1 = ld16(ws + r * kRowBytes + swz(r, 4 * q + 2 * half + 1) * 16);
+              af[tn][0] = __uint_as_float(u0.x); af[tn][1] = __uint_as_float(u0.y);
+              af[tn][2] = __uint_as_float(u0.z); af[tn][3] = __uint_as_float(u0.w);
+              af[tn][4] = __uint_as_float(u1.x); af[tn][5] = __uint_as_float(u1.y);
+              af[tn][6] = __uint_as_float(u1.z); af[tn][7] = __uint_as_float(u1.w);
+            }
+#pragma unroll
+            for (int tm = 0; tm < TM; ++tm) {
+              const int r = wm * WM + tm * 32 + l32;
+              const uint4 u0 = ld16(xs + r * kRowBytes + swz(r, 4 * q + 2 * half) * 16);
+              const uint4 u1 = ld16(xs + r * kRowBytes + swz(r, 4 * q + 2 * half + 1) * 16);
+              bfr[tm][0] = __uint_as_float(u0.x); bfr[tm][1] = __uint_as_float(u0.y);
+              bfr[tm][2] = __uint_as_float(u0.z); bfr[tm][3] = __uint_as_float(u0.w);
+              bfr[tm][4] = __uint_as_float(u1.x); bfr[tm][5] = __uint_as_float(u1.y);
+              bfr[tm][6] = __uint_as_float(u1.z); bfr[tm][7] = __uint_as_float(u1.w);
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+              for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+                for (int tn = 0; tn < TN; ++tn)
+                  acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tn][i], bfr[tm][i], acc[tm][tn], 0, 0, 0);
+          }
         }
-        if constexpr (E != Epi::None) {
-          float4 bb = *reinterpret_cast<const float4*>(p.bias + n);
-          v[0] += bb.x; v[1] += bb.y; v[2] += bb.z; v[3] += bb.w;
-        }
-        if constexpr (E == Epi::BiasGelu) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = gelu_erf(v[j]);
-        }
-        if constexpr (E == Epi::BiasResidual) {
-          float r[4];
-          OutVec<T>::load4(res + (size_t)m * N + n, r);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] += r[j];
-        }
-        OutVec<T>::store4(y + (size_t)m * N + n, v);
       }
     }
+  }
+
+  constexpr int NRB = BM * (BN * 4 + 16) <= (int)sizeof(smem) ? 1 : 2;
+  static_assert(BM / NRB * (BN * 4 + 16) <= (int)sizeof(smem), "epilogue row block fits the stage memory");
+  store_tile<BM, BN, T, Quant::None, E, TM, TN, NRB>(acc, smem, p, m0, n0, M);
+}
+
+template <int BM, int BN, int STAGES, typename T>
+hipError_t launch_dma_tile(const GemmParams& p, hipStream_t s) {
+  const dim3 grid((p.N / BN) * ((p.M + BM - 1) / BM));
+  switch (p.epi) {
+    case Epi::None:
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::None>), grid, dim3(kThreads), 0, s, p);
+      break;
+    case Epi::Bias:
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::Bias>), grid, dim3(kThreads), 0, s, p);
+      break;
+    case Epi::BiasGelu:
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::BiasGelu>), grid, dim3(kThreads), 0, s, p);
+      break;
+    case Epi::BiasResidual:
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::BiasResidual>), grid, dim3(kThreads), 0, s, p);
+      break;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_dense(const GemmParams& p, hipStream_t s) {
+  int tile = p.tile;
+  if (tile == kTileAuto) {
+    // measured at the encoder's shapes (2-4 k tokens): 64x64 for N = 384, 64x128
+    // for the wide projections; 128x128 only pays off from ~16 k rows up
+    if (p.N % 128 == 0 && p.M >= 16384) tile = kTile128x128;
+    else if (p.N % 128 == 0 && p.N >= 1024) tile = kTile64x128;
+    else tile = kTile64x64;
+  }
+  if (p.N % 128 != 0 && (tile == kTile128x128 || tile == kTile64x128)) tile = kTile64x64;
+  switch (tile) {
+    // stage counts keep every configuration within 80 KB of LDS: two blocks per CU
+    case kTile128x128: return launch_dma_tile<128, 128, 2, T>(p, s);
+    case kTile64x128: return launch_dma_tile<64, 128, 3, T>(p, s);
+    case kTile128x64: return launch_dma_tile<128, 64, 3, T>(p, s);
+    default: return launch_dma_tile<64, 64, 4, T>(p, s);
   }
 }
 
@@ -343,9 +655,9 @@ __global__ void dequant_unpack_kernel(const uint8_t* w, Quant q, const uint16_t*
 
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
-  if (p.dtype == DType::F32) return launch_typed<float, Quant::None>(p, s);
+  if (p.dtype == DType::F32) return launch_dense<float>(p, s);
   switch (p.quant) {
-    case Quant::None: return launch_typed<bf16_t, Quant::None>(p, s);
+    case Quant::None: return launch_dense<bf16_t>(p, s);
     case Quant::Int8: return launch_typed<bf16_t, Quant::Int8>(p, s);
     case Quant::Int4: return launch_typed<bf16_t, Quant::Int4>(p, s);
   }

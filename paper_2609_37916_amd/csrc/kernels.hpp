@@ -24,7 +24,11 @@ struct GemmParams {
   DType dtype;
   Quant quant;
   Epi epi;
+  int tile;              // 0: choose automatically; otherwise a GemmTile value (tuning)
+  int x_head_rows;       // 0: x is row-major [M,K]; > 0: x is head-major [K/32][x_head_rows][32]
+                         // (dense bf16 only), as written by the fused attention
 };
+enum GemmTile : int { kTileAuto = 0, kTile128x128 = 1, kTile64x128 = 2, kTile64x64 = 3, kTile128x64 = 4 };
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 
 hipError_t launch_dequant_unpack(const void* w, Quant q, const void* scales, const void* zeros, int N, int K,
@@ -42,6 +46,22 @@ struct AttnParams {
   DType dtype;
 };
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
+
+// QKV projection fused with attention, one block per (head, sequence), for the
+// variable-length layout with at most 128 tokens per sequence, bf16, dense
+// weights, head_dim 32:  out[t, h*32+d] = attention of head h over the
+// sequence's rows of x * Wqkv^T + bqkv.
+struct FusedAttnParams {
+  const void* x;        // [T, H] bf16 compact activations
+  const void* wqkv;     // [3H, H] bf16
+  const float* bqkv;    // [3H]
+  const int* cu_seqlens;
+  void* out;            // head-major [heads][out_rows][32] bf16
+  int out_rows;         // row pitch of one head block (>= real tokens)
+  int B, H, heads;
+  float scale;
+};
+hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s);
 
 // Raises per-kernel dynamic-LDS limits once per process (idempotent).
 hipError_t init_kernel_attributes();

@@ -8,8 +8,8 @@
 // per forward (tok_src, prefix offsets cu), all later kernels work on that
 // dense list, and pooling / the hidden-state output map back.
 //
-// Every row kernel gives one wave to one row; lane l owns columns l, l+64, ...
-// so each wave-wide access is one contiguous run of the row.  LayerNorm
+// Every row kernel gives one wave to one row; lane l owns the 16-byte chunks
+// l, l+64, ... of the row, so each wave-wide access is one contiguous run.  LayerNorm
 // statistics are fp32, two passes over registers (mean, then centred sum of
 // squares), with butterfly wave reductions.
 #include <math.h>
@@ -19,8 +19,6 @@
 
 namespace rlx {
 namespace {
-
-constexpr int kMaxCols = 16;  // H <= 1024
 
 __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, int B, int S, int* cu, int* tok_src,
                                                          int* tok_dst) {
@@ -65,30 +63,76 @@ __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, in
   }
 }
 
+// Row held by one wave as 16-byte chunks: lane owns chunks lane, lane+64, ...
+// (EPC elements each), so every wave-wide load or store is one contiguous run.
+template <typename T> struct Chunk;
+template <> struct Chunk<bf16_t> {
+  static constexpr int EPC = 8;
+  static __device__ __forceinline__ void load(const bf16_t* p, float v[8]) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+  static __device__ __forceinline__ void store(bf16_t* p, const float v[8]) {
+    *reinterpret_cast<uint4*>(p) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                              pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+  }
+};
+template <> struct Chunk<float> {
+  static constexpr int EPC = 4;
+  static __device__ __forceinline__ void load(const float* p, float v[4]) {
+    const float4 u = *reinterpret_cast<const float4*>(p);
+    v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float v[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+};
+
+// Chunks per lane: H <= 1024 gives at most 2 (bf16) or 4 (f32).
+template <typename T> constexpr int kMaxCpl = 8 / Chunk<T>::EPC * 2;
+
+// LayerNorm of the wave's row held in v (fp32), written as T.
 template <typename T>
-__device__ __forceinline__ void ln_store(float (&v)[kMaxCols], int ncol, const float* gamma, const float* beta,
-                                         float eps, int H, T* out) {
+__device__ __forceinline__ void ln_row_store(float (&v)[kMaxCpl<T>][Chunk<T>::EPC], int H, const float* gamma,
+                                             const float* beta, float eps, T* out) {
+  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
   const int lane = threadIdx.x & 63;
+  const int nch = H / EPC;
   float sum = 0.0f;
 #pragma unroll
-  for (int i = 0; i < kMaxCols; ++i)
-    if (i < ncol) sum += v[i];
+  for (int i = 0; i < CPL; ++i)
+    if (lane + 64 * i < nch)
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) sum += v[i][e];
   const float mean = wave_sum(sum) / (float)H;
   float sq = 0.0f;
 #pragma unroll
-  for (int i = 0; i < kMaxCols; ++i)
-    if (i < ncol) {
-      const float c = v[i] - mean;
-      sq += c * c;
-    }
-  const float var = wave_sum(sq) / (float)H;
-  const float rstd = 1.0f / sqrtf(var + eps);
+  for (int i = 0; i < CPL; ++i)
+    if (lane + 64 * i < nch)
 #pragma unroll
-  for (int i = 0; i < kMaxCols; ++i)
-    if (i < ncol) {
-      const int c = i * 64 + lane;
-      ElemTraits<T>::store(out + c, (v[i] - mean) * rstd * gamma[c] + beta[c]);
+      for (int e = 0; e < EPC; ++e) {
+        const float c = v[i][e] - mean;
+        sq += c * c;
+      }
+  const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)H + eps);
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nch) {
+      float o[EPC];
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        const int c = ch * EPC + e;
+        o[e] = (v[i][e] - mean) * rstd * gamma[c] + beta[c];
+      }
+      Chunk<T>::store(out + ch * EPC, o);
     }
+  }
 }
 
 template <typename T>
@@ -96,6 +140,7 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int* ids, const T* 
                                                        const float* gamma, const float* beta, float eps, int vocab,
                                                        int S, int H, const int* tok_src, const int* n_dev, int n_max,
                                                        T* x) {
+  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int n = min(n_max, *n_dev);
   if (t >= n) return;
@@ -103,31 +148,39 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int* ids, const T* 
   const int src = tok_src[t];
   const int s = src % S;
   const int id = min(max(ids[src], 0), vocab - 1);
-  const int ncol = H >> 6;
-  float v[kMaxCols];
+  const int nch = H / EPC;
+  float v[CPL][EPC];
 #pragma unroll
-  for (int i = 0; i < kMaxCols; ++i)
-    if (i < ncol) {
-      const int c = i * 64 + lane;
-      v[i] = ElemTraits<T>::load(word + (size_t)id * H + c) + ElemTraits<T>::load(pos + (size_t)s * H + c) +
-             ElemTraits<T>::load(type + c);
+  for (int i = 0; i < CPL; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nch) {
+      float a[EPC], b[EPC], c[EPC];
+      Chunk<T>::load(word + (size_t)id * H + ch * EPC, a);
+      Chunk<T>::load(pos + (size_t)s * H + ch * EPC, b);
+      Chunk<T>::load(type + ch * EPC, c);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) v[i][e] = a[e] + b[e] + c[e];
     }
-  ln_store<T>(v, ncol, gamma, beta, eps, H, x + (size_t)t * H);
+  }
+  ln_row_store<T>(v, H, gamma, beta, eps, x + (size_t)t * H);
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void layer_norm_kernel(const T* a, const float* gamma, const float* beta, float eps,
                                                          int H, const int* n_dev, int n_max, T* y) {
+  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int n = n_dev ? min(n_max, *n_dev) : n_max;
   if (t >= n) return;
   const int lane = threadIdx.x & 63;
-  const int ncol = H >> 6;
-  float v[kMaxCols];
+  const int nch = H / EPC;
+  float v[CPL][EPC];
 #pragma unroll
-  for (int i = 0; i < kMaxCols; ++i)
-    if (i < ncol) v[i] = ElemTraits<T>::load(a + (size_t)t * H + i * 64 + lane);
-  ln_store<T>(v, ncol, gamma, beta, eps, H, y + (size_t)t * H);
+  for (int i = 0; i < CPL; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nch) Chunk<T>::load(a + (size_t)t * H + ch * EPC, v[i]);
+  }
+  ln_row_store<T>(v, H, gamma, beta, eps, y + (size_t)t * H);
 }
 
 template <typename T>
@@ -141,58 +194,62 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T* hidden, int H
   for (int c = lane; c < H; c += 64) x[(size_t)t * H + c] = src[c];
 }
 
-// One block of 256 threads per sequence: two row groups of 128 threads sum
-// alternate rows, then the block forms the mean and its L2 norm.
+// Masked mean-pool + L2 normalisation: one block of 1024 threads (16 waves)
+// per sequence; wave w sums rows w, w+16, ... with 16-byte chunk loads, the
+// 16 partial rows are combined in LDS, then the block forms the mean and its
+// norm.
 template <typename T>
-__global__ __launch_bounds__(256) void pool_l2_kernel(const T* x, int H, const int* cu, float* out) {
-  __shared__ float part[1024];
-  __shared__ float red[4];
+__global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const int* cu, float* out) {
+  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
+  extern __shared__ float part[];  // [16][H]
+  __shared__ float red[16];
   const int b = blockIdx.x;
   const int r0 = cu[b], L = cu[b + 1] - r0;
-  const int g = threadIdx.x >> 7, c0 = threadIdx.x & 127;
-  float acc[8];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nch = H / EPC;
+  float acc[CPL][EPC];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-  for (int r = g; r < L; r += 2) {
+  for (int i = 0; i < CPL; ++i)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[i][e] = 0.0f;
+  for (int r = wave; r < L; r += 16) {
     const T* row = x + (size_t)(r0 + r) * H;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = c0 + 128 * j;
-      if (c < H) acc[j] += ElemTraits<T>::load(row + c);
-    }
-  }
-  if (g == 1) {
+    for (int i = 0; i < CPL; ++i) {
+      const int ch = lane + 64 * i;
+      if (ch < nch) {
+        float v[EPC];
+        Chunk<T>::load(row + ch * EPC, v);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = c0 + 128 * j;
-      if (c < H) part[c] = acc[j];
-    }
-  }
-  __syncthreads();
-  const float denom = fmaxf((float)L, 1e-9f);
-  float ss = 0.0f;
-  if (g == 0) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = c0 + 128 * j;
-      if (c < H) {
-        acc[j] = (acc[j] + part[c]) / denom;
-        ss += acc[j] * acc[j];
+        for (int e = 0; e < EPC; ++e) acc[i][e] += v[e];
       }
     }
   }
-  ss = wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
-  const float inv = 1.0f / fmaxf(sqrtf(tot), 1e-12f);
-  if (g == 0) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = c0 + 128 * j;
-      if (c < H) out[(size_t)b * H + c] = acc[j] * inv;
-    }
+  for (int i = 0; i < CPL; ++i) {
+    const int ch = lane + 64 * i;
+    if (ch < nch)
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) part[wave * H + ch * EPC + e] = acc[i][e];
   }
+  __syncthreads();
+  const float denom = fmaxf((float)L, 1e-9f);
+  const int c = threadIdx.x;
+  float mean = 0.0f;
+  if (c < H) {
+    float sum = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) sum += part[w * H + c];
+    mean = sum / denom;
+  }
+  const float ss = wave_sum(mean * mean);
+  if (lane == 0) red[wave] = ss;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) tot += red[w];
+  const float inv = 1.0f / fmaxf(sqrtf(tot), 1e-12f);
+  if (c < H) out[(size_t)b * H + c] = mean * inv;
 }
 
 template <typename T>
@@ -257,10 +314,11 @@ hipError_t launch_layer_norm(const void* a, const float* gamma, const float* bet
 
 hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s) {
   if (B <= 0) return hipSuccess;
+  const size_t lds = (size_t)16 * H * sizeof(float);
   if (dt == DType::BF16)
-    hipLaunchKernelGGL(pool_l2_kernel<bf16_t>, dim3(B), dim3(256), 0, s, (const bf16_t*)x, H, cu, out);
+    hipLaunchKernelGGL(pool_l2_kernel<bf16_t>, dim3(B), dim3(1024), lds, s, (const bf16_t*)x, H, cu, out);
   else
-    hipLaunchKernelGGL(pool_l2_kernel<float>, dim3(B), dim3(256), 0, s, (const float*)x, H, cu, out);
+    hipLaunchKernelGGL(pool_l2_kernel<float>, dim3(B), dim3(1024), lds, s, (const float*)x, H, cu, out);
   return hipGetLastError();
 }
 

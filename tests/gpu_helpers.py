@@ -11,16 +11,25 @@ def to_bf16_exact(a):
     return workloads.round_to_bf16(np.asarray(a, np.float32))
 
 
-def gemm_tolerance(x, w, ref, *, out_bf16, weight_rel=0.0):
+# The GELU epilogue evaluates erf with Abramowitz & Stegun 7.1.28 (|error| <= 3e-7)
+# in fp32: GELU(v) = v/2 (1 + erf(v / sqrt 2)) is then off by at most
+# |v|/2 * (3e-7 + a few fp32 roundings) <= 5e-7 |v|.
+GELU_REL = 5e-7
+
+
+def gemm_tolerance(x, w, ref, *, out_bf16, weight_rel=0.0, pre=None):
     """Per-element bound for y = x W^T (+ epilogue) computed in fp32 from exact
     operands: fp32 accumulation (K * 2^-24 * sum|x||w|), optional relative
     weight rounding (weight_rel * sum|x||w|), bf16 output rounding
-    (2^-8 * |ref|) and a small floor for the erf-GELU epilogue."""
+    (2^-8 * |ref|), the GELU approximation (GELU_REL * |pre-activation|) when
+    `pre` is given, and a small floor."""
     ax = np.abs(np.asarray(x, np.float64))
     aw = np.abs(np.asarray(w, np.float64))
     s1 = ax @ aw.T
     K = ax.shape[1]
     tol = (K * F32_EPS + weight_rel) * s1 + 1e-6 * np.abs(ref) + 1e-6
+    if pre is not None:
+        tol = tol + GELU_REL * np.abs(pre)
     if out_bf16:
         tol = tol + BF16_REL * np.abs(ref)
     return tol

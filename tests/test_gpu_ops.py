@@ -64,7 +64,8 @@ def test_gemm_dense(rlx, dt, epi, M, N, K):
                            epi=_epi_code(rlx, epi))
     got = y.float().cpu().numpy()
     ref = _oracle_gemm(x, w, b, r, epi)
-    tol = gemm_tolerance(x, w, ref, out_bf16=dt == "bf16")
+    pre = oracle.linear(x, w, b) if epi == "gelu" else None
+    tol = gemm_tolerance(x, w, ref, out_bf16=dt == "bf16", pre=pre)
     assert_within(got, ref, tol, f"gemm {dt} {epi} {M}x{N}x{K}")
 
 
@@ -93,10 +94,27 @@ def test_gemm_dequant(rlx, scheme, epi, M, N, K):
         wrel = 2.0 ** -9  # each dequantised weight is rounded to bf16 before the product
     got = y.float().cpu().numpy()
     ref = _oracle_gemm(x, wdeq, b, r, epi)
-    tol = gemm_tolerance(x, wdeq, ref, out_bf16=True, weight_rel=wrel)
+    pre = oracle.linear(x, wdeq, b) if epi == "gelu" else None
+    tol = gemm_tolerance(x, wdeq, ref, out_bf16=True, weight_rel=wrel, pre=pre)
     if scheme == "int8":
         tol = tol + 2.0 ** -24 * np.abs(ref) * 4  # scale applied to the fp32 sum: a few fp32 roundings
     assert_within(got, ref, tol, f"gemm {scheme} {epi} {M}x{N}x{K}")
+
+
+def test_gelu_epilogue_accuracy_over_a_dense_range(rlx):
+    """fp32 GEMM with an identity weight: every output is GELU(x + b) of one
+    input, so the epilogue's GELU is compared directly with the erf definition
+    over pre-activations densely covering [-10, 10]."""
+    from gpu_helpers import GELU_REL
+    M, K = 1024, 64
+    x = np.linspace(-10, 10, M * K).reshape(M, K).astype(np.float32)
+    w = np.eye(K, dtype=np.float32)
+    b = np.zeros(K, np.float32)
+    y = rlx.dequant_matmul(_dev(x, torch.float32), _dev(w, torch.float32), bias=_dev(b, torch.float32),
+                           epi=rlx.EPI_BIAS_GELU)
+    got = y.cpu().numpy().astype(np.float64)
+    ref = oracle.gelu(x.astype(np.float64))
+    assert_within(got, ref, GELU_REL * np.abs(x) + 1e-7, "GELU epilogue")
 
 
 @pytest.mark.parametrize("scheme", ["int8", "int4"])
