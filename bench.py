@@ -43,10 +43,13 @@ def attention_flops(sp, lengths):
 
 
 def kernel_source_digest():
+    """Digest of every kernel source: counter figures taken before a change to
+    any of them are no longer reported."""
     h = hashlib.sha256()
-    for f in ("gemm.hip", "common.hpp", "kernels.hpp"):
-        with open(os.path.join(ROOT, "paper_2609_37916_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    csrc = os.path.join(ROOT, "paper_2609_37916_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
 
 
@@ -96,9 +99,11 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="minilm_b32_s128_bf16")
-    ap.add_argument("--profile-steps", type=int, default=20, help="forwards timed kernel by kernel")
+    ap.add_argument("--profile-steps", type=int, default=20, help="profiled forwards (per-kernel event times)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy (counter calibration for FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -120,6 +125,16 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "device copy", "bytes_read": src.numel() * 4, "bytes_written": dst.numel() * 4,
+                          "launches": 3}), flush=True)
+        return
 
     sp = workloads.spec(args.workload)
     wl = workloads.make(sp)
@@ -149,7 +164,7 @@ def main():
     p10, p90 = np.percentile(step_ms, [10, 90]).tolist()
     seq_per_s = sp.batch * args.steps / (total_ms / 1e3)
 
-    # per-kernel times: the same forward launched kernel by kernel, an event pair around every launch
+    # per-kernel times: the same forward replayed from a graph with an event pair around every kernel
     enc.set_profiling(True)
     for _ in range(args.profile_steps):
         enc.forward(inputs["input"], inputs["mask"], out=out)
@@ -162,7 +177,9 @@ def main():
     fpt = gemm_flops_per_token(sp)
     flops_launch = {k: v * tokens for k, v in fpt.items()}
     flops_launch["attention"] = attention_flops(sp, wl.mask.sum(axis=1))
-    matrix_classes = list(flops_launch)
+    # sequences of <= 128 tokens run the QKV projection inside the attention kernel
+    flops_launch["qkv_attention"] = flops_launch["gemm_qkv"] + flops_launch["attention"]
+    matrix_classes = [k for k in flops_launch if k in per_fwd_us]
     dominant = max(matrix_classes, key=lambda k: per_fwd_us.get(k, 0.0))
     achieved = flops_launch[dominant] / (per_launch_us[dominant] * 1e-6) / 1e12
     traffic = committed_traffic(dominant, args.workload)

@@ -217,10 +217,12 @@ rlx_status rlx_encoder_forward(rlx_encoder* enc, const void* input, const uint8_
 void rlx_encoder_destroy(rlx_encoder* enc);
 
 /* Per-kernel timing of forward passes (a native counterpart of a per-operator
- * dispatch report).  While enabled, forwards run kernel by kernel (never from
- * a graph) with a HIP event pair around every launch; rlx_encoder_profile_read
- * returns, per kernel class, the number of launches and the summed event time
- * in milliseconds.  Names are static strings owned by the library. */
+ * dispatch report).  While enabled, each forward replays a HIP graph that
+ * carries a HIP event pair around every kernel, waits for it (the call is then
+ * synchronous), and adds each kernel's event time to its class.
+ * rlx_encoder_profile_read returns, per kernel class, the number of launches
+ * and the summed time in milliseconds, then clears the totals.  Names are
+ * static strings owned by the library. */
 rlx_status rlx_encoder_set_profiling(rlx_encoder* enc, int enable);
 rlx_status rlx_encoder_profile_read(rlx_encoder* enc, int max_entries, const char** names, int* launches,
                                     double* total_ms, int* n_entries);

@@ -14,6 +14,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -44,6 +45,7 @@ rlx_status ok() {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 rlx_status hip_fail(hipError_t e, const char* what) {
+  (void)hipGetLastError();  // the error is reported here; do not leave it for the caller's next HIP call
   return fail(RLX_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
@@ -143,10 +145,17 @@ struct GraphEntry {
   uint64_t last_use;
 };
 
-struct ProfRec {
+struct KernelSlot {  // one launch of a forward: its class and a replayable closure
   int cls;
-  hipEvent_t a, b;
+  std::function<hipError_t(hipStream_t)> launch;
 };
+
+struct ProfGraph {  // per forward configuration: one graph of kProfReps launches per kernel
+  GraphEntry g;
+  std::vector<int> slot_cls;
+  std::vector<hipGraphExec_t> slot_exec;
+};
+constexpr int kProfReps = 8;
 
 }  // namespace
 
@@ -165,7 +174,10 @@ struct rlx_encoder {
   std::vector<GraphEntry> graphs;
   uint64_t use_clock = 0;
   bool profiling = false;
-  std::vector<ProfRec> prof;
+  hipEvent_t prof_ev[2] = {nullptr, nullptr};
+  std::vector<ProfGraph> prof_graphs;
+  int prof_cnt[K_NUM_CLASSES] = {0};
+  double prof_ms[K_NUM_CLASSES] = {0};
 };
 
 namespace {
@@ -238,40 +250,33 @@ rlx_status check_weights(const rlx_encoder_config* c, const rlx_encoder_weights*
   return RLX_OK;
 }
 
-// Enqueue one forward on `s`.  `prof` records an event pair around every launch.
+// Enqueue one forward on `s`.  With `slots` non-null every launch is also
+// recorded (kernel class + a closure holding a copy of its arguments) so that
+// the profiling mode can replay single kernels.
 rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
-                           hipStream_t s, bool prof) {
+                           hipStream_t s, std::vector<KernelSlot>* slots) {
   const rlx_encoder_config& c = e->cfg;
   const int H = c.hidden, F = c.ffn, T = B * S;
   const int* n_dev = e->cu + B;  // number of real tokens, written by the mask scan
-  auto step = [&](int cls, auto&& fn) -> rlx_status {
-    hipEvent_t a = nullptr, b = nullptr;
-    if (prof) {
-      RLX_HIP(hipEventCreate(&a), "hipEventCreate");
-      RLX_HIP(hipEventCreate(&b), "hipEventCreate");
-      RLX_HIP(hipEventRecord(a, s), "hipEventRecord");
-    }
-    hipError_t err = fn();
+  auto step = [&](int cls, std::function<hipError_t(hipStream_t)> fn) -> rlx_status {
+    hipError_t err = fn(s);
     if (err != hipSuccess) return hip_fail(err, kClassNames[cls]);
-    if (prof) {
-      RLX_HIP(hipEventRecord(b, s), "hipEventRecord");
-      e->prof.push_back({cls, a, b});
-    }
+    if (slots) slots->push_back({cls, std::move(fn)});
     return RLX_OK;
   };
-#define STEP(cls, expr)                                                   \
-  do {                                                                    \
-    rlx_status st_ = step(cls, [&]() -> hipError_t { return (expr); }); \
-    if (st_ != RLX_OK) return st_;                                        \
+#define STEP(cls, expr)                                                            \
+  do {                                                                             \
+    rlx_status st_ = step(cls, [=](hipStream_t ss) -> hipError_t { return (expr); }); \
+    if (st_ != RLX_OK) return st_;                                                 \
   } while (0)
 
-  STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, e->cu, e->tok_src, e->tok_dst, s));
+  STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, e->cu, e->tok_src, e->tok_dst, ss));
   if (c.input_kind == RLX_INPUT_IDS) {
     STEP(K_EMBED_LN, launch_embed_ln(static_cast<const int*>(input), e->w.word_emb, e->w.pos_emb, e->w.type_emb,
                                      e->w.emb_ln_gamma, e->w.emb_ln_beta, c.ln_eps, c.vocab, S, H, e->tok_src, n_dev,
-                                     T, e->X, e->dt, s));
+                                     T, e->X, e->dt, ss));
   } else {
-    STEP(K_GATHER_ROWS, launch_gather_rows(input, H, e->tok_src, n_dev, T, e->X, e->dt, s));
+    STEP(K_GATHER_ROWS, launch_gather_rows(input, H, e->tok_src, n_dev, T, e->X, e->dt, ss));
   }
   const Quant q = to_quant(c.quant);
   for (int l = 0; l < c.layers; ++l) {
@@ -287,11 +292,11 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
       FusedAttnParams fa{};
       fa.x = e->X; fa.wqkv = L.wqkv; fa.bqkv = L.bqkv; fa.cu_seqlens = e->cu; fa.out = e->CTX; fa.out_rows = T;
       fa.B = B; fa.H = H; fa.heads = c.heads; fa.scale = 1.0f / std::sqrt((float)c.head_dim);
-      STEP(K_QKV_ATTENTION, launch_qkv_attention(fa, s));
+      STEP(K_QKV_ATTENTION, launch_qkv_attention(fa, ss));
     } else {
       g.x = e->X; g.w = L.wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = L.bqkv;
       g.residual = nullptr; g.y = e->QKV; g.N = 3 * H; g.K = H; g.epi = Epi::Bias;
-      STEP(K_GEMM_QKV, launch_gemm(g, s));
+      STEP(K_GEMM_QKV, launch_gemm(g, ss));
 
       AttnParams a{};
       const size_t es = e->dt == DType::BF16 ? 2 : 4;
@@ -304,29 +309,29 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
       a.scale = 1.0f / std::sqrt((float)c.head_dim);
       a.cu_seqlens = e->cu;
       a.dtype = e->dt;
-      STEP(K_ATTENTION, launch_attention(a, s));
+      STEP(K_ATTENTION, launch_attention(a, ss));
     }
 
     g.x = e->CTX; g.w = L.wo; g.scales = L.wo_scales; g.zeros = L.wo_zeros; g.bias = L.bo;
     g.residual = e->X; g.y = e->A; g.N = H; g.K = H; g.epi = Epi::BiasResidual;
     g.x_head_rows = fused_attn ? T : 0;  // the fused attention writes the context head-major
-    STEP(K_GEMM_ATTN_OUT, launch_gemm(g, s));
+    STEP(K_GEMM_ATTN_OUT, launch_gemm(g, ss));
     g.x_head_rows = 0;
-    STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, s));
+    STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, ss));
 
     g.x = e->X1; g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;
     g.residual = nullptr; g.y = e->G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
-    STEP(K_GEMM_FFN_UP, launch_gemm(g, s));
+    STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
 
     g.x = e->G; g.w = L.w2; g.scales = L.w2_scales; g.zeros = L.w2_zeros; g.bias = L.b2;
     g.residual = e->X1; g.y = e->A; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
-    STEP(K_GEMM_FFN_DOWN, launch_gemm(g, s));
-    STEP(K_LN2, launch_layer_norm(e->A, L.ln2_gamma, L.ln2_beta, c.ln_eps, H, n_dev, T, e->X, e->dt, s));
+    STEP(K_GEMM_FFN_DOWN, launch_gemm(g, ss));
+    STEP(K_LN2, launch_layer_norm(e->A, L.ln2_gamma, L.ln2_beta, c.ln_eps, H, n_dev, T, e->X, e->dt, ss));
   }
   if (c.output_kind == RLX_OUTPUT_POOLED) {
-    STEP(K_POOL, launch_pool_l2(e->X, H, e->cu, B, static_cast<float*>(output), e->dt, s));
+    STEP(K_POOL, launch_pool_l2(e->X, H, e->cu, B, static_cast<float*>(output), e->dt, ss));
   } else {
-    STEP(K_SCATTER, launch_scatter_hidden(e->X, H, e->tok_dst, T, static_cast<float*>(output), e->dt, s));
+    STEP(K_SCATTER, launch_scatter_hidden(e->X, H, e->tok_dst, T, static_cast<float*>(output), e->dt, ss));
   }
 #undef STEP
   return RLX_OK;
@@ -335,14 +340,127 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
 void destroy_graphs(rlx_encoder* e) {
   for (auto& g : e->graphs) (void)hipGraphExecDestroy(g.exec);
   e->graphs.clear();
+  for (auto& g : e->prof_graphs)
+    for (auto x : g.slot_exec) (void)hipGraphExecDestroy(x);
+  e->prof_graphs.clear();
 }
 
 void clear_profile(rlx_encoder* e) {
-  for (auto& r : e->prof) {
-    (void)hipEventDestroy(r.a);
-    (void)hipEventDestroy(r.b);
+  for (int c = 0; c < K_NUM_CLASSES; ++c) {
+    e->prof_cnt[c] = 0;
+    e->prof_ms[c] = 0.0;
   }
-  e->prof.clear();
+}
+
+// Records the forward as a HIP graph on the capture stream; `slots` as in enqueue_forward.
+rlx_status capture_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
+                           std::vector<KernelSlot>* slots, hipGraphExec_t* exec) {
+  RLX_HIP(hipStreamBeginCapture(e->cap_stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+  rlx_status st = enqueue_forward(e, input, mask, B, S, output, e->cap_stream, slots);
+  hipGraph_t graph = nullptr;
+  hipError_t he = hipStreamEndCapture(e->cap_stream, &graph);
+  if (st != RLX_OK) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return st;
+  }
+  if (he != hipSuccess) return hip_fail(he, "hipStreamEndCapture");
+  he = hipGraphInstantiate(exec, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  if (he != hipSuccess) return hip_fail(he, "hipGraphInstantiate");
+  return RLX_OK;
+}
+
+// Profiled forward.  Per kernel of the forward, a graph of kProfReps
+// back-to-back launches of that kernel alone (same arguments) is replayed
+// between two events on the caller's stream; the mean is the kernel's time
+// with only graph-replay gaps, like in the forward's own graph.  No kernel
+// writes its own input, so repeats are idempotent.  A plain forward runs first
+// (the token counts every kernel indexes with must be set for this mask) and
+// again last, so the output is the forward's result.
+rlx_status run_graph_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
+                             hipStream_t s);
+
+rlx_status profiled_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
+                            hipStream_t s) {
+  if (!e->prof_ev[0]) {
+    RLX_HIP(hipEventCreate(&e->prof_ev[0]), "hipEventCreate");
+    RLX_HIP(hipEventCreate(&e->prof_ev[1]), "hipEventCreate");
+  }
+  rlx_status st = run_graph_forward(e, input, mask, B, S, output, s);
+  if (st != RLX_OK) return st;
+  ProfGraph* hit = nullptr;
+  for (auto& g : e->prof_graphs)
+    if (g.g.B == B && g.g.S == S && g.g.input == input && g.g.mask == mask && g.g.output == output) hit = &g;
+  if (!hit) {
+    if (e->prof_graphs.size() >= kMaxGraphs) {
+      RLX_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
+      for (auto x : e->prof_graphs.front().slot_exec) (void)hipGraphExecDestroy(x);
+      e->prof_graphs.erase(e->prof_graphs.begin());
+    }
+    // record the launches of one forward (also a real forward on the capture stream)
+    std::vector<KernelSlot> slots;
+    RLX_HIP(hipStreamSynchronize(s), "hipStreamSynchronize");
+    st = enqueue_forward(e, input, mask, B, S, output, e->cap_stream, &slots);
+    if (st != RLX_OK) return st;
+    RLX_HIP(hipStreamSynchronize(e->cap_stream), "hipStreamSynchronize");
+    ProfGraph pg;
+    pg.g = {B, S, input, mask, output, nullptr, 0};
+    for (auto& sl : slots) {
+      RLX_HIP(hipStreamBeginCapture(e->cap_stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+      hipError_t le = hipSuccess;
+      for (int r = 0; r < kProfReps && le == hipSuccess; ++r) le = sl.launch(e->cap_stream);
+      hipGraph_t graph = nullptr;
+      hipError_t he = hipStreamEndCapture(e->cap_stream, &graph);
+      if (le != hipSuccess || he != hipSuccess) {
+        if (graph) (void)hipGraphDestroy(graph);
+        return hip_fail(le != hipSuccess ? le : he, "profiling capture");
+      }
+      hipGraphExec_t x = nullptr;
+      he = hipGraphInstantiate(&x, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      if (he != hipSuccess) return hip_fail(he, "hipGraphInstantiate");
+      pg.slot_cls.push_back(sl.cls);
+      pg.slot_exec.push_back(x);
+    }
+    e->prof_graphs.push_back(std::move(pg));
+    hit = &e->prof_graphs.back();
+  }
+  for (size_t k = 0; k < hit->slot_exec.size(); ++k) {
+    RLX_HIP(hipEventRecord(e->prof_ev[0], s), "hipEventRecord");
+    RLX_HIP(hipGraphLaunch(hit->slot_exec[k], s), "hipGraphLaunch");
+    RLX_HIP(hipEventRecord(e->prof_ev[1], s), "hipEventRecord");
+    RLX_HIP(hipEventSynchronize(e->prof_ev[1]), "hipEventSynchronize");
+    float t = 0.0f;
+    RLX_HIP(hipEventElapsedTime(&t, e->prof_ev[0], e->prof_ev[1]), "hipEventElapsedTime");
+    e->prof_cnt[hit->slot_cls[k]] += 1;
+    e->prof_ms[hit->slot_cls[k]] += t / kProfReps;
+  }
+  return run_graph_forward(e, input, mask, B, S, output, s);
+}
+
+// The normal path: replay (recording on first use) the graph of this forward.
+rlx_status run_graph_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
+                             hipStream_t s) {
+  GraphEntry* hit = nullptr;
+  for (auto& g : e->graphs)
+    if (g.B == B && g.S == S && g.input == input && g.mask == mask && g.output == output) hit = &g;
+  if (!hit) {
+    if (e->graphs.size() >= kMaxGraphs) {
+      auto lru = std::min_element(e->graphs.begin(), e->graphs.end(),
+                                  [](const GraphEntry& a, const GraphEntry& b) { return a.last_use < b.last_use; });
+      RLX_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
+      (void)hipGraphExecDestroy(lru->exec);
+      e->graphs.erase(lru);
+    }
+    hipGraphExec_t exec = nullptr;
+    rlx_status st = capture_forward(e, input, mask, B, S, output, nullptr, &exec);
+    if (st != RLX_OK) return st;
+    e->graphs.push_back({B, S, input, mask, output, exec, 0});
+    hit = &e->graphs.back();
+  }
+  hit->last_use = ++e->use_clock;
+  RLX_HIP(hipGraphLaunch(hit->exec, s), "hipGraphLaunch");
+  return RLX_OK;
 }
 
 }  // namespace
@@ -483,50 +601,23 @@ rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t*
                 e->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (e->profiling) {
-    rlx_status st = enqueue_forward(e, input, attention_mask, B, S, output, s, true);
+    rlx_status st = profiled_forward(e, input, attention_mask, B, S, output, s);
     return st == RLX_OK ? ok() : st;
   }
   if (!e->cfg.use_graph) {
-    rlx_status st = enqueue_forward(e, input, attention_mask, B, S, output, s, false);
+    rlx_status st = enqueue_forward(e, input, attention_mask, B, S, output, s, nullptr);
     return st == RLX_OK ? ok() : st;
   }
-  GraphEntry* hit = nullptr;
-  for (auto& g : e->graphs)
-    if (g.B == B && g.S == S && g.input == input && g.mask == attention_mask && g.output == output) hit = &g;
-  if (!hit) {
-    if (e->graphs.size() >= kMaxGraphs) {
-      auto lru = std::min_element(e->graphs.begin(), e->graphs.end(),
-                                  [](const GraphEntry& a, const GraphEntry& b) { return a.last_use < b.last_use; });
-      RLX_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
-      (void)hipGraphExecDestroy(lru->exec);
-      e->graphs.erase(lru);
-    }
-    RLX_HIP(hipStreamBeginCapture(e->cap_stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
-    rlx_status st = enqueue_forward(e, input, attention_mask, B, S, output, e->cap_stream, false);
-    hipGraph_t graph = nullptr;
-    hipError_t he = hipStreamEndCapture(e->cap_stream, &graph);
-    if (st != RLX_OK) {
-      if (graph) (void)hipGraphDestroy(graph);
-      return st;
-    }
-    if (he != hipSuccess) return hip_fail(he, "hipStreamEndCapture");
-    hipGraphExec_t exec = nullptr;
-    he = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
-    (void)hipGraphDestroy(graph);
-    if (he != hipSuccess) return hip_fail(he, "hipGraphInstantiate");
-    e->graphs.push_back({B, S, input, attention_mask, output, exec, 0});
-    hit = &e->graphs.back();
-  }
-  hit->last_use = ++e->use_clock;
-  RLX_HIP(hipGraphLaunch(hit->exec, s), "hipGraphLaunch");
-  return ok();
+  rlx_status st = run_graph_forward(e, input, attention_mask, B, S, output, s);
+  return st == RLX_OK ? ok() : st;
 }
 
 void rlx_encoder_destroy(rlx_encoder* e) {
   if (!e) return;
   (void)hipDeviceSynchronize();
   destroy_graphs(e);
-  clear_profile(e);
+  for (auto ev : e->prof_ev)
+    if (ev) (void)hipEventDestroy(ev);
   if (e->cap_stream) (void)hipStreamDestroy(e->cap_stream);
   if (e->ws) (void)hipFree(e->ws);
   delete e;
@@ -535,10 +626,7 @@ void rlx_encoder_destroy(rlx_encoder* e) {
 rlx_status rlx_encoder_set_profiling(rlx_encoder* e, int enable) {
   if (!e) return fail(RLX_ERR_INVALID_ARG, "encoder_set_profiling: null handle");
   e->profiling = enable != 0;
-  if (!e->profiling) {
-    (void)hipDeviceSynchronize();
-    clear_profile(e);
-  }
+  clear_profile(e);
   return ok();
 }
 
@@ -547,15 +635,8 @@ rlx_status rlx_encoder_profile_read(rlx_encoder* e, int max_entries, const char*
   if (!e || !n_entries) return fail(RLX_ERR_INVALID_ARG, "encoder_profile_read: null handle or n_entries");
   if (max_entries < 0 || (max_entries > 0 && (!names || !launches || !total_ms)))
     return fail(RLX_ERR_INVALID_ARG, "encoder_profile_read: output arrays required for max_entries > 0");
-  int cnt[K_NUM_CLASSES] = {0};
-  double ms[K_NUM_CLASSES] = {0};
-  for (auto& r : e->prof) {
-    RLX_HIP(hipEventSynchronize(r.b), "hipEventSynchronize");
-    float t = 0.0f;
-    RLX_HIP(hipEventElapsedTime(&t, r.a, r.b), "hipEventElapsedTime");
-    cnt[r.cls] += 1;
-    ms[r.cls] += t;
-  }
+  const int* cnt = e->prof_cnt;
+  const double* ms = e->prof_ms;
   int n = 0;
   for (int c = 0; c < K_NUM_CLASSES; ++c) {
     if (!cnt[c]) continue;
