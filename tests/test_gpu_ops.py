@@ -69,6 +69,47 @@ def test_gemm_dense(rlx, dt, epi, M, N, K):
     assert_within(got, ref, tol, f"gemm {dt} {epi} {M}x{N}x{K}")
 
 
+def _rne_bf16_bits(f32):
+    """IEEE round-to-nearest-even of binary32 to bfloat16 bits, for finite
+    values and infinities."""
+    u = np.asarray(f32, np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+# signed zeros, largest finite (rounds to infinity), infinities, and ties / near-ties next to 1.0
+SPECIAL_F32_BITS = [0x00000000, 0x80000000, 0x7F7FFFFF, 0xFF7FFFFF, 0x7F800000, 0xFF800000, 0x3F808000, 0x3F818000,
+                    0x3F807FFF, 0x3F808001, 0xBF808000, 0xBF818000]
+
+
+@pytest.mark.parametrize("N", [384, 1536])
+def test_bf16_output_rounding_is_round_to_nearest_even(rlx, N):
+    """With x = 0 the bias epilogue's bf16 output is 0 + bias rounded once:
+    checked bit for bit on random normal numbers of every exponent, low halves
+    on and next to the rounding boundary (both parities of the kept bit),
+    subnormals, signed zeros, overflow to infinity and infinities."""
+    rng = np.random.default_rng(77 + N)
+    sign = rng.integers(0, 2, N).astype(np.uint32) << np.uint32(31)
+    expo = rng.integers(1, 255, N).astype(np.uint32) << np.uint32(23)
+    mant = rng.integers(0, 1 << 23, N).astype(np.uint32)
+    bits = sign | expo | mant
+    low = np.repeat(np.array([0x8000, 0x7FFF, 0x8001, 0x0000, 0xFFFF], np.uint32), 16)
+    bits[:80] = (bits[:80] & np.uint32(0xFFFF0000)) | low
+    bits[80:88] = sign[80:88] | rng.integers(1, 1 << 23, 8).astype(np.uint32)  # subnormals
+    bits[88:88 + len(SPECIAL_F32_BITS)] = SPECIAL_F32_BITS
+    bias = bits.view(np.float32)
+    M, K = 300, 64
+    x = torch.zeros((M, K), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((N, K), dtype=torch.bfloat16, device="cuda")
+    y = rlx.dequant_matmul(x, w, bias=_dev(bias, torch.float32), epi=rlx.EPI_BIAS)
+    torch.cuda.synchronize()
+    got = y.view(torch.int16).cpu().numpy().view(np.uint16)
+    want = _rne_bf16_bits(np.float32(0.0) + bias)  # 0 + (-0) = +0
+    bad = np.nonzero(got != want[None, :])
+    assert bad[0].size == 0, (f"{bad[0].size} outputs differ; first at column {bad[1][0]}: bias bits "
+                              f"{int(bits[bad[1][0]]):#010x} got {int(got[bad[0][0], bad[1][0]]):#06x} "
+                              f"want {int(want[bad[1][0]]):#06x}")
+
+
 @pytest.mark.parametrize("scheme", ["int8", "int4"])
 @pytest.mark.parametrize("epi", EPIS)
 @pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 1152, 384), (129, 1536, 384), (200, 384, 1536)])
