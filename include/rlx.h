@@ -168,7 +168,7 @@ typedef struct {
  * pointing at the f16 scale / zero-point arrays (NULL when unused).
  * wqkv stacks the Q, K and V projections: rows [0,H) Q, [H,2H) K, [2H,3H) V;
  * head h owns rows h*head_dim .. h*head_dim+head_dim-1 of each block.
- * Biases and LayerNorm parameters are f32.
+ * Biases are f32 and 16-byte aligned; LayerNorm parameters are f32.
  */
 typedef struct {
   const void* wqkv; const void* wqkv_scales; const void* wqkv_zeros; const float* bqkv;  /* [3H,H], [3H] */
@@ -196,7 +196,7 @@ typedef struct rlx_encoder rlx_encoder;
  * Errors: RLX_ERR_INVALID_ARG (nulls, non-positive sizes, H != heads*head_dim),
  * RLX_ERR_UNSUPPORTED (head_dim != 32, H or F not a multiple of 64,
  * max_seq > 512 or > max_pos, quantised weights with f32 activations,
- * group_size != 32), RLX_ERR_OOM, RLX_ERR_HIP. */
+ * group_size != 32, biases not 16-byte aligned), RLX_ERR_OOM, RLX_ERR_HIP. */
 rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_weights* w, rlx_encoder** out);
 
 /* One forward pass.
@@ -217,12 +217,14 @@ rlx_status rlx_encoder_forward(rlx_encoder* enc, const void* input, const uint8_
 void rlx_encoder_destroy(rlx_encoder* enc);
 
 /* Per-kernel timing of forward passes (a native counterpart of a per-operator
- * dispatch report).  While enabled, each forward replays a HIP graph that
- * carries a HIP event pair around every kernel, waits for it (the call is then
- * synchronous), and adds each kernel's event time to its class.
- * rlx_encoder_profile_read returns, per kernel class, the number of launches
- * and the summed time in milliseconds, then clears the totals.  Names are
- * static strings owned by the library. */
+ * dispatch report).  While enabled, each forward runs normally, then replays,
+ * kernel by kernel in forward order, a HIP graph holding 8 back-to-back
+ * launches of that kernel alone between two HIP events, and finally runs the
+ * forward again, so the output is the forward's result; the call is then
+ * synchronous.  Each kernel adds one launch and its mean time per launch to
+ * its class.  rlx_encoder_profile_read returns, for every class with launches,
+ * the number of launches and the summed time in milliseconds, then clears the
+ * totals.  Names are static strings owned by the library. */
 rlx_status rlx_encoder_set_profiling(rlx_encoder* enc, int enable);
 rlx_status rlx_encoder_profile_read(rlx_encoder* enc, int max_entries, const char** names, int* launches,
                                     double* total_ms, int* n_entries);

@@ -402,12 +402,16 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 template <int LPS, int MAXA>
 __device__ __forceinline__ void wait_stage(int ahead) {
-  // ahead stages (LPS loads each) may stay in flight
-  if constexpr (MAXA >= 4) { if (ahead >= 4) { wait_vmcnt<4 * LPS>(); return; } }
-  if constexpr (MAXA >= 3) { if (ahead == 3) { wait_vmcnt<3 * LPS>(); return; } }
-  if constexpr (MAXA >= 2) { if (ahead == 2) { wait_vmcnt<2 * LPS>(); return; } }
-  if constexpr (MAXA >= 1) { if (ahead == 1) { wait_vmcnt<LPS>(); return; } }
-  wait_vmcnt<0>();
+  // ahead (<= MAXA) later stages of LPS loads each may stay in flight
+  if constexpr (MAXA > 0) {
+    if (ahead >= MAXA) {
+      wait_vmcnt<MAXA * LPS>();
+      return;
+    }
+    wait_stage<LPS, MAXA - 1>(ahead);
+  } else {
+    wait_vmcnt<0>();
+  }
 }
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
@@ -499,36 +503,41 @@ __global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
       if (kt < KT) {
         wait_stage<LPS, STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
         __syncthreads();  // stage kt visible to all waves; buffer of stage kt-1 is free
-        if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, (u + STAGES - 1) % STAGES);
+        const bool prefetch = kt + STAGES - 1 < KT;
         const uint8_t* xs = smem + u * kStage;
         const uint8_t* ws = xs + BM * kRowBytes;
         if constexpr (ES == 2) {
-          // fragments of chunk q+1 are read while chunk q is on the matrix cores
-          bf16x8_t af[2][TN], bfr[2][TM];
-          auto load_frags = [&](int q, int slot) {
+          // All of the stage's fragments are requested before the first MFMA,
+          // so the LDS latency is paid once per stage.  The scheduling barrier
+          // keeps the compiler from sinking each read next to its MFMA (with a
+          // full wait in between), which exposes the latency once per chunk.
+          bf16x8_t af[CH][TN], bfr[CH][TM];
+#pragma unroll
+          for (int q = 0; q < CH; ++q) {
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) {
               const int r = wn * WN + tn * 32 + l32;
-              af[slot][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
+              af[q][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
             }
 #pragma unroll
             for (int tm = 0; tm < TM; ++tm) {
               const int r = wm * WM + tm * 32 + l32;
-              bfr[slot][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
+              bfr[q][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
             }
-          };
-          load_frags(0, 0);
+          }
+          // the next stage's DMA goes out after the reads: its issue can stall
+          // while the memory pipeline is busy, and the reads are then in flight
+          if (prefetch) issue(kt + STAGES - 1, (u + STAGES - 1) % STAGES);
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int q = 0; q < CH; ++q) {
-            if (q + 1 < CH) load_frags(q + 1, (q + 1) & 1);
+          for (int q = 0; q < CH; ++q)
 #pragma unroll
             for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
               for (int tn = 0; tn < TN; ++tn)
-                acc[tm][tn] =
-                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][tn], bfr[q & 1][tm], acc[tm][tn], 0, 0, 0);
-          }
+                acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q][tn], bfr[q][tm], acc[tm][tn], 0, 0, 0);
         } else {
+          if (prefetch) issue(kt + STAGES - 1, (u + STAGES - 1) % STAGES);
 #pragma unroll
           for (int q = 0; q < CH; ++q) {
             float af[TN][8], bfr[TM][8];
@@ -606,7 +615,7 @@ hipError_t launch_dense(const GemmParams& p, hipStream_t s) {
     case kTile128x128: return launch_dma_tile<128, 128, 2, T>(p, s);
     case kTile64x128: return launch_dma_tile<64, 128, 3, T>(p, s);
     case kTile128x64: return launch_dma_tile<128, 64, 3, T>(p, s);
-    default: return launch_dma_tile<64, 64, 4, T>(p, s);
+    default: return launch_dma_tile<64, 64, 3, T>(p, s);  // three stages: measured faster than four at N = 384
   }
 }
 
