@@ -168,7 +168,7 @@ typedef struct {
  * pointing at the f16 scale / zero-point arrays (NULL when unused).
  * wqkv stacks the Q, K and V projections: rows [0,H) Q, [H,2H) K, [2H,3H) V;
  * head h owns rows h*head_dim .. h*head_dim+head_dim-1 of each block.
- * Biases are f32 and 16-byte aligned; LayerNorm parameters are f32.
+ * Biases and LayerNorm parameters are f32 and 16-byte aligned.
  */
 typedef struct {
   const void* wqkv; const void* wqkv_scales; const void* wqkv_zeros; const float* bqkv;  /* [3H,H], [3H] */
@@ -196,7 +196,8 @@ typedef struct rlx_encoder rlx_encoder;
  * Errors: RLX_ERR_INVALID_ARG (nulls, non-positive sizes, H != heads*head_dim),
  * RLX_ERR_UNSUPPORTED (head_dim != 32, H or F not a multiple of 64,
  * max_seq > 512 or > max_pos, quantised weights with f32 activations,
- * group_size != 32, biases not 16-byte aligned), RLX_ERR_OOM, RLX_ERR_HIP. */
+ * group_size != 32, biases or LayerNorm parameters not 16-byte aligned),
+ * RLX_ERR_OOM, RLX_ERR_HIP. */
 rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_weights* w, rlx_encoder** out);
 
 /* One forward pass.

@@ -533,7 +533,10 @@ hipError_t set_lds_limits() {
   return once;
 }
 
-hipError_t init_kernel_attributes() { return set_lds_limits(); }
+hipError_t init_kernel_attributes() {
+  const hipError_t e = set_lds_limits();
+  return e != hipSuccess ? e : gemm_init_attributes();
+}
 
 hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
   if (p.B <= 0 || p.S <= 0) return hipSuccess;

@@ -129,12 +129,12 @@ namespace {
 
 enum KernelClass {
   K_MASK_SCAN = 0, K_EMBED_LN, K_GATHER_ROWS, K_GEMM_QKV, K_ATTENTION, K_GEMM_ATTN_OUT, K_LN1, K_GEMM_FFN_UP,
-  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_NUM_CLASSES
+  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_GEMM_FFN_UP_LN, K_NUM_CLASSES
 };
 const char* kClassNames[K_NUM_CLASSES] = {"mask_scan",     "embed_ln",    "gather_rows", "gemm_qkv",
                                           "attention",     "gemm_attn_out", "layer_norm_1", "gemm_ffn_up",
                                           "gemm_ffn_down", "layer_norm_2", "pool_l2",     "scatter_hidden",
-                                          "qkv_attention"};
+                                          "qkv_attention", "gemm_ffn_up_ln"};
 
 struct GraphEntry {
   int B, S;
@@ -234,6 +234,8 @@ rlx_status check_weights(const rlx_encoder_config* c, const rlx_encoder_weights*
     const rlx_layer_weights& L = w->layers[l];
     if (!L.bqkv || !L.bo || !L.b1 || !L.b2 || !L.ln1_gamma || !L.ln1_beta || !L.ln2_gamma || !L.ln2_beta)
       return fail(RLX_ERR_INVALID_ARG, "encoder: layer %d has a null bias or LayerNorm parameter", l);
+    if (!aligned16(L.ln1_gamma) || !aligned16(L.ln1_beta) || !aligned16(L.ln2_gamma) || !aligned16(L.ln2_beta))
+      return fail(RLX_ERR_UNSUPPORTED, "encoder: layer %d LayerNorm parameters must be 16-byte aligned", l);
     struct { const char* nm; const void *w, *s, *z; int N, K; const float* b; } lin[4] = {
         {"wqkv", L.wqkv, L.wqkv_scales, L.wqkv_zeros, 3 * H, H, L.bqkv},
         {"wo", L.wo, L.wo_scales, L.wo_zeros, H, H, L.bo},
@@ -317,11 +319,22 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
     g.x_head_rows = fused_attn ? T : 0;  // the fused attention writes the context head-major
     STEP(K_GEMM_ATTN_OUT, launch_gemm(g, ss));
     g.x_head_rows = 0;
-    STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, ss));
 
-    g.x = e->X1; g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;
+    // LN1 feeds the FFN-up projection and, as the residual, the FFN-down one.
+    // With dense bf16 weights the FFN-up kernel normalises its input rows
+    // itself and its first column tile stores them (X1).
+    g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;
     g.residual = nullptr; g.y = e->G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
-    STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
+    if (gemm_ln_input_supported(e->dt, q, H)) {
+      g.x = e->A; g.ln_gamma = L.ln1_gamma; g.ln_beta = L.ln1_beta; g.ln_eps = c.ln_eps; g.ln_out = e->X1;
+      STEP(K_GEMM_FFN_UP_LN, launch_gemm(g, ss));
+      g.ln_gamma = g.ln_beta = nullptr;
+      g.ln_out = nullptr;
+    } else {
+      STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, ss));
+      g.x = e->X1;
+      STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
+    }
 
     g.x = e->G; g.w = L.w2; g.scales = L.w2_scales; g.zeros = L.w2_zeros; g.bias = L.b2;
     g.residual = e->X1; g.y = e->A; g.N = H; g.K = F; g.epi = Epi::BiasResidual;

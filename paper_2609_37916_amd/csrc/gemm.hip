@@ -175,7 +175,12 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
           }
     }
     __syncthreads();
-    for (int idx = tid; idx < RB * CPR; idx += kThreads) {
+    // compile-time trip count: the bias and residual loads of all of a
+    // thread's chunks are issued together instead of one round trip each
+#pragma unroll
+    for (int it = 0; it < (RB * CPR + kThreads - 1) / kThreads; ++it) {
+      const int idx = tid + it * kThreads;
+      if (RB * CPR % kThreads != 0 && idx >= RB * CPR) continue;
       const int r = idx / CPR, cc = idx % CPR;
       const int m = m0 + rb * RB + r;
       if (m >= M) continue;
@@ -599,8 +604,241 @@ hipError_t launch_dma_tile(const GemmParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------------------
+// Dense bf16 kernel with the row LayerNorm of its input fused in front
+// ---------------------------------------------------------------------------
+//
+// Post-LN blocks feed LN(a) into the next projection.  A 64-row block of a
+// (K <= 512) fits in LDS whole, so the block loads its rows once, forms each
+// row's mean and variance (fp32, mean first, then the centred sum of squares,
+// as the LayerNorm kernel), writes the normalised bf16 values back in place,
+// and then streams only the weights through the stage ring.  The blocks of
+// column tile 0 also store the normalised rows (the residual of the next
+// block), so no separate LayerNorm pass over the activations remains.
+constexpr int kLnxStages = 2;
+
+template <int BN, int KC, Epi E>
+__global__ __launch_bounds__(kThreads) void gemm_lnx_kernel(GemmParams p) {
+  constexpr int BM = 64, WM = BM / 2, WN = BN / 2;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int WStage = BN * kRowBytes;
+  constexpr int WLps = BN / 32;           // weight DMAs per thread per stage (8 rows each per wave)
+  constexpr int ABlock = BM * kRowBytes;  // one 64-k block of the activation rows
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lnx_smem[];
+
+  int M = p.M;
+  if (p.m_dev) M = min(M, *p.m_dev);
+  const int n_tiles = p.N / BN;
+  const int live = n_tiles * ((M + BM - 1) / BM);
+  const int bid = blockIdx.x;
+  if (bid >= live) return;
+  const int q8 = live >> 3, r8 = live & 7, xcd = bid & 7;  // XCD-aware tile order, as gemm_dma_kernel
+  const int tile = xcd * q8 + min(xcd, r8) + (bid >> 3);
+  const int m0 = (tile / n_tiles) * BM;
+  const int n0 = (tile % n_tiles) * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int l32 = lane & 31, half = lane >> 5;
+  constexpr int K = 64 * KC, KT = KC;  // K = 64 * KC (p.K)
+  const size_t pitch = (size_t)K * 2;
+  uint8_t* a_lds = lnx_smem;                    // [KT][64 rows][128 B], swizzled like a stage
+  uint8_t* w_lds = lnx_smem + KT * ABlock;      // [kLnxStages][BN rows][128 B]
+  const uint32_t a0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)a_lds;
+  const uint32_t w0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)w_lds;
+
+  // All activation rows of the block: DMA g (0 .. 8*KT-1) fills rows 8(g%8)..+7
+  // of 64-k block g/8; wave w issues g = w, w+4, ... (2*KT per wave).
+  {
+    const int rl = lane >> 3;
+    for (int g = wave; g < 8 * KT; g += 4) {
+      const int kt = g >> 3, row = 8 * (g & 7) + rl;
+      const int c = swz(row, lane & 7);
+      const uint8_t* src = reinterpret_cast<const uint8_t*>(p.x) + (size_t)min(m0 + row, M - 1) * pitch + kt * 128 + c * 16;
+      lds_dma16(src, __builtin_amdgcn_readfirstlane(a0 + kt * ABlock + 8 * (g & 7) * kRowBytes));
+    }
+  }
+  const uint8_t* wsrc[WLps];
+#pragma unroll
+  for (int i = 0; i < WLps; ++i) {
+    const int row = wave * 8 + i * 32 + (lane >> 3);
+    wsrc[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row) * pitch + swz(row, lane & 7) * 16;
+  }
+  auto issue_w = [&](int kt, int buf) {
+#pragma unroll
+    for (int i = 0; i < WLps; ++i)
+      lds_dma16(wsrc[i] + (size_t)kt * kRowBytes,
+                __builtin_amdgcn_readfirstlane(w0 + buf * WStage + (wave * 8 + i * 32) * kRowBytes));
+  };
+#pragma unroll
+  for (int st = 0; st < kLnxStages - 1; ++st)
+    if (st < KT) issue_w(st, st);
+  // gamma and beta go to the last weight buffer, which the first DMA of the
+  // main loop fills only after the barrier that ends the normalisation
+  static_assert(kLnxStages >= 2 && 2 * 512 * 4 <= WStage, "gamma/beta staging");
+  float* gb_lds = reinterpret_cast<float*>(w_lds + (kLnxStages - 1) * WStage);  // [gamma K][beta K]
+  for (int i = tid; i < K; i += kThreads) {
+    gb_lds[i] = p.ln_gamma[i];
+    gb_lds[K + i] = p.ln_beta[i];
+  }
+  // the activation rows were issued first: they have landed once only the
+  // weight stages are outstanding
+  if (KT >= kLnxStages - 1) wait_vmcnt<(kLnxStages - 1) * WLps>();
+  else wait_vmcnt<0>();
+  __syncthreads();
+
+  // LayerNorm of the 64 rows in place: four threads per row, each holding a
+  // quarter of the row's 8-element chunks in registers.
+  {
+    constexpr int CPT = K / 32;  // chunks per thread
+    const int r = tid >> 2, qd = tid & 3;
+    uint4 raw[CPT];
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int cc = qd * CPT + j;  // 8-element chunk of the row
+      raw[j] = ld16(a_lds + (cc >> 3) * ABlock + r * kRowBytes + swz(r, cc & 7) * 16);
+    }
+    auto val = [&](int j, int e) {
+      const uint32_t w = e == 0 || e == 1 ? raw[j].x : e == 2 || e == 3 ? raw[j].y : e == 4 || e == 5 ? raw[j].z : raw[j].w;
+      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    };
+    float sum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sum += val(j, e);
+    sum += __shfl_xor(sum, 1, 64);
+    sum += __shfl_xor(sum, 2, 64);
+    const float mean = sum / (float)K;
+    float sq = 0.0f;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float c = val(j, e) - mean;
+        sq += c * c;
+      }
+    sq += __shfl_xor(sq, 1, 64);
+    sq += __shfl_xor(sq, 2, 64);
+    const float rstd = 1.0f / sqrtf(sq / (float)K + p.ln_eps);
+    const bool store_rows = p.ln_out != nullptr && n0 == 0 && m0 + r < M;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+      const int cc = qd * CPT + j, col = cc * 8;
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 8; e += 4) {
+        const float4 g = *reinterpret_cast<const float4*>(gb_lds + col + e);
+        const float4 b = *reinterpret_cast<const float4*>(gb_lds + K + col + e);
+        o[e] = (val(j, e) - mean) * rstd * g.x + b.x;
+        o[e + 1] = (val(j, e + 1) - mean) * rstd * g.y + b.y;
+        o[e + 2] = (val(j, e + 2) - mean) * rstd * g.z + b.z;
+        o[e + 3] = (val(j, e + 3) - mean) * rstd * g.w + b.w;
+      }
+      Vec16<bf16_t>::store(reinterpret_cast<bf16_t*>(a_lds + (cc >> 3) * ABlock + r * kRowBytes + swz(r, cc & 7) * 16), o);
+      if (store_rows) Vec16<bf16_t>::store(reinterpret_cast<bf16_t*>(p.ln_out) + (size_t)(m0 + r) * K + col, o);
+    }
+  }
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
+
+  for (int kt = 0; kt < KT; ++kt) {
+    wait_stage<WLps, kLnxStages - 2>(min(kLnxStages - 2, KT - 1 - kt));
+    __syncthreads();  // weight stage kt (and, at kt = 0, the normalised rows) visible; buffer kt-1 free
+    const uint8_t* xs = a_lds + kt * ABlock;
+    const uint8_t* ws = w_lds + (kt % kLnxStages) * WStage;
+    bf16x8_t af[4][TN], bfr[4][TM];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int r = wn * WN + tn * 32 + l32;
+        af[q][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
+      }
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        const int r = wm * WM + tm * 32 + l32;
+        bfr[q][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
+      }
+    }
+    if (kt + kLnxStages - 1 < KT) issue_w(kt + kLnxStages - 1, (kt + kLnxStages - 1) % kLnxStages);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+          acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q][tn], bfr[q][tm], acc[tm][tn], 0, 0, 0);
+  }
+  // the epilogue stages the tile through the block's LDS (K >= 256)
+  static_assert(BM * (BN * 4 + 16) <= 4 * ABlock + kLnxStages * WStage, "epilogue staging fits the LDS");
+  store_tile<BM, BN, bf16_t, Quant::None, E, TM, TN, 1>(acc, lnx_smem, p, m0, n0, M);
+}
+
+size_t lnx_lds_bytes(int K, int BN) { return (size_t)(K / 64) * 64 * kRowBytes + (size_t)kLnxStages * BN * kRowBytes; }
+
+template <int BN, int KC>
+hipError_t launch_lnx_k(const GemmParams& p, hipStream_t s) {
+  const dim3 grid((p.N / BN) * ((p.M + 63) / 64));
+  const size_t lds = lnx_lds_bytes(64 * KC, BN);
+  switch (p.epi) {
+    case Epi::None: hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::None>), grid, dim3(kThreads), lds, s, p); break;
+    case Epi::Bias: hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::Bias>), grid, dim3(kThreads), lds, s, p); break;
+    case Epi::BiasGelu:
+      hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::BiasGelu>), grid, dim3(kThreads), lds, s, p);
+      break;
+    case Epi::BiasResidual:
+      hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::BiasResidual>), grid, dim3(kThreads), lds, s, p);
+      break;
+  }
+  return hipGetLastError();
+}
+
+template <int BN>
+hipError_t launch_lnx(const GemmParams& p, hipStream_t s) {
+  switch (p.K) {
+    case 256: return launch_lnx_k<BN, 4>(p, s);
+    case 384: return launch_lnx_k<BN, 6>(p, s);
+    case 512: return launch_lnx_k<BN, 8>(p, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int BN, int KC>
+hipError_t lnx_attributes_k() {
+  const void* fns[4] = {reinterpret_cast<const void*>(gemm_lnx_kernel<BN, KC, Epi::None>),
+                        reinterpret_cast<const void*>(gemm_lnx_kernel<BN, KC, Epi::Bias>),
+                        reinterpret_cast<const void*>(gemm_lnx_kernel<BN, KC, Epi::BiasGelu>),
+                        reinterpret_cast<const void*>(gemm_lnx_kernel<BN, KC, Epi::BiasResidual>)};
+  for (const void* f : fns) {
+    const hipError_t e =
+        hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lnx_lds_bytes(64 * KC, BN));
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+template <int BN>
+hipError_t lnx_attributes() {
+  hipError_t e = lnx_attributes_k<BN, 4>();
+  if (e == hipSuccess) e = lnx_attributes_k<BN, 6>();
+  if (e == hipSuccess) e = lnx_attributes_k<BN, 8>();
+  return e;
+}
+
 template <typename T>
 hipError_t launch_dense(const GemmParams& p, hipStream_t s) {
+  if constexpr (sizeof(T) == 2) {
+    if (p.ln_gamma) return p.N % 128 == 0 ? launch_lnx<128>(p, s) : launch_lnx<64>(p, s);
+  }
   int tile = p.tile;
   if (tile == kTileAuto) {
     // measured at the encoder's shapes (2-4 k tokens): 64x64 for N = 384, 64x128
@@ -662,8 +900,21 @@ __global__ void dequant_unpack_kernel(const uint8_t* w, Quant q, const uint16_t*
 
 }  // namespace
 
+bool gemm_ln_input_supported(DType dt, Quant q, int K) {
+  return dt == DType::BF16 && q == Quant::None && (K == 256 || K == 384 || K == 512);
+}
+
+hipError_t gemm_init_attributes() {
+  static const hipError_t once = [] {
+    const hipError_t e = lnx_attributes<128>();
+    return e != hipSuccess ? e : lnx_attributes<64>();
+  }();
+  return once;
+}
+
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
+  if (p.ln_gamma && !gemm_ln_input_supported(p.dtype, p.quant, p.K)) return hipErrorInvalidValue;
   if (p.dtype == DType::F32) return launch_dense<float>(p, s);
   switch (p.quant) {
     case Quant::None: return launch_dense<bf16_t>(p, s);

@@ -27,7 +27,17 @@ struct GemmParams {
   int tile;              // 0: choose automatically; otherwise a GemmTile value (tuning)
   int x_head_rows;       // 0: x is row-major [M,K]; > 0: x is head-major [K/32][x_head_rows][32]
                          // (dense bf16 only), as written by the fused attention
+  // Optional LayerNorm of the activation rows before the product (dense bf16,
+  // K <= 512): the kernel multiplies LN(x) * ln_gamma + ln_beta, and when
+  // ln_out is set also stores those normalised rows there ([M,K]).
+  const float* ln_gamma;
+  const float* ln_beta;
+  float ln_eps;
+  void* ln_out;
 };
+// True when launch_gemm can normalise the activation rows in the kernel.
+bool gemm_ln_input_supported(DType dt, Quant q, int K);
+hipError_t gemm_init_attributes();  // once per process, outside graph capture
 enum GemmTile : int { kTileAuto = 0, kTile128x128 = 1, kTile64x128 = 2, kTile64x64 = 3, kTile128x64 = 4 };
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 

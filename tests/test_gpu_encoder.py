@@ -162,7 +162,9 @@ def test_encoder_profile_mode(rlx, name, attn_kernel):
     enc.forward(inputs["input"], inputs["mask"])
     enc.forward(inputs["input"], inputs["mask"])
     prof = enc.profile_read()
-    assert prof["gemm_ffn_up"][0] == 12 and prof[attn_kernel][0] == 12 and prof["mask_scan"][0] == 2
+    up = "gemm_ffn_up_ln" if name.endswith("bf16") else "gemm_ffn_up"  # bf16 normalises the FFN-up input in the GEMM
+    assert prof[up][0] == 12 and prof[attn_kernel][0] == 12 and prof["mask_scan"][0] == 2
+    assert ("layer_norm_1" in prof) == (up == "gemm_ffn_up")
     assert all(ms >= 0 for _, ms in prof.values())
     enc.set_profiling(False)
     enc.close()
