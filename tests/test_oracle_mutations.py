@@ -1,0 +1,244 @@
+"""The oracle's pins are strong enough to catch plausible mistakes.
+
+Each case plants one mistake in the CPU oracle (a dropped term, a wrong sign,
+an off-by-one mask, a transposed operand, a swapped nibble ...), runs every pin
+of tests/test_oracle_pins.py against the mutated oracle and requires that at
+least one pin fails.  Mistakes are planted on the CPU only, by patching the
+oracle's module attributes for the duration of one case.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import oracle.encoder as enc
+import oracle.quant as qnt
+import test_oracle_pins as pins
+
+_f64 = enc._f64
+# the unmutated functions, for mutants that wrap them
+ORIG = {n: getattr(enc, n) for n in ("layer_norm", "gelu", "linear", "visible_keys", "attention_probs",
+                                     "masked_attention", "embed", "encoder_layer", "mean_pool_l2")}
+ORIG.update({n: getattr(qnt, n) for n in ("unpack_int4", "dequant_int4", "dequant_int8")})
+
+
+def _pin_calls():
+    calls = [
+        pins.test_linear_matches_brute_force_nonsquare,
+        pins.test_linear_identity_weight_closed_form,
+        pins.test_gelu_closed_forms,
+        pins.test_layer_norm_moments_and_constant_rows,
+        pins.test_attention_probs_rows_sum_to_one_and_masked_keys_zero,
+        pins.test_attention_padding_extension_invariance,
+        pins.test_attention_identical_keys_gives_mean_of_values,
+        pins.test_attention_single_valid_key_and_empty_rows,
+        pins.test_pooling_unit_norm_and_special_cases,
+        pins.test_embed_brute_force,
+        pins.test_encoder_layer_matches_brute_force_tiny,
+        pins.test_encoder_padding_extension_invariance,
+        pins.test_unpack_int4_matches_bit_loop,
+        pins.test_int4_dequant_bit_loop_and_round_trip,
+        pins.test_int8_dequant_round_trip,
+    ]
+    for kind, window in [(oracle.MASK_NONE, 0), (oracle.MASK_CUSTOM, 0), (oracle.MASK_CAUSAL, 0),
+                         (oracle.MASK_SLIDING_WINDOW, 1), (oracle.MASK_SLIDING_WINDOW, 3)]:
+        calls.append(lambda kind=kind, window=window: pins.test_attention_matches_brute_force(kind, window))
+    return calls
+
+
+# --- planted mistakes (each returns a replacement for one oracle function) ---
+
+def ln_unbiased_variance(x, gamma, beta, eps):
+    x = _f64(x)
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).sum(axis=-1, keepdims=True) / (x.shape[-1] - 1)
+    return (x - mu) / np.sqrt(var + eps) * _f64(gamma) + _f64(beta)
+
+
+def ln_eps_outside_sqrt(x, gamma, beta, eps):
+    x = _f64(x)
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
+    return (x - mu) / (np.sqrt(var) + eps) * _f64(gamma) + _f64(beta)
+
+
+def ln_no_beta(x, gamma, beta, eps):
+    x = _f64(x)
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + eps) * _f64(gamma)
+
+
+def gelu_tanh(x):
+    x = _f64(x)
+    return 0.5 * x * (1.0 + np.tanh(math.sqrt(2.0 / math.pi) * (x + 0.044715 * x ** 3)))
+
+
+def gelu_no_sqrt2(x):
+    from scipy.special import erf
+    x = _f64(x)
+    return 0.5 * x * (1.0 + erf(x))
+
+
+def linear_no_bias(x, w, b=None):
+    return _f64(x) @ _f64(w).T
+
+
+def linear_untransposed(x, w, b=None):
+    y = _f64(x) @ _f64(w)
+    return y if b is None else y + _f64(b)
+
+
+def vis_causal_strict(S, kind, key_mask_row=None, window=0):
+    i, j = np.arange(S)[:, None], np.arange(S)[None, :]
+    vis = ORIG["visible_keys"](S, kind, key_mask_row, window)
+    if kind == oracle.MASK_CAUSAL:
+        vis = vis & (j < i)
+    return vis
+
+
+def vis_window_inclusive(S, kind, key_mask_row=None, window=0):
+    i, j = np.arange(S)[:, None], np.arange(S)[None, :]
+    vis = ORIG["visible_keys"](S, kind, key_mask_row, window)
+    if kind == oracle.MASK_SLIDING_WINDOW:
+        vis = (j <= i) & (j >= i - window)
+        if key_mask_row is not None:
+            vis = vis & (np.asarray(key_mask_row)[None, :] != 0)
+    return vis
+
+
+def vis_key_mask_ignored(S, kind, key_mask_row=None, window=0):
+    return ORIG["visible_keys"](S, oracle.MASK_NONE if kind == oracle.MASK_CUSTOM else kind, None, window)
+
+
+def probs_no_scale(q, k, vis, scale):
+    return ORIG["attention_probs"](q, k, vis, 1.0)
+
+
+def probs_softmax_over_queries(q, k, vis, scale):
+    s = scale * (_f64(q) @ _f64(k).T)
+    s = np.where(vis, s, -np.inf)
+    with np.errstate(invalid="ignore"):  # columns no query sees
+        e = np.exp(s - s.max(axis=0, keepdims=True))
+    e = np.where(vis, e, 0.0)
+    tot = e.sum(axis=0, keepdims=True)
+    return np.divide(e, tot, out=np.zeros_like(e), where=tot > 0)
+
+
+def attention_heads_mixed(q, k, v, kind=oracle.MASK_CUSTOM, key_mask=None, window=0, scale=None):
+    k = np.roll(_f64(k), 1, axis=2)  # head h attends with head h-1's keys
+    return ORIG["masked_attention"](q, k, v, kind, key_mask, window, scale)
+
+
+def pool_l1_norm(x, mask):
+    # (dividing the sum by S instead of the token count is no mistake here: the
+    # L2 normalisation removes any positive scale)
+    x = _f64(x)
+    m = _f64(mask)[:, :, None]
+    e = (x * m).sum(axis=1) / np.maximum(m.sum(axis=1), 1e-9)
+    n = np.abs(e).sum(axis=1, keepdims=True)
+    return e / np.maximum(n, 1e-12)
+
+
+def pool_mask_ignored(x, mask):
+    return ORIG["mean_pool_l2"](x, np.ones_like(np.asarray(mask)))
+
+
+def embed_pos_off_by_one(ids, word, pos, typ, gamma, beta, eps):
+    ids = np.asarray(ids)
+    B, S = ids.shape
+    x = _f64(word)[ids] + _f64(pos)[np.arange(1, S + 1)][None] + _f64(typ)[0][None, None]
+    return enc.layer_norm(x, gamma, beta, eps)
+
+
+def embed_type_one(ids, word, pos, typ, gamma, beta, eps):
+    ids = np.asarray(ids)
+    B, S = ids.shape
+    x = _f64(word)[ids] + _f64(pos)[np.arange(S)][None] + _f64(typ)[1][None, None]
+    return enc.layer_norm(x, gamma, beta, eps)
+
+
+def layer_pre_ln(x, mask, lw, heads, eps):
+    x = _f64(x)
+    B, S, H = x.shape
+    d = H // heads
+    h = enc.layer_norm(x, lw["ln1_g"], lw["ln1_b"], eps)
+    qkv = enc.linear(h, lw["wqkv"], lw["bqkv"])
+    q, k, v = (qkv[..., i * H:(i + 1) * H].reshape(B, S, heads, d) for i in range(3))
+    ctx = enc.masked_attention(q, k, v, oracle.MASK_CUSTOM, mask, 0, 1.0 / math.sqrt(d)).reshape(B, S, H)
+    x1 = x + enc.linear(ctx, lw["wo"], lw["bo"])
+    g = enc.gelu(enc.linear(enc.layer_norm(x1, lw["ln2_g"], lw["ln2_b"], eps), lw["w1"], lw["b1"]))
+    return x1 + enc.linear(g, lw["w2"], lw["b2"])
+
+
+def layer_no_ffn_residual(x, mask, lw, heads, eps):
+    x = _f64(x)
+    B, S, H = x.shape
+    d = H // heads
+    qkv = enc.linear(x, lw["wqkv"], lw["bqkv"])
+    q, k, v = (qkv[..., i * H:(i + 1) * H].reshape(B, S, heads, d) for i in range(3))
+    ctx = enc.masked_attention(q, k, v, oracle.MASK_CUSTOM, mask, 0, 1.0 / math.sqrt(d)).reshape(B, S, H)
+    x1 = enc.layer_norm(enc.linear(ctx, lw["wo"], lw["bo"]) + x, lw["ln1_g"], lw["ln1_b"], eps)
+    g = enc.gelu(enc.linear(x1, lw["w1"], lw["b1"]))
+    return enc.layer_norm(enc.linear(g, lw["w2"], lw["b2"]), lw["ln2_g"], lw["ln2_b"], eps)
+
+
+def unpack_high_nibble_first(packed):
+    p = np.asarray(packed, dtype=np.uint8)
+    n, kh = p.shape
+    q = np.empty((n, 2 * kh), dtype=np.uint8)
+    q[:, 0::2] = p >> 4
+    q[:, 1::2] = p & 0x0F
+    return q
+
+
+def int4_zero_ignored(packed, scales, zeros, group):
+    return ORIG["dequant_int4"](packed, scales, np.zeros_like(np.asarray(zeros)), group)
+
+
+def int8_scale_ignored(q, scales):
+    return np.asarray(q, dtype=np.int8).astype(np.float64)
+
+
+MUTANTS = {
+    "layer_norm: unbiased variance": ("layer_norm", ln_unbiased_variance),
+    "layer_norm: eps outside the square root": ("layer_norm", ln_eps_outside_sqrt),
+    "layer_norm: beta dropped": ("layer_norm", ln_no_beta),
+    "gelu: tanh approximation": ("gelu", gelu_tanh),
+    "gelu: erf(x) instead of erf(x/sqrt 2)": ("gelu", gelu_no_sqrt2),
+    "linear: bias dropped": ("linear", linear_no_bias),
+    "linear: weight not transposed": ("linear", linear_untransposed),
+    "mask: causal excludes the diagonal": ("visible_keys", vis_causal_strict),
+    "mask: sliding window one key too wide": ("visible_keys", vis_window_inclusive),
+    "mask: key mask ignored": ("visible_keys", vis_key_mask_ignored),
+    "attention: scale dropped": ("attention_probs", probs_no_scale),
+    "attention: softmax over queries": ("attention_probs", probs_softmax_over_queries),
+    "attention: keys of the wrong head": ("masked_attention", attention_heads_mixed),
+    "pooling: L1 instead of L2 normalisation": ("mean_pool_l2", pool_l1_norm),
+    "pooling: mask ignored": ("mean_pool_l2", pool_mask_ignored),
+    "embed: positions shifted by one": ("embed", embed_pos_off_by_one),
+    "embed: token type 1": ("embed", embed_type_one),
+    "layer: pre-LN instead of post-LN": ("encoder_layer", layer_pre_ln),
+    "layer: FFN residual dropped": ("encoder_layer", layer_no_ffn_residual),
+    "int4: high nibble first": ("unpack_int4", unpack_high_nibble_first),
+    "int4: zero-point ignored": ("dequant_int4", int4_zero_ignored),
+    "int8: scale ignored": ("dequant_int8", int8_scale_ignored),
+}
+
+
+@pytest.mark.parametrize("name", list(MUTANTS))
+def test_planted_mistake_fails_a_pin(name, monkeypatch):
+    attr, fake = MUTANTS[name]
+    home = qnt if attr in ("unpack_int4", "dequant_int4", "dequant_int8") else enc
+    monkeypatch.setattr(home, attr, fake)
+    monkeypatch.setattr(oracle, attr, fake)
+    if home is qnt and hasattr(enc, attr):
+        monkeypatch.setattr(enc, attr, fake)  # the encoder module holds its own binding
+    failed = []
+    for call in _pin_calls():
+        try:
+            call()
+        except Exception as e:  # an assertion, or a shape error from the planted mistake
+            failed.append(type(e).__name__)
+    assert failed, f"no pin caught the planted mistake '{name}'"
