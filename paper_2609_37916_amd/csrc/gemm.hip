@@ -49,6 +49,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kRowBytes = 128;            // bytes of one operand row per K stage
 constexpr int kLdsRow = kRowBytes + 16;   // padded LDS row pitch in bytes
+constexpr int BK_BF16 = kRowBytes / 2;   // bf16 K elements per stage
 
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ void st16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
@@ -143,17 +144,24 @@ template <> struct OutVec<float> {
 // residual and output all move as coalesced 16-byte vectors.  (Storing straight
 // from the MFMA layout spreads each wave's store over 32 rows, 16 bytes per
 // row, and runs several times slower.)
-template <int BM, int BN, typename T, Quant Q, Epi E, int TM, int TN, int NRB>
+// KS > 1: the block's 4*KS waves form KS groups that each accumulated a share
+// of the K range for the same 64-row tile layout; the staging sums the groups'
+// partials (group 0 writes, the others add in turn) before the epilogue, which
+// then runs on all 256*KS threads.
+template <int BM, int BN, typename T, Quant Q, Epi E, int TM, int TN, int NRB, int KS = 1>
 __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_t* lds, const GemmParams& p, int m0,
                                            int n0, int M) {
   static_assert(NRB == 1 || NRB == 2, "row blocks follow the 2 wave rows");
+  static_assert(KS == 1 || NRB == 1, "split-K tiles stage all rows at once");
+  constexpr int NT = kThreads * KS;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int PITCH = BN * 4 + 16;  // bytes; 16 rows of a column land on distinct banks
   constexpr int EPC = 16 / (int)sizeof(T);
   constexpr int CPR = BN / EPC;
   constexpr int RB = BM / NRB;        // rows staged at a time
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, half = lane >> 5;
+  const int kg = wave >> 2;  // K group
+  const int wm = (wave & 3) >> 1, wn = wave & 1, l32 = lane & 31, half = lane >> 5;
   const int N = p.N;
   T* y = reinterpret_cast<T*>(p.y);
   const T* res = reinterpret_cast<const T*>(p.residual);
@@ -161,26 +169,36 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
     __syncthreads();  // the operand stages (or the previous row block) are no longer read
-    if (NRB == 1 || wm == rb) {
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
+    for (int g = 0; g < KS; ++g) {
+      if (g > 0) __syncthreads();  // the previous group's partial is in place
+      if (kg == g && (NRB == 1 || wm == rb)) {
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn)
+        for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = wm * WM + tm * 32 + l32 - rb * RB;
-            const int c = wn * WN + tn * 32 + 8 * i + 4 * half;
-            *reinterpret_cast<float4*>(lds + r * PITCH + c * 4) = make_float4(
-                acc[tm][tn][4 * i], acc[tm][tn][4 * i + 1], acc[tm][tn][4 * i + 2], acc[tm][tn][4 * i + 3]);
-          }
+          for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int r = wm * WM + tm * 32 + l32 - rb * RB;
+              const int c = wn * WN + tn * 32 + 8 * i + 4 * half;
+              float4* dst = reinterpret_cast<float4*>(lds + r * PITCH + c * 4);
+              float4 v = make_float4(acc[tm][tn][4 * i], acc[tm][tn][4 * i + 1], acc[tm][tn][4 * i + 2],
+                                     acc[tm][tn][4 * i + 3]);
+              if (g > 0) {
+                const float4 o = *dst;
+                v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+              }
+              *dst = v;
+            }
+      }
     }
     __syncthreads();
     // compile-time trip count: the bias and residual loads of all of a
     // thread's chunks are issued together instead of one round trip each
 #pragma unroll
-    for (int it = 0; it < (RB * CPR + kThreads - 1) / kThreads; ++it) {
-      const int idx = tid + it * kThreads;
-      if (RB * CPR % kThreads != 0 && idx >= RB * CPR) continue;
+    for (int it = 0; it < (RB * CPR + NT - 1) / NT; ++it) {
+      const int idx = tid + it * NT;
+      if (RB * CPR % NT != 0 && idx >= RB * CPR) continue;
       const int r = idx / CPR, cc = idx % CPR;
       const int m = m0 + rb * RB + r;
       if (m >= M) continue;
@@ -421,16 +439,22 @@ __device__ __forceinline__ void wait_stage(int ahead) {
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-template <int BM, int BN, int STAGES, typename T, Epi E>
-__global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
+// KS > 1 (bf16): 4*KS waves; wave group g multiplies chunks [g*CH/KS, (g+1)*CH/KS)
+// of every stage into its own accumulators, summed in the epilogue.  With one
+// block per CU this gives each SIMD KS waves to interleave.
+template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1>
+__global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   static_assert(BM % 64 == 0 && BN % 64 == 0 && STAGES >= 2 && STAGES <= 6, "tile");
+  static_assert(KS == 1 || (sizeof(T) == 2 && (BK_BF16 / 16) % KS == 0), "K split over bf16 chunks");
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int ES = sizeof(T);
   constexpr int BK = kRowBytes / ES;
   constexpr int CH = BK / 16;
+  constexpr int NW = 4 * KS;            // waves
   constexpr int kStage = (BM + BN) * kRowBytes;
-  constexpr int LPS = (BM + BN) / 32;   // DMA instructions per thread per stage (8 rows each per wave)
+  constexpr int LPS = (BM + BN) / (8 * NW);  // DMA instructions per thread per stage (8 rows each per wave)
+  static_assert((BM + BN) % (8 * NW) == 0, "DMA rows split evenly over the waves");
   static_assert((STAGES - 2) * LPS < 64, "vmcnt range");
 
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * kStage];
@@ -450,7 +474,8 @@ __global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int kg = wave >> 2;  // K group (KS > 1)
+  const int wm = (wave & 3) >> 1, wn = wave & 1;
   const int l32 = lane & 31, half = lane >> 5;
   const int K = p.K;
   const int KT = K / BK;
@@ -468,7 +493,7 @@ __global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
   bool is_x[LPS];
 #pragma unroll
   for (int i = 0; i < LPS; ++i) {
-    const int row = wave * 8 + i * 32 + (lane >> 3);
+    const int row = wave * 8 + i * 8 * NW + (lane >> 3);
     const int c = swz(row, lane & 7);
     is_x[i] = row < BM;
     if (row < BM) {
@@ -484,7 +509,7 @@ __global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
   auto issue = [&](int kt, int buf) {
 #pragma unroll
     for (int i = 0; i < LPS; ++i) {
-      const uint32_t la = lds0 + buf * kStage + (wave * 8 + i * 32) * kRowBytes;
+      const uint32_t la = lds0 + buf * kStage + (wave * 8 + i * 8 * NW) * kRowBytes;
       lds_dma16(src[i] + (size_t)kt * (is_x[i] ? x_stage : (size_t)kRowBytes), __builtin_amdgcn_readfirstlane(la));
     }
   };
@@ -516,18 +541,20 @@ __global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
           // so the LDS latency is paid once per stage.  The scheduling barrier
           // keeps the compiler from sinking each read next to its MFMA (with a
           // full wait in between), which exposes the latency once per chunk.
-          bf16x8_t af[CH][TN], bfr[CH][TM];
+          constexpr int CG = CH / KS;  // chunks of this wave's K group
+          bf16x8_t af[CG][TN], bfr[CG][TM];
 #pragma unroll
-          for (int q = 0; q < CH; ++q) {
+          for (int qq = 0; qq < CG; ++qq) {
+            const int q = kg * CG + qq;
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) {
               const int r = wn * WN + tn * 32 + l32;
-              af[q][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
+              af[qq][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
             }
 #pragma unroll
             for (int tm = 0; tm < TM; ++tm) {
               const int r = wm * WM + tm * 32 + l32;
-              bfr[q][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
+              bfr[qq][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
             }
           }
           // the next stage's DMA goes out after the reads: its issue can stall
@@ -535,12 +562,12 @@ __global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
           if (prefetch) issue(kt + STAGES - 1, (u + STAGES - 1) % STAGES);
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int q = 0; q < CH; ++q)
+          for (int qq = 0; qq < CG; ++qq)
 #pragma unroll
             for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
               for (int tn = 0; tn < TN; ++tn)
-                acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q][tn], bfr[q][tm], acc[tm][tn], 0, 0, 0);
+                acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[qq][tn], bfr[qq][tm], acc[tm][tn], 0, 0, 0);
         } else {
           if (prefetch) issue(kt + STAGES - 1, (u + STAGES - 1) % STAGES);
 #pragma unroll
@@ -581,24 +608,24 @@ __global__ __launch_bounds__(kThreads) void gemm_dma_kernel(GemmParams p) {
 
   constexpr int NRB = BM * (BN * 4 + 16) <= (int)sizeof(smem) ? 1 : 2;
   static_assert(BM / NRB * (BN * 4 + 16) <= (int)sizeof(smem), "epilogue row block fits the stage memory");
-  store_tile<BM, BN, T, Quant::None, E, TM, TN, NRB>(acc, smem, p, m0, n0, M);
+  store_tile<BM, BN, T, Quant::None, E, TM, TN, NRB, KS>(acc, smem, p, m0, n0, M);
 }
 
-template <int BM, int BN, int STAGES, typename T>
+template <int BM, int BN, int STAGES, typename T, int KS = 1>
 hipError_t launch_dma_tile(const GemmParams& p, hipStream_t s) {
   const dim3 grid((p.N / BN) * ((p.M + BM - 1) / BM));
   switch (p.epi) {
     case Epi::None:
-      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::None>), grid, dim3(kThreads), 0, s, p);
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::None, KS>), grid, dim3(kThreads * KS), 0, s, p);
       break;
     case Epi::Bias:
-      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::Bias>), grid, dim3(kThreads), 0, s, p);
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::Bias, KS>), grid, dim3(kThreads * KS), 0, s, p);
       break;
     case Epi::BiasGelu:
-      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::BiasGelu>), grid, dim3(kThreads), 0, s, p);
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::BiasGelu, KS>), grid, dim3(kThreads * KS), 0, s, p);
       break;
     case Epi::BiasResidual:
-      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::BiasResidual>), grid, dim3(kThreads), 0, s, p);
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::BiasResidual, KS>), grid, dim3(kThreads * KS), 0, s, p);
       break;
   }
   return hipGetLastError();
@@ -853,7 +880,9 @@ hipError_t launch_dense(const GemmParams& p, hipStream_t s) {
     case kTile128x128: return launch_dma_tile<128, 128, 2, T>(p, s);
     case kTile64x128: return launch_dma_tile<64, 128, 3, T>(p, s);
     case kTile128x64: return launch_dma_tile<128, 64, 3, T>(p, s);
-    default: return launch_dma_tile<64, 64, 3, T>(p, s);  // three stages: measured faster than four at N = 384
+    // 64 x 64: one block per CU at the encoder's N = 384 shapes, so bf16 splits
+    // each stage's K between two groups of four waves (eight waves per CU)
+    default: return launch_dma_tile<64, 64, 3, T, sizeof(T) == 2 ? 2 : 1>(p, s);
   }
 }
 
