@@ -644,13 +644,16 @@ hipError_t launch_dma_tile(const GemmParams& p, hipStream_t s) {
 // column tile 0 also store the normalised rows (the residual of the next
 // block), so no separate LayerNorm pass over the activations remains.
 constexpr int kLnxStages = 2;
+constexpr int kLnxKs = 2;  // wave groups splitting each stage's K (two blocks of eight waves per CU)
 
 template <int BN, int KC, Epi E>
-__global__ __launch_bounds__(kThreads) void gemm_lnx_kernel(GemmParams p) {
+__global__ __launch_bounds__(kThreads * kLnxKs) void gemm_lnx_kernel(GemmParams p) {
   constexpr int BM = 64, WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int NW = 4 * kLnxKs, NT = kThreads * kLnxKs;  // waves / threads: kLnxKs groups of four waves
   constexpr int WStage = BN * kRowBytes;
-  constexpr int WLps = BN / 32;           // weight DMAs per thread per stage (8 rows each per wave)
+  constexpr int WLps = BN / (8 * NW);     // weight DMAs per thread per stage (8 rows each per wave)
+  static_assert(BN % (8 * NW) == 0, "weight rows split evenly over the waves");
   constexpr int ABlock = BM * kRowBytes;  // one 64-k block of the activation rows
   extern __shared__ __attribute__((aligned(1024))) uint8_t lnx_smem[];
 
@@ -666,7 +669,8 @@ __global__ __launch_bounds__(kThreads) void gemm_lnx_kernel(GemmParams p) {
   const int n0 = (tile % n_tiles) * BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int kg = wave >> 2;  // K group: multiplies chunks [kg*CG, (kg+1)*CG) of every stage
+  const int wm = (wave & 3) >> 1, wn = wave & 1;
   const int l32 = lane & 31, half = lane >> 5;
   constexpr int K = 64 * KC, KT = KC;  // K = 64 * KC (p.K)
   const size_t pitch = (size_t)K * 2;
@@ -676,50 +680,56 @@ __global__ __launch_bounds__(kThreads) void gemm_lnx_kernel(GemmParams p) {
   const uint32_t w0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)w_lds;
 
   // All activation rows of the block: DMA g (0 .. 8*KT-1) fills rows 8(g%8)..+7
-  // of 64-k block g/8; wave w issues g = w, w+4, ... (2*KT per wave).
+  // of 64-k block g/8; wave w issues g = w, w+NW, ...
   {
     const int rl = lane >> 3;
-    for (int g = wave; g < 8 * KT; g += 4) {
+    for (int g = wave; g < 8 * KT; g += NW) {
       const int kt = g >> 3, row = 8 * (g & 7) + rl;
       const int c = swz(row, lane & 7);
       const uint8_t* src = reinterpret_cast<const uint8_t*>(p.x) + (size_t)min(m0 + row, M - 1) * pitch + kt * 128 + c * 16;
       lds_dma16(src, __builtin_amdgcn_readfirstlane(a0 + kt * ABlock + 8 * (g & 7) * kRowBytes));
     }
   }
+  // gamma and beta go by DMA too (a plain load would make the compiler wait for
+  // every outstanding DMA before its LDS store), into the last weight buffer,
+  // which the main loop fills only after the barrier that ends the
+  // normalisation: DMA w < 8K/1024 carries bytes [1024w, 1024w+1024) of
+  // [gamma (4K bytes); beta (4K bytes)].
+  static_assert(kLnxStages >= 2 && 2 * 512 * 4 <= WStage && 8 * K / 1024 <= NW, "gamma/beta staging");
+  float* gb_lds = reinterpret_cast<float*>(w_lds + (kLnxStages - 1) * WStage);  // [gamma K][beta K]
+  if (wave < 8 * K / 1024) {
+    const int o = wave * 1024 + lane * 16;
+    const uint8_t* src = o < 4 * K ? reinterpret_cast<const uint8_t*>(p.ln_gamma) + o
+                                   : reinterpret_cast<const uint8_t*>(p.ln_beta) + (o - 4 * K);
+    lds_dma16(src, __builtin_amdgcn_readfirstlane(w0 + (kLnxStages - 1) * WStage + wave * 1024));
+  }
   const uint8_t* wsrc[WLps];
 #pragma unroll
   for (int i = 0; i < WLps; ++i) {
-    const int row = wave * 8 + i * 32 + (lane >> 3);
+    const int row = wave * 8 + i * 8 * NW + (lane >> 3);
     wsrc[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row) * pitch + swz(row, lane & 7) * 16;
   }
   auto issue_w = [&](int kt, int buf) {
 #pragma unroll
     for (int i = 0; i < WLps; ++i)
       lds_dma16(wsrc[i] + (size_t)kt * kRowBytes,
-                __builtin_amdgcn_readfirstlane(w0 + buf * WStage + (wave * 8 + i * 32) * kRowBytes));
+                __builtin_amdgcn_readfirstlane(w0 + buf * WStage + (wave * 8 + i * 8 * NW) * kRowBytes));
   };
 #pragma unroll
   for (int st = 0; st < kLnxStages - 1; ++st)
     if (st < KT) issue_w(st, st);
-  // gamma and beta go to the last weight buffer, which the first DMA of the
-  // main loop fills only after the barrier that ends the normalisation
-  static_assert(kLnxStages >= 2 && 2 * 512 * 4 <= WStage, "gamma/beta staging");
-  float* gb_lds = reinterpret_cast<float*>(w_lds + (kLnxStages - 1) * WStage);  // [gamma K][beta K]
-  for (int i = tid; i < K; i += kThreads) {
-    gb_lds[i] = p.ln_gamma[i];
-    gb_lds[K + i] = p.ln_beta[i];
-  }
-  // the activation rows were issued first: they have landed once only the
-  // weight stages are outstanding
+  // the activation rows and gamma/beta were issued first: they have landed
+  // once only the weight stages are outstanding
   if (KT >= kLnxStages - 1) wait_vmcnt<(kLnxStages - 1) * WLps>();
   else wait_vmcnt<0>();
   __syncthreads();
 
-  // LayerNorm of the 64 rows in place: four threads per row, each holding a
-  // quarter of the row's 8-element chunks in registers.
+  // LayerNorm of the 64 rows in place: NT/64 threads per row, each holding its
+  // share of the row's 8-element chunks in registers.
   {
-    constexpr int CPT = K / 32;  // chunks per thread
-    const int r = tid >> 2, qd = tid & 3;
+    constexpr int TPR = NT / 64;      // threads per row
+    constexpr int CPT = K / 8 / TPR;  // chunks per thread
+    const int r = tid / TPR, qd = tid % TPR;
     uint4 raw[CPT];
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
@@ -735,8 +745,8 @@ __global__ __launch_bounds__(kThreads) void gemm_lnx_kernel(GemmParams p) {
     for (int j = 0; j < CPT; ++j)
 #pragma unroll
       for (int e = 0; e < 8; ++e) sum += val(j, e);
-    sum += __shfl_xor(sum, 1, 64);
-    sum += __shfl_xor(sum, 2, 64);
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) sum += __shfl_xor(sum, o, 64);
     const float mean = sum / (float)K;
     float sq = 0.0f;
 #pragma unroll
@@ -746,8 +756,8 @@ __global__ __launch_bounds__(kThreads) void gemm_lnx_kernel(GemmParams p) {
         const float c = val(j, e) - mean;
         sq += c * c;
       }
-    sq += __shfl_xor(sq, 1, 64);
-    sq += __shfl_xor(sq, 2, 64);
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) sq += __shfl_xor(sq, o, 64);
     const float rstd = 1.0f / sqrtf(sq / (float)K + p.ln_eps);
     const bool store_rows = p.ln_out != nullptr && n0 == 0 && m0 + r < M;
 #pragma unroll
@@ -781,33 +791,35 @@ __global__ __launch_bounds__(kThreads) void gemm_lnx_kernel(GemmParams p) {
     __syncthreads();  // weight stage kt (and, at kt = 0, the normalised rows) visible; buffer kt-1 free
     const uint8_t* xs = a_lds + kt * ABlock;
     const uint8_t* ws = w_lds + (kt % kLnxStages) * WStage;
-    bf16x8_t af[4][TN], bfr[4][TM];
+    constexpr int CG = 4 / kLnxKs;  // 16-k chunks of this wave's K group
+    bf16x8_t af[CG][TN], bfr[CG][TM];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int qq = 0; qq < CG; ++qq) {
+      const int q = kg * CG + qq;
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int r = wn * WN + tn * 32 + l32;
-        af[q][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
+        af[qq][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
       }
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) {
         const int r = wm * WM + tm * 32 + l32;
-        bfr[q][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
+        bfr[qq][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
       }
     }
     if (kt + kLnxStages - 1 < KT) issue_w(kt + kLnxStages - 1, (kt + kLnxStages - 1) % kLnxStages);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+    for (int qq = 0; qq < CG; ++qq)
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn)
-          acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q][tn], bfr[q][tm], acc[tm][tn], 0, 0, 0);
+          acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[qq][tn], bfr[qq][tm], acc[tm][tn], 0, 0, 0);
   }
   // the epilogue stages the tile through the block's LDS (K >= 256)
   static_assert(BM * (BN * 4 + 16) <= 4 * ABlock + kLnxStages * WStage, "epilogue staging fits the LDS");
-  store_tile<BM, BN, bf16_t, Quant::None, E, TM, TN, 1>(acc, lnx_smem, p, m0, n0, M);
+  store_tile<BM, BN, bf16_t, Quant::None, E, TM, TN, 1, kLnxKs>(acc, lnx_smem, p, m0, n0, M);
 }
 
 size_t lnx_lds_bytes(int K, int BN) { return (size_t)(K / 64) * 64 * kRowBytes + (size_t)kLnxStages * BN * kRowBytes; }
@@ -817,13 +829,13 @@ hipError_t launch_lnx_k(const GemmParams& p, hipStream_t s) {
   const dim3 grid((p.N / BN) * ((p.M + 63) / 64));
   const size_t lds = lnx_lds_bytes(64 * KC, BN);
   switch (p.epi) {
-    case Epi::None: hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::None>), grid, dim3(kThreads), lds, s, p); break;
-    case Epi::Bias: hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::Bias>), grid, dim3(kThreads), lds, s, p); break;
+    case Epi::None: hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::None>), grid, dim3(kThreads * kLnxKs), lds, s, p); break;
+    case Epi::Bias: hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::Bias>), grid, dim3(kThreads * kLnxKs), lds, s, p); break;
     case Epi::BiasGelu:
-      hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::BiasGelu>), grid, dim3(kThreads), lds, s, p);
+      hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::BiasGelu>), grid, dim3(kThreads * kLnxKs), lds, s, p);
       break;
     case Epi::BiasResidual:
-      hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::BiasResidual>), grid, dim3(kThreads), lds, s, p);
+      hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::BiasResidual>), grid, dim3(kThreads * kLnxKs), lds, s, p);
       break;
   }
   return hipGetLastError();
