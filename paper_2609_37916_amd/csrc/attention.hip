@@ -328,7 +328,9 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   static_assert(STAGES * kFStage >= kFOutOff + 4 * 2048, "K/V and output staging reuse the stage memory");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * kFStage];
   __shared__ float bias_lds[kFwRows];
-  const int h = blockIdx.x, b = blockIdx.y;
+  // blocks run sequence by sequence (all heads of one together), longest
+  // sequences first when an order is given, so those get a CU to themselves
+  const int h = blockIdx.x, b = p.seq_order ? p.seq_order[blockIdx.y] : blockIdx.y;
   const int row0 = p.cu_seqlens[b];
   const int L = p.cu_seqlens[b + 1] - row0;
   if (L <= 0) return;

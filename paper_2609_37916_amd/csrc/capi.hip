@@ -169,6 +169,7 @@ struct rlx_encoder {
   int* cu = nullptr;
   int* tok_src = nullptr;
   int* tok_dst = nullptr;
+  int* order = nullptr;  // sequences by token count, longest first (mask scan, B <= kMaxOrderedBatch)
   void *X = nullptr, *X1 = nullptr, *A = nullptr, *CTX = nullptr, *QKV = nullptr, *G = nullptr;
   hipStream_t cap_stream = nullptr;
   std::vector<GraphEntry> graphs;
@@ -272,7 +273,7 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
     if (st_ != RLX_OK) return st_;                                                 \
   } while (0)
 
-  STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, e->cu, e->tok_src, e->tok_dst, ss));
+  STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, e->cu, e->tok_src, e->tok_dst, e->order, ss));
   if (c.input_kind == RLX_INPUT_IDS) {
     STEP(K_EMBED_LN, launch_embed_ln(static_cast<const int*>(input), e->w.word_emb, e->w.pos_emb, e->w.type_emb,
                                      e->w.emb_ln_gamma, e->w.emb_ln_beta, c.ln_eps, c.vocab, S, H, e->tok_src, n_dev,
@@ -294,6 +295,7 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
       FusedAttnParams fa{};
       fa.x = e->X; fa.wqkv = L.wqkv; fa.bqkv = L.bqkv; fa.cu_seqlens = e->cu; fa.out = e->CTX; fa.out_rows = T;
       fa.B = B; fa.H = H; fa.heads = c.heads; fa.scale = 1.0f / std::sqrt((float)c.head_dim);
+      fa.seq_order = B <= kMaxOrderedBatch ? e->order : nullptr;  // written by the mask scan
       STEP(K_QKV_ATTENTION, launch_qkv_attention(fa, ss));
     } else {
       g.x = e->X; g.w = L.wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = L.bqkv;
@@ -575,6 +577,7 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
   const size_t o_cu = take((cfg->max_batch + 1) * sizeof(int));
   const size_t o_src = take(T * sizeof(int));
   const size_t o_dst = take(T * sizeof(int));
+  const size_t o_ord = take((size_t)cfg->max_batch * sizeof(int));
   const size_t o_X = take(T * H * es), o_X1 = take(T * H * es), o_A = take(T * H * es), o_C = take(T * H * es);
   const size_t o_Q = take(T * 3 * H * es), o_G = take(T * F * es);
   he = hipMalloc(&e->ws, off);
@@ -586,6 +589,7 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
   e->cu = reinterpret_cast<int*>(base + o_cu);
   e->tok_src = reinterpret_cast<int*>(base + o_src);
   e->tok_dst = reinterpret_cast<int*>(base + o_dst);
+  e->order = reinterpret_cast<int*>(base + o_ord);
   e->X = base + o_X; e->X1 = base + o_X1; e->A = base + o_A; e->CTX = base + o_C; e->QKV = base + o_Q;
   e->G = base + o_G;
   he = hipStreamCreateWithFlags(&e->cap_stream, hipStreamNonBlocking);

@@ -70,6 +70,7 @@ struct FusedAttnParams {
   int out_rows;         // row pitch of one head block (>= real tokens)
   int B, H, heads;
   float scale;
+  const int* seq_order;  // optional [B]: the sequences in launch order (longest first)
 };
 hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s);
 
@@ -80,7 +81,11 @@ hipError_t init_kernel_attributes();
 //   cu[0..B]    exclusive prefix of valid counts (cu[B] = valid tokens)
 //   tok_src[t]  = b*S + s of compact token t            (t < cu[B])
 //   tok_dst[i]  = compact index of padded token i, or -1 (i < B*S)
-hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, hipStream_t s);
+// order (optional, [B]): the sequences sorted by token count, longest first;
+// written only for B <= kMaxOrderedBatch (consumers must then also check B).
+constexpr int kMaxOrderedBatch = 256;
+hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, int* order,
+                            hipStream_t s);
 
 // x[t] = LN(word[id] + pos[s] + type[0]) for compact tokens t < cu[B].
 hipError_t launch_embed_ln(const int* ids, const void* word, const void* pos, const void* type, const float* gamma,

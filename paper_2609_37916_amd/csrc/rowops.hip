@@ -21,8 +21,8 @@ namespace rlx {
 namespace {
 
 __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, int B, int S, int* cu, int* tok_src,
-                                                         int* tok_dst) {
-  extern __shared__ int offs[];  // [B+1]
+                                                         int* tok_dst, int* order) {
+  extern __shared__ int offs[];  // [B+1]: token counts, then their exclusive prefix; then [B] ranks
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
   for (int b = wave; b < B; b += nw) {
@@ -35,14 +35,43 @@ __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, in
     if (lane == 0) offs[b] = cnt;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int run = 0;
-    for (int b = 0; b < B; ++b) {
-      const int c = offs[b];
-      offs[b] = run;
-      run += c;
+  // Sequences by token count, longest first (ties by index), for kernels that
+  // give each sequence its own blocks: launched in this order, the long ones
+  // are placed first and get a CU each.  Small batches only (quadratic).
+  if (order) {
+    // thread (t, part): sequences u = part, part + P, ... of the comparison
+    // for sequence t; the P = blockDim/B partial ranks are summed in LDS
+    const int P = max(1, (int)blockDim.x / B);
+    int* rank = offs + B + 1;  // [B]
+    for (int t = threadIdx.x; t < B; t += blockDim.x) rank[t] = 0;
+    __syncthreads();
+    const int t = threadIdx.x / P, part = threadIdx.x % P;
+    if (t < B) {
+      const int c = offs[t];
+      int r = 0;
+#pragma unroll 4
+      for (int u = part; u < B; u += P) r += (offs[u] > c || (offs[u] == c && u < t)) ? 1 : 0;
+      atomicAdd(&rank[t], r);
     }
-    offs[B] = run;
+    __syncthreads();
+    for (int i = threadIdx.x; i < B; i += blockDim.x) order[rank[i]] = i;
+    __syncthreads();
+  }
+  // exclusive prefix of the counts: wave 0, 64 sequences at a time
+  if (wave == 0) {
+    int carry = 0;
+    for (int c0 = 0; c0 < B; c0 += 64) {
+      const int v = c0 + lane < B ? offs[c0 + lane] : 0;
+      int incl = v;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int n = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += n;
+      }
+      if (c0 + lane < B) offs[c0 + lane] = carry + incl - v;
+      carry += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) offs[B] = carry;
   }
   __syncthreads();
   for (int i = threadIdx.x; i <= B; i += blockDim.x) cu[i] = offs[i];
@@ -267,9 +296,10 @@ inline int blocks_for_rows(int rows) { return (rows + 3) / 4; }
 
 }  // namespace
 
-hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, hipStream_t s) {
-  hipLaunchKernelGGL(mask_scan_kernel, dim3(1), dim3(1024), (size_t)(B + 1) * sizeof(int), s, mask, B, S, cu,
-                     tok_src, tok_dst);
+hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, int* order,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(mask_scan_kernel, dim3(1), dim3(1024), (size_t)(2 * B + 1) * sizeof(int), s, mask, B, S, cu,
+                     tok_src, tok_dst, B <= kMaxOrderedBatch ? order : nullptr);
   return hipGetLastError();
 }
 
