@@ -179,8 +179,6 @@ def main():
     flops_launch["attention"] = attention_flops(sp, wl.mask.sum(axis=1))
     # sequences of <= 128 tokens run the QKV projection inside the attention kernel
     flops_launch["qkv_attention"] = flops_launch["gemm_qkv"] + flops_launch["attention"]
-    # dense bf16 weights normalise the FFN-up input (LN1) inside that GEMM
-    flops_launch["gemm_ffn_up_ln"] = flops_launch["gemm_ffn_up"]
     matrix_classes = [k for k in flops_launch if k in per_fwd_us]
     dominant = max(matrix_classes, key=lambda k: per_fwd_us.get(k, 0.0))
     achieved = flops_launch[dominant] / (per_launch_us[dominant] * 1e-6) / 1e12

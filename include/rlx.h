@@ -10,7 +10,8 @@
  *  - All tensor pointers are DEVICE pointers unless marked "host".  The
  *    caller owns every buffer it passes; the library never frees or keeps
  *    them beyond the call, except the weights bound by rlx_encoder_create,
- *    which must outlive the encoder handle.
+ *    which must outlive the encoder handle and keep their values while it
+ *    exists (part of them are read once, at create).
  *  - Tensors are dense and row-major unless a row stride is given; strides
  *    are in elements.
  *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
@@ -193,6 +194,13 @@ typedef struct rlx_encoder rlx_encoder;
 /* Validates cfg and the weight pointers, allocates the workspace for
  * max_batch * max_seq tokens on the current HIP device, and returns a handle
  * in *out.  `cfg` and `w` are host pointers; they are copied.
+ * With dense bf16 weights (quant RLX_Q_NONE) and hidden a multiple of 128,
+ * the forward applies each post-LN LayerNorm in the kernels that read its
+ * output (Section VIII-B's encoder, same result up to rounding): create then
+ * derives, synchronously, copies of w1 of every layer and wqkv of layers
+ * 1.. with the preceding LayerNorm's gamma folded in, and folded biases from
+ * beta, bqkv and b1; later changes to those arrays, the LayerNorm parameters
+ * or bqkv/b1 are not seen by the handle.
  * Errors: RLX_ERR_INVALID_ARG (nulls, non-positive sizes, H != heads*head_dim),
  * RLX_ERR_UNSUPPORTED (head_dim != 32, H or F not a multiple of 64,
  * max_seq > 512 or > max_pos, quantised weights with f32 activations,

@@ -327,7 +327,8 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   static_assert(kFxRows * kFKPitch + 32 * kFVts * 2 <= kFOutOff, "K/V before the output staging");
   static_assert(STAGES * kFStage >= kFOutOff + 4 * 2048, "K/V and output staging reuse the stage memory");
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * kFStage];
-  __shared__ float bias_lds[kFwRows];
+  __shared__ __attribute__((aligned(16))) float vec_lds[2 * kFwRows];  // this head's bias, then fold_u
+  __shared__ __attribute__((aligned(16))) float2 st_lds[kFxRows * kLnMaxParts];  // [token][np] partial statistics
   // blocks run sequence by sequence (all heads of one together), longest
   // sequences first when an order is given, so those get a CU to themselves
   const int h = blockIdx.x, b = p.seq_order ? p.seq_order[blockIdx.y] : blockIdx.y;
@@ -339,8 +340,29 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   const int l32 = lane & 31, half = lane >> 5;
   const bool active = wave * 32 < L;
   const size_t pitch = (size_t)H * 2;
-  // this head's 96 bias values, read early (visible after the first barrier)
-  if (tid < kFwRows) bias_lds[tid] = p.bqkv[(tid >> 5) * H + h * 32 + (tid & 31)];
+  // This head's 96 bias values and (deferred LayerNorm input) 96 row sums of
+  // the gamma-scaled weights, and the sequence's row statistics, go to LDS by
+  // DMA ahead of the first stage: eight lanes per 32-value segment, and the
+  // statistics as one contiguous run clamped to the sequence's last row.
+  const bool deferred = p.x_stats != nullptr;
+  const int np = H >> 6;
+  {
+    const uint32_t v0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float*)vec_lds;
+    if (wave == 0 && lane < (deferred ? 48 : 24)) {
+      const int seg = lane >> 3, part = seg % 3;  // segments 0-2: bias Q, K, V; 3-5: fold_u Q, K, V
+      const float* vp = (seg < 3 ? p.bqkv : p.fold_u) + part * H + h * 32 + (lane & 7) * 4;
+      lds_dma16_attn(vp, __builtin_amdgcn_readfirstlane(v0));
+    }
+    if (deferred) {
+      const uint32_t s0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float2*)st_lds;
+      const size_t first = (size_t)row0 * np * 8, end = (size_t)(row0 + L) * np * 8;
+      const int jobs = (L * np * 8 + 1023) >> 10;
+      for (int j = wave; j < jobs; j += 4) {
+        const size_t o = min(first + (size_t)j * 1024 + lane * 16, end - 16);
+        lds_dma16_attn(reinterpret_cast<const uint8_t*>(p.x_stats) + o, __builtin_amdgcn_readfirstlane(s0 + j * 1024));
+      }
+    }
+  }
   const int KT = H / 64;
 
   const uint8_t* src[kFLps];
@@ -413,15 +435,27 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   uint32_t qpk[8];
   if (active) {
     const int tok = wave * 32 + l32;
+    // (mean, rstd) of this lane's token; (0, 1) leaves a plain input's product as is
+    const float2 lnst = deferred ? merge_ln_lds(st_lds + min(tok, L - 1) * np, np, p.ln_eps) : make_float2(0.0f, 1.0f);
+    const float* bias_lds = vec_lds;
+    const float* u_lds = vec_lds + kFwRows;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int d = 8 * i + 4 * half;
       float qv[4], kv[4], vv[4];
+      // deferred LayerNorm of the input rows: sum_k LN(x)_k W_nk =
+      // rstd * (sum_k x_k W'_nk - mean * u_n) + (W beta)_n, W'_nk = gamma_k W_nk
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        qv[j] = acc[0][4 * i + j] + bias_lds[d + j];
-        kv[j] = acc[1][4 * i + j] + bias_lds[32 + d + j];
-        vv[j] = acc[2][4 * i + j] + bias_lds[64 + d + j];
+        float a0 = acc[0][4 * i + j], a1 = acc[1][4 * i + j], a2 = acc[2][4 * i + j];
+        if (deferred) {  // (u_lds is only written for a deferred input)
+          a0 = fmaf(-lnst.x, u_lds[d + j], a0);
+          a1 = fmaf(-lnst.x, u_lds[32 + d + j], a1);
+          a2 = fmaf(-lnst.x, u_lds[64 + d + j], a2);
+        }
+        qv[j] = fmaf(lnst.y, a0, bias_lds[d + j]);
+        kv[j] = fmaf(lnst.y, a1, bias_lds[32 + d + j]);
+        vv[j] = fmaf(lnst.y, a2, bias_lds[64 + d + j]);
       }
       qpk[2 * i] = pack_bf16x2(qv[0], qv[1]);
       qpk[2 * i + 1] = pack_bf16x2(qv[2], qv[3]);
@@ -435,7 +469,6 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   if (!active) return;
 
   const int ntiles = (L + 31) >> 5;
-  const int qi = wave * 32 + l32;
   const bf16x8_t qf0 = as_bf16x8(make_uint4(qpk[0], qpk[1], qpk[2], qpk[3]));
   const bf16x8_t qf1 = as_bf16x8(make_uint4(qpk[4], qpk[5], qpk[6], qpk[7]));
   const float sl2 = p.scale * kLog2e;
@@ -535,10 +568,7 @@ hipError_t set_lds_limits() {
   return once;
 }
 
-hipError_t init_kernel_attributes() {
-  const hipError_t e = set_lds_limits();
-  return e != hipSuccess ? e : gemm_init_attributes();
-}
+hipError_t init_kernel_attributes() { return set_lds_limits(); }
 
 hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
   if (p.B <= 0 || p.S <= 0) return hipSuccess;

@@ -129,12 +129,12 @@ namespace {
 
 enum KernelClass {
   K_MASK_SCAN = 0, K_EMBED_LN, K_GATHER_ROWS, K_GEMM_QKV, K_ATTENTION, K_GEMM_ATTN_OUT, K_LN1, K_GEMM_FFN_UP,
-  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_GEMM_FFN_UP_LN, K_NUM_CLASSES
+  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_NUM_CLASSES
 };
 const char* kClassNames[K_NUM_CLASSES] = {"mask_scan",     "embed_ln",    "gather_rows", "gemm_qkv",
                                           "attention",     "gemm_attn_out", "layer_norm_1", "gemm_ffn_up",
                                           "gemm_ffn_down", "layer_norm_2", "pool_l2",     "scatter_hidden",
-                                          "qkv_attention", "gemm_ffn_up_ln"};
+                                          "qkv_attention"};
 
 struct GraphEntry {
   int B, S;
@@ -171,6 +171,21 @@ struct rlx_encoder {
   int* tok_dst = nullptr;
   int* order = nullptr;  // sequences by token count, longest first (mask scan, B <= kMaxOrderedBatch)
   void *X = nullptr, *X1 = nullptr, *A = nullptr, *CTX = nullptr, *QKV = nullptr, *G = nullptr;
+  // Deferred LayerNorm (dense bf16 weights): no kernel writes a LayerNorm
+  // output.  The output projection and FFN-down store their pre-norm sums (A,
+  // and X from the second layer on) with per-row partial statistics (S1, S2);
+  // the kernels that read those rows normalise them.  The QKV projection of
+  // layers 1.. and every FFN-up projection take weights with the preceding
+  // LayerNorm folded in, derived at create time.
+  bool deferred = false;
+  float2* S1 = nullptr;  // statistics of A (LN1 input)
+  float2* S2 = nullptr;  // statistics of X from the second layer on (LN2 input)
+  struct Folded {
+    void* wqkv = nullptr; float* uq = nullptr; float* vq = nullptr;  // layers >= 1: LN2 of the previous layer
+    void* w1 = nullptr; float* u1 = nullptr; float* v1 = nullptr;    // LN1 of the same layer
+  };
+  std::vector<Folded> folded;
+  void* fold_mem = nullptr;
   hipStream_t cap_stream = nullptr;
   std::vector<GraphEntry> graphs;
   uint64_t use_clock = 0;
@@ -284,23 +299,34 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
   const Quant q = to_quant(c.quant);
   for (int l = 0; l < c.layers; ++l) {
     const rlx_layer_weights& L = e->layers[l];
+    // From the second layer on, a deferred-LayerNorm forward's layer input X
+    // holds the previous layer's LN2 input, normalised by its readers.
+    const bool x_def = e->deferred && l > 0;
+    const rlx_layer_weights* prev = l > 0 ? &e->layers[l - 1] : nullptr;
+    const void* wqkv = x_def ? e->folded[l].wqkv : L.wqkv;
+    const float* bqkv = x_def ? e->folded[l].vq : L.bqkv;
+    const float* uqkv = x_def ? e->folded[l].uq : nullptr;
     GemmParams g{};
     g.m_dev = n_dev;
     g.M = T;
     g.dtype = e->dt;
     g.quant = q;
+    g.ln_eps = c.ln_eps;
 
     const bool fused_attn = e->dt == DType::BF16 && q == Quant::None && S <= 128;
     if (fused_attn) {
       FusedAttnParams fa{};
-      fa.x = e->X; fa.wqkv = L.wqkv; fa.bqkv = L.bqkv; fa.cu_seqlens = e->cu; fa.out = e->CTX; fa.out_rows = T;
+      fa.x = e->X; fa.wqkv = wqkv; fa.bqkv = bqkv; fa.cu_seqlens = e->cu; fa.out = e->CTX; fa.out_rows = T;
       fa.B = B; fa.H = H; fa.heads = c.heads; fa.scale = 1.0f / std::sqrt((float)c.head_dim);
       fa.seq_order = B <= kMaxOrderedBatch ? e->order : nullptr;  // written by the mask scan
+      fa.x_stats = x_def ? e->S2 : nullptr; fa.fold_u = uqkv; fa.ln_eps = c.ln_eps;
       STEP(K_QKV_ATTENTION, launch_qkv_attention(fa, ss));
     } else {
-      g.x = e->X; g.w = L.wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = L.bqkv;
+      g.x = e->X; g.w = wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = bqkv;
       g.residual = nullptr; g.y = e->QKV; g.N = 3 * H; g.K = H; g.epi = Epi::Bias;
+      g.x_stats = x_def ? e->S2 : nullptr; g.fold_u = uqkv;
       STEP(K_GEMM_QKV, launch_gemm(g, ss));
+      g.x_stats = nullptr; g.fold_u = nullptr;
 
       AttnParams a{};
       const size_t es = e->dt == DType::BF16 ? 2 : 4;
@@ -319,34 +345,56 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
     g.x = e->CTX; g.w = L.wo; g.scales = L.wo_scales; g.zeros = L.wo_zeros; g.bias = L.bo;
     g.residual = e->X; g.y = e->A; g.N = H; g.K = H; g.epi = Epi::BiasResidual;
     g.x_head_rows = fused_attn ? T : 0;  // the fused attention writes the context head-major
+    if (x_def) {
+      g.res_stats = e->S2; g.res_gamma = prev->ln2_gamma; g.res_beta = prev->ln2_beta;
+    }
+    g.y_stats = e->deferred ? e->S1 : nullptr;
     STEP(K_GEMM_ATTN_OUT, launch_gemm(g, ss));
     g.x_head_rows = 0;
+    g.res_stats = nullptr; g.res_gamma = g.res_beta = nullptr; g.y_stats = nullptr;
+
+    if (e->deferred) {
+      // FFN-up on LN1(A) with LN1 folded into W1; FFN-down's residual LN1(A)
+      // is normalised in its epilogue, and its output is LN2's input
+      g.x = e->A; g.x_stats = e->S1; g.fold_u = e->folded[l].u1;
+      g.w = e->folded[l].w1; g.scales = nullptr; g.zeros = nullptr; g.bias = e->folded[l].v1;
+      g.residual = nullptr; g.y = e->G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
+      STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
+      g.x_stats = nullptr; g.fold_u = nullptr;
+
+      g.x = e->G; g.w = L.w2; g.scales = nullptr; g.zeros = nullptr; g.bias = L.b2;
+      g.residual = e->A; g.res_stats = e->S1; g.res_gamma = L.ln1_gamma; g.res_beta = L.ln1_beta;
+      g.y = e->X; g.y_stats = e->S2; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
+      STEP(K_GEMM_FFN_DOWN, launch_gemm(g, ss));
+      continue;
+    }
 
     // LN1 feeds the FFN-up projection and, as the residual, the FFN-down one.
-    // With dense bf16 weights the FFN-up kernel normalises its input rows
-    // itself and its first column tile stores them (X1).
-    g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;
+    STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, ss));
+    g.x = e->X1; g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;
     g.residual = nullptr; g.y = e->G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
-    if (gemm_ln_input_supported(e->dt, q, H)) {
-      g.x = e->A; g.ln_gamma = L.ln1_gamma; g.ln_beta = L.ln1_beta; g.ln_eps = c.ln_eps; g.ln_out = e->X1;
-      STEP(K_GEMM_FFN_UP_LN, launch_gemm(g, ss));
-      g.ln_gamma = g.ln_beta = nullptr;
-      g.ln_out = nullptr;
-    } else {
-      STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, ss));
-      g.x = e->X1;
-      STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
-    }
+    STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
 
     g.x = e->G; g.w = L.w2; g.scales = L.w2_scales; g.zeros = L.w2_zeros; g.bias = L.b2;
     g.residual = e->X1; g.y = e->A; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
     STEP(K_GEMM_FFN_DOWN, launch_gemm(g, ss));
     STEP(K_LN2, launch_layer_norm(e->A, L.ln2_gamma, L.ln2_beta, c.ln_eps, H, n_dev, T, e->X, e->dt, ss));
   }
+  const rlx_layer_weights& last = e->layers[c.layers - 1];
   if (c.output_kind == RLX_OUTPUT_POOLED) {
-    STEP(K_POOL, launch_pool_l2(e->X, H, e->cu, B, static_cast<float*>(output), e->dt, ss));
+    if (e->deferred) {
+      STEP(K_POOL, launch_pool_l2(e->X, H, e->cu, B, static_cast<float*>(output), e->dt, ss, e->S2,
+                                  last.ln2_gamma, last.ln2_beta, c.ln_eps));
+    } else {
+      STEP(K_POOL, launch_pool_l2(e->X, H, e->cu, B, static_cast<float*>(output), e->dt, ss));
+    }
   } else {
-    STEP(K_SCATTER, launch_scatter_hidden(e->X, H, e->tok_dst, T, static_cast<float*>(output), e->dt, ss));
+    const void* hid = e->X;
+    if (e->deferred) {  // the hidden states are LN2's output: materialise it once
+      STEP(K_LN2, launch_layer_norm(e->X, last.ln2_gamma, last.ln2_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, ss));
+      hid = e->X1;
+    }
+    STEP(K_SCATTER, launch_scatter_hidden(hid, H, e->tok_dst, T, static_cast<float*>(output), e->dt, ss));
   }
 #undef STEP
   return RLX_OK;
@@ -478,6 +526,56 @@ rlx_status run_graph_forward(rlx_encoder* e, const void* input, const uint8_t* m
   return RLX_OK;
 }
 
+// Deferred LayerNorm: folds each LayerNorm into the weights of the linear
+// layer that reads it (LN1 into W1; LN2 of layer l-1 into Wqkv of layer l),
+// once, on the capture stream, and waits for it.
+rlx_status fold_layer_norms(rlx_encoder* e) {
+  const rlx_encoder_config& c = e->cfg;
+  const size_t H = c.hidden, F = c.ffn;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+  struct Offs { size_t wqkv, uq, vq, w1, u1, v1; };
+  std::vector<Offs> offs(c.layers);
+  for (int l = 0; l < c.layers; ++l) {
+    if (l > 0) {
+      offs[l].wqkv = take(3 * H * H * 2);
+      offs[l].uq = take(3 * H * sizeof(float));
+      offs[l].vq = take(3 * H * sizeof(float));
+    }
+    offs[l].w1 = take(F * H * 2);
+    offs[l].u1 = take(F * sizeof(float));
+    offs[l].v1 = take(F * sizeof(float));
+  }
+  hipError_t he = hipMalloc(&e->fold_mem, off);
+  if (he != hipSuccess) {
+    e->fold_mem = nullptr;
+    return fail(RLX_ERR_OOM, "encoder_create: folded weights of %zu bytes: %s", off, hipGetErrorString(he));
+  }
+  uint8_t* base = static_cast<uint8_t*>(e->fold_mem);
+  e->folded.assign(c.layers, rlx_encoder::Folded{});
+  for (int l = 0; l < c.layers; ++l) {
+    const rlx_layer_weights& L = e->layers[l];
+    rlx_encoder::Folded& f = e->folded[l];
+    if (l > 0) {
+      const rlx_layer_weights& P = e->layers[l - 1];
+      f.wqkv = base + offs[l].wqkv;
+      f.uq = reinterpret_cast<float*>(base + offs[l].uq);
+      f.vq = reinterpret_cast<float*>(base + offs[l].vq);
+      RLX_HIP(launch_fold_ln_weights(L.wqkv, 3 * c.hidden, c.hidden, P.ln2_gamma, P.ln2_beta, L.bqkv, f.wqkv, f.uq,
+                                     f.vq, e->cap_stream),
+              "encoder_create: fold LN2 into Wqkv");
+    }
+    f.w1 = base + offs[l].w1;
+    f.u1 = reinterpret_cast<float*>(base + offs[l].u1);
+    f.v1 = reinterpret_cast<float*>(base + offs[l].v1);
+    RLX_HIP(launch_fold_ln_weights(L.w1, c.ffn, c.hidden, L.ln1_gamma, L.ln1_beta, L.b1, f.w1, f.u1, f.v1,
+                                   e->cap_stream),
+            "encoder_create: fold LN1 into W1");
+  }
+  RLX_HIP(hipStreamSynchronize(e->cap_stream), "encoder_create: fold LayerNorms");
+  return RLX_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -580,6 +678,9 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
   const size_t o_ord = take((size_t)cfg->max_batch * sizeof(int));
   const size_t o_X = take(T * H * es), o_X1 = take(T * H * es), o_A = take(T * H * es), o_C = take(T * H * es);
   const size_t o_Q = take(T * 3 * H * es), o_G = take(T * F * es);
+  e->deferred = gemm_deferred_ln_supported(e->dt, to_quant(cfg->quant), cfg->hidden);
+  const size_t stats_bytes = e->deferred ? T * (H / 64) * sizeof(float2) : 0;
+  const size_t o_S1 = take(stats_bytes), o_S2 = take(stats_bytes);
   he = hipMalloc(&e->ws, off);
   if (he != hipSuccess) {
     delete e;
@@ -592,11 +693,22 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
   e->order = reinterpret_cast<int*>(base + o_ord);
   e->X = base + o_X; e->X1 = base + o_X1; e->A = base + o_A; e->CTX = base + o_C; e->QKV = base + o_Q;
   e->G = base + o_G;
+  if (e->deferred) {
+    e->S1 = reinterpret_cast<float2*>(base + o_S1);
+    e->S2 = reinterpret_cast<float2*>(base + o_S2);
+  }
   he = hipStreamCreateWithFlags(&e->cap_stream, hipStreamNonBlocking);
   if (he != hipSuccess) {
     (void)hipFree(e->ws);
     delete e;
     return hip_fail(he, "hipStreamCreateWithFlags");
+  }
+  if (e->deferred) {
+    st = fold_layer_norms(e);
+    if (st != RLX_OK) {
+      rlx_encoder_destroy(e);
+      return st;
+    }
   }
   *out = e;
   return ok();
@@ -637,6 +749,7 @@ void rlx_encoder_destroy(rlx_encoder* e) {
     if (ev) (void)hipEventDestroy(ev);
   if (e->cap_stream) (void)hipStreamDestroy(e->cap_stream);
   if (e->ws) (void)hipFree(e->ws);
+  if (e->fold_mem) (void)hipFree(e->fold_mem);
   delete e;
 }
 

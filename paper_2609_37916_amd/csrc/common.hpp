@@ -83,6 +83,69 @@ __device__ __forceinline__ float gelu_erf(float x) {
   return fmaf(h, erf_as7128(x * 0.70710678118654752f), h);
 }
 
+// Deferred LayerNorm (Section VIII-B's post-LN blocks, computed by the
+// consumers of an activation): a row of `np` * 64 columns carries, per 64
+// columns j, (mean_j, sum over those columns of (a - mean_j)^2).  They merge
+// into the row's mean and 1/sqrt(var + eps) with the pairwise update of Chan,
+// Golub and LeVeque (equal counts): mean = average of mean_j,
+// M2 = sum_j M2_j + 64 * sum_j (mean_j - mean)^2, var = M2 / (64 np).
+constexpr int kLnMaxParts = 16;  // rows of up to 1024 columns
+__device__ __forceinline__ void load_ln_parts(const float2* part, int np, float2 (&v)[kLnMaxParts]) {
+#pragma unroll
+  for (int j = 0; j < kLnMaxParts; ++j) v[j] = j < np ? part[j] : make_float2(0.0f, 0.0f);
+}
+__device__ __forceinline__ float2 merge_ln_parts(const float2 (&v)[kLnMaxParts], int np, float eps) {
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kLnMaxParts; ++j) s += v[j].x;
+  const float mean = s / (float)np;
+  float m2 = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kLnMaxParts; ++j)
+    if (j < np) {
+      const float d = v[j].x - mean;
+      m2 += fmaf(64.0f * d, d, v[j].y);
+    }
+  return make_float2(mean, 1.0f / sqrtf(m2 / (float)(64 * np) + eps));
+}
+__device__ __forceinline__ float2 row_ln_stats(const float2* part, int np, float eps) {
+  float2 v[kLnMaxParts];
+  load_ln_parts(part, np, v);
+  return merge_ln_parts(v, np, eps);
+}
+// The same from statistics staged in LDS.  All kLnMaxParts entries are read
+// at once (16-byte aligned, 128 readable bytes: the caller pads) and the ones
+// past np are masked, so the merge costs one LDS round trip.
+__device__ __forceinline__ float2 merge_ln_lds(const float2* part, int np, float eps) {
+  const float4* q = reinterpret_cast<const float4*>(part);
+  float4 v[kLnMaxParts / 2];
+#pragma unroll
+  for (int j = 0; j < kLnMaxParts / 2; ++j) v[j] = q[j];
+  const float inv_np = __builtin_amdgcn_rcpf((float)np);
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kLnMaxParts / 2; ++j) s += 2 * j < np ? v[j].x + v[j].z : 0.0f;
+  const float mean = s * inv_np;
+  float m2 = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kLnMaxParts / 2; ++j) {
+    const float d0 = v[j].x - mean, d1 = v[j].z - mean;
+    const float t = fmaf(64.0f * d0, d0, fmaf(64.0f * d1, d1, v[j].y + v[j].w));
+    m2 += 2 * j < np ? t : 0.0f;
+  }
+  return make_float2(mean, rsqrtf(fmaf(m2, inv_np * (1.0f / 64.0f), eps)));
+}
+
+// Sum over each group of 8 consecutive lanes, by DPP lane swaps (no LDS):
+// quad_perm [1,0,3,2] (xor 1), quad_perm [2,3,0,1] (xor 2), then the half-row
+// mirror (lane i <-> 7-i of each 8), which pairs the two quads' sums.
+__device__ __forceinline__ float dpp_sum8(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x141, 0xF, 0xF, false));
+  return v;
+}
+
 // Reinterpret 16 bytes as eight bf16 MFMA operands.
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 

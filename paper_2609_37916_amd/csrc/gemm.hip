@@ -91,7 +91,6 @@ __device__ __forceinline__ void int4x32_to_bf16(uint4 src, float s, float z, uin
 // 16 bytes of output: 8 bf16 or 4 f32, converted to / from fp32.
 template <typename T> struct Vec16;
 template <> struct Vec16<bf16_t> {
-  static constexpr int N = 8;
   static __device__ __forceinline__ void load(const bf16_t* p, float v[8]) {
     const uint4 u = *reinterpret_cast<const uint4*>(p);
     const uint32_t w[4] = {u.x, u.y, u.z, u.w};
@@ -107,7 +106,6 @@ template <> struct Vec16<bf16_t> {
   }
 };
 template <> struct Vec16<float> {
-  static constexpr int N = 4;
   static __device__ __forceinline__ void load(const float* p, float v[4]) {
     const float4 u = *reinterpret_cast<const float4*>(p);
     v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
@@ -148,11 +146,54 @@ template <> struct OutVec<float> {
 // of the K range for the same 64-row tile layout; the staging sums the groups'
 // partials (group 0 writes, the others add in turn) before the epilogue, which
 // then runs on all 256*KS threads.
-template <int BM, int BN, typename T, Quant Q, Epi E, int TM, int TN, int NRB, int KS = 1>
+// Deferred-LayerNorm roles of a dense bf16 GEMM (the GemmParams fields):
+// normalise the product of a deferred input, normalise a deferred residual,
+// write the partial statistics of the output.
+constexpr int kLnX = 1, kLnRes = 2, kLnOut = 4;
+
+// Epilogue operands staged in LDS (dense bf16 kernels): the block's per-column
+// vectors [bias, fold_u, res_gamma, res_beta][BN] (f32), its residual tile
+// [BM][BN] (bf16) and the partial statistics of its rows ([BM][K/64] for x,
+// [BM][N/64] for the residual).  Every region is a whole number of 1 KB DMA
+// blocks.  They are requested before the first operand stage, so by the
+// epilogue they have long landed and the epilogue reads no global memory.
+// Each statistics region has 128 bytes of slack (a row's merge reads
+// kLnMaxParts entries), and is followed by the rows' merged (mean, rstd)
+// ([2][BM] float2: x, residual), which the epilogue forms once per row.
+struct EpiLayout {
+  int res_off, xst_off, rst_off, mrg_off, bytes;
+};
+__host__ __device__ inline EpiLayout epi_layout(int BM, int BN, bool res, bool xst, bool rst, int K, int N) {
+  EpiLayout L;
+  int off = 16 * BN;  // four f32 vectors of BN
+  L.res_off = off;
+  if (res) off += BM * BN * 2;
+  L.xst_off = off;
+  if (xst) off += (BM * (K / 64) * 8 + 128 + 1023) / 1024 * 1024;
+  L.rst_off = off;
+  if (rst) off += (BM * (N / 64) * 8 + 128 + 1023) / 1024 * 1024;
+  L.mrg_off = off;
+  if (xst || rst) off += (2 * BM * 8 + 1023) / 1024 * 1024;
+  L.bytes = off;
+  return L;
+}
+template <int BM, int BN, Epi E, int LN>
+__host__ __device__ inline EpiLayout epi_layout_of(int K, int N) {
+  return epi_layout(BM, BN, E == Epi::BiasResidual, (LN & kLnX) != 0, (LN & kLnRes) != 0, K, N);
+}
+
+// STAGED: the epilogue operands come from LDS at `epi` (EpiLayout), else from
+// global memory (no deferred LayerNorm then).
+template <int BM, int BN, typename T, Quant Q, Epi E, int TM, int TN, int NRB, int KS = 1, int LN = 0,
+          bool STAGED = false>
 __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_t* lds, const GemmParams& p, int m0,
-                                           int n0, int M) {
+                                           int n0, int M, uint8_t* epi = nullptr) {
   static_assert(NRB == 1 || NRB == 2, "row blocks follow the 2 wave rows");
+  static_assert(LN == 0 || (sizeof(T) == 2 && Q == Quant::None && STAGED), "deferred LayerNorm: dense bf16");
+  static_assert(!STAGED || sizeof(T) == 2, "staged epilogue operands: bf16");
+  static_assert(!(LN & kLnRes) || E == Epi::BiasResidual, "a deferred residual needs the residual epilogue");
   static_assert(KS == 1 || NRB == 1, "split-K tiles stage all rows at once");
+  static_assert(kThreads * KS >= BM, "one thread per row merges the row statistics");
   constexpr int NT = kThreads * KS;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int PITCH = BN * 4 + 16;  // bytes; 16 rows of a column land on distinct banks
@@ -166,6 +207,19 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
   T* y = reinterpret_cast<T*>(p.y);
   const T* res = reinterpret_cast<const T*>(p.residual);
   const uint16_t* qs = reinterpret_cast<const uint16_t*>(p.scales);
+  const EpiLayout lay = epi_layout_of<BM, BN, E, LN>(p.K, N);
+  const float* vec = reinterpret_cast<const float*>(epi);  // [4][BN]: bias, fold_u, res_gamma, res_beta
+  float2* mrg = reinterpret_cast<float2*>(epi + lay.mrg_off);  // [2][BM]: (mean, rstd) of x rows, residual rows
+  if constexpr ((LN & kLnX) != 0) {
+    // one thread per row, while the others stage their accumulators; the
+    // barrier after the staging publishes them
+    if (tid < BM) mrg[tid] = merge_ln_lds(reinterpret_cast<const float2*>(epi + lay.xst_off) + tid * (p.K >> 6),
+                                          p.K >> 6, p.ln_eps);
+  }
+  if constexpr ((LN & kLnRes) != 0) {
+    if (tid < BM) mrg[BM + tid] = merge_ln_lds(reinterpret_cast<const float2*>(epi + lay.rst_off) + tid * (N >> 6),
+                                               N >> 6, p.ln_eps);
+  }
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
     __syncthreads();  // the operand stages (or the previous row block) are no longer read
@@ -213,10 +267,25 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
 #pragma unroll
         for (int e = 0; e < EPC; ++e) v[e] *= f16_bits_to_f32(qs[n + e]);
       }
+      const int rl = rb * RB + r, cl = cc * EPC;  // row and column within the tile
+      if constexpr ((LN & kLnX) != 0) {
+        // sum_k LN(x)_k W_nk = rstd * (sum_k x_k W'_nk - mean * u_n) + (W beta)_n, with
+        // W'_nk = gamma_k W_nk; the (W beta)_n term is part of the folded bias
+        const float2 st = mrg[rl];
+#pragma unroll
+        for (int e = 0; e < EPC; e += 4) {
+          const float4 u = *reinterpret_cast<const float4*>(vec + BN + cl + e);
+          v[e] = st.y * fmaf(-st.x, u.x, v[e]);
+          v[e + 1] = st.y * fmaf(-st.x, u.y, v[e + 1]);
+          v[e + 2] = st.y * fmaf(-st.x, u.z, v[e + 2]);
+          v[e + 3] = st.y * fmaf(-st.x, u.w, v[e + 3]);
+        }
+      }
       if constexpr (E != Epi::None) {
 #pragma unroll
         for (int e = 0; e < EPC; e += 4) {
-          const float4 bb = *reinterpret_cast<const float4*>(p.bias + n + e);
+          const float4 bb = STAGED ? *reinterpret_cast<const float4*>(vec + cl + e)
+                                   : *reinterpret_cast<const float4*>(p.bias + n + e);
           v[e] += bb.x; v[e + 1] += bb.y; v[e + 2] += bb.z; v[e + 3] += bb.w;
         }
       }
@@ -226,11 +295,50 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
       }
       if constexpr (E == Epi::BiasResidual) {
         float rr[EPC];
-        Vec16<T>::load(res + (size_t)m * N + n, rr);
+        if constexpr (STAGED)
+          Vec16<T>::load(reinterpret_cast<const T*>(epi + lay.res_off + rl * (BN * 2) + cc * 16), rr);
+        else
+          Vec16<T>::load(res + (size_t)m * N + n, rr);
+        if constexpr ((LN & kLnRes) != 0) {
+          const float2 st = mrg[BM + rl];
+#pragma unroll
+          for (int e = 0; e < EPC; e += 4) {
+            const float4 g = *reinterpret_cast<const float4*>(vec + 2 * BN + cl + e);
+            const float4 b = *reinterpret_cast<const float4*>(vec + 3 * BN + cl + e);
+            rr[e] = fmaf((rr[e] - st.x) * st.y, g.x, b.x);
+            rr[e + 1] = fmaf((rr[e + 1] - st.x) * st.y, g.y, b.y);
+            rr[e + 2] = fmaf((rr[e + 2] - st.x) * st.y, g.z, b.z);
+            rr[e + 3] = fmaf((rr[e + 3] - st.x) * st.y, g.w, b.w);
+          }
+        }
 #pragma unroll
         for (int e = 0; e < EPC; ++e) v[e] += rr[e];
       }
-      Vec16<T>::store(y + (size_t)m * N + n, v);
+      if constexpr ((LN & kLnOut) != 0) {
+        // Partial statistics of the stored (rounded) values over the 64
+        // columns of this chunk's 8-lane group (lanes 8j .. 8j+7 hold the
+        // consecutive 16-byte chunks of one row; a group is all in or all out).
+        const uint4 w = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                                   pack_bf16x2(v[6], v[7]));
+        *reinterpret_cast<uint4*>(y + (size_t)m * N + n) = w;
+        const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
+        float f[8], sum = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          f[2 * i] = __uint_as_float(wv[i] << 16);
+          f[2 * i + 1] = __uint_as_float(wv[i] & 0xffff0000u);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum += f[e];
+        const float mean = dpp_sum8(sum) * (1.0f / 64.0f);
+        float m2 = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) m2 = fmaf(f[e] - mean, f[e] - mean, m2);
+        m2 = dpp_sum8(m2);
+        if ((cc & 7) == 0) p.y_stats[(size_t)m * (N >> 6) + (n >> 6)] = make_float2(mean, m2);
+      } else {
+        Vec16<T>::store(y + (size_t)m * N + n, v);
+      }
     }
   }
 }
@@ -439,10 +547,42 @@ __device__ __forceinline__ void wait_stage(int ahead) {
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
+// Requests the block's epilogue operands (EpiLayout) into LDS at `epi`, one
+// 1 KB DMA block at a time, spread over the block's NW waves.  Rows at or past
+// M read row M-1 (as the operand stages do); statistics are read as one
+// contiguous run per block, clamped to the last whole 16 bytes of row M-1.
+template <int BM, int BN, Epi E, int LN, int NW>
+__device__ __forceinline__ void issue_epilogue_operands(const GemmParams& p, int m0, int n0, int M, uint8_t* epi,
+                                                        int wave, int lane) {
+  const EpiLayout lay = epi_layout_of<BM, BN, E, LN>(p.K, p.N);
+  const uint32_t e0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)epi;
+  for (int j = wave; j < lay.mrg_off / 1024; j += NW) {  // (the merged statistics are formed in place)
+    const int o = j * 1024 + lane * 16;  // byte of the staged operands this lane fetches
+    const uint8_t* src = nullptr;
+    if (o < lay.res_off) {
+      const int v = o / (BN * 4), c = (o % (BN * 4)) / 4;
+      const float* vp = v == 0 ? (E != Epi::None ? p.bias : nullptr)
+                               : v == 1 ? ((LN & kLnX) ? p.fold_u : nullptr)
+                                        : v == 2 ? ((LN & kLnRes) ? p.res_gamma : nullptr)
+                                                 : ((LN & kLnRes) ? p.res_beta : nullptr);
+      if (vp) src = reinterpret_cast<const uint8_t*>(vp + n0 + c);
+    } else if (o < lay.xst_off) {
+      const int b = o - lay.res_off, r = b / (BN * 2);
+      src = reinterpret_cast<const uint8_t*>(p.residual) + ((size_t)min(m0 + r, M - 1) * p.N + n0) * 2 + b % (BN * 2);
+    } else if (o < lay.mrg_off) {
+      const bool xs = o < lay.rst_off;
+      const int np = xs ? p.K >> 6 : p.N >> 6;
+      const size_t b = (size_t)m0 * np * 8 + (o - (xs ? lay.xst_off : lay.rst_off));
+      src = reinterpret_cast<const uint8_t*>(xs ? p.x_stats : p.res_stats) + min(b, (size_t)M * np * 8 - 16);
+    }
+    if (src) lds_dma16(src, __builtin_amdgcn_readfirstlane(e0 + j * 1024));
+  }
+}
+
 // KS > 1 (bf16): 4*KS waves; wave group g multiplies chunks [g*CH/KS, (g+1)*CH/KS)
 // of every stage into its own accumulators, summed in the epilogue.  With one
 // block per CU this gives each SIMD KS waves to interleave.
-template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1>
+template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1, int LN = 0>
 __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   static_assert(BM % 64 == 0 && BN % 64 == 0 && STAGES >= 2 && STAGES <= 6, "tile");
   static_assert(KS == 1 || (sizeof(T) == 2 && (BK_BF16 / 16) % KS == 0), "K split over bf16 chunks");
@@ -458,6 +598,8 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   static_assert((STAGES - 2) * LPS < 64, "vmcnt range");
 
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * kStage];
+  extern __shared__ __attribute__((aligned(1024))) uint8_t epi_lds[];  // bf16: EpiLayout (dynamic size)
+  constexpr bool STAGED = ES == 2;
 
   int M = p.M;
   if (p.m_dev) M = min(M, *p.m_dev);
@@ -474,6 +616,8 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  // oldest in every wave's memory queue: landed before the first stage is waited for
+  if constexpr (STAGED) issue_epilogue_operands<BM, BN, E, LN, NW>(p, m0, n0, M, epi_lds, wave, lane);
   const int kg = wave >> 2;  // K group (KS > 1)
   const int wm = (wave & 3) >> 1, wn = wave & 1;
   const int l32 = lane & 31, half = lane >> 5;
@@ -608,276 +752,58 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
 
   constexpr int NRB = BM * (BN * 4 + 16) <= (int)sizeof(smem) ? 1 : 2;
   static_assert(BM / NRB * (BN * 4 + 16) <= (int)sizeof(smem), "epilogue row block fits the stage memory");
-  store_tile<BM, BN, T, Quant::None, E, TM, TN, NRB, KS>(acc, smem, p, m0, n0, M);
+  store_tile<BM, BN, T, Quant::None, E, TM, TN, NRB, KS, LN, STAGED>(acc, smem, p, m0, n0, M, epi_lds);
+}
+
+template <int BM, int BN, int STAGES, typename T, Epi E, int KS, int LN>
+hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
+  const dim3 grid((p.N / BN) * ((p.M + BM - 1) / BM));
+  const size_t epi = sizeof(T) == 2 ? (size_t)epi_layout_of<BM, BN, E, LN>(p.K, p.N).bytes : 0;
+  hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, E, KS, LN>), grid, dim3(kThreads * KS), epi, s, p);
+  return hipGetLastError();
 }
 
 template <int BM, int BN, int STAGES, typename T, int KS = 1>
 hipError_t launch_dma_tile(const GemmParams& p, hipStream_t s) {
-  const dim3 grid((p.N / BN) * ((p.M + BM - 1) / BM));
-  switch (p.epi) {
-    case Epi::None:
-      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::None, KS>), grid, dim3(kThreads * KS), 0, s, p);
-      break;
-    case Epi::Bias:
-      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::Bias, KS>), grid, dim3(kThreads * KS), 0, s, p);
-      break;
-    case Epi::BiasGelu:
-      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::BiasGelu, KS>), grid, dim3(kThreads * KS), 0, s, p);
-      break;
-    case Epi::BiasResidual:
-      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, Epi::BiasResidual, KS>), grid, dim3(kThreads * KS), 0, s, p);
-      break;
-  }
-  return hipGetLastError();
-}
-
-
-// ---------------------------------------------------------------------------
-// Dense bf16 kernel with the row LayerNorm of its input fused in front
-// ---------------------------------------------------------------------------
-//
-// Post-LN blocks feed LN(a) into the next projection.  A 64-row block of a
-// (K <= 512) fits in LDS whole, so the block loads its rows once, forms each
-// row's mean and variance (fp32, mean first, then the centred sum of squares,
-// as the LayerNorm kernel), writes the normalised bf16 values back in place,
-// and then streams only the weights through the stage ring.  The blocks of
-// column tile 0 also store the normalised rows (the residual of the next
-// block), so no separate LayerNorm pass over the activations remains.
-constexpr int kLnxStages = 2;
-constexpr int kLnxKs = 2;  // wave groups splitting each stage's K (two blocks of eight waves per CU)
-
-template <int BN, int KC, Epi E>
-__global__ __launch_bounds__(kThreads * kLnxKs) void gemm_lnx_kernel(GemmParams p) {
-  constexpr int BM = 64, WM = BM / 2, WN = BN / 2;
-  constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int NW = 4 * kLnxKs, NT = kThreads * kLnxKs;  // waves / threads: kLnxKs groups of four waves
-  constexpr int WStage = BN * kRowBytes;
-  constexpr int WLps = BN / (8 * NW);     // weight DMAs per thread per stage (8 rows each per wave)
-  static_assert(BN % (8 * NW) == 0, "weight rows split evenly over the waves");
-  constexpr int ABlock = BM * kRowBytes;  // one 64-k block of the activation rows
-  extern __shared__ __attribute__((aligned(1024))) uint8_t lnx_smem[];
-
-  int M = p.M;
-  if (p.m_dev) M = min(M, *p.m_dev);
-  const int n_tiles = p.N / BN;
-  const int live = n_tiles * ((M + BM - 1) / BM);
-  const int bid = blockIdx.x;
-  if (bid >= live) return;
-  const int q8 = live >> 3, r8 = live & 7, xcd = bid & 7;  // XCD-aware tile order, as gemm_dma_kernel
-  const int tile = xcd * q8 + min(xcd, r8) + (bid >> 3);
-  const int m0 = (tile / n_tiles) * BM;
-  const int n0 = (tile % n_tiles) * BN;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kg = wave >> 2;  // K group: multiplies chunks [kg*CG, (kg+1)*CG) of every stage
-  const int wm = (wave & 3) >> 1, wn = wave & 1;
-  const int l32 = lane & 31, half = lane >> 5;
-  constexpr int K = 64 * KC, KT = KC;  // K = 64 * KC (p.K)
-  const size_t pitch = (size_t)K * 2;
-  uint8_t* a_lds = lnx_smem;                    // [KT][64 rows][128 B], swizzled like a stage
-  uint8_t* w_lds = lnx_smem + KT * ABlock;      // [kLnxStages][BN rows][128 B]
-  const uint32_t a0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)a_lds;
-  const uint32_t w0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)w_lds;
-
-  // All activation rows of the block: DMA g (0 .. 8*KT-1) fills rows 8(g%8)..+7
-  // of 64-k block g/8; wave w issues g = w, w+NW, ...
-  {
-    const int rl = lane >> 3;
-    for (int g = wave; g < 8 * KT; g += NW) {
-      const int kt = g >> 3, row = 8 * (g & 7) + rl;
-      const int c = swz(row, lane & 7);
-      const uint8_t* src = reinterpret_cast<const uint8_t*>(p.x) + (size_t)min(m0 + row, M - 1) * pitch + kt * 128 + c * 16;
-      lds_dma16(src, __builtin_amdgcn_readfirstlane(a0 + kt * ABlock + 8 * (g & 7) * kRowBytes));
+  const int ln = (p.x_stats ? kLnX : 0) | (p.res_stats ? kLnRes : 0) | (p.y_stats ? kLnOut : 0);
+  if constexpr (sizeof(T) == 2) {
+    // the deferred-LayerNorm combinations of the encoder layer: the QKV and
+    // FFN-up projections read a deferred input; the output projection writes
+    // LN1's input (its residual is the deferred layer input, or the plain
+    // embedding output in the first layer); FFN-down writes LN2's input
+    switch (p.epi) {
+      case Epi::None:
+        if (ln == 0) return launch_dma<BM, BN, STAGES, T, Epi::None, KS, 0>(p, s);
+        break;
+      case Epi::Bias:
+        if (ln == 0) return launch_dma<BM, BN, STAGES, T, Epi::Bias, KS, 0>(p, s);
+        if (ln == kLnX) return launch_dma<BM, BN, STAGES, T, Epi::Bias, KS, kLnX>(p, s);
+        break;
+      case Epi::BiasGelu:
+        if (ln == 0) return launch_dma<BM, BN, STAGES, T, Epi::BiasGelu, KS, 0>(p, s);
+        if (ln == kLnX) return launch_dma<BM, BN, STAGES, T, Epi::BiasGelu, KS, kLnX>(p, s);
+        break;
+      case Epi::BiasResidual:
+        if (ln == 0) return launch_dma<BM, BN, STAGES, T, Epi::BiasResidual, KS, 0>(p, s);
+        if (ln == kLnOut) return launch_dma<BM, BN, STAGES, T, Epi::BiasResidual, KS, kLnOut>(p, s);
+        if (ln == (kLnRes | kLnOut)) return launch_dma<BM, BN, STAGES, T, Epi::BiasResidual, KS, kLnRes | kLnOut>(p, s);
+        break;
     }
-  }
-  // gamma and beta go by DMA too (a plain load would make the compiler wait for
-  // every outstanding DMA before its LDS store), into the last weight buffer,
-  // which the main loop fills only after the barrier that ends the
-  // normalisation: DMA w < 8K/1024 carries bytes [1024w, 1024w+1024) of
-  // [gamma (4K bytes); beta (4K bytes)].
-  static_assert(kLnxStages >= 2 && 2 * 512 * 4 <= WStage && 8 * K / 1024 <= NW, "gamma/beta staging");
-  float* gb_lds = reinterpret_cast<float*>(w_lds + (kLnxStages - 1) * WStage);  // [gamma K][beta K]
-  if (wave < 8 * K / 1024) {
-    const int o = wave * 1024 + lane * 16;
-    const uint8_t* src = o < 4 * K ? reinterpret_cast<const uint8_t*>(p.ln_gamma) + o
-                                   : reinterpret_cast<const uint8_t*>(p.ln_beta) + (o - 4 * K);
-    lds_dma16(src, __builtin_amdgcn_readfirstlane(w0 + (kLnxStages - 1) * WStage + wave * 1024));
-  }
-  const uint8_t* wsrc[WLps];
-#pragma unroll
-  for (int i = 0; i < WLps; ++i) {
-    const int row = wave * 8 + i * 8 * NW + (lane >> 3);
-    wsrc[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row) * pitch + swz(row, lane & 7) * 16;
-  }
-  auto issue_w = [&](int kt, int buf) {
-#pragma unroll
-    for (int i = 0; i < WLps; ++i)
-      lds_dma16(wsrc[i] + (size_t)kt * kRowBytes,
-                __builtin_amdgcn_readfirstlane(w0 + buf * WStage + (wave * 8 + i * 8 * NW) * kRowBytes));
-  };
-#pragma unroll
-  for (int st = 0; st < kLnxStages - 1; ++st)
-    if (st < KT) issue_w(st, st);
-  // the activation rows and gamma/beta were issued first: they have landed
-  // once only the weight stages are outstanding
-  if (KT >= kLnxStages - 1) wait_vmcnt<(kLnxStages - 1) * WLps>();
-  else wait_vmcnt<0>();
-  __syncthreads();
-
-  // LayerNorm of the 64 rows in place: NT/64 threads per row, each holding its
-  // share of the row's 8-element chunks in registers.
-  {
-    constexpr int TPR = NT / 64;      // threads per row
-    constexpr int CPT = K / 8 / TPR;  // chunks per thread
-    const int r = tid / TPR, qd = tid % TPR;
-    uint4 raw[CPT];
-#pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int cc = qd * CPT + j;  // 8-element chunk of the row
-      raw[j] = ld16(a_lds + (cc >> 3) * ABlock + r * kRowBytes + swz(r, cc & 7) * 16);
+    return hipErrorInvalidValue;
+  } else {
+    if (ln != 0) return hipErrorInvalidValue;
+    switch (p.epi) {
+      case Epi::None: return launch_dma<BM, BN, STAGES, T, Epi::None, KS, 0>(p, s);
+      case Epi::Bias: return launch_dma<BM, BN, STAGES, T, Epi::Bias, KS, 0>(p, s);
+      case Epi::BiasGelu: return launch_dma<BM, BN, STAGES, T, Epi::BiasGelu, KS, 0>(p, s);
+      case Epi::BiasResidual: return launch_dma<BM, BN, STAGES, T, Epi::BiasResidual, KS, 0>(p, s);
     }
-    auto val = [&](int j, int e) {
-      const uint32_t w = e == 0 || e == 1 ? raw[j].x : e == 2 || e == 3 ? raw[j].y : e == 4 || e == 5 ? raw[j].z : raw[j].w;
-      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
-    };
-    float sum = 0.0f;
-#pragma unroll
-    for (int j = 0; j < CPT; ++j)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sum += val(j, e);
-#pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) sum += __shfl_xor(sum, o, 64);
-    const float mean = sum / (float)K;
-    float sq = 0.0f;
-#pragma unroll
-    for (int j = 0; j < CPT; ++j)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float c = val(j, e) - mean;
-        sq += c * c;
-      }
-#pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) sq += __shfl_xor(sq, o, 64);
-    const float rstd = 1.0f / sqrtf(sq / (float)K + p.ln_eps);
-    const bool store_rows = p.ln_out != nullptr && n0 == 0 && m0 + r < M;
-#pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int cc = qd * CPT + j, col = cc * 8;
-      float o[8];
-#pragma unroll
-      for (int e = 0; e < 8; e += 4) {
-        const float4 g = *reinterpret_cast<const float4*>(gb_lds + col + e);
-        const float4 b = *reinterpret_cast<const float4*>(gb_lds + K + col + e);
-        o[e] = (val(j, e) - mean) * rstd * g.x + b.x;
-        o[e + 1] = (val(j, e + 1) - mean) * rstd * g.y + b.y;
-        o[e + 2] = (val(j, e + 2) - mean) * rstd * g.z + b.z;
-        o[e + 3] = (val(j, e + 3) - mean) * rstd * g.w + b.w;
-      }
-      Vec16<bf16_t>::store(reinterpret_cast<bf16_t*>(a_lds + (cc >> 3) * ABlock + r * kRowBytes + swz(r, cc & 7) * 16), o);
-      if (store_rows) Vec16<bf16_t>::store(reinterpret_cast<bf16_t*>(p.ln_out) + (size_t)(m0 + r) * K + col, o);
-    }
+    return hipErrorInvalidValue;
   }
-
-  f32x16_t acc[TM][TN];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < TN; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
-
-  for (int kt = 0; kt < KT; ++kt) {
-    wait_stage<WLps, kLnxStages - 2>(min(kLnxStages - 2, KT - 1 - kt));
-    __syncthreads();  // weight stage kt (and, at kt = 0, the normalised rows) visible; buffer kt-1 free
-    const uint8_t* xs = a_lds + kt * ABlock;
-    const uint8_t* ws = w_lds + (kt % kLnxStages) * WStage;
-    constexpr int CG = 4 / kLnxKs;  // 16-k chunks of this wave's K group
-    bf16x8_t af[CG][TN], bfr[CG][TM];
-#pragma unroll
-    for (int qq = 0; qq < CG; ++qq) {
-      const int q = kg * CG + qq;
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const int r = wn * WN + tn * 32 + l32;
-        af[qq][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
-      }
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        const int r = wm * WM + tm * 32 + l32;
-        bfr[qq][tm] = as_bf16x8(ld16(xs + r * kRowBytes + swz(r, 2 * q + half) * 16));
-      }
-    }
-    if (kt + kLnxStages - 1 < KT) issue_w(kt + kLnxStages - 1, (kt + kLnxStages - 1) % kLnxStages);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int qq = 0; qq < CG; ++qq)
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn)
-          acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[qq][tn], bfr[qq][tm], acc[tm][tn], 0, 0, 0);
-  }
-  // the epilogue stages the tile through the block's LDS (K >= 256)
-  static_assert(BM * (BN * 4 + 16) <= 4 * ABlock + kLnxStages * WStage, "epilogue staging fits the LDS");
-  store_tile<BM, BN, bf16_t, Quant::None, E, TM, TN, 1, kLnxKs>(acc, lnx_smem, p, m0, n0, M);
-}
-
-size_t lnx_lds_bytes(int K, int BN) { return (size_t)(K / 64) * 64 * kRowBytes + (size_t)kLnxStages * BN * kRowBytes; }
-
-template <int BN, int KC>
-hipError_t launch_lnx_k(const GemmParams& p, hipStream_t s) {
-  const dim3 grid((p.N / BN) * ((p.M + 63) / 64));
-  const size_t lds = lnx_lds_bytes(64 * KC, BN);
-  switch (p.epi) {
-    case Epi::None: hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::None>), grid, dim3(kThreads * kLnxKs), lds, s, p); break;
-    case Epi::Bias: hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::Bias>), grid, dim3(kThreads * kLnxKs), lds, s, p); break;
-    case Epi::BiasGelu:
-      hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::BiasGelu>), grid, dim3(kThreads * kLnxKs), lds, s, p);
-      break;
-    case Epi::BiasResidual:
-      hipLaunchKernelGGL((gemm_lnx_kernel<BN, KC, Epi::BiasResidual>), grid, dim3(kThreads * kLnxKs), lds, s, p);
-      break;
-  }
-  return hipGetLastError();
-}
-
-template <int BN>
-hipError_t launch_lnx(const GemmParams& p, hipStream_t s) {
-  switch (p.K) {
-    case 256: return launch_lnx_k<BN, 4>(p, s);
-    case 384: return launch_lnx_k<BN, 6>(p, s);
-    case 512: return launch_lnx_k<BN, 8>(p, s);
-    default: return hipErrorInvalidValue;
-  }
-}
-
-template <int BN, int KC>
-hipError_t lnx_attributes_k() {
-  const void* fns[4] = {reinterpret_cast<const void*>(gemm_lnx_kernel<BN, KC, Epi::None>),
-                        reinterpret_cast<const void*>(gemm_lnx_kernel<BN, KC, Epi::Bias>),
-                        reinterpret_cast<const void*>(gemm_lnx_kernel<BN, KC, Epi::BiasGelu>),
-                        reinterpret_cast<const void*>(gemm_lnx_kernel<BN, KC, Epi::BiasResidual>)};
-  for (const void* f : fns) {
-    const hipError_t e =
-        hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lnx_lds_bytes(64 * KC, BN));
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
-}
-
-template <int BN>
-hipError_t lnx_attributes() {
-  hipError_t e = lnx_attributes_k<BN, 4>();
-  if (e == hipSuccess) e = lnx_attributes_k<BN, 6>();
-  if (e == hipSuccess) e = lnx_attributes_k<BN, 8>();
-  return e;
 }
 
 template <typename T>
 hipError_t launch_dense(const GemmParams& p, hipStream_t s) {
-  if constexpr (sizeof(T) == 2) {
-    if (p.ln_gamma) return p.N % 128 == 0 ? launch_lnx<128>(p, s) : launch_lnx<64>(p, s);
-  }
   int tile = p.tile;
   if (tile == kTileAuto) {
     // measured at the encoder's shapes (2-4 k tokens): 64x64 for N = 384, 64x128
@@ -939,23 +865,58 @@ __global__ void dequant_unpack_kernel(const uint8_t* w, Quant q, const uint16_t*
   }
 }
 
-}  // namespace
-
-bool gemm_ln_input_supported(DType dt, Quant q, int K) {
-  return dt == DType::BF16 && q == Quant::None && (K == 256 || K == 384 || K == 512);
+// One block per weight row n (256 threads over k).
+__global__ __launch_bounds__(256) void fold_ln_weights_kernel(const bf16_t* w, int K, const float* gamma,
+                                                               const float* beta, const float* bias, bf16_t* w_out,
+                                                               float* u_out, float* v_out) {
+  const int n = blockIdx.x, tid = threadIdx.x;
+  const bf16_t* row = w + (size_t)n * K;
+  bf16_t* orow = w_out + (size_t)n * K;
+  double u = 0.0, v = 0.0;
+  for (int k = tid; k < K; k += 256) {
+    const float wk = bf16_to_f32(row[k]);
+    const bf16_t f = f32_to_bf16(gamma[k] * wk);  // the product of two floats, rounded once to bf16
+    orow[k] = f;
+    u += (double)bf16_to_f32(f);
+    v += (double)beta[k] * (double)wk;
+  }
+  __shared__ double red[2][4];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    u += __shfl_xor(u, o, 64);
+    v += __shfl_xor(v, o, 64);
+  }
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = u;
+    red[1][tid >> 6] = v;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    u_out[n] = (float)(red[0][0] + red[0][1] + red[0][2] + red[0][3]);
+    v_out[n] = (float)(red[1][0] + red[1][1] + red[1][2] + red[1][3] + (bias ? (double)bias[n] : 0.0));
+  }
 }
 
-hipError_t gemm_init_attributes() {
-  static const hipError_t once = [] {
-    const hipError_t e = lnx_attributes<128>();
-    return e != hipSuccess ? e : lnx_attributes<64>();
-  }();
-  return once;
+}  // namespace
+
+hipError_t launch_fold_ln_weights(const void* w, int N, int K, const float* gamma, const float* beta,
+                                  const float* bias, void* w_out, float* u_out, float* v_out, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fold_ln_weights_kernel, dim3(N), dim3(256), 0, s, reinterpret_cast<const bf16_t*>(w), K, gamma,
+                     beta, bias, reinterpret_cast<bf16_t*>(w_out), u_out, v_out);
+  return hipGetLastError();
+}
+
+bool gemm_deferred_ln_supported(DType dt, Quant q, int H) {
+  // rows of an even number of 64-column parts (whole 16-byte statistics runs), up to 1024 columns
+  return dt == DType::BF16 && q == Quant::None && H % 128 == 0 && H <= 64 * kLnMaxParts;
 }
 
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
-  if (p.ln_gamma && !gemm_ln_input_supported(p.dtype, p.quant, p.K)) return hipErrorInvalidValue;
+  if ((p.x_stats && !gemm_deferred_ln_supported(p.dtype, p.quant, p.K)) ||
+      ((p.res_stats || p.y_stats) && !gemm_deferred_ln_supported(p.dtype, p.quant, p.N)))
+    return hipErrorInvalidValue;
   if (p.dtype == DType::F32) return launch_dense<float>(p, s);
   switch (p.quant) {
     case Quant::None: return launch_dense<bf16_t>(p, s);

@@ -27,17 +27,25 @@ struct GemmParams {
   int tile;              // 0: choose automatically; otherwise a GemmTile value (tuning)
   int x_head_rows;       // 0: x is row-major [M,K]; > 0: x is head-major [K/32][x_head_rows][32]
                          // (dense bf16 only), as written by the fused attention
-  // Optional LayerNorm of the activation rows before the product (dense bf16,
-  // K <= 512): the kernel multiplies LN(x) * ln_gamma + ln_beta, and when
-  // ln_out is set also stores those normalised rows there ([M,K]).
-  const float* ln_gamma;
-  const float* ln_beta;
+  // Deferred LayerNorm (dense bf16 only).  A post-LN activation can travel as
+  // its pre-norm rows a plus, per row and per 64 columns, the mean and the
+  // centred sum of squares of the stored values (float2 [rows][cols/64],
+  // "partial statistics"); whoever reads it applies the norm.
+  //  x_stats: x is such an activation and W holds gamma-scaled weights:
+  //           y = rstd[m] * (acc - mean[m] * fold_u[n]) + bias[n], then the epilogue
+  //  res_stats: the residual is such an activation:
+  //           residual[m,n] = (a[m,n] - mean[m]) * rstd[m] * res_gamma[n] + res_beta[n]
+  //  y_stats: also write the partial statistics of the stored y
+  const float2* x_stats;
+  const float* fold_u;
+  const float2* res_stats;
+  const float* res_gamma;
+  const float* res_beta;
+  float2* y_stats;
   float ln_eps;
-  void* ln_out;
 };
-// True when launch_gemm can normalise the activation rows in the kernel.
-bool gemm_ln_input_supported(DType dt, Quant q, int K);
-hipError_t gemm_init_attributes();  // once per process, outside graph capture
+// True when the deferred-LayerNorm fields are implemented for rows of H columns.
+bool gemm_deferred_ln_supported(DType dt, Quant q, int H);
 enum GemmTile : int { kTileAuto = 0, kTile128x128 = 1, kTile64x128 = 2, kTile64x64 = 3, kTile128x64 = 4 };
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 
@@ -71,8 +79,20 @@ struct FusedAttnParams {
   int B, H, heads;
   float scale;
   const int* seq_order;  // optional [B]: the sequences in launch order (longest first)
+  // optional deferred LayerNorm of x (as GemmParams::x_stats): wqkv holds
+  // gamma-scaled weights, bqkv the folded bias, fold_u [3H] the row sums
+  const float2* x_stats;
+  const float* fold_u;
+  float ln_eps;
 };
 hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s);
+
+// Folds a LayerNorm (gamma, beta) into the linear layer that consumes it, for
+// the deferred-LayerNorm path: w_out[n,k] = bf16(gamma[k] * w[n,k]),
+// u_out[n] = sum_k w_out[n,k], v_out[n] = sum_k beta[k] * w[n,k] + bias[n]
+// (sums in fp64).  w: bf16 [N,K].
+hipError_t launch_fold_ln_weights(const void* w, int N, int K, const float* gamma, const float* beta,
+                                  const float* bias, void* w_out, float* u_out, float* v_out, hipStream_t s);
 
 // Raises per-kernel dynamic-LDS limits once per process (idempotent).
 hipError_t init_kernel_attributes();
@@ -101,7 +121,11 @@ hipError_t launch_layer_norm(const void* a, const float* gamma, const float* bet
                              const int* n_dev, int n_max, void* y, DType dt, hipStream_t s);
 
 // out[b] = normalize(mean over the sequence's compact rows) (f32 [B,H]).
-hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s);
+// With x_stats (bf16), x is a deferred-LayerNorm activation (see GemmParams)
+// and the rows are normalised with gamma, beta and eps first.
+hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s,
+                          const float2* x_stats = nullptr, const float* gamma = nullptr,
+                          const float* beta = nullptr, float eps = 0.0f);
 
 // out[b,s,:] = x[tok_dst[b*S+s]] or 0 (f32 [B,S,H]).
 hipError_t launch_scatter_hidden(const void* x, int H, const int* tok_dst, int n_tok, float* out, DType dt,

@@ -227,14 +227,25 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T* hidden, int H
 // per sequence; wave w sums rows w, w+16, ... with 16-byte chunk loads, the
 // 16 partial rows are combined in LDS, then the block forms the mean and its
 // norm.
+constexpr int kMaxPoolRows = 512;  // the longest sequence
+// With x_stats the rows are pre-LayerNorm values with their partial
+// statistics (deferred LayerNorm): the block averages (x - mean) * rstd and
+// applies gamma and beta to the average.
 template <typename T>
-__global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const int* cu, float* out) {
+__global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const int* cu, float* out,
+                                                       const float2* x_stats, const float* gamma, const float* beta,
+                                                       float eps) {
   constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
   extern __shared__ float part[];  // [16][H]
   __shared__ float red[16];
+  __shared__ float2 row_st[kMaxPoolRows];  // (mean, rstd) per row of a deferred-LayerNorm input
   const int b = blockIdx.x;
   const int r0 = cu[b], L = cu[b + 1] - r0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (x_stats) {  // all rows' statistics in one round of loads, one row per thread
+    for (int r = threadIdx.x; r < L; r += 1024) row_st[r] = row_ln_stats(x_stats + (size_t)(r0 + r) * (H >> 6), H >> 6, eps);
+    __syncthreads();
+  }
   const int nch = H / EPC;
   float acc[CPL][EPC];
 #pragma unroll
@@ -243,6 +254,8 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
     for (int e = 0; e < EPC; ++e) acc[i][e] = 0.0f;
   for (int r = wave; r < L; r += 16) {
     const T* row = x + (size_t)(r0 + r) * H;
+    // (0, 1) leaves plain rows as they are
+    const float2 st = x_stats ? row_st[r] : make_float2(0.0f, 1.0f);
 #pragma unroll
     for (int i = 0; i < CPL; ++i) {
       const int ch = lane + 64 * i;
@@ -250,7 +263,7 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
         float v[EPC];
         Chunk<T>::load(row + ch * EPC, v);
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) acc[i][e] += v[e];
+        for (int e = 0; e < EPC; ++e) acc[i][e] += (v[e] - st.x) * st.y;
       }
     }
   }
@@ -270,6 +283,7 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
 #pragma unroll
     for (int w = 0; w < 16; ++w) sum += part[w * H + c];
     mean = sum / denom;
+    if (x_stats) mean = L > 0 ? fmaf(gamma[c], mean, beta[c]) : 0.0f;
   }
   const float ss = wave_sum(mean * mean);
   if (lane == 0) red[wave] = ss;
@@ -342,13 +356,18 @@ hipError_t launch_layer_norm(const void* a, const float* gamma, const float* bet
   return hipGetLastError();
 }
 
-hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s) {
+hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s,
+                          const float2* x_stats, const float* gamma, const float* beta, float eps) {
   if (B <= 0) return hipSuccess;
   const size_t lds = (size_t)16 * H * sizeof(float);
   if (dt == DType::BF16)
-    hipLaunchKernelGGL(pool_l2_kernel<bf16_t>, dim3(B), dim3(1024), lds, s, (const bf16_t*)x, H, cu, out);
+    hipLaunchKernelGGL(pool_l2_kernel<bf16_t>, dim3(B), dim3(1024), lds, s, (const bf16_t*)x, H, cu, out, x_stats,
+                       gamma, beta, eps);
+  else if (x_stats)
+    return hipErrorInvalidValue;
   else
-    hipLaunchKernelGGL(pool_l2_kernel<float>, dim3(B), dim3(1024), lds, s, (const float*)x, H, cu, out);
+    hipLaunchKernelGGL(pool_l2_kernel<float>, dim3(B), dim3(1024), lds, s, (const float*)x, H, cu, out, nullptr,
+                       nullptr, nullptr, 0.0f);
   return hipGetLastError();
 }
 
