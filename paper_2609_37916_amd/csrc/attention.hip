@@ -329,9 +329,18 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * kFStage];
   __shared__ __attribute__((aligned(16))) float vec_lds[2 * kFwRows];  // this head's bias, then fold_u
   __shared__ __attribute__((aligned(16))) float2 st_lds[kFxRows * kLnMaxParts];  // [token][np] partial statistics
-  // blocks run sequence by sequence (all heads of one together), longest
-  // sequences first when an order is given, so those get a CU to themselves
-  const int h = blockIdx.x, b = p.seq_order ? p.seq_order[blockIdx.y] : blockIdx.y;
+  // Block -> (sequence, head), XCD-aware: workgroups are dispatched
+  // round-robin over the 8 XCDs (block i to XCD i % 8), and all heads of one
+  // sequence are given to one XCD, so its L2 fetches the sequence's token rows
+  // once instead of once per XCD.  Sequences are taken in groups of 8 by rank
+  // (longest first when an order is given), one per XCD, the direction
+  // alternating between groups to balance the XCDs' work; within an XCD the
+  // blocks follow the ranks, so long sequences are placed first.
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int grp = slot / p.heads, h = slot - grp * p.heads;
+  const int rank = 8 * grp + ((grp & 1) ? 7 - xcd : xcd);
+  if (rank >= p.B) return;
+  const int b = p.seq_order ? p.seq_order[rank] : rank;
   const int row0 = p.cu_seqlens[b];
   const int L = p.cu_seqlens[b + 1] - row0;
   if (L <= 0) return;
@@ -388,6 +397,8 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
     }
   };
 
+  // (0, 1) leaves a plain input's product as is
+  float2 lnst = make_float2(0.0f, 1.0f);
   f32x16_t acc[3];
 #pragma unroll
   for (int t = 0; t < 3; ++t)
@@ -423,6 +434,10 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
               acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf, xf, acc[t], 0, 0, 0);
             }
           }
+          // (mean, rstd) of this lane's token, while the first stage's MFMAs
+          // run: the statistics were requested before stage 0 and the stage-0
+          // barrier published them
+          if (kt == 0 && deferred) lnst = merge_ln_lds(st_lds + min(wave * 32 + l32, L - 1) * np, np, p.ln_eps);
         }
       }
     }
@@ -435,8 +450,6 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   uint32_t qpk[8];
   if (active) {
     const int tok = wave * 32 + l32;
-    // (mean, rstd) of this lane's token; (0, 1) leaves a plain input's product as is
-    const float2 lnst = deferred ? merge_ln_lds(st_lds + min(tok, L - 1) * np, np, p.ln_eps) : make_float2(0.0f, 1.0f);
     const float* bias_lds = vec_lds;
     const float* u_lds = vec_lds + kFwRows;
 #pragma unroll
@@ -551,7 +564,7 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
 
 hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(qkv_attn_bf16_kernel<2>, dim3(p.heads, p.B), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(qkv_attn_bf16_kernel<2>, dim3(((p.B + 7) / 8) * 8 * p.heads), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

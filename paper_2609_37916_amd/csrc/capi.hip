@@ -288,13 +288,20 @@ rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mas
     if (st_ != RLX_OK) return st_;                                                 \
   } while (0)
 
-  STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, e->cu, e->tok_src, e->tok_dst, e->order, ss));
-  if (c.input_kind == RLX_INPUT_IDS) {
-    STEP(K_EMBED_LN, launch_embed_ln(static_cast<const int*>(input), e->w.word_emb, e->w.pos_emb, e->w.type_emb,
-                                     e->w.emb_ln_gamma, e->w.emb_ln_beta, c.ln_eps, c.vocab, S, H, e->tok_src, n_dev,
-                                     T, e->X, e->dt, ss));
+  if (c.input_kind == RLX_INPUT_IDS && embed_scan_supported(B, S)) {
+    // small masks: the scan runs inside the embedding kernel
+    STEP(K_EMBED_LN, launch_embed_scan(mask, static_cast<const int*>(input), B, S, e->w.word_emb, e->w.pos_emb,
+                                       e->w.type_emb, e->w.emb_ln_gamma, e->w.emb_ln_beta, c.ln_eps, c.vocab, H,
+                                       e->cu, e->tok_src, e->tok_dst, e->order, e->X, e->dt, ss));
   } else {
-    STEP(K_GATHER_ROWS, launch_gather_rows(input, H, e->tok_src, n_dev, T, e->X, e->dt, ss));
+    STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, e->cu, e->tok_src, e->tok_dst, e->order, ss));
+    if (c.input_kind == RLX_INPUT_IDS) {
+      STEP(K_EMBED_LN, launch_embed_ln(static_cast<const int*>(input), e->w.word_emb, e->w.pos_emb, e->w.type_emb,
+                                       e->w.emb_ln_gamma, e->w.emb_ln_beta, c.ln_eps, c.vocab, S, H, e->tok_src,
+                                       n_dev, T, e->X, e->dt, ss));
+    } else {
+      STEP(K_GATHER_ROWS, launch_gather_rows(input, H, e->tok_src, n_dev, T, e->X, e->dt, ss));
+    }
   }
   const Quant q = to_quant(c.quant);
   for (int l = 0; l < c.layers; ++l) {

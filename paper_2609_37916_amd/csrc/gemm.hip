@@ -182,6 +182,25 @@ __host__ __device__ inline EpiLayout epi_layout_of(int K, int N) {
   return epi_layout(BM, BN, E == Epi::BiasResidual, (LN & kLnX) != 0, (LN & kLnRes) != 0, K, N);
 }
 
+// Merges the partial statistics staged at `epi` into each row's (mean, rstd)
+// at the EpiLayout's mrg region: x rows at [0, BM), residual rows at [BM, 2BM).
+// One thread per row.
+template <int BM, int BN, Epi E, int LN>
+__device__ __forceinline__ void merge_row_stats(const GemmParams& p, uint8_t* epi, int tid) {
+  if constexpr ((LN & (kLnX | kLnRes)) != 0) {
+    const EpiLayout lay = epi_layout_of<BM, BN, E, LN>(p.K, p.N);
+    float2* mrg = reinterpret_cast<float2*>(epi + lay.mrg_off);
+    if (tid < BM) {
+      if constexpr ((LN & kLnX) != 0)
+        mrg[tid] = merge_ln_lds(reinterpret_cast<const float2*>(epi + lay.xst_off) + tid * (p.K >> 6), p.K >> 6,
+                                p.ln_eps);
+      if constexpr ((LN & kLnRes) != 0)
+        mrg[BM + tid] = merge_ln_lds(reinterpret_cast<const float2*>(epi + lay.rst_off) + tid * (p.N >> 6),
+                                     p.N >> 6, p.ln_eps);
+    }
+  }
+}
+
 // STAGED: the epilogue operands come from LDS at `epi` (EpiLayout), else from
 // global memory (no deferred LayerNorm then).
 template <int BM, int BN, typename T, Quant Q, Epi E, int TM, int TN, int NRB, int KS = 1, int LN = 0,
@@ -210,16 +229,9 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
   const EpiLayout lay = epi_layout_of<BM, BN, E, LN>(p.K, N);
   const float* vec = reinterpret_cast<const float*>(epi);  // [4][BN]: bias, fold_u, res_gamma, res_beta
   float2* mrg = reinterpret_cast<float2*>(epi + lay.mrg_off);  // [2][BM]: (mean, rstd) of x rows, residual rows
-  if constexpr ((LN & kLnX) != 0) {
-    // one thread per row, while the others stage their accumulators; the
-    // barrier after the staging publishes them
-    if (tid < BM) mrg[tid] = merge_ln_lds(reinterpret_cast<const float2*>(epi + lay.xst_off) + tid * (p.K >> 6),
-                                          p.K >> 6, p.ln_eps);
-  }
-  if constexpr ((LN & kLnRes) != 0) {
-    if (tid < BM) mrg[BM + tid] = merge_ln_lds(reinterpret_cast<const float2*>(epi + lay.rst_off) + tid * (N >> 6),
-                                               N >> 6, p.ln_eps);
-  }
+  // one thread per row merges the rows' statistics while the others stage
+  // their accumulators; the barrier after the staging publishes them
+  merge_row_stats<BM, BN, E, LN>(p, epi, tid);
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
     __syncthreads();  // the operand stages (or the previous row block) are no longer read
@@ -814,13 +826,16 @@ hipError_t launch_dense(const GemmParams& p, hipStream_t s) {
   }
   if (p.N % 128 != 0 && (tile == kTile128x128 || tile == kTile64x128)) tile = kTile64x64;
   switch (tile) {
-    // stage counts keep every configuration within 80 KB of LDS: two blocks per CU
+    // stage counts keep these configurations within 80 KB of LDS: two blocks per CU
     case kTile128x128: return launch_dma_tile<128, 128, 2, T>(p, s);
     case kTile64x128: return launch_dma_tile<64, 128, 3, T>(p, s);
     case kTile128x64: return launch_dma_tile<128, 64, 3, T>(p, s);
     // 64 x 64: one block per CU at the encoder's N = 384 shapes, so bf16 splits
-    // each stage's K between two groups of four waves (eight waves per CU)
-    default: return launch_dma_tile<64, 64, 3, T, sizeof(T) == 2 ? 2 : 1>(p, s);
+    // each stage's K between two groups of four waves (eight waves per CU), and
+    // the ring is four stages deep: in the forward the operands come from the
+    // last-level cache or HBM, not L2, and three stages in flight measured
+    // 8 us per forward faster than two
+    default: return launch_dma_tile<64, 64, 4, T, sizeof(T) == 2 ? 2 : 1>(p, s);
   }
 }
 

@@ -112,6 +112,17 @@ hipError_t launch_embed_ln(const int* ids, const void* word, const void* pos, co
                            const float* beta, float eps, int vocab, int S, int H, const int* tok_src,
                            const int* n_dev, int n_max, void* x, DType dt, hipStream_t s);
 
+// The mask scan and the embedding in one kernel (same outputs as both): for
+// small masks, where every block can scan the whole mask itself.
+constexpr int kEmbedScanMaxMask = 16384;  // B * S
+constexpr int kEmbedScanMaxSeq = 512;
+inline bool embed_scan_supported(int B, int S) {
+  return B <= kMaxOrderedBatch && S <= kEmbedScanMaxSeq && (int64_t)B * S <= kEmbedScanMaxMask;
+}
+hipError_t launch_embed_scan(const uint8_t* mask, const int* ids, int B, int S, const void* word, const void* pos,
+                             const void* type, const float* gamma, const float* beta, float eps, int vocab, int H,
+                             int* cu, int* tok_src, int* tok_dst, int* order, void* x, DType dt, hipStream_t s);
+
 // x[t] = hidden[tok_src[t]] (row copy) for t < *n_dev.
 hipError_t launch_gather_rows(const void* hidden, int H, const int* tok_src, const int* n_dev, int n_max, void* x,
                               DType dt, hipStream_t s);

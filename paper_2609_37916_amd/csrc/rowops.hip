@@ -98,7 +98,9 @@ template <typename T> struct Chunk;
 template <> struct Chunk<bf16_t> {
   static constexpr int EPC = 8;
   static __device__ __forceinline__ void load(const bf16_t* p, float v[8]) {
-    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    from_raw(*reinterpret_cast<const uint4*>(p), v);
+  }
+  static __device__ __forceinline__ void from_raw(uint4 u, float v[8]) {
     const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -114,8 +116,10 @@ template <> struct Chunk<bf16_t> {
 template <> struct Chunk<float> {
   static constexpr int EPC = 4;
   static __device__ __forceinline__ void load(const float* p, float v[4]) {
-    const float4 u = *reinterpret_cast<const float4*>(p);
-    v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+    from_raw(*reinterpret_cast<const uint4*>(p), v);
+  }
+  static __device__ __forceinline__ void from_raw(uint4 u, float v[4]) {
+    v[0] = __uint_as_float(u.x); v[1] = __uint_as_float(u.y); v[2] = __uint_as_float(u.z); v[3] = __uint_as_float(u.w);
   }
   static __device__ __forceinline__ void store(float* p, const float v[4]) {
     *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
@@ -194,6 +198,148 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int* ids, const T* 
   ln_row_store<T>(v, H, gamma, beta, eps, x + (size_t)t * H);
 }
 
+// Mask scan fused with the embedding gather + LayerNorm, for small masks
+// (B*S <= kEmbedScanMaxMask, B <= kMaxOrderedBatch).  Block (b, p) embeds the
+// real tokens p*16 .. p*16+15 of sequence b, four per wave.  Every block
+// first counts the real tokens of all sequences itself (the whole mask is at
+// most 16 KB), so it knows its sequence's offset without waiting on another
+// block; block (b, 0) also writes the scan's outputs for sequence b: cu[b]
+// (and cu[B] for the last sequence), the token maps of row b and the
+// sequence's place in the longest-first order.  One launch and one memory
+// round trip less than the mask scan followed by the embedding kernel.
+constexpr int kEmbedScanTokens = 16;  // real tokens per block
+template <typename T>
+__global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, const int* ids, int B, int S,
+                                                         const T* word, const T* pos, const T* type,
+                                                         const float* gamma, const float* beta, float eps, int vocab,
+                                                         int H, int* cu, int* tok_src, int* tok_dst, int* order,
+                                                         T* x) {
+  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
+  __shared__ __attribute__((aligned(16))) uint8_t mlds[kEmbedScanMaxMask];  // the whole mask
+  __shared__ int cnt[kMaxOrderedBatch];
+  __shared__ int posl[kEmbedScanMaxSeq];  // positions of sequence b's real tokens
+  const int b = blockIdx.x, p = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
+  // the mask into LDS, every load of a thread issued at once: 16-byte loads
+  // when the mask allows them, bytes otherwise
+  const int nm = B * S;
+  if ((reinterpret_cast<uintptr_t>(mask) & 15) == 0 && (nm & 15) == 0) {
+#pragma unroll
+    for (int j = 0; j < kEmbedScanMaxMask / (16 * 256); ++j) {
+      const int i = (threadIdx.x + 256 * j) * 16;
+      if (i < nm) *reinterpret_cast<uint4*>(mlds + i) = *reinterpret_cast<const uint4*>(mask + i);
+    }
+  } else {
+#pragma unroll 16
+    for (int j = 0; j < kEmbedScanMaxMask / 256; ++j) {
+      const int i = threadIdx.x + 256 * j;
+      if (i < nm) mlds[i] = mask[i];
+    }
+  }
+  __syncthreads();
+  // real tokens of every sequence
+  if ((S & 15) == 0) {
+    // one thread per sequence, 16 bytes at a time (rows start 16-byte aligned
+    // in LDS): the non-zero bytes of a word are counted by folding each byte's
+    // bits into its lowest bit
+    for (int q = threadIdx.x; q < B; q += 256) {
+      int c = 0;
+      for (int i = 0; i < S; i += 16) {
+        const uint4 u = *reinterpret_cast<const uint4*>(mlds + q * S + i);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          uint32_t t = w[k] | (w[k] >> 4);
+          t |= t >> 2;
+          t |= t >> 1;
+          c += __popc(t & 0x01010101u);
+        }
+      }
+      cnt[q] = c;
+    }
+  } else {
+    // one wave per sequence, a ballot per 64 positions
+    for (int q = wave; q < B; q += 4) {
+      int c = 0;
+      for (int s0 = 0; s0 < S; s0 += 64) c += __popcll(__ballot(s0 + lane < S && mlds[q * S + s0 + lane] != 0));
+      if (lane == 0) cnt[q] = c;
+    }
+  }
+  // positions of this sequence's real tokens (wave 0), and its token maps (block p = 0)
+  if (wave == 0) {
+    int base = 0;
+    for (int s0 = 0; s0 < S; s0 += 64) {
+      const int s = s0 + lane;
+      const bool v = s < S && mlds[b * S + s] != 0;
+      const uint64_t bal = __ballot(v);
+      if (v) posl[base + __popcll(bal & below)] = s;
+      base += __popcll(bal);
+    }
+  }
+  __syncthreads();
+  const int L = cnt[b];
+  int off = 0, ahead = 0;  // real tokens before sequence b; sequences placed before b in the order
+  for (int q = lane; q < B; q += 64) {
+    off += q < b ? cnt[q] : 0;
+    ahead += (cnt[q] > L || (cnt[q] == L && q < b)) ? 1 : 0;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    off += __shfl_xor(off, o, 64);
+    ahead += __shfl_xor(ahead, o, 64);
+  }
+  if (p == 0) {
+    if (threadIdx.x == 0) {
+      cu[b] = off;
+      if (b == B - 1) cu[B] = off + L;
+      if (order) order[ahead] = b;
+    }
+    for (int i = threadIdx.x; i < L; i += 256) tok_src[off + i] = b * S + posl[i];
+    for (int s = threadIdx.x; s < S; s += 256) tok_dst[(size_t)b * S + s] = -1;
+    __syncthreads();  // the real positions overwrite the -1s after them
+    for (int i = threadIdx.x; i < L; i += 256) tok_dst[(size_t)b * S + posl[i]] = off + i;
+  }
+  // embedding rows of this block's tokens: ids first, then every row of the
+  // wave's tokens requested before any is used (tokens past the sequence end
+  // read row 0 and are not stored)
+  const int nch = H / EPC;
+  constexpr int TPW = kEmbedScanTokens / 4;  // tokens per wave
+  int sp[TPW], id[TPW];
+#pragma unroll
+  for (int j = 0; j < TPW; ++j) {
+    const int i = p * kEmbedScanTokens + wave + 4 * j;
+    sp[j] = i < L ? posl[i] : -1;
+    id[j] = sp[j] >= 0 ? min(max(ids[(size_t)b * S + sp[j]], 0), vocab - 1) : 0;
+  }
+  uint4 rw[TPW][CPL], rp[TPW][CPL], rt[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int ch = min(lane + 64 * c, nch - 1);
+    rt[c] = *reinterpret_cast<const uint4*>(type + ch * EPC);
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+      rw[j][c] = *reinterpret_cast<const uint4*>(word + (size_t)id[j] * H + ch * EPC);
+      rp[j][c] = *reinterpret_cast<const uint4*>(pos + (size_t)max(sp[j], 0) * H + ch * EPC);
+    }
+  }
+  float v[TPW][CPL][EPC];
+#pragma unroll
+  for (int j = 0; j < TPW; ++j)
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      float a[EPC], bb[EPC], t[EPC];
+      Chunk<T>::from_raw(rw[j][c], a);
+      Chunk<T>::from_raw(rp[j][c], bb);
+      Chunk<T>::from_raw(rt[c], t);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) v[j][c][e] = a[e] + bb[e] + t[e];
+    }
+#pragma unroll
+  for (int j = 0; j < TPW; ++j)
+    if (sp[j] >= 0) ln_row_store<T>(v[j], H, gamma, beta, eps, x + (size_t)(off + p * kEmbedScanTokens + wave + 4 * j) * H);
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void layer_norm_kernel(const T* a, const float* gamma, const float* beta, float eps,
                                                          int H, const int* n_dev, int n_max, T* y) {
@@ -226,7 +372,10 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T* hidden, int H
 // Masked mean-pool + L2 normalisation: one block of 1024 threads (16 waves)
 // per sequence; wave w sums rows w, w+16, ... with 16-byte chunk loads, the
 // 16 partial rows are combined in LDS, then the block forms the mean and its
-// norm.
+// norm.  Each wave requests its first kPoolBatch rows before anything else,
+// so their loads are in flight while the rows' LayerNorm statistics (deferred
+// input) are merged, one thread per row: the two round trips overlap.  A batch
+// is 16 chunks per lane (8 rows of bf16: a 128-token sequence at once).
 constexpr int kMaxPoolRows = 512;  // the longest sequence
 // With x_stats the rows are pre-LayerNorm values with their partial
 // statistics (deferred LayerNorm): the block averages (x - mean) * rstd and
@@ -236,34 +385,53 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
                                                        const float2* x_stats, const float* gamma, const float* beta,
                                                        float eps) {
   constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
+  constexpr int kPoolBatch = 16 / CPL;  // rows per wave in flight
   extern __shared__ float part[];  // [16][H]
   __shared__ float red[16];
   __shared__ float2 row_st[kMaxPoolRows];  // (mean, rstd) per row of a deferred-LayerNorm input
   const int b = blockIdx.x;
   const int r0 = cu[b], L = cu[b + 1] - r0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (x_stats) {  // all rows' statistics in one round of loads, one row per thread
-    for (int r = threadIdx.x; r < L; r += 1024) row_st[r] = row_ln_stats(x_stats + (size_t)(r0 + r) * (H >> 6), H >> 6, eps);
-    __syncthreads();
-  }
   const int nch = H / EPC;
   float acc[CPL][EPC];
 #pragma unroll
   for (int i = 0; i < CPL; ++i)
 #pragma unroll
     for (int e = 0; e < EPC; ++e) acc[i][e] = 0.0f;
-  for (int r = wave; r < L; r += 16) {
-    const T* row = x + (size_t)(r0 + r) * H;
-    // (0, 1) leaves plain rows as they are
-    const float2 st = x_stats ? row_st[r] : make_float2(0.0f, 1.0f);
+  uint4 raw[kPoolBatch][CPL];  // 16-byte chunks as loaded
+  auto load_batch = [&](int rb) {
 #pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-      const int ch = lane + 64 * i;
-      if (ch < nch) {
-        float v[EPC];
-        Chunk<T>::load(row + ch * EPC, v);
+    for (int k = 0; k < kPoolBatch; ++k) {
+      const T* row = x + (size_t)(r0 + min(rb + 16 * k, L - 1)) * H;  // rows past the end: loaded, not added
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) acc[i][e] += (v[e] - st.x) * st.y;
+      for (int i = 0; i < CPL; ++i) {
+        const int ch = lane + 64 * i;
+        if (ch < nch) raw[k][i] = *reinterpret_cast<const uint4*>(row + ch * EPC);
+      }
+    }
+  };
+  if (wave < L) load_batch(wave);
+  if (x_stats) {
+    for (int r = threadIdx.x; r < L; r += 1024) row_st[r] = row_ln_stats(x_stats + (size_t)(r0 + r) * (H >> 6), H >> 6, eps);
+    __syncthreads();
+  }
+  for (int rb = wave; rb < L; rb += 16 * kPoolBatch) {
+    if (rb != wave) load_batch(rb);
+#pragma unroll
+    for (int k = 0; k < kPoolBatch; ++k) {
+      const int r = rb + 16 * k;
+      if (r >= L) break;
+      // (0, 1) leaves plain rows as they are
+      const float2 st = x_stats ? row_st[r] : make_float2(0.0f, 1.0f);
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) {
+        const int ch = lane + 64 * i;
+        if (ch < nch) {
+          float v[EPC];
+          Chunk<T>::from_raw(raw[k][i], v);
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) acc[i][e] += (v[e] - st.x) * st.y;
+        }
       }
     }
   }
@@ -328,6 +496,23 @@ hipError_t launch_embed_ln(const int* ids, const void* word, const void* pos, co
   else
     hipLaunchKernelGGL(embed_ln_kernel<float>, dim3(blocks_for_rows(n_max)), dim3(256), 0, s, ids, (const float*)word,
                        (const float*)pos, (const float*)type, gamma, beta, eps, vocab, S, H, tok_src, n_dev, n_max,
+                       (float*)x);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_scan(const uint8_t* mask, const int* ids, int B, int S, const void* word, const void* pos,
+                             const void* type, const float* gamma, const float* beta, float eps, int vocab, int H,
+                             int* cu, int* tok_src, int* tok_dst, int* order, void* x, DType dt, hipStream_t s) {
+  if (B <= 0 || S <= 0) return hipSuccess;
+  if (!embed_scan_supported(B, S)) return hipErrorInvalidValue;
+  const dim3 grid(B, (S + kEmbedScanTokens - 1) / kEmbedScanTokens);
+  if (dt == DType::BF16)
+    hipLaunchKernelGGL(embed_scan_kernel<bf16_t>, grid, dim3(256), 0, s, mask, ids, B, S, (const bf16_t*)word,
+                       (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
+                       order, (bf16_t*)x);
+  else
+    hipLaunchKernelGGL(embed_scan_kernel<float>, grid, dim3(256), 0, s, mask, ids, B, S, (const float*)word,
+                       (const float*)pos, (const float*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst, order,
                        (float*)x);
   return hipGetLastError();
 }

@@ -185,7 +185,9 @@ def test_encoder_profile_mode(rlx, name, attn_kernel):
     enc.forward(inputs["input"], inputs["mask"])
     enc.forward(inputs["input"], inputs["mask"])
     prof = enc.profile_read()
-    assert prof["gemm_ffn_up"][0] == 12 and prof[attn_kernel][0] == 12 and prof["mask_scan"][0] == 2
+    assert prof["gemm_ffn_up"][0] == 12 and prof[attn_kernel][0] == 12 and prof["embed_ln"][0] == 2
+    # a 4 x 128 mask is small enough for the embedding kernel to scan it itself
+    assert "mask_scan" not in prof
     # dense bf16 weights: the LayerNorms are applied by the kernels that read their inputs
     deferred = name.endswith("bf16")
     assert ("layer_norm_1" in prof) != deferred and ("layer_norm_2" in prof) != deferred
