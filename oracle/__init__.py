@@ -23,6 +23,10 @@ of all-MiniLM-L6-v2 (Section VIII-B), but prints no formula for the encoder.
 The layer-level definitions are the standard post-LN BERT encoder; every point
 where a reading had to be chosen is listed in the module docstrings below.
 
+``oracle.mx`` is the block-scaled minifloat matmul of the ScaledMatMul path
+(FP8 / FP6 / FP4 elements with E8M0 block scales), decoded from the format
+definitions and multiplied in float64.
+
 Pins (tests/test_oracle_*.py) tie each function to something other than
 itself: brute force on tiny inputs, closed forms, invariants, library special
 cases (torch SDPA, nn.TransformerEncoderLayer, transformers.BertModel in
@@ -34,3 +38,4 @@ from .encoder import (  # noqa: F401
     embed, encoder_layer, mean_pool_l2, encoder_forward, layer_weights,
 )
 from .quant import unpack_int4, dequant_int8, dequant_int4  # noqa: F401
+from . import mx  # noqa: F401

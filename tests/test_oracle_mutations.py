@@ -242,3 +242,92 @@ def test_planted_mistake_fails_a_pin(name, monkeypatch):
         except Exception as e:  # an assertion, or a shape error from the planted mistake
             failed.append(type(e).__name__)
     assert failed, f"no pin caught the planted mistake '{name}'"
+
+
+# --- planted mistakes in the block-scaled minifloat matmul oracle ---
+
+import oracle.mx as omx  # noqa: E402
+import test_oracle_mx as mxpins  # noqa: E402
+
+MX_ORIG = {n: getattr(omx, n) for n in ("decode", "decode_scale", "unpack", "dequant", "MX_FORMATS")}
+
+
+def _mx_pin_calls():
+    calls = [mxpins.test_decode_values_fixed_by_the_format_definitions,
+             mxpins.test_float8_decode_matches_torch_for_every_code,
+             mxpins.test_block_scale_multiplies_its_block_only]
+    for fmt in mxpins.FORMATS:
+        calls.append(lambda fmt=fmt: mxpins.test_grid_structure(fmt))
+        calls.append(lambda fmt=fmt: mxpins.test_unpack_matches_bit_loop(fmt))
+    for fa, fb in [("e4m3", "e4m3"), ("e5m2", "e2m1"), ("e2m3", "e3m2"), ("e2m1", "e2m1")]:
+        calls.append(lambda fa=fa, fb=fb: mxpins.test_scaled_matmul_matches_exact_rational_brute_force(fa, fb))
+    return calls
+
+
+def mx_subnormal_as_normal(codes, fmt):
+    c = np.asarray(codes, dtype=np.int64)
+    ebits, mbits, bias = MX_ORIG["MX_FORMATS"][fmt]
+    v = MX_ORIG["decode"](codes, fmt)
+    e = (c >> mbits) & ((1 << ebits) - 1)
+    m = (c & ((1 << mbits) - 1)).astype(np.float64)
+    sign = np.where((c >> (ebits + mbits)) & 1, -1.0, 1.0)
+    return np.where(e == 0, sign * np.ldexp(1.0 + m / (1 << mbits), -bias), v)
+
+
+def mx_e4m3_ieee_specials(codes, fmt):
+    v = MX_ORIG["decode"](codes, fmt)
+    if fmt != "e4m3":
+        return v
+    c = np.asarray(codes, dtype=np.int64)
+    return np.where((c & 0x78) == 0x78, np.where((c & 7) == 0, np.inf, np.nan), v)
+
+
+def mx_scale_bias_128(s):
+    return MX_ORIG["decode_scale"](s) / 2.0
+
+
+def mx_fp4_high_nibble_first(packed, fmt, K):
+    q = MX_ORIG["unpack"](packed, fmt, K)
+    if fmt == "e2m1":
+        q = q.reshape(q.shape[0], -1, 2)[:, :, ::-1].reshape(q.shape)
+    return q
+
+
+def mx_fp6_big_endian(packed, fmt, K):
+    if fmt not in ("e2m3", "e3m2"):
+        return MX_ORIG["unpack"](packed, fmt, K)
+    p = np.asarray(packed, dtype=np.uint8)
+    w = p.reshape(p.shape[0], K // 4, 3).astype(np.uint32)
+    word = (w[:, :, 0] << 16) | (w[:, :, 1] << 8) | w[:, :, 2]
+    q = np.stack([(word >> (18 - 6 * i)) & 0x3F for i in range(4)], axis=-1)
+    return q.reshape(p.shape[0], K).astype(np.uint8)
+
+
+def mx_scale_per_element_block_shifted(packed, scales, fmt, K):
+    v = omx.decode(omx.unpack(packed, fmt, K), fmt)
+    x = omx.decode_scale(scales)
+    idx = np.minimum((np.arange(K) + 1) // 32, K // 32 - 1)  # block boundary off by one
+    return v * x[:, idx]
+
+
+MX_MUTANTS = {
+    "mx: subnormals decoded as normals": ("decode", mx_subnormal_as_normal),
+    "mx: E4M3 with IEEE infinities": ("decode", mx_e4m3_ieee_specials),
+    "mx: E8M0 bias 128": ("decode_scale", mx_scale_bias_128),
+    "mx: FP4 high nibble first": ("unpack", mx_fp4_high_nibble_first),
+    "mx: FP6 big-endian packing": ("unpack", mx_fp6_big_endian),
+    "mx: block boundary off by one": ("dequant", mx_scale_per_element_block_shifted),
+}
+
+
+@pytest.mark.parametrize("name", list(MX_MUTANTS))
+def test_planted_mx_mistake_fails_a_pin(name, monkeypatch):
+    attr, fake = MX_MUTANTS[name]
+    monkeypatch.setattr(omx, attr, fake)
+    failed = []
+    for call in _mx_pin_calls():
+        try:
+            call()
+        except Exception as e:
+            failed.append(type(e).__name__)
+    assert failed, f"no pin caught the planted mistake '{name}'"
