@@ -42,12 +42,17 @@ def attention_flops(sp, lengths):
     return sum(4 * sp.head_dim * sp.heads * int(L) ** 2 for L in lengths)
 
 
-def kernel_source_digest():
-    """Digest of every kernel source: counter figures taken before a change to
-    any of them are no longer reported."""
+# the source file that holds each measured kernel class (with the shared device helpers)
+KERNEL_SOURCES = {"qkv_attention": "attention.hip", "attention": "attention.hip", "mx_gemm": "mx_gemm.hip"}
+
+
+def kernel_source_digest(kernel_class="gemm"):
+    """Digest of the sources of one kernel class (its .hip file and the shared
+    device helpers): counter figures taken before a change to them are no
+    longer reported."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_37916_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in sorted({KERNEL_SOURCES.get(kernel_class, "gemm.hip"), "common.hpp"}):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
@@ -55,14 +60,14 @@ def kernel_source_digest():
 
 def committed_traffic(kernel_class, workload):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when no summary exists or the GEMM sources changed since it was taken."""
+    None when no summary exists or the kernel's sources changed since it was taken."""
     path = os.path.join(ROOT, "profiles", f"{kernel_class}_{workload}_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m_b = re.search(r"^hbm_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
     m_h = re.search(r"^kernel_source_digest:\s*([0-9a-f]+)", text, re.M)
-    if not m_b or not m_h or m_h.group(1) != kernel_source_digest():
+    if not m_b or not m_h or m_h.group(1) != kernel_source_digest(kernel_class):
         return None
     return float(m_b.group(1))
 
@@ -98,6 +103,76 @@ def cpu_baseline(workload_name, target_s):
             "sample": f"{what} of {workload_name}, float64 NumPy oracle, {dt:.1f} s"}
 
 
+MX_PEAK_TFLOPS = {"e4m3": 5000.0, "e5m2": 5000.0, "e2m3": 10100.0, "e3m2": 10100.0, "e2m1": 10100.0}
+
+
+def bench_scaled_matmul(args):
+    """Block-scaled minifloat matmul (rlx_scaled_matmul) on one shape: the
+    encoder's FFN-down at batch 256 x 128 by default (18048 real tokens)."""
+    import numpy as np
+    import torch
+
+    import paper_2609_37916_amd as rlx
+    from workloads import mx as wmx
+
+    M, N, K = args.mx_shape
+    fx = fw = args.mx_format
+    x, w = wmx.matmul_inputs(1, M, N, K, fx, fw)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+    xp, xs, wp, ws = dev(x.packed), dev(x.scales), dev(w.packed), dev(w.scales)
+    y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        rlx.scaled_matmul(xp, xs, fx, wp, ws, fw, K=K, out=y)
+    torch.cuda.synchronize()
+    # K back-to-back launches between two events on the launch stream (per-launch
+    # event pairs would add the enqueue gap to every launch)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(args.steps):
+        rlx.scaled_matmul(xp, xs, fx, wp, ws, fw, K=K, out=y)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = 1e3 * e0.elapsed_time(e1) / args.steps
+    launch_us = [us]
+    flops = 2.0 * M * N * K
+    tf = flops / (us * 1e-6) / 1e12
+    peak = MX_PEAK_TFLOPS[fx]
+    name = f"mx_{fx}_m{M}_n{N}_k{K}"
+    rec = {
+        "metric": f"scaled matmul TFLOP/s (MX {fx} x {fw}, {M}x{N}x{K}, 1 MI355X)",
+        "value": round(tf, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(us / 1e3, 5), "p50_ms": round(statistics.median(launch_us) / 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": fx,
+        "data": "synthetic (seeded finite codes, E8M0 scales 2^-7 .. 2^7)",
+        "config": {"workload": name, "M": M, "N": N, "K": K, "format_x": fx, "format_w": fw,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "mx_gemm_kernel", "achieved": round(tf, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(tf / peak, 4), "traffic": committed_traffic("mx_gemm", name),
+                     "flops_per_launch": flops, "avg_launch_us": round(us, 3)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        rows = min(M, 2048)
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            oracle.mx.scaled_matmul(x.packed[:rows], x.scales[:rows], fx, w.packed, w.scales, fw, K)
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= args.cpu_seconds or reps >= 1000:
+                break
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+        except Exception:
+            threads = os.cpu_count() or 1
+        rec["cpu_baseline"] = {"value": round(2.0 * rows * N * K * reps / dt / 1e12, 4), "unit": "TFLOP/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"first {rows} rows of X, {reps} times, float64 NumPy oracle, {dt:.1f} s"}
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -107,6 +182,10 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=20, help="profiled forwards (per-kernel event times)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--op", choices=("encoder", "scaled_matmul"), default="encoder",
+                    help="encoder: the encoder forward (default); scaled_matmul: the block-scaled minifloat matmul")
+    ap.add_argument("--mx-format", default="e4m3", choices=sorted(MX_PEAK_TFLOPS))
+    ap.add_argument("--mx-shape", type=int, nargs=3, default=(18048, 384, 1536), metavar=("M", "N", "K"))
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (counter calibration for FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
@@ -139,6 +218,10 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"calibration": "device copy", "bytes_read": src.numel() * 4, "bytes_written": dst.numel() * 4,
                           "launches": 3}), flush=True)
+        return
+
+    if args.op == "scaled_matmul":
+        bench_scaled_matmul(args)
         return
 
     sp = workloads.spec(args.workload)

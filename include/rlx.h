@@ -136,6 +136,39 @@ rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scale
                               int group_size, int N, int K, float* w_out, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Block-scaled minifloat matmul (the ScaledMatMul path of Section VI:
+ * block-scaled FP8 / FP6 / FP4 minifloats, checked bit for bit against an
+ * F32 reference), with the OCP Microscaling (MX v1.0) element formats:
+ *
+ *   y[m,n] = sum_k X(m,k) * W(n,k),   0 <= m < M, 0 <= n < N
+ *   X(m,k) = 2^(x_scales[m*K/32 + k/32] - 127) * decode_fx(code of x at (m,k)),
+ *   W(n,k) likewise (nn.Linear convention: one W row per output column).
+ *
+ * Element formats (rlx_mx_format): E4M3 and E5M2 (one byte per code), E2M3
+ * and E3M2 (four codes per three bytes: code i of a row occupies bits
+ * 6i .. 6i+5 of the row's bytes read as one little-endian integer), E2M1
+ * (two codes per byte, the lower k in the low nibble).  Every row of x is
+ * K*bits/8 bytes, rows contiguous; likewise w.  Scales: one E8M0 byte per
+ * row and 32-element block, [M, K/32] and [N, K/32].  y: f32 [M, N].
+ * The products are exact and the sums are accumulated in fp32 by the matrix
+ * cores, which add the 64 products of one instruction with a narrow aligned
+ * adder: the result is bit-exact when the products of each 64-element step
+ * are close in magnitude and every partial sum is exact in fp32; otherwise its
+ * error stays below 2^-10 * sum_k |X(m,k) W(n,k)| (measured: 2^-11.3).
+ * NaN / Inf codes and the NaN scale (255) give unspecified results.
+ * Supported: M >= 0 (M == 0 is a no-op; x, x_scales and y may then be
+ * NULL), N and K positive multiples of 128;
+ * x, w and y 16-byte aligned, x_scales and w_scales 4-byte aligned.
+ * Otherwise RLX_ERR_UNSUPPORTED (alignment, sizes) or RLX_ERR_INVALID_ARG.
+ * All pointers are device pointers owned by the caller.
+ */
+typedef enum { RLX_MX_E4M3 = 0, RLX_MX_E5M2 = 1, RLX_MX_E2M3 = 2, RLX_MX_E3M2 = 3, RLX_MX_E2M1 = 4 } rlx_mx_format;
+
+rlx_status rlx_scaled_matmul(const void* x, const uint8_t* x_scales, rlx_mx_format fx, const void* w,
+                             const uint8_t* w_scales, rlx_mx_format fw, int M, int N, int K, float* y,
+                             void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Encoder: compile once (bind weights, plan the workspace), run many times
  * (the paper's Session::compile -> CompiledGraph executed with bound inputs,
  * Section III-C).

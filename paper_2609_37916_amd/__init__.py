@@ -22,13 +22,16 @@ F32, BF16, F16, I8, U4X2, I32, U8 = range(7)
 MASK_NONE, MASK_CAUSAL, MASK_SLIDING_WINDOW, MASK_CUSTOM = range(4)
 Q_NONE, Q_INT8_PER_CHANNEL, Q_INT4_GROUP_ZP = range(3)
 EPI_NONE, EPI_BIAS, EPI_BIAS_GELU, EPI_BIAS_RESIDUAL = range(4)
+MX_E4M3, MX_E5M2, MX_E2M3, MX_E3M2, MX_E2M1 = range(5)
+MX_FORMAT_CODES = {"e4m3": MX_E4M3, "e5m2": MX_E5M2, "e2m3": MX_E2M3, "e3m2": MX_E3M2, "e2m1": MX_E2M1}
 INPUT_IDS, INPUT_HIDDEN = range(2)
 OUTPUT_POOLED, OUTPUT_HIDDEN = range(2)
 
 STATUS_NAMES = {0: "RLX_OK", 1: "RLX_ERR_INVALID_ARG", 2: "RLX_ERR_UNSUPPORTED", 3: "RLX_ERR_HIP", 4: "RLX_ERR_OOM"}
 
 # every symbol include/rlx.h declares
-EXPORTS = ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_encoder_create",
+EXPORTS = ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_scaled_matmul",
+           "rlx_encoder_create",
            "rlx_encoder_forward", "rlx_encoder_destroy", "rlx_encoder_set_profiling", "rlx_encoder_profile_read",
            "rlx_last_error", "rlx_version")
 
@@ -84,6 +87,7 @@ def lib() -> ctypes.CDLL:
     L.rlx_masked_attention.argtypes = [_vp, _vp, _vp, i64, _vp, i64, i32, i32, i32, i32, i32, i32, _vp, i32, f32, _vp]
     L.rlx_dequant_matmul.argtypes = [_vp, i32, i32, i32, _vp, i32, _vp, _vp, i32, i32, _vp, _vp, i32, _vp, _vp]
     L.rlx_dequant_unpack.argtypes = [_vp, i32, _vp, _vp, i32, i32, i32, _vp, _vp]
+    L.rlx_scaled_matmul.argtypes = [_vp, _vp, i32, _vp, _vp, i32, i32, i32, i32, _vp, _vp]
     L.rlx_encoder_create.argtypes = [ctypes.POINTER(EncoderConfig), ctypes.POINTER(EncoderWeights),
                                      ctypes.POINTER(_vp)]
     L.rlx_encoder_forward.argtypes = [_vp, _vp, _vp, i32, i32, _vp, _vp]
@@ -92,7 +96,7 @@ def lib() -> ctypes.CDLL:
     L.rlx_encoder_set_profiling.argtypes = [_vp, i32]
     L.rlx_encoder_profile_read.argtypes = [_vp, i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(i32),
                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
-    for nm in ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_encoder_create",
+    for nm in ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_scaled_matmul", "rlx_encoder_create",
                "rlx_encoder_forward", "rlx_encoder_set_profiling", "rlx_encoder_profile_read"):
         getattr(L, nm).restype = ctypes.c_int
     L.rlx_last_error.restype = ctypes.c_char_p
@@ -177,6 +181,32 @@ def dequant_matmul(x, w, *, scheme: int = Q_NONE, scales=None, zeros=None, group
         out = torch.empty((M, N), dtype=x.dtype, device=x.device)
     check(lib().rlx_dequant_matmul(_ptr(x), _dt(x), M, K, _ptr(w), scheme, _ptr(scales), _ptr(zeros), group_size, N,
                                    _ptr(bias), _ptr(residual), epi, _ptr(out), _stream(stream)))
+    return out
+
+
+def scaled_matmul(x, x_scales, fx, w, w_scales, fw, *, K: int, out=None, stream=None):
+    """y = X W^T for block-scaled minifloat operands (see rlx_scaled_matmul).
+
+    x, w: uint8 device tensors of packed rows ([M, K*bits/8], [N, K*bits/8]);
+    x_scales, w_scales: uint8 [M, K/32], [N, K/32]; fx, fw: format names
+    ("e4m3", "e5m2", "e2m3", "e3m2", "e2m1") or codes.  Returns float32 [M, N]."""
+    torch = _torch()
+    fx = MX_FORMAT_CODES.get(fx, fx)
+    fw = MX_FORMAT_CODES.get(fw, fw)
+    M, N = x.shape[0], w.shape[0]
+    bits = {MX_E4M3: 8, MX_E5M2: 8, MX_E2M3: 6, MX_E3M2: 6, MX_E2M1: 4}
+    if fx not in bits or fw not in bits:
+        raise ValueError(f"unknown element format {fx!r} / {fw!r}")
+    # the C ABI cannot see buffer sizes: check them here so no kernel reads past a tensor
+    for t, rows, nbytes, what in ((x, M, K * bits[fx] // 8, "x"), (w, N, K * bits[fw] // 8, "w"),
+                                  (x_scales, M, K // 32, "x_scales"), (w_scales, N, K // 32, "w_scales")):
+        if t.dtype != torch.uint8 or not t.is_contiguous() or t.numel() != rows * nbytes:
+            raise ValueError(f"{what}: expected a contiguous uint8 tensor of {rows} x {nbytes} bytes, "
+                             f"got {t.dtype} {tuple(t.shape)}")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=x.device)
+    check(lib().rlx_scaled_matmul(_ptr(x), _ptr(x_scales), fx, _ptr(w), _ptr(w_scales), fw, M, N, K, _ptr(out),
+                                  _stream(stream)))
     return out
 
 

@@ -640,6 +640,29 @@ rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const
   return ok();
 }
 
+rlx_status rlx_scaled_matmul(const void* x, const uint8_t* x_scales, rlx_mx_format fx, const void* w,
+                             const uint8_t* w_scales, rlx_mx_format fw, int M, int N, int K, float* y,
+                             void* stream) {
+  if (M < 0 || N <= 0 || K <= 0)
+    return fail(RLX_ERR_INVALID_ARG, "scaled_matmul: M=%d must be >= 0, N=%d and K=%d positive", M, N, K);
+  if (fx < RLX_MX_E4M3 || fx > RLX_MX_E2M1 || fw < RLX_MX_E4M3 || fw > RLX_MX_E2M1)
+    return fail(RLX_ERR_INVALID_ARG, "scaled_matmul: unknown element format (%d, %d)", (int)fx, (int)fw);
+  if (!w || !w_scales || (M > 0 && (!x || !x_scales || !y)))
+    return fail(RLX_ERR_INVALID_ARG, "scaled_matmul: x, x_scales, w, w_scales and y must be non-null");
+  if (!mx_gemm_supported(M, N, K))
+    return fail(RLX_ERR_UNSUPPORTED, "scaled_matmul: N=%d and K=%d must be multiples of 128", N, K);
+  if (!aligned16(x) || !aligned16(w) || !aligned16(y) || (reinterpret_cast<uintptr_t>(x_scales) & 3) ||
+      (reinterpret_cast<uintptr_t>(w_scales) & 3))
+    return fail(RLX_ERR_UNSUPPORTED, "scaled_matmul: x, w, y must be 16-byte and the scales 4-byte aligned");
+  if (M == 0) return ok();  // (x, x_scales and y may then be null)
+  MxGemmParams p{};
+  p.x = x; p.x_scales = x_scales; p.fx = (int)fx;
+  p.w = w; p.w_scales = w_scales; p.fw = (int)fw;
+  p.y = y; p.M = M; p.N = N; p.K = K;
+  RLX_HIP(launch_mx_gemm(p, static_cast<hipStream_t>(stream)), "scaled matmul launch");
+  return ok();
+}
+
 rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scales, const void* zeros, int group_size,
                               int N, int K, float* w_out, void* stream) {
   if (N <= 0 || K <= 0) return fail(RLX_ERR_INVALID_ARG, "dequant_unpack: N=%d and K=%d must be positive", N, K);

@@ -87,6 +87,19 @@ struct FusedAttnParams {
 };
 hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s);
 
+// Block-scaled minifloat matmul (ScaledMatMul): y[m,n] = sum_k X(m,k) W(n,k)
+// with OCP MX operands (format codes 0 E4M3, 1 E5M2, 2 E2M3, 3 E3M2, 4 E2M1;
+// 32 codes per E8M0 scale).  x: [M, K*bits/8], w: [N, K*bits/8] packed rows;
+// x_scales [M, K/32], w_scales [N, K/32] (4-byte aligned); y f32 [M, N].
+struct MxGemmParams {
+  const void* x; const uint8_t* x_scales; int fx;
+  const void* w; const uint8_t* w_scales; int fw;
+  float* y;
+  int M, N, K;
+};
+bool mx_gemm_supported(int M, int N, int K);  // N, K multiples of 128
+hipError_t launch_mx_gemm(const MxGemmParams& p, hipStream_t s);
+
 // Folds a LayerNorm (gamma, beta) into the linear layer that consumes it, for
 // the deferred-LayerNorm path: w_out[n,k] = bf16(gamma[k] * w[n,k]),
 // u_out[n] = sum_k w_out[n,k], v_out[n] = sum_k beta[k] * w[n,k] + bias[n]

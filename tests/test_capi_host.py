@@ -144,3 +144,23 @@ def test_encoder_create_weight_errors(L):
 def test_encoder_forward_null_handle(L):
     assert L.rlx_encoder_forward(None, 4096, 4096, 1, 1, 4096, None) == rlx.ERR_INVALID_ARG
     L.rlx_encoder_destroy(None)
+
+
+def test_scaled_matmul_argument_errors(L):
+    f = L.rlx_scaled_matmul
+    P = 4096  # aligned stand-in addresses: validation rejects before any use
+    E4M3, E2M1 = rlx.MX_E4M3, rlx.MX_E2M1
+    assert f(None, P, E4M3, P, P, E4M3, 8, 128, 128, P, None) == rlx.ERR_INVALID_ARG
+    assert b"non-null" in L.rlx_last_error()
+    assert f(P, P, 5, P, P, E4M3, 8, 128, 128, P, None) == rlx.ERR_INVALID_ARG
+    assert f(P, P, E4M3, P, P, -1, 8, 128, 128, P, None) == rlx.ERR_INVALID_ARG
+    assert f(P, P, E4M3, P, P, E2M1, -1, 128, 128, P, None) == rlx.ERR_INVALID_ARG
+    assert f(P, P, E4M3, P, P, E2M1, 8, 0, 128, P, None) == rlx.ERR_INVALID_ARG
+    assert f(P, P, E4M3, P, P, E2M1, 8, 192, 128, P, None) == rlx.ERR_UNSUPPORTED
+    assert b"multiples of 128" in L.rlx_last_error()
+    assert f(P, P, E4M3, P, P, E2M1, 8, 128, 96, P, None) == rlx.ERR_UNSUPPORTED
+    assert f(P + 8, P, E4M3, P, P, E2M1, 8, 128, 128, P, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, P + 2, E4M3, P, P, E2M1, 8, 128, 128, P, None) == rlx.ERR_UNSUPPORTED
+    assert b"aligned" in L.rlx_last_error()
+    # M == 0: a no-op that succeeds without touching the device
+    assert f(P, P, E4M3, P, P, E2M1, 0, 128, 128, P, None) == rlx.OK

@@ -1,0 +1,108 @@
+"""GPU parity of rlx_scaled_matmul (block-scaled FP8 / FP6 / FP4 matmul on the
+MX matrix cores) against the CPU oracle, through the C ABI.
+
+* Inputs whose float32 partial sums are exact (workloads.mx.exact_codes,
+  scales 2^-1 .. 2^1, K <= 512): the result must equal the oracle bit for bit,
+  for every pair of element formats.
+* General finite inputs: within 2^-10 sum_k |X(m,k)| |W(n,k)| of the exact
+  result.  The products are exact, but the matrix cores add the 64 products
+  of one instruction with a narrow aligned adder: measured on the GPU, the
+  error of an instruction reaches 2^-11.3 of its largest product when the
+  products span many binades (FP8, E3M2), and is 0 when they are close in
+  magnitude (the exact inputs above).  Summed over the K/64 instructions this
+  stays below 2^-11.3 sum_k |X Y|; the bound keeps a factor 2.5 of margin,
+  plus the float32 accumulation bound 2 K 2^-24 sum_k |X Y|.
+* The benchmark shape (18048 x 1536 x 384) on sampled rows, ragged row
+  counts, M = 0 and rejected sizes.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from workloads import mx as wmx
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+FORMATS = ("e4m3", "e5m2", "e2m3", "e3m2", "e2m1")
+PAIRS = [(fx, fw) for fx in FORMATS for fw in FORMATS]
+
+
+@pytest.fixture(scope="module")
+def rlx():
+    import paper_2609_37916_amd as m
+    m.lib()
+    return m
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def _run(rlx, x, w, K):
+    y = rlx.scaled_matmul(_dev(x.packed), _dev(x.scales), x.fmt, _dev(w.packed), _dev(w.scales), w.fmt, K=K)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def _abs_bound(x, w, K):
+    A = np.abs(oracle.mx.dequant(x.packed, x.scales, x.fmt, K))
+    B = np.abs(oracle.mx.dequant(w.packed, w.scales, w.fmt, K))
+    return (2.0 ** -10 + 2.0 * K * 2.0 ** -24) * (A @ B.T)
+
+
+@pytest.mark.parametrize("fx,fw", PAIRS)
+def test_bit_exact_on_exact_inputs(rlx, fx, fw):
+    M, N, K = 200, 256, 512  # a ragged second row tile, two column tiles, four stages
+    x, w = wmx.matmul_inputs(1000 + 7 * FORMATS.index(fx) + FORMATS.index(fw), M, N, K, fx, fw, exact=True)
+    got = _run(rlx, x, w, K)
+    ref = oracle.mx.scaled_matmul(x.packed, x.scales, fx, w.packed, w.scales, fw, K)
+    assert np.array_equal(got, ref.astype(np.float32)), (fx, fw, np.abs(got - ref).max())
+
+
+@pytest.mark.parametrize("fx,fw", PAIRS)
+def test_general_inputs_within_fp32_bound(rlx, fx, fw):
+    M, N, K = 77, 128, 256
+    x, w = wmx.matmul_inputs(2000 + 7 * FORMATS.index(fx) + FORMATS.index(fw), M, N, K, fx, fw)
+    got = _run(rlx, x, w, K).astype(np.float64)
+    ref = oracle.mx.scaled_matmul(x.packed, x.scales, fx, w.packed, w.scales, fw, K)
+    tol = _abs_bound(x, w, K)
+    assert np.all(np.isfinite(got))
+    bad = np.abs(got - ref) > tol
+    assert not bad.any(), (fx, fw, int(bad.sum()), float(np.abs(got - ref).max()))
+
+
+@pytest.mark.parametrize("fx,fw", [("e4m3", "e4m3"), ("e2m1", "e2m1"), ("e4m3", "e2m1")])
+def test_benchmark_shape_sampled_rows(rlx, fx, fw):
+    M, N, K = 18048, 1536, 384
+    x, w = wmx.matmul_inputs(3000 + FORMATS.index(fx), M, N, K, fx, fw)
+    got = _run(rlx, x, w, K)
+    rows = np.random.default_rng(1).choice(M, 48, replace=False)
+    rows = np.concatenate([rows, [0, M - 1]])
+    xs = wmx.MxOperand(fx, x.codes[rows], x.packed[rows], x.scales[rows])
+    ref = oracle.mx.scaled_matmul(xs.packed, xs.scales, fx, w.packed, w.scales, fw, K)
+    tol = _abs_bound(xs, w, K)
+    assert np.all(np.abs(got[rows] - ref) <= tol)
+
+
+def test_wider_scale_range_and_single_row(rlx):
+    """Scales spanning 2^-27 .. 2^27 (products far from 1), one row."""
+    rng = np.random.default_rng(9)
+    K, N = 128, 128
+    x = wmx.operand(rng, 1, K, "e4m3", 100, 154)
+    w = wmx.operand(rng, N, K, "e5m2", 100, 154)
+    got = _run(rlx, x, w, K).astype(np.float64)
+    ref = oracle.mx.scaled_matmul(x.packed, x.scales, "e4m3", w.packed, w.scales, "e5m2", K)
+    assert np.all(np.abs(got - ref) <= _abs_bound(x, w, K))
+
+
+def test_zero_rows_and_rejected_sizes(rlx):
+    x, w = wmx.matmul_inputs(5, 4, 128, 128, "e4m3", "e4m3")
+    empty = rlx.scaled_matmul(_dev(x.packed[:0]), _dev(x.scales[:0]), "e4m3", _dev(w.packed), _dev(w.scales),
+                              "e4m3", K=128)
+    assert tuple(empty.shape) == (0, 128)
+    w2 = wmx.operand(np.random.default_rng(0), 192, 128, "e4m3")
+    with pytest.raises(rlx.RlxError) as e:
+        rlx.scaled_matmul(_dev(x.packed), _dev(x.scales), "e4m3", _dev(w2.packed), _dev(w2.scales), "e4m3", K=128)
+    assert e.value.status == rlx.ERR_UNSUPPORTED
