@@ -450,32 +450,43 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   uint32_t qpk[8];
   if (active) {
     const int tok = wave * 32 + l32;
-    const float* bias_lds = vec_lds;
-    const float* u_lds = vec_lds + kFwRows;
+    // this lane's bias and (deferred input) fold_u values, every LDS read
+    // issued at once: vector reads of 4 dims per part; fold_u is zero for a
+    // plain input (its LDS region is only written for a deferred one), so the
+    // loop below has no branch
+    float4 bb[3][4], uu[3][4];
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        bb[t][i] = *reinterpret_cast<const float4*>(vec_lds + 32 * t + 8 * i + 4 * half);
+        uu[t][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    if (deferred) {
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) uu[t][i] = *reinterpret_cast<const float4*>(vec_lds + kFwRows + 32 * t + 8 * i + 4 * half);
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int d = 8 * i + 4 * half;
-      float qv[4], kv[4], vv[4];
+      float out[3][4];
       // deferred LayerNorm of the input rows: sum_k LN(x)_k W_nk =
       // rstd * (sum_k x_k W'_nk - mean * u_n) + (W beta)_n, W'_nk = gamma_k W_nk
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float a0 = acc[0][4 * i + j], a1 = acc[1][4 * i + j], a2 = acc[2][4 * i + j];
-        if (deferred) {  // (u_lds is only written for a deferred input)
-          a0 = fmaf(-lnst.x, u_lds[d + j], a0);
-          a1 = fmaf(-lnst.x, u_lds[32 + d + j], a1);
-          a2 = fmaf(-lnst.x, u_lds[64 + d + j], a2);
-        }
-        qv[j] = fmaf(lnst.y, a0, bias_lds[d + j]);
-        kv[j] = fmaf(lnst.y, a1, bias_lds[32 + d + j]);
-        vv[j] = fmaf(lnst.y, a2, bias_lds[64 + d + j]);
-      }
-      qpk[2 * i] = pack_bf16x2(qv[0], qv[1]);
-      qpk[2 * i + 1] = pack_bf16x2(qv[2], qv[3]);
-      *reinterpret_cast<uint2*>(k_lds + tok * kFKPitch + d * 2) =
-          make_uint2(pack_bf16x2(kv[0], kv[1]), pack_bf16x2(kv[2], kv[3]));
+      for (int t = 0; t < 3; ++t) {
+        const float b4[4] = {bb[t][i].x, bb[t][i].y, bb[t][i].z, bb[t][i].w};
+        const float u4[4] = {uu[t][i].x, uu[t][i].y, uu[t][i].z, uu[t][i].w};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) vt_lds[(d + j) * kFVts + tok] = f32_to_bf16(vv[j]);
+        for (int j = 0; j < 4; ++j) out[t][j] = fmaf(lnst.y, fmaf(-lnst.x, u4[j], acc[t][4 * i + j]), b4[j]);
+      }
+      qpk[2 * i] = pack_bf16x2(out[0][0], out[0][1]);
+      qpk[2 * i + 1] = pack_bf16x2(out[0][2], out[0][3]);
+      *reinterpret_cast<uint2*>(k_lds + tok * kFKPitch + d * 2) =
+          make_uint2(pack_bf16x2(out[1][0], out[1][1]), pack_bf16x2(out[1][2], out[1][3]));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) vt_lds[(d + j) * kFVts + tok] = f32_to_bf16(out[2][j]);
     }
   }
   __syncthreads();
@@ -485,11 +496,17 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   const bf16x8_t qf0 = as_bf16x8(make_uint4(qpk[0], qpk[1], qpk[2], qpk[3]));
   const bf16x8_t qf1 = as_bf16x8(make_uint4(qpk[4], qpk[5], qpk[6], qpk[7]));
   const float sl2 = p.scale * kLog2e;
-  float m_run = -INFINITY, l_run = 0.0f;
+  float l_run = 0.0f;
   f32x16_t o;
 #pragma unroll
   for (int v = 0; v < 16; ++v) o[v] = 0.0f;
-  for (int t = 0; t < ntiles; ++t) {
+  // Two passes over the (at most four) key tiles, the scores kept in
+  // registers: all S^T tiles first, then the row maximum over every key, then
+  // P = 2^(s - max) and P.V -- no running-max rescale of the output.
+  f32x16_t sc[kFxRows / 32];
+#pragma unroll
+  for (int t = 0; t < kFxRows / 32; ++t) {
+    if (t >= ntiles) break;
     const int kb = t * 32;
     // K operand in the same head-dim order as Q: dims 4*half + {0..3} and 8 + 4*half + {0..3} (+16 for step 2)
     const uint8_t* krow = k_lds + (kb + l32) * kFKPitch + 8 * half;
@@ -497,32 +514,36 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
     const uint2 k01 = *reinterpret_cast<const uint2*>(krow + 16);
     const uint2 k10 = *reinterpret_cast<const uint2*>(krow + 32);
     const uint2 k11 = *reinterpret_cast<const uint2*>(krow + 48);
-    f32x16_t s;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) s[v] = 0.0f;
-    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(make_uint4(k00.x, k00.y, k01.x, k01.y)), qf0, s, 0, 0, 0);
-    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(make_uint4(k10.x, k10.y, k11.x, k11.y)), qf1, s, 0, 0, 0);
-    float tv[16];
-    float tmax = -INFINITY;
+    for (int v = 0; v < 16; ++v) sc[t][v] = 0.0f;
+    sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(make_uint4(k00.x, k00.y, k01.x, k01.y)), qf0, sc[t], 0, 0, 0);
+    sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(make_uint4(k10.x, k10.y, k11.x, k11.y)), qf1, sc[t], 0, 0, 0);
+  }
+  float m_all = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < kFxRows / 32; ++t) {
+    if (t >= ntiles) break;
+    const int kb = t * 32;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int key = kb + 8 * (v >> 2) + 4 * half + (v & 3);
-      tv[v] = key < L ? s[v] * sl2 : -INFINITY;
-      tmax = fmaxf(tmax, tv[v]);
+      sc[t][v] = (kb + 32 <= L || key < L) ? sc[t][v] * sl2 : -INFINITY;  // only the last tile is partial
+      m_all = fmaxf(m_all, sc[t][v]);
     }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float m_new = fmaxf(m_run, tmax);  // finite: every tile holds at least one real key
-    const float alpha = exp2f(m_run - m_new);
-    float pv[16], psum = 0.0f;
+  }
+  m_all = fmaxf(m_all, __shfl_xor(m_all, 32, 64));  // finite: the sequence has a real key
+#pragma unroll
+  for (int t = 0; t < kFxRows / 32; ++t) {
+    if (t >= ntiles) break;
+    const int kb = t * 32;
+    // v_exp_f32 directly: the arguments are <= 0 and results below 2^-126
+    // (flushed to 0) are far under the bf16 rounding of P
+    float pv[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      pv[v] = exp2f(tv[v] - m_new);
-      psum += pv[v];
+      pv[v] = __builtin_amdgcn_exp2f(sc[t][v] - m_all);
+      l_run += pv[v];
     }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) o[v] *= alpha;
     const uint4 pb0 = make_uint4(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]), pack_bf16x2(pv[4], pv[5]),
                                  pack_bf16x2(pv[6], pv[7]));
     const uint4 pb1 = make_uint4(pack_bf16x2(pv[8], pv[9]), pack_bf16x2(pv[10], pv[11]),
