@@ -43,7 +43,8 @@ def attention_flops(sp, lengths):
 
 
 # the source file that holds each measured kernel class (with the shared device helpers)
-KERNEL_SOURCES = {"qkv_attention": "attention.hip", "attention": "attention.hip", "mx_gemm": "mx_gemm.hip"}
+KERNEL_SOURCES = {"qkv_attention": "attention.hip", "attention": "attention.hip", "mx_gemm": "mx_gemm.hip",
+                  "gemv": "gemv.hip"}
 
 
 def kernel_source_digest(kernel_class="gemm"):
@@ -173,6 +174,100 @@ def bench_scaled_matmul(args):
     print(json.dumps(rec), flush=True)
 
 
+def gemv_bytes(scheme, M, N, K, epi_bias=True):
+    """Algorithmic HBM bytes of one few-row dequantising matmul: every weight
+    code, scale and zero-point once, the activations, the bias and the output."""
+    codes = N * K // 2 if scheme == "int4" else N * K
+    meta = 2 * N * (K // 32) * 2 if scheme == "int4" else 2 * N
+    return codes + meta + 2 * M * K + 2 * M * N + (4 * N if epi_bias else 0)
+
+
+def bench_dequant_gemv(args):
+    """Few-row dequantising matmul (rlx_dequant_matmul with M <= 16 rows, the
+    GEMV regime): a decode-sized product, N 14336 x K 4096 by default.  The
+    launches cycle through enough weight copies (> 512 MB) that every launch
+    streams its weights from HBM rather than from the 256 MB last-level cache."""
+    import numpy as np
+    import torch
+
+    import paper_2609_37916_amd as rlx
+    import workloads
+
+    M, N, K = args.gemv_shape
+    scheme = args.gemv_scheme
+    rng = np.random.default_rng(7)
+    x = workloads.round_to_bf16(rng.normal(0, 1, (M, K)).astype(np.float32))
+    wf = rng.normal(0, 0.02, (N, K)).astype(np.float32)
+    b = rng.normal(0, 0.5, N).astype(np.float32)
+    dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=dt)
+    if scheme == "int8":
+        q, s = workloads.quantize_int8_per_channel(wf)
+        one = (dev(q, torch.int8), dev(s, torch.float16), None)
+        kw = dict(scheme=rlx.Q_INT8_PER_CHANNEL)
+    else:
+        q, s, z = workloads.quantize_int4_grouped(wf, 32)
+        one = (dev(q, torch.uint8), dev(s, torch.float16), dev(z, torch.float16))
+        kw = dict(scheme=rlx.Q_INT4_GROUP_ZP, group_size=32)
+    nbytes = gemv_bytes(scheme, M, N, K)
+    copies = max(1, -(-512 * 2 ** 20 // nbytes))
+    ws = [one] + [tuple(None if t is None else t.clone() for t in one) for _ in range(copies - 1)]
+    xd, bd = dev(x, torch.bfloat16), dev(b, torch.float32)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def launch(i):
+        w, sc, zr = ws[i % copies]
+        rlx.dequant_matmul(xd, w, scales=sc, zeros=zr, N=N, bias=bd, epi=rlx.EPI_BIAS, out=y, **kw)
+
+    for i in range(args.warmup):
+        launch(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(args.steps):
+        launch(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = 1e3 * e0.elapsed_time(e1) / args.steps
+    gbs = nbytes / (us * 1e-6) / 1e9
+    name = f"gemv_{scheme}_m{M}_n{N}_k{K}"
+    rec = {
+        "metric": f"dequant GEMV GB/s ({scheme} weights, bf16 x, {M}x{N}x{K}, 1 MI355X)",
+        "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(us / 1e3, 5), "p50_ms": round(us / 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": f"synthetic (N(0,0.02) weights quantised {scheme}, N(0,1) bf16 activations), {copies} weight copies",
+        "config": {"workload": name, "M": M, "N": N, "K": K, "scheme": scheme, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": "gemv_q_kernel", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": committed_traffic("gemv", name),
+                     "bytes_per_launch": nbytes, "avg_launch_us": round(us, 3)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        cols = min(N, 1024)
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            if scheme == "int8":
+                wd = oracle.dequant_int8(q[:cols], s[:cols])
+            else:
+                wd = oracle.dequant_int4(q[:cols], s[:cols], z[:cols], 32)
+            oracle.linear(x, wd, b[:cols])
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= args.cpu_seconds or reps >= 1000:
+                break
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+        except Exception:
+            threads = os.cpu_count() or 1
+        rec["cpu_baseline"] = {"value": round(gemv_bytes(scheme, M, cols, K) * reps / dt / 1e9, 4), "unit": "GB/s",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"first {cols} weight rows, {reps} times, float64 NumPy oracle, {dt:.1f} s"}
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -182,8 +277,11 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=20, help="profiled forwards (per-kernel event times)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", choices=("encoder", "scaled_matmul"), default="encoder",
-                    help="encoder: the encoder forward (default); scaled_matmul: the block-scaled minifloat matmul")
+    ap.add_argument("--op", choices=("encoder", "scaled_matmul", "dequant_gemv"), default="encoder",
+                    help="encoder: the encoder forward (default); scaled_matmul: the block-scaled minifloat matmul; "
+                         "dequant_gemv: the few-row dequantising matmul")
+    ap.add_argument("--gemv-scheme", default="int4", choices=("int4", "int8"))
+    ap.add_argument("--gemv-shape", type=int, nargs=3, default=(1, 14336, 4096), metavar=("M", "N", "K"))
     ap.add_argument("--mx-format", default="e4m3", choices=sorted(MX_PEAK_TFLOPS))
     ap.add_argument("--mx-shape", type=int, nargs=3, default=(18048, 384, 1536), metavar=("M", "N", "K"))
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -222,6 +320,9 @@ def main():
 
     if args.op == "scaled_matmul":
         bench_scaled_matmul(args)
+        return
+    if args.op == "dequant_gemv":
+        bench_dequant_gemv(args)
         return
 
     sp = workloads.spec(args.workload)

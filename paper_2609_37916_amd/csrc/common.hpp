@@ -146,6 +146,55 @@ __device__ __forceinline__ float dpp_sum8(float v) {
   return v;
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS loads and explicit waits
+// ---------------------------------------------------------------------------
+// global_load_lds: each lane's 16 (or 4) bytes go from global memory straight
+// into LDS at m0 + lane * 16 (* 4).  Inline assembly keeps the compiler from
+// inserting a full vmcnt wait before every later LDS read (it cannot tell
+// which LDS bytes the load writes); the kernels place their own waits.  M0 is
+// used by nothing else in these kernels.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void lds_dma4(const void* g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_addr)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Wait until this wave's LDS reads (and scalar loads) have returned.
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14)); }
+
+// ahead (<= MAXA) later stages of LPS loads each may stay in flight
+template <int LPS, int MAXA>
+__device__ __forceinline__ void wait_stage(int ahead) {
+  if constexpr (MAXA > 0) {
+    if (ahead >= MAXA) {
+      wait_vmcnt<MAXA * LPS>();
+      return;
+    }
+    wait_stage<LPS, MAXA - 1>(ahead);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+
+// LDS byte address of a __shared__ pointer (for m0).
+__device__ __forceinline__ uint32_t lds_addr_of(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
+
 // Reinterpret 16 bytes as eight bf16 MFMA operands.
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 

@@ -524,39 +524,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
 // LDS-DMA kernel for dense weights
 // ---------------------------------------------------------------------------
 
-// 16 bytes per lane from global memory straight into LDS at m0 + lane * 16.
-// Inline assembly keeps the compiler from inserting a full vmcnt wait before
-// every later LDS read (it cannot tell which LDS bytes the DMA writes); the
-// kernel places its own waits.  M0 is used by nothing else in these kernels.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-// Wait until at most N vector-memory operations of this wave are outstanding.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
-template <int LPS, int MAXA>
-__device__ __forceinline__ void wait_stage(int ahead) {
-  // ahead (<= MAXA) later stages of LPS loads each may stay in flight
-  if constexpr (MAXA > 0) {
-    if (ahead >= MAXA) {
-      wait_vmcnt<MAXA * LPS>();
-      return;
-    }
-    wait_stage<LPS, MAXA - 1>(ahead);
-  } else {
-    wait_vmcnt<0>();
-  }
-}
-
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
 // Requests the block's epilogue operands (EpiLayout) into LDS at `epi`, one
@@ -929,6 +896,7 @@ bool gemm_deferred_ln_supported(DType dt, Quant q, int H) {
 
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
+  if (gemv_supported(p)) return launch_gemv(p, s);
   if ((p.x_stats && !gemm_deferred_ln_supported(p.dtype, p.quant, p.K)) ||
       ((p.res_stats || p.y_stats) && !gemm_deferred_ln_supported(p.dtype, p.quant, p.N)))
     return hipErrorInvalidValue;

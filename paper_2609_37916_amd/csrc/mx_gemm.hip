@@ -47,24 +47,6 @@ constexpr int kMxLps = (kMxBM + kMxBN) * kMxPitch / (4 * 1024) + 1;
 
 __host__ __device__ constexpr int mx_bits(int fmt) { return fmt <= 1 ? 8 : (fmt <= 3 ? 6 : 4); }
 
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void mx_dma16(const void* g, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void mx_dma4(const void* g, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_addr)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-template <int N>
-__device__ __forceinline__ void mx_wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
 __device__ __forceinline__ int mx_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
 typedef int mx_v8i __attribute__((ext_vector_type(8)));
@@ -147,8 +129,8 @@ __global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
     const uint32_t sbase = lds0 + buf * kMxStageBytes;
 #pragma unroll
     for (int i = 0; i < CL; ++i)
-      mx_dma16(src[i] + (size_t)kt * step_bytes[i], __builtin_amdgcn_readfirstlane(sbase + (wave + 4 * i) * 8 * kMxPitch));
-    mx_dma4(ssrc + kt * 4, __builtin_amdgcn_readfirstlane(sbase + kMxOpBytes + wave * 256));
+      lds_dma16(src[i] + (size_t)kt * step_bytes[i], __builtin_amdgcn_readfirstlane(sbase + (wave + 4 * i) * 8 * kMxPitch));
+    lds_dma4(ssrc + kt * 4, __builtin_amdgcn_readfirstlane(sbase + kMxOpBytes + wave * 256));
   };
 
   typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -165,9 +147,9 @@ __global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
     const int buf = kt & 1;
     if (kt + 1 < KT) {
       issue(kt + 1, buf ^ 1);
-      mx_wait_vmcnt<kMxLps>();  // stage kt landed; kt + 1 in flight
+      wait_vmcnt<kMxLps>();  // stage kt landed; kt + 1 in flight
     } else {
-      mx_wait_vmcnt<0>();
+      wait_vmcnt<0>();
     }
     __syncthreads();
     const uint8_t* xs = smem + buf * kMxStageBytes;
