@@ -8,14 +8,19 @@
 // arithmetic per byte: it is bound by HBM bandwidth and by the vector-ALU
 // work of unpacking the codes, not by the matrix cores.
 //
-//  * One block per 16 output columns.  Its 8 waves split K in 128-k units
-//    (unit u goes to wave u mod 8); the 8 partial 16 x 16 tiles are added in
-//    LDS in wave order (deterministic) before the epilogue.
-//  * Each wave streams its units through a private ring of LDS slots with
-//    direct-to-LDS loads, four units in flight, so the K loop needs no
-//    barrier.  A unit's 16 weight rows land group-major ([16-byte chunk]
-//    [row][16 B]): lane (n, G) then reads the 4 (int4) or 8 (int8) bytes of
-//    k-octet G of each group with conflict-free ds_read2.
+//  * Output columns go in tiles of 16.  Each block takes a contiguous run of
+//    tiles (about two blocks per CU, so the activations are staged once per
+//    block and no second wave of blocks leaves a tail).  Within a tile the 8
+//    waves split K in 128-k units (unit u goes to wave u mod 8); at the end of
+//    the tile the 8 partial 16 x 16 tiles are added in LDS in wave order
+//    (deterministic) and the epilogue is applied.
+//  * Each wave streams its (tile, unit) items through a private ring of LDS
+//    slots with direct-to-LDS loads, four items in flight across tile
+//    boundaries; the only barrier is the one per tile that hands the wave
+//    partials to the epilogue (double-buffered).  A unit's 16 weight rows land
+//    group-major ([16-byte chunk][row][16 B]): lane (n, G) then reads the 4
+//    (int4) or 8 (int8) bytes of k-octet G of each group with conflict-free
+//    ds_read2.
 //  * v_mfma_f32_16x16x32_bf16 takes the activations as the A operand (rows m;
 //    rows M..15 repeat row M-1 and their results are dropped) and the codes
 //    as B, one 32-k group per instruction.  Lane l supplies row / column
@@ -43,7 +48,6 @@ namespace {
 constexpr int kGvWaves = 8;
 constexpr int kGvThreads = kGvWaves * 64;
 constexpr int kGvUnitK = 128;       // k per unit (four 32-k groups)
-constexpr int kGvDepth = 4;         // units in flight per wave
 constexpr int kGvMaxRows = 16;
 constexpr int kGvMaxXBytes = 64 * 1024;  // activations staged in LDS (bf16)
 
@@ -51,12 +55,15 @@ template <Quant Q>
 struct GvUnit;
 template <>
 struct GvUnit<Quant::Int4> {
-  // codes: 16 rows x 64 bytes; meta: scales then zeros, 16 rows x 4 f16 each
-  static constexpr int kCodeBytes = 1024, kMetaBytes = 256, kLoads = 2;
+  // codes: 16 rows x 64 bytes; meta: scales then zeros, 16 rows x 4 f16 each;
+  // kDepth items in flight per wave (measured on the 14336 x 4096 product:
+  // 2 in flight 12.0 us, 3 13.3 us, 4 14.0 us)
+  static constexpr int kCodeBytes = 1024, kMetaBytes = 256, kLoads = 2, kDepth = 2;
 };
 template <>
 struct GvUnit<Quant::Int8> {
-  static constexpr int kCodeBytes = 2048, kMetaBytes = 0, kLoads = 2;
+  // (2 in flight 14.2 us, 3 14.0 us, 4 13.6 us)
+  static constexpr int kCodeBytes = 2048, kMetaBytes = 0, kLoads = 2, kDepth = 4;
 };
 
 __device__ __forceinline__ float f16_lo(uint32_t v) { return f16_bits_to_f32((uint16_t)(v & 0xffffu)); }
@@ -86,27 +93,55 @@ __device__ __forceinline__ bf16x8_t int8_octet_as_bf16(uint32_t lo, uint32_t hi)
   return as_bf16x8(make_uint4(o[0], o[1], o[2], o[3]));
 }
 
+// Epilogue operands of a block's run of tpb tiles in LDS (byte offsets);
+// every part is 256-byte aligned, the whole a multiple of 1 KB.
+struct GvEpiLayout {
+  int bias, scale, res, res_pitch, bytes;
+};
+__host__ __device__ constexpr int gv_round(int v, int a) { return (v + a - 1) / a * a; }
+__host__ __device__ inline GvEpiLayout gv_epi_layout(Quant q, Epi e, int M, int tpb) {
+  GvEpiLayout l{};
+  int off = 0;
+  l.bias = off;
+  if (e != Epi::None) off += gv_round(tpb * 16 * 4, 256);
+  l.scale = off;
+  if (q == Quant::Int8) off += gv_round(tpb * 16 * 2, 256);
+  l.res = off;
+  l.res_pitch = gv_round(tpb * 16 * 2, 256);
+  if (e == Epi::BiasResidual) off += M * l.res_pitch;
+  l.bytes = gv_round(off, 1024);
+  return l;
+}
+
 template <Quant Q, Epi E>
 __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
   using U = GvUnit<Q>;
   extern __shared__ __attribute__((aligned(16))) uint8_t gv_lds[];
   const int M = p.M, N = p.N, K = p.K;
-  const int n0 = blockIdx.x * 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l16 = lane & 15, G = lane >> 4;
   const int units = K / kGvUnitK;
-  const int nu = units > wave ? (units - wave + kGvWaves - 1) / kGvWaves : 0;  // this wave's units
+  const int nu = units > wave ? (units - wave + kGvWaves - 1) / kGvWaves : 0;  // this wave's units per tile
+  // this block's tiles of 16 columns: t0 .. t0 + nt - 1
+  const int tiles = N / 16;
+  const int tpb = (tiles + gridDim.x - 1) / gridDim.x;
+  const int t0 = blockIdx.x * tpb;
+  const int nt = max(0, min(tiles - t0, tpb));
+  const int items = nt * nu;  // (tile, unit) items of this wave, tile-major
 
-  // LDS: code slots [kGvWaves][kGvDepth] | int4 scale/zero slots [kGvWaves][kGvDepth]
-  //      | activations [K/8][M][16 B] | group sums [K/32][M] f32
-  // (every direct-to-LDS destination is aligned to its own size)
-  uint8_t* ring = gv_lds + wave * kGvDepth * U::kCodeBytes;
-  uint8_t* meta = gv_lds + kGvWaves * kGvDepth * U::kCodeBytes + wave * kGvDepth * U::kMetaBytes;
-  uint8_t* xl = gv_lds + kGvWaves * kGvDepth * (U::kCodeBytes + U::kMetaBytes);
+  // LDS: code slots [kGvWaves][kDepth] | int4 scale/zero slots [kGvWaves][kDepth]
+  //      | wave partials [2][kGvWaves][64 lanes][4] f32 | epilogue operands of
+  //      the block's tiles (GvEpiLayout) | activations [K/8][M][16 B]
+  //      | group sums [K/32][M] f32   (direct-to-LDS destinations 256-byte aligned)
+  uint8_t* ring = gv_lds + wave * U::kDepth * U::kCodeBytes;
+  uint8_t* meta = gv_lds + kGvWaves * U::kDepth * U::kCodeBytes + wave * U::kDepth * U::kMetaBytes;
+  uint8_t* red = gv_lds + kGvWaves * U::kDepth * (U::kCodeBytes + U::kMetaBytes);
+  const GvEpiLayout el = gv_epi_layout(Q, E, M, tpb);
+  uint8_t* epi = red + 2 * kGvWaves * 1024;
+  uint8_t* xl = epi + el.bytes;
   float* xs = reinterpret_cast<float*>(xl + (size_t)M * K * 2);
 
-  // 1. Activations, as stored, into LDS: direct loads issued before the
-  //    unit loads, so that waiting for them leaves the units in flight.
+  // 1. Activations, as stored, into LDS.
   constexpr int kOctPerThread = kGvMaxXBytes / 16 / kGvThreads;
   const int octets = M * K / 8;  // 16-byte octets of x, a multiple of 16
   const int oct_per_row = K / 8;
@@ -119,36 +154,59 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
                 __builtin_amdgcn_readfirstlane(xl_addr + q0 * 16));
   }
 
-  // 2. Unit loads.  Unit u, columns n0..n0+15: lane (row l16, chunk G) of the
-  //    wave moves 16 bytes; slot layout [chunk][row][16 B].
+  // Epilogue operands of the block's tiles (bias, int8 scales, residual
+  // rows), 4 bytes a lane: each wave moves the rows m = wave mod 8 of the
+  // residual; wave 0 the bias, wave 1 the scales.
+  const int ncol = nt * 16;  // this block's columns, from column 16 t0
+  auto dma_run = [&](const void* src, uint8_t* dst, int dwords) {
+    for (int j = 0; j * 64 < dwords; ++j)
+      if (j * 64 + lane < dwords)
+        lds_dma4(reinterpret_cast<const uint32_t*>(src) + j * 64 + lane,
+                 __builtin_amdgcn_readfirstlane(lds_addr_of(dst) + j * 256));
+  };
+  if constexpr (E != Epi::None)
+    if (wave == 0) dma_run(p.bias + (size_t)t0 * 16, epi + el.bias, ncol);
+  if constexpr (Q == Quant::Int8)
+    if (wave == 1) dma_run(reinterpret_cast<const uint16_t*>(p.scales) + (size_t)t0 * 16, epi + el.scale, ncol / 2);
+  if constexpr (E == Epi::BiasResidual)
+    for (int m = wave; m < M; m += kGvWaves)
+      dma_run(reinterpret_cast<const bf16_t*>(p.residual) + (size_t)m * N + (size_t)t0 * 16, epi + el.res + m * el.res_pitch,
+              ncol / 2);
+
+  // 2. Item loads.  Item (tile t, unit u): lane (row l16, chunk G) of the
+  //    wave moves 16 bytes of row 16 t + l16; slot layout [chunk][row][16 B].
   const size_t wpitch = Q == Quant::Int4 ? (size_t)K / 2 : (size_t)K;
-  const uint8_t* wbase = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + l16) * wpitch + G * 16;
+  const uint8_t* wlane = reinterpret_cast<const uint8_t*>(p.w) + (size_t)l16 * wpitch + G * 16;
   // int4 scales and zeros ([N][K/32] f16): lanes < 32 move the scales of row
   // lane/2, the others the zeros of row (lane-32)/2, two groups (4 bytes) each
   const size_t gpitch = (size_t)K / 32 * 2;
-  const uint8_t* sz_base =
-      Q == Quant::Int4 ? reinterpret_cast<const uint8_t*>(lane < 32 ? p.scales : p.zeros) +
-                             (size_t)(n0 + ((lane & 31) >> 1)) * gpitch + (lane & 1) * 4
-                       : nullptr;
+  const uint8_t* mlane = Q == Quant::Int4 ? reinterpret_cast<const uint8_t*>(lane < 32 ? p.scales : p.zeros) +
+                                                (size_t)((lane & 31) >> 1) * gpitch + (lane & 1) * 4
+                                          : nullptr;
   const uint32_t ring_addr = lds_addr_of(ring), meta_addr = lds_addr_of(meta);
   auto issue = [&](int i) {
-    const int u = wave + i * kGvWaves;
-    const uint32_t slot = ring_addr + (uint32_t)((i % kGvDepth) * U::kCodeBytes);
+    const int tt = i / nu, u = wave + (i - tt * nu) * kGvWaves;
+    const size_t row0 = (size_t)(t0 + tt) * 16;
+    const uint32_t slot = ring_addr + (uint32_t)((i % U::kDepth) * U::kCodeBytes);
     if constexpr (Q == Quant::Int4) {
-      lds_dma16(wbase + (size_t)u * 64, __builtin_amdgcn_readfirstlane(slot));
-      lds_dma4(sz_base + (size_t)u * 8,
-               __builtin_amdgcn_readfirstlane(meta_addr + (uint32_t)((i % kGvDepth) * U::kMetaBytes)));
+      lds_dma16(wlane + row0 * wpitch + (size_t)u * 64, __builtin_amdgcn_readfirstlane(slot));
+      lds_dma4(mlane + row0 * gpitch + (size_t)u * 8,
+               __builtin_amdgcn_readfirstlane(meta_addr + (uint32_t)((i % U::kDepth) * U::kMetaBytes)));
     } else {
-      lds_dma16(wbase + (size_t)u * 128, __builtin_amdgcn_readfirstlane(slot));
-      lds_dma16(wbase + (size_t)u * 128 + 64, __builtin_amdgcn_readfirstlane(slot + 1024));
+      lds_dma16(wlane + row0 * wpitch + (size_t)u * 128, __builtin_amdgcn_readfirstlane(slot));
+      lds_dma16(wlane + row0 * wpitch + (size_t)u * 128 + 64, __builtin_amdgcn_readfirstlane(slot + 1024));
     }
   };
-  const int pro = min(nu, kGvDepth);
+  // The activations are waited for before any item load goes out: issued
+  // together, they would queue behind every block's first weight bytes and
+  // reach the blocks only after those (measured: 2.5 us median, 7.8 us max,
+  // against about 1 us alone).
+  wait_vmcnt<0>();
+  const int pro = min(items, U::kDepth);
   for (int i = 0; i < pro; ++i) issue(i);
 
   // 3. Activations rewritten in place in slot order ([K/8][M][16 B], bf16
   //    pairs (i, i + 4) of each octet), and the per-group sums.
-  wait_stage<U::kLoads, kGvDepth>(pro);  // this wave's activation loads (older) have landed
   uint4 xr[kOctPerThread];
 #pragma unroll
   for (int i = 0; i < kOctPerThread; ++i) {
@@ -177,81 +235,125 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
   }
   __syncthreads();
 
-  // 4. K loop.
+  // 4. Tiles: K loop per tile, then the wave partials to the epilogue.
   const int mc = min(l16, M - 1);  // A-operand row of this lane
-  f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
   const f32x4_t zero4 = {0.0f, 0.0f, 0.0f, 0.0f};
   // nibble pair mask and the bf16 exponent of 128, as register values the
   // compiler cannot fold back into literals (see int4_octet_as_offset_bf16)
   uint32_t kMask, kExp;
   asm volatile("v_mov_b32 %0, 0x000F000F" : "=v"(kMask));
   asm volatile("v_mov_b32 %0, 0x43004300" : "=v"(kExp));
-  for (int i = 0; i < nu; ++i) {
-    wait_stage<U::kLoads, kGvDepth - 1>(min(nu - 1 - i, kGvDepth - 1));  // unit i has landed
-    const int u = wave + i * kGvWaves;
-    const uint8_t* slot = ring + (i % kGvDepth) * U::kCodeBytes;
-    const uint8_t* mslot = meta + (i % kGvDepth) * U::kMetaBytes;
-    bf16x8_t xa[4];
+  for (int tt = 0; tt < nt; ++tt) {
+    f32x4_t acc = zero4;
+    for (int j = 0; j < nu; ++j) {
+      const int i = tt * nu + j;
+      wait_stage<U::kLoads, U::kDepth - 1>(min(items - 1 - i, U::kDepth - 1));  // item i has landed
+      const int u = wave + j * kGvWaves;
+      const uint8_t* slot = ring + (i % U::kDepth) * U::kCodeBytes;
+      const uint8_t* mslot = meta + (i % U::kDepth) * U::kMetaBytes;
+      bf16x8_t xa[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      xa[j] = as_bf16x8(*reinterpret_cast<const uint4*>(xl + ((size_t)(16 * u + 4 * j + G) * M + mc) * 16));
-    if constexpr (Q == Quant::Int4) {
-      const uint32_t* cw = reinterpret_cast<const uint32_t*>(slot + l16 * 16 + G * 4);
-      const uint32_t c0 = cw[0], c1 = cw[64], c2 = cw[128], c3 = cw[192];
-      const uint2 sv = *reinterpret_cast<const uint2*>(mslot + l16 * 8);
-      const uint16_t zg = *reinterpret_cast<const uint16_t*>(mslot + 128 + l16 * 8 + G * 2);
-      const uint16_t sg = *reinterpret_cast<const uint16_t*>(mslot + l16 * 8 + G * 2);
-      const float xsum = xs[(4 * u + G) * M + mc];
-      wait_lgkmcnt0();
-      if (i + kGvDepth < nu) issue(i + kGvDepth);  // the slot's bytes are all in registers
-      const f32x4_t v0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[0], int4_octet_as_offset_bf16(c0, kMask, kExp), zero4, 0, 0, 0);
-      const f32x4_t v1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[1], int4_octet_as_offset_bf16(c1, kMask, kExp), zero4, 0, 0, 0);
-      const f32x4_t v2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[2], int4_octet_as_offset_bf16(c2, kMask, kExp), zero4, 0, 0, 0);
-      const f32x4_t v3 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[3], int4_octet_as_offset_bf16(c3, kMask, kExp), zero4, 0, 0, 0);
-      const float negc = -f16_bits_to_f32(sg) * (128.0f + f16_bits_to_f32(zg));
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xsum, negc, acc, 0, 0, 0);
-      const float s0 = f16_lo(sv.x), s1 = f16_hi(sv.x), s2 = f16_lo(sv.y), s3 = f16_hi(sv.y);
+      for (int q = 0; q < 4; ++q)
+        xa[q] = as_bf16x8(*reinterpret_cast<const uint4*>(xl + ((size_t)(16 * u + 4 * q + G) * M + mc) * 16));
+      if constexpr (Q == Quant::Int4) {
+        const uint32_t* cw = reinterpret_cast<const uint32_t*>(slot + l16 * 16 + G * 4);
+        const uint32_t c0 = cw[0], c1 = cw[64], c2 = cw[128], c3 = cw[192];
+        const uint2 sv = *reinterpret_cast<const uint2*>(mslot + l16 * 8);
+        const uint16_t zg = *reinterpret_cast<const uint16_t*>(mslot + 128 + l16 * 8 + G * 2);
+        const uint16_t sg = *reinterpret_cast<const uint16_t*>(mslot + l16 * 8 + G * 2);
+        const float xsum = xs[(4 * u + G) * M + mc];
+        wait_lgkmcnt0();
+        if (i + U::kDepth < items) issue(i + U::kDepth);  // the slot's bytes are all in registers
+        const f32x4_t v0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[0], int4_octet_as_offset_bf16(c0, kMask, kExp), zero4, 0, 0, 0);
+        const f32x4_t v1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[1], int4_octet_as_offset_bf16(c1, kMask, kExp), zero4, 0, 0, 0);
+        const f32x4_t v2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[2], int4_octet_as_offset_bf16(c2, kMask, kExp), zero4, 0, 0, 0);
+        const f32x4_t v3 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[3], int4_octet_as_offset_bf16(c3, kMask, kExp), zero4, 0, 0, 0);
+        const float negc = -f16_bits_to_f32(sg) * (128.0f + f16_bits_to_f32(zg));
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xsum, negc, acc, 0, 0, 0);
+        const float s0 = f16_lo(sv.x), s1 = f16_hi(sv.x), s2 = f16_lo(sv.y), s3 = f16_hi(sv.y);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] = fmaf(s0, v0[r], fmaf(s1, v1[r], fmaf(s2, v2[r], fmaf(s3, v3[r], acc[r]))));
-    } else {
-      const uint2* cw = reinterpret_cast<const uint2*>(slot + (G >> 1) * 256 + l16 * 16 + (G & 1) * 8);
-      const uint2 c0 = cw[0], c1 = cw[64], c2 = cw[128], c3 = cw[192];
-      wait_lgkmcnt0();
-      if (i + kGvDepth < nu) issue(i + kGvDepth);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[0], int8_octet_as_bf16(c0.x, c0.y), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[1], int8_octet_as_bf16(c1.x, c1.y), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[2], int8_octet_as_bf16(c2.x, c2.y), acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[3], int8_octet_as_bf16(c3.x, c3.y), acc, 0, 0, 0);
+        for (int r = 0; r < 4; ++r) acc[r] = fmaf(s0, v0[r], fmaf(s1, v1[r], fmaf(s2, v2[r], fmaf(s3, v3[r], acc[r]))));
+      } else {
+        const uint2* cw = reinterpret_cast<const uint2*>(slot + (G >> 1) * 256 + l16 * 16 + (G & 1) * 8);
+        const uint2 c0 = cw[0], c1 = cw[64], c2 = cw[128], c3 = cw[192];
+        wait_lgkmcnt0();
+        if (i + U::kDepth < items) issue(i + U::kDepth);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[0], int8_octet_as_bf16(c0.x, c0.y), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[1], int8_octet_as_bf16(c1.x, c1.y), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[2], int8_octet_as_bf16(c2.x, c2.y), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[3], int8_octet_as_bf16(c3.x, c3.y), acc, 0, 0, 0);
+      }
     }
-  }
-
-  // 5. Wave partials -> LDS (each wave into its own ring: its loads have all
-  //    landed and been read), then one thread per output adds them in wave order.
-  *reinterpret_cast<f32x4_t*>(ring + lane * 16) = acc;
-  __syncthreads();
-  if (tid < 16 * kGvMaxRows) {
-    const int m = tid >> 4, n = tid & 15;  // output (m, n0 + n) is register m % 4 of lane n + 16 (m / 4)
-    if (m < M) {
-      const int src = (n + 16 * (m >> 2)) * 16 + (m & 3) * 4;
-      float v = 0.0f;
+    // The partials of tile tt go to buffer tt % 2: the epilogue of tile tt - 2,
+    // the last reader of that buffer, ran before the barrier of tile tt - 1.
+    uint8_t* rb = red + (tt & 1) * kGvWaves * 1024;
+    *reinterpret_cast<f32x4_t*>(rb + wave * 1024 + lane * 16) = acc;
+    __syncthreads();
+    if (tid < 16 * kGvMaxRows) {
+      const int m = tid >> 4, n = (t0 + tt) * 16 + (tid & 15);
+      if (m < M) {  // output (m, n) is register m % 4 of lane n % 16 + 16 (m / 4)
+        const int src = ((tid & 15) + 16 * (m >> 2)) * 16 + (m & 3) * 4;
+        float v = 0.0f;
 #pragma unroll
-      for (int w = 0; w < kGvWaves; ++w) v += *reinterpret_cast<const float*>(gv_lds + w * kGvDepth * U::kCodeBytes + src);
-      if constexpr (Q == Quant::Int8) v *= f16_bits_to_f32(reinterpret_cast<const uint16_t*>(p.scales)[n0 + n]);
-      if constexpr (E != Epi::None) v += p.bias[n0 + n];
-      if constexpr (E == Epi::BiasGelu) v = gelu_erf(v);
-      if constexpr (E == Epi::BiasResidual) v += bf16_to_f32(reinterpret_cast<const bf16_t*>(p.residual)[(size_t)m * N + n0 + n]);
-      reinterpret_cast<bf16_t*>(p.y)[(size_t)m * N + n0 + n] = f32_to_bf16(v);
+        for (int w = 0; w < kGvWaves; ++w) v += *reinterpret_cast<const float*>(rb + w * 1024 + src);
+        const int c = tt * 16 + (tid & 15);  // column within the block's run
+        if constexpr (Q == Quant::Int8) v *= f16_bits_to_f32(reinterpret_cast<const uint16_t*>(epi + el.scale)[c]);
+        if constexpr (E != Epi::None) v += reinterpret_cast<const float*>(epi + el.bias)[c];
+        if constexpr (E == Epi::BiasGelu) v = gelu_erf(v);
+        if constexpr (E == Epi::BiasResidual)
+          v += bf16_to_f32(reinterpret_cast<const bf16_t*>(epi + el.res + m * el.res_pitch)[c]);
+        reinterpret_cast<bf16_t*>(p.y)[(size_t)m * N + n] = f32_to_bf16(v);
+      }
     }
   }
 }
 
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+struct GvPlan {
+  int grid, tpb;
+  size_t lds;
+};
+
+// Up to two blocks per CU (as many as the LDS allows), each with an equal run
+// of tpb 16-column tiles; the LDS holds the rings, the wave partials, the
+// run's epilogue operands and the activations.
+GvPlan gemv_plan(const GemmParams& p) {
+  using U4 = GvUnit<Quant::Int4>;
+  using U8 = GvUnit<Quant::Int8>;
+  const int ring = p.quant == Quant::Int4 ? U4::kDepth * (U4::kCodeBytes + U4::kMetaBytes)
+                                          : U8::kDepth * (U8::kCodeBytes + U8::kMetaBytes);
+  const size_t base = (size_t)kGvWaves * ring + 2 * kGvWaves * 1024 + (size_t)p.M * p.K * 2 +
+                      (size_t)p.M * (p.K / 32) * 4;
+  const int tiles = p.N / 16;
+  GvPlan g{};
+  for (int per_cu = 2; per_cu >= 1; --per_cu) {
+    g.tpb = (tiles + device_cus() * per_cu - 1) / (device_cus() * per_cu);
+    g.lds = base + gv_epi_layout(p.quant, p.epi, p.M, g.tpb).bytes;
+    if (g.lds * per_cu <= 160 * 1024) break;
+  }
+  g.grid = (tiles + g.tpb - 1) / g.tpb;
+  return g;
+}
+
 template <Quant Q, Epi E>
 hipError_t launch_gemv_typed(const GemmParams& p, hipStream_t s) {
-  const size_t lds = gemv_lds_bytes(p);
+  const GvPlan g = gemv_plan(p);
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(gemv_q_kernel<Q, E>),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((gemv_q_kernel<Q, E>), dim3(p.N / 16), dim3(kGvThreads), lds, s, p);
+  hipLaunchKernelGGL((gemv_q_kernel<Q, E>), dim3(g.grid), dim3(kGvThreads), g.lds, s, p);
   return hipGetLastError();
 }
 
@@ -268,18 +370,12 @@ hipError_t launch_gemv_q(const GemmParams& p, hipStream_t s) {
 
 }  // namespace
 
-size_t gemv_lds_bytes(const GemmParams& p) {
-  const int slot = p.quant == Quant::Int4 ? GvUnit<Quant::Int4>::kCodeBytes + GvUnit<Quant::Int4>::kMetaBytes
-                                          : GvUnit<Quant::Int8>::kCodeBytes + GvUnit<Quant::Int8>::kMetaBytes;
-  return (size_t)kGvWaves * kGvDepth * slot + (size_t)p.M * p.K * 2 + (size_t)p.M * (p.K / 32) * 4;
-}
-
 bool gemv_supported(const GemmParams& p) {
   auto a4 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 3) == 0; };
   return (p.quant == Quant::Int4 || p.quant == Quant::Int8) && p.dtype == DType::BF16 && p.m_dev == nullptr &&
          p.x_head_rows == 0 && !p.x_stats && !p.res_stats && !p.y_stats && p.M >= 1 && p.M <= kGvMaxRows &&
          p.N % 16 == 0 && p.K % kGvUnitK == 0 && (size_t)p.M * p.K * 2 <= (size_t)kGvMaxXBytes &&
-         (p.quant == Quant::Int8 || (a4(p.scales) && a4(p.zeros)));
+         a4(p.scales) && (p.quant == Quant::Int8 || a4(p.zeros)) && gemv_plan(p).lds <= 160 * 1024;
 }
 
 hipError_t launch_gemv(const GemmParams& p, hipStream_t s) {

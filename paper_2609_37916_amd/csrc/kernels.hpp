@@ -50,11 +50,10 @@ enum GemmTile : int { kTileAuto = 0, kTile128x128 = 1, kTile64x128 = 2, kTile64x
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 
 // Few-row dequantising matmul (gemv.hip): int8 / int4 weights, bf16 x with
-// 1 <= M <= 16 rows, N % 16 == 0, K % 128 == 0, M * K * 2 <= 64 KB, no
-// device-side row count and no deferred-LayerNorm fields.  launch_gemm takes
+// 1 <= M <= 16 rows, N % 16 == 0, K % 128 == 0, M * K * 2 <= 64 KB, 4-byte
+// aligned scales and zeros, no device-side row count and no deferred-LayerNorm fields.  launch_gemm takes
 // this path by itself whenever it applies.
 bool gemv_supported(const GemmParams& p);
-size_t gemv_lds_bytes(const GemmParams& p);
 hipError_t launch_gemv(const GemmParams& p, hipStream_t s);
 
 hipError_t launch_dequant_unpack(const void* w, Quant q, const void* scales, const void* zeros, int N, int K,
