@@ -239,7 +239,8 @@ def bench_dequant_gemv(args):
         "data": f"synthetic (N(0,0.02) weights quantised {scheme}, N(0,1) bf16 activations), {copies} weight copies",
         "config": {"workload": name, "M": M, "N": N, "K": K, "scheme": scheme, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "gemv_q_kernel", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
-                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": committed_traffic("gemv", name),
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": committed_traffic("gemv", f"{scheme}_m{M}_n{N}_k{K}"),
                      "bytes_per_launch": nbytes, "avg_launch_us": round(us, 3)},
     }
     if not args.no_cpu_baseline:

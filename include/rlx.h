@@ -117,7 +117,15 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
  * bf16 outputs are rounded once at the end.
  * int8: the integer codes enter the bf16 matrix cores exactly and the
  * per-channel scale is applied to the fp32 sum.  int4: each weight
- * (q - z) * s is formed in fp32 and rounded to bf16 before the product.
+ * (q - z) * s is formed in fp32 and rounded to bf16 before the product,
+ * except in the few-row path below.
+ * Few rows (the GEMV regime: 1 <= M <= 16, quantised weights, K a multiple
+ * of 128, M * K * 2 <= 65536, scales and zeros 4-byte aligned) take a
+ * dedicated kernel that streams the weights once: int8 as above; int4 without
+ * rounding any weight, as s * (sum_k x_k (128 + q_k) - (128 + z) sum_k x_k)
+ * per 32-k group in fp32.  Results of both paths are deterministic (the same
+ * inputs give the same bits), and a row's result does not depend on the
+ * other rows of the call.
  * Supported: M >= 0 (M == 0 is a no-op), N and K positive multiples of 64,
  * group_size == 32 for RLX_Q_INT4_GROUP_ZP (ignored otherwise), 16-byte
  * aligned x, w, residual and y.  Otherwise RLX_ERR_UNSUPPORTED.
