@@ -331,3 +331,77 @@ def test_planted_mx_mistake_fails_a_pin(name, monkeypatch):
         except Exception as e:
             failed.append(type(e).__name__)
     assert failed, f"no pin caught the planted mistake '{name}'"
+
+
+# --- planted mistakes in the GGUF block oracle ---
+
+import oracle.gguf as ogg  # noqa: E402
+import test_oracle_gguf as ggpins  # noqa: E402
+
+GG_ORIG = {n: getattr(ogg, n) for n in ("parse", "dequant", "_f16")}
+
+
+def _gguf_pin_calls():
+    calls = [ggpins.test_block_sizes_and_bits_per_weight, ggpins.test_hand_built_blocks,
+             ggpins.test_formats_equal_their_internal_layouts]
+    for fmt in ggpins.FMTS:
+        calls.append(lambda fmt=fmt: ggpins.test_element_order_matches_byte_loop(fmt))
+        calls.append(lambda fmt=fmt: ggpins.test_quantise_dequantise_error_bound(fmt))
+    return calls
+
+
+def gg_interleaved_nibbles(blocks, fmt, K):
+    codes, d, m = GG_ORIG["parse"](blocks, fmt, K)
+    if fmt != "q8_0":  # elements 2j / 2j+1 in byte j instead of j / j+16
+        c = codes.reshape(codes.shape[0], -1, 2, 16)
+        codes = np.stack([c[:, :, 0, :], c[:, :, 1, :]], axis=3).reshape(codes.shape)
+    return codes, d, m
+
+
+def gg_q8_unsigned(blocks, fmt, K):
+    codes, d, m = GG_ORIG["parse"](blocks, fmt, K)
+    if fmt == "q8_0":
+        codes = codes.view(np.uint8)
+    return codes, d, m
+
+
+def gg_q4_0_no_offset(blocks, fmt, K):
+    w = GG_ORIG["dequant"](blocks, fmt, K)
+    if fmt == "q4_0":
+        _, d, _ = GG_ORIG["parse"](blocks, fmt, K)
+        w = w + 8.0 * np.repeat(d, 32, axis=1)
+    return w
+
+
+def gg_q4_1_min_subtracted(blocks, fmt, K):
+    w = GG_ORIG["dequant"](blocks, fmt, K)
+    if fmt == "q4_1":
+        _, _, m = GG_ORIG["parse"](blocks, fmt, K)
+        w = w - 2.0 * np.repeat(m, 32, axis=1)
+    return w
+
+
+def gg_f16_big_endian(lo, hi):
+    return GG_ORIG["_f16"](hi, lo)
+
+
+GG_MUTANTS = {
+    "gguf: 4-bit elements interleaved": ("parse", gg_interleaved_nibbles),
+    "gguf: Q8_0 codes unsigned": ("parse", gg_q8_unsigned),
+    "gguf: Q4_0 without the -8": ("dequant", gg_q4_0_no_offset),
+    "gguf: Q4_1 min subtracted": ("dequant", gg_q4_1_min_subtracted),
+    "gguf: f16 big-endian": ("_f16", gg_f16_big_endian),
+}
+
+
+@pytest.mark.parametrize("name", list(GG_MUTANTS))
+def test_planted_gguf_mistake_fails_a_pin(name, monkeypatch):
+    attr, fake = GG_MUTANTS[name]
+    monkeypatch.setattr(ogg, attr, fake)
+    failed = []
+    for call in _gguf_pin_calls():
+        try:
+            call()
+        except Exception as e:
+            failed.append(type(e).__name__)
+    assert failed, f"no pin caught the planted mistake '{name}'"
