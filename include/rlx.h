@@ -62,10 +62,15 @@ typedef enum {
 typedef enum {
   RLX_Q_NONE = 0,              /* w has the activation dtype (f32 or bf16), [N,K]      */
   RLX_Q_INT8_PER_CHANNEL = 1,  /* w int8 [N,K]; scales f16 [N]; W = q * s[n]          */
-  RLX_Q_INT4_GROUP_ZP = 2      /* w u8 [N,K/2], two codes per byte (k = 2j in the low
+  RLX_Q_INT4_GROUP_ZP = 2,     /* w u8 [N,K/2], two codes per byte (k = 2j in the low
                                   nibble, 2j+1 in the high nibble); scales and zeros
                                   f16 [N, K/group]; W = (q - z[n,g]) * s[n,g],
                                   g = k / group                                       */
+  RLX_Q_INT8_GROUP = 3,        /* w int8 [N,K]; scales f16 [N, K/group];
+                                  W = q * s[n,g] (GGUF Q8_0 after rlx_gguf_repack)    */
+  RLX_Q_INT4_GROUP_MIN = 4     /* w as RLX_Q_INT4_GROUP_ZP; `zeros` holds mins m, f16
+                                  [N, K/group]; W = q * s[n,g] + m[n,g]
+                                  (GGUF Q4_1 after rlx_gguf_repack)                  */
 } rlx_quant;
 
 typedef enum {
@@ -121,14 +126,18 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
  * except in the few-row path below.
  * Few rows (the GEMV regime: 1 <= M <= 16, quantised weights, K a multiple
  * of 128, M * K * 2 <= 65536, scales and zeros 4-byte aligned) take a
- * dedicated kernel that streams the weights once: int8 as above; int4 without
- * rounding any weight, as s * (sum_k x_k (128 + q_k) - (128 + z) sum_k x_k)
- * per 32-k group in fp32.  Results of both paths are deterministic (the same
+ * dedicated kernel that streams the weights once: int8 per-channel as above;
+ * no group-scheme weight is rounded: per 32-k group, int8 group gives
+ * s * sum_k x_k q_k, int4 s * (sum_k x_k (128 + q_k) - (128 + z) sum_k x_k),
+ * int4 min s * sum_k x_k (128 + q_k) + (m - 128 s) sum_k x_k, all in fp32.  Results of both paths are deterministic (the same
  * inputs give the same bits), and a row's result does not depend on the
  * other rows of the call.
+ * int8 group: q * s formed in fp32 and rounded to bf16 before the product;
+ * int4 min: q * s + m formed in fp32 (one rounding) and rounded to bf16
+ * (both except in the few-row path below).
  * Supported: M >= 0 (M == 0 is a no-op), N and K positive multiples of 64,
- * group_size == 32 for RLX_Q_INT4_GROUP_ZP (ignored otherwise), 16-byte
- * aligned x, w, residual and y.  Otherwise RLX_ERR_UNSUPPORTED.
+ * group_size == 32 for the group schemes (ignored for int8 per-channel),
+ * 16-byte aligned x, w, residual and y.  Otherwise RLX_ERR_UNSUPPORTED.
  */
 rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const void* w, rlx_quant scheme,
                               const void* scales, const void* zeros, int group_size, int N,
@@ -136,12 +145,38 @@ rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const
                               void* stream);
 
 /* Test support for the dequantisation step alone: writes the dequantised
- * weights W[n,k] as f32 [N,K] (exact: both products are representable in
- * fp32).  Same weight layouts and limits as rlx_dequant_matmul;
+ * weights W[n,k] as f32 [N,K] (products of a code and an f16 scale are exact
+ * in fp32; q * s + m of int4 min is rounded once, by a fused multiply-add).
+ * Same weight layouts and limits as rlx_dequant_matmul;
  * scheme must not be RLX_Q_NONE.
  */
 rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scales, const void* zeros,
                               int group_size, int N, int K, float* w_out, void* stream);
+
+/* GGUF weight blocks (the llama.cpp scheme set of Op::DequantMatMul, Section
+ * VI).  A tensor of N rows of K weights is N * K/32 consecutive 32-weight
+ * blocks, row-major; the tensor type ids and blocks are GGUF's:
+ *   RLX_GGUF_Q4_0  18 bytes: f16 d, 16 bytes of nibbles   W = (q - 8) * d
+ *   RLX_GGUF_Q4_1  20 bytes: f16 d, f16 m, 16 bytes        W = q * d + m
+ *   RLX_GGUF_Q8_0  34 bytes: f16 d, 32 int8                W = q * d
+ * (4-bit blocks: element j < 16 in the low nibble of byte j, element j + 16
+ * in its high nibble; f16 little-endian).
+ * rlx_gguf_repack rewrites such a tensor, once, into the layout of an
+ * rlx_quant scheme that represents the same weights exactly, and stores that
+ * scheme in *scheme (if non-NULL):
+ *   Q4_0 -> RLX_Q_INT4_GROUP_ZP  (codes [N,K/2], scales = d, zeros = 8)
+ *   Q4_1 -> RLX_Q_INT4_GROUP_MIN (codes [N,K/2], scales = d, zeros = m)
+ *   Q8_0 -> RLX_Q_INT8_GROUP     (codes [N,K] int8, scales = d; zeros unused)
+ * scales and zeros are f16 [N, K/32].  Pass the results to
+ * rlx_dequant_matmul with group_size 32.  Device pointers owned by the
+ * caller; blocks, scales and zeros 2-byte aligned, codes 16-byte aligned;
+ * K a positive multiple of 64, N >= 0 (N == 0 is a no-op).  Otherwise
+ * RLX_ERR_UNSUPPORTED (type, alignment, K) or RLX_ERR_INVALID_ARG.
+ */
+typedef enum { RLX_GGUF_Q4_0 = 2, RLX_GGUF_Q4_1 = 3, RLX_GGUF_Q8_0 = 8 } rlx_gguf_type;
+
+rlx_status rlx_gguf_repack(const void* blocks, rlx_gguf_type type, int N, int K, void* codes, void* scales,
+                           void* zeros, rlx_quant* scheme, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Block-scaled minifloat matmul (the ScaledMatMul path of Section VI:

@@ -20,7 +20,10 @@ LIB_PATH = os.path.join(PKG_DIR, "librlx.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_OOM = range(5)
 F32, BF16, F16, I8, U4X2, I32, U8 = range(7)
 MASK_NONE, MASK_CAUSAL, MASK_SLIDING_WINDOW, MASK_CUSTOM = range(4)
-Q_NONE, Q_INT8_PER_CHANNEL, Q_INT4_GROUP_ZP = range(3)
+Q_NONE, Q_INT8_PER_CHANNEL, Q_INT4_GROUP_ZP, Q_INT8_GROUP, Q_INT4_GROUP_MIN = range(5)
+GGUF_Q4_0, GGUF_Q4_1, GGUF_Q8_0 = 2, 3, 8
+GGUF_TYPES = {"q4_0": GGUF_Q4_0, "q4_1": GGUF_Q4_1, "q8_0": GGUF_Q8_0}
+GGUF_BLOCK_BYTES = {GGUF_Q4_0: 18, GGUF_Q4_1: 20, GGUF_Q8_0: 34}
 EPI_NONE, EPI_BIAS, EPI_BIAS_GELU, EPI_BIAS_RESIDUAL = range(4)
 MX_E4M3, MX_E5M2, MX_E2M3, MX_E3M2, MX_E2M1 = range(5)
 MX_FORMAT_CODES = {"e4m3": MX_E4M3, "e5m2": MX_E5M2, "e2m3": MX_E2M3, "e3m2": MX_E3M2, "e2m1": MX_E2M1}
@@ -30,7 +33,7 @@ OUTPUT_POOLED, OUTPUT_HIDDEN = range(2)
 STATUS_NAMES = {0: "RLX_OK", 1: "RLX_ERR_INVALID_ARG", 2: "RLX_ERR_UNSUPPORTED", 3: "RLX_ERR_HIP", 4: "RLX_ERR_OOM"}
 
 # every symbol include/rlx.h declares
-EXPORTS = ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_scaled_matmul",
+EXPORTS = ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_gguf_repack", "rlx_scaled_matmul",
            "rlx_encoder_create",
            "rlx_encoder_forward", "rlx_encoder_destroy", "rlx_encoder_set_profiling", "rlx_encoder_profile_read",
            "rlx_last_error", "rlx_version")
@@ -88,6 +91,7 @@ def lib() -> ctypes.CDLL:
     L.rlx_dequant_matmul.argtypes = [_vp, i32, i32, i32, _vp, i32, _vp, _vp, i32, i32, _vp, _vp, i32, _vp, _vp]
     L.rlx_dequant_unpack.argtypes = [_vp, i32, _vp, _vp, i32, i32, i32, _vp, _vp]
     L.rlx_scaled_matmul.argtypes = [_vp, _vp, i32, _vp, _vp, i32, i32, i32, i32, _vp, _vp]
+    L.rlx_gguf_repack.argtypes = [_vp, i32, i32, i32, _vp, _vp, _vp, ctypes.POINTER(i32), _vp]
     L.rlx_encoder_create.argtypes = [ctypes.POINTER(EncoderConfig), ctypes.POINTER(EncoderWeights),
                                      ctypes.POINTER(_vp)]
     L.rlx_encoder_forward.argtypes = [_vp, _vp, _vp, i32, i32, _vp, _vp]
@@ -96,7 +100,8 @@ def lib() -> ctypes.CDLL:
     L.rlx_encoder_set_profiling.argtypes = [_vp, i32]
     L.rlx_encoder_profile_read.argtypes = [_vp, i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(i32),
                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
-    for nm in ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_scaled_matmul", "rlx_encoder_create",
+    for nm in ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_gguf_repack", "rlx_scaled_matmul",
+               "rlx_encoder_create",
                "rlx_encoder_forward", "rlx_encoder_set_profiling", "rlx_encoder_profile_read"):
         getattr(L, nm).restype = ctypes.c_int
     L.rlx_last_error.restype = ctypes.c_char_p
@@ -217,6 +222,29 @@ def dequant_unpack(w, *, scheme: int, scales, zeros=None, group_size: int = 32, 
     check(lib().rlx_dequant_unpack(_ptr(w), scheme, _ptr(scales), _ptr(zeros), group_size, N, K, _ptr(out),
                                    _stream(stream)))
     return out
+
+
+def gguf_repack(blocks, gguf_type, *, N: int, K: int, stream=None):
+    """GGUF blocks (uint8 device tensor of N * K/32 blocks) -> (scheme, codes,
+    scales, zeros) for dequant_matmul (see rlx_gguf_repack); zeros is None for Q8_0."""
+    torch = _torch()
+    t = GGUF_TYPES.get(gguf_type, gguf_type)
+    if t not in GGUF_BLOCK_BYTES:
+        raise ValueError(f"unknown GGUF type {gguf_type!r}")
+    # the C ABI cannot see buffer sizes: check the block tensor here so no kernel reads past it
+    want = N * (K // 32) * GGUF_BLOCK_BYTES[t]
+    if blocks.dtype != torch.uint8 or not blocks.is_contiguous() or blocks.numel() != want or K % 32:
+        raise ValueError(f"blocks: expected a contiguous uint8 tensor of {want} bytes, got {blocks.dtype} "
+                         f"{tuple(blocks.shape)}")
+    dev = blocks.device
+    codes = torch.empty((N, K // 2 if t != GGUF_Q8_0 else K), dtype=torch.uint8 if t != GGUF_Q8_0 else torch.int8,
+                        device=dev)
+    scales = torch.empty((N, K // 32), dtype=torch.float16, device=dev)
+    zeros = torch.empty((N, K // 32), dtype=torch.float16, device=dev) if t != GGUF_Q8_0 else None
+    scheme = ctypes.c_int(-1)
+    check(lib().rlx_gguf_repack(_ptr(blocks), t, N, K, _ptr(codes), _ptr(scales), _ptr(zeros), ctypes.byref(scheme),
+                                _stream(stream)))
+    return scheme.value, codes, scales, zeros
 
 
 class Encoder:

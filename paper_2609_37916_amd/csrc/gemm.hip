@@ -71,6 +71,34 @@ __device__ __forceinline__ void int8x16_to_bf16(uint4 src, uint4& lo, uint4& hi)
   hi = make_uint4(o[4], o[5], o[6], o[7]);
 }
 
+// 16 int8 codes of one group -> 16 bf16 of q * s, RNE.
+__device__ __forceinline__ void int8x16_scaled_to_bf16(uint4 src, float s, uint4& lo, uint4& hi) {
+  uint32_t w[4] = {src.x, src.y, src.z, src.w};
+  uint32_t o[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    o[2 * i] = pack_bf16x2((float)(int8_t)(w[i] & 0xff) * s, (float)(int8_t)((w[i] >> 8) & 0xff) * s);
+    o[2 * i + 1] = pack_bf16x2((float)(int8_t)((w[i] >> 16) & 0xff) * s, (float)(int8_t)(w[i] >> 24) * s);
+  }
+  lo = make_uint4(o[0], o[1], o[2], o[3]);
+  hi = make_uint4(o[4], o[5], o[6], o[7]);
+}
+
+// 32 packed int4 codes (one group) -> 32 bf16 of q * s + m (one fp32 rounding), RNE.
+__device__ __forceinline__ void int4x32_min_to_bf16(uint4 src, float s, float m, uint4 out[4]) {
+  uint32_t w[4] = {src.x, src.y, src.z, src.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t byte = (w[i] >> (8 * j)) & 0xffu;
+      o[j] = pack_bf16x2(fmaf((float)(byte & 0xfu), s, m), fmaf((float)(byte >> 4), s, m));
+    }
+    out[i] = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
 // 32 packed int4 codes (one group) -> 32 bf16 of (q - z) * s, RNE.
 __device__ __forceinline__ void int4x32_to_bf16(uint4 src, float s, float z, uint4 out[4]) {
   uint32_t w[4] = {src.x, src.y, src.z, src.w};
@@ -365,8 +393,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
   constexpr int CH = BK / 16;                  // 16-k chunks per stage
   constexpr int kStage = (BM + BN) * kLdsRow;
   // weight global chunks per row per stage and LDS bytes each expands to
-  constexpr int WCPR = Q == Quant::None ? 8 : (Q == Quant::Int8 ? 4 : 2);
-  constexpr int WLDS = Q == Quant::None ? 16 : (Q == Quant::Int8 ? 32 : 64);
+  constexpr int WCPR = Q == Quant::None ? 8 : (quant_int8(Q) ? 4 : 2);
+  constexpr int WLDS = Q == Quant::None ? 16 : (quant_int8(Q) ? 32 : 64);
   constexpr int XLOADS = BM * 8 / kThreads;
   constexpr int WLOADS = (BN * WCPR + kThreads - 1) / kThreads;
 
@@ -389,8 +417,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
   const uint8_t* xg = reinterpret_cast<const uint8_t*>(p.x);
   const uint8_t* wg = reinterpret_cast<const uint8_t*>(p.w);
   const size_t x_pitch = (size_t)K * ES;
-  const size_t w_pitch = Q == Quant::None ? (size_t)K * ES : (Q == Quant::Int8 ? (size_t)K : (size_t)K / 2);
-  const int wk_bytes = Q == Quant::None ? kRowBytes : (Q == Quant::Int8 ? 64 : 32);  // weight bytes per row per stage
+  const size_t w_pitch = Q == Quant::None ? (size_t)K * ES : (quant_int8(Q) ? (size_t)K : (size_t)K / 2);
+  const int wk_bytes = Q == Quant::None ? kRowBytes : (quant_int8(Q) ? 64 : 32);  // weight bytes per row per stage
 
   uint4 xr[XLOADS];
   uint4 wr[WLOADS];
@@ -435,6 +463,21 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
           int8x16_to_bf16(wr[i], lo, hi);
           st16(dst, lo);
           st16(dst + 16, hi);
+        } else if constexpr (Q == Quant::Int8G) {
+          const int g = kt * 2 + (c >> 1);  // 16 codes per chunk, two chunks per group
+          const float sg = f16_bits_to_f32(reinterpret_cast<const uint16_t*>(p.scales)[(size_t)(n0 + r) * (K / 32) + g]);
+          uint4 lo, hi;
+          int8x16_scaled_to_bf16(wr[i], sg, lo, hi);
+          st16(dst, lo);
+          st16(dst + 16, hi);
+        } else if constexpr (Q == Quant::Int4M) {
+          const size_t gi = (size_t)(n0 + r) * (K / 32) + kt * 2 + c;
+          const float sg = f16_bits_to_f32(reinterpret_cast<const uint16_t*>(p.scales)[gi]);
+          const float mg = f16_bits_to_f32(reinterpret_cast<const uint16_t*>(p.zeros)[gi]);
+          uint4 o[4];
+          int4x32_min_to_bf16(wr[i], sg, mg, o);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) st16(dst + 16 * j, o[j]);
         } else {
           const int groups = K / 32;
           const int g = kt * 2 + c;
@@ -838,6 +881,13 @@ __global__ void dequant_unpack_kernel(const uint8_t* w, Quant q, const uint16_t*
     const int n = (int)(i / K), k = (int)(i % K);
     if (q == Quant::Int8) {
       out[i] = (float)(int8_t)w[i] * f16_bits_to_f32(scales[n]);
+    } else if (q == Quant::Int8G) {
+      out[i] = (float)(int8_t)w[i] * f16_bits_to_f32(scales[(size_t)n * (K / 32) + k / 32]);
+    } else if (q == Quant::Int4M) {
+      const uint8_t byte = w[(size_t)n * (K / 2) + k / 2];
+      const float code = (float)((k & 1) ? (byte >> 4) : (byte & 0xf));
+      const size_t g = (size_t)n * (K / 32) + k / 32;
+      out[i] = fmaf(code, f16_bits_to_f32(scales[g]), f16_bits_to_f32(zeros[g]));
     } else {
       const uint8_t byte = w[(size_t)n * (K / 2) + k / 2];
       const float code = (float)((k & 1) ? (byte >> 4) : (byte & 0xf));
@@ -905,6 +955,8 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
     case Quant::None: return launch_dense<bf16_t>(p, s);
     case Quant::Int8: return launch_typed<bf16_t, Quant::Int8>(p, s);
     case Quant::Int4: return launch_typed<bf16_t, Quant::Int4>(p, s);
+    case Quant::Int8G: return launch_typed<bf16_t, Quant::Int8G>(p, s);
+    case Quant::Int4M: return launch_typed<bf16_t, Quant::Int4M>(p, s);
   }
   return hipErrorInvalidValue;
 }

@@ -61,6 +61,13 @@ struct GvUnit<Quant::Int4> {
   static constexpr int kCodeBytes = 1024, kMetaBytes = 256, kLoads = 2, kDepth = 2;
 };
 template <>
+struct GvUnit<Quant::Int4M> : GvUnit<Quant::Int4> {};  // zeros hold the mins
+template <>
+struct GvUnit<Quant::Int8G> {
+  // codes: 16 rows x 128 bytes; meta: 16 rows x 4 f16 scales (then a copy)
+  static constexpr int kCodeBytes = 2048, kMetaBytes = 256, kLoads = 3, kDepth = 3;
+};
+template <>
 struct GvUnit<Quant::Int8> {
   // (2 in flight 14.2 us, 3 14.0 us, 4 13.6 us)
   static constexpr int kCodeBytes = 2048, kMetaBytes = 0, kLoads = 2, kDepth = 4;
@@ -175,27 +182,30 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
 
   // 2. Item loads.  Item (tile t, unit u): lane (row l16, chunk G) of the
   //    wave moves 16 bytes of row 16 t + l16; slot layout [chunk][row][16 B].
-  const size_t wpitch = Q == Quant::Int4 ? (size_t)K / 2 : (size_t)K;
+  const size_t wpitch = quant_int4(Q) ? (size_t)K / 2 : (size_t)K;
   const uint8_t* wlane = reinterpret_cast<const uint8_t*>(p.w) + (size_t)l16 * wpitch + G * 16;
   // int4 scales and zeros ([N][K/32] f16): lanes < 32 move the scales of row
   // lane/2, the others the zeros of row (lane-32)/2, two groups (4 bytes) each
   const size_t gpitch = (size_t)K / 32 * 2;
-  const uint8_t* mlane = Q == Quant::Int4 ? reinterpret_cast<const uint8_t*>(lane < 32 ? p.scales : p.zeros) +
-                                                (size_t)((lane & 31) >> 1) * gpitch + (lane & 1) * 4
-                                          : nullptr;
+  // (int8 group scales: every lane moves scales, lanes >= 32 a second copy)
+  const uint8_t* mlane =
+      U::kMetaBytes == 0 ? nullptr
+                         : reinterpret_cast<const uint8_t*>(lane < 32 || Q == Quant::Int8G ? p.scales : p.zeros) +
+                               (size_t)((lane & 31) >> 1) * gpitch + (lane & 1) * 4;
   const uint32_t ring_addr = lds_addr_of(ring), meta_addr = lds_addr_of(meta);
   auto issue = [&](int i) {
     const int tt = i / nu, u = wave + (i - tt * nu) * kGvWaves;
     const size_t row0 = (size_t)(t0 + tt) * 16;
     const uint32_t slot = ring_addr + (uint32_t)((i % U::kDepth) * U::kCodeBytes);
-    if constexpr (Q == Quant::Int4) {
+    if constexpr (quant_int4(Q)) {
       lds_dma16(wlane + row0 * wpitch + (size_t)u * 64, __builtin_amdgcn_readfirstlane(slot));
-      lds_dma4(mlane + row0 * gpitch + (size_t)u * 8,
-               __builtin_amdgcn_readfirstlane(meta_addr + (uint32_t)((i % U::kDepth) * U::kMetaBytes)));
     } else {
       lds_dma16(wlane + row0 * wpitch + (size_t)u * 128, __builtin_amdgcn_readfirstlane(slot));
       lds_dma16(wlane + row0 * wpitch + (size_t)u * 128 + 64, __builtin_amdgcn_readfirstlane(slot + 1024));
     }
+    if constexpr (U::kMetaBytes > 0)
+      lds_dma4(mlane + row0 * gpitch + (size_t)u * 8,
+               __builtin_amdgcn_readfirstlane(meta_addr + (uint32_t)((i % U::kDepth) * U::kMetaBytes)));
   };
   // The activations are waited for before any item load goes out: issued
   // together, they would queue behind every block's first weight bytes and
@@ -255,7 +265,7 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         xa[q] = as_bf16x8(*reinterpret_cast<const uint4*>(xl + ((size_t)(16 * u + 4 * q + G) * M + mc) * 16));
-      if constexpr (Q == Quant::Int4) {
+      if constexpr (quant_int4(Q)) {
         const uint32_t* cw = reinterpret_cast<const uint32_t*>(slot + l16 * 16 + G * 4);
         const uint32_t c0 = cw[0], c1 = cw[64], c2 = cw[128], c3 = cw[192];
         const uint2 sv = *reinterpret_cast<const uint2*>(mslot + l16 * 8);
@@ -268,8 +278,23 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
         const f32x4_t v1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[1], int4_octet_as_offset_bf16(c1, kMask, kExp), zero4, 0, 0, 0);
         const f32x4_t v2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[2], int4_octet_as_offset_bf16(c2, kMask, kExp), zero4, 0, 0, 0);
         const f32x4_t v3 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[3], int4_octet_as_offset_bf16(c3, kMask, kExp), zero4, 0, 0, 0);
-        const float negc = -f16_bits_to_f32(sg) * (128.0f + f16_bits_to_f32(zg));
+        // int4: s V - s (128 + z) X;  int4 min (zg holds m): s V + (m - 128 s) X
+        const float negc = Q == Quant::Int4 ? -f16_bits_to_f32(sg) * (128.0f + f16_bits_to_f32(zg))
+                                            : fmaf(-128.0f, f16_bits_to_f32(sg), f16_bits_to_f32(zg));
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xsum, negc, acc, 0, 0, 0);
+        const float s0 = f16_lo(sv.x), s1 = f16_hi(sv.x), s2 = f16_lo(sv.y), s3 = f16_hi(sv.y);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] = fmaf(s0, v0[r], fmaf(s1, v1[r], fmaf(s2, v2[r], fmaf(s3, v3[r], acc[r]))));
+      } else if constexpr (Q == Quant::Int8G) {
+        const uint2* cw = reinterpret_cast<const uint2*>(slot + (G >> 1) * 256 + l16 * 16 + (G & 1) * 8);
+        const uint2 c0 = cw[0], c1 = cw[64], c2 = cw[128], c3 = cw[192];
+        const uint2 sv = *reinterpret_cast<const uint2*>(mslot + l16 * 8);
+        wait_lgkmcnt0();
+        if (i + U::kDepth < items) issue(i + U::kDepth);
+        const f32x4_t v0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[0], int8_octet_as_bf16(c0.x, c0.y), zero4, 0, 0, 0);
+        const f32x4_t v1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[1], int8_octet_as_bf16(c1.x, c1.y), zero4, 0, 0, 0);
+        const f32x4_t v2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[2], int8_octet_as_bf16(c2.x, c2.y), zero4, 0, 0, 0);
+        const f32x4_t v3 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[3], int8_octet_as_bf16(c3.x, c3.y), zero4, 0, 0, 0);
         const float s0 = f16_lo(sv.x), s1 = f16_hi(sv.x), s2 = f16_lo(sv.y), s3 = f16_hi(sv.y);
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[r] = fmaf(s0, v0[r], fmaf(s1, v1[r], fmaf(s2, v2[r], fmaf(s3, v3[r], acc[r]))));
@@ -332,8 +357,10 @@ struct GvPlan {
 GvPlan gemv_plan(const GemmParams& p) {
   using U4 = GvUnit<Quant::Int4>;
   using U8 = GvUnit<Quant::Int8>;
-  const int ring = p.quant == Quant::Int4 ? U4::kDepth * (U4::kCodeBytes + U4::kMetaBytes)
-                                          : U8::kDepth * (U8::kCodeBytes + U8::kMetaBytes);
+  using U8G = GvUnit<Quant::Int8G>;
+  const int ring = quant_int4(p.quant) ? U4::kDepth * (U4::kCodeBytes + U4::kMetaBytes)
+                   : p.quant == Quant::Int8G ? U8G::kDepth * (U8G::kCodeBytes + U8G::kMetaBytes)
+                                             : U8::kDepth * (U8::kCodeBytes + U8::kMetaBytes);
   const size_t base = (size_t)kGvWaves * ring + 2 * kGvWaves * 1024 + (size_t)p.M * p.K * 2 +
                       (size_t)p.M * (p.K / 32) * 4;
   const int tiles = p.N / 16;
@@ -372,15 +399,21 @@ hipError_t launch_gemv_q(const GemmParams& p, hipStream_t s) {
 
 bool gemv_supported(const GemmParams& p) {
   auto a4 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 3) == 0; };
-  return (p.quant == Quant::Int4 || p.quant == Quant::Int8) && p.dtype == DType::BF16 && p.m_dev == nullptr &&
+  return p.quant != Quant::None && p.dtype == DType::BF16 && p.m_dev == nullptr &&
          p.x_head_rows == 0 && !p.x_stats && !p.res_stats && !p.y_stats && p.M >= 1 && p.M <= kGvMaxRows &&
          p.N % 16 == 0 && p.K % kGvUnitK == 0 && (size_t)p.M * p.K * 2 <= (size_t)kGvMaxXBytes &&
-         a4(p.scales) && (p.quant == Quant::Int8 || a4(p.zeros)) && gemv_plan(p).lds <= 160 * 1024;
+         a4(p.scales) && (!quant_int4(p.quant) || a4(p.zeros)) && gemv_plan(p).lds <= 160 * 1024;
 }
 
 hipError_t launch_gemv(const GemmParams& p, hipStream_t s) {
   if (!gemv_supported(p)) return hipErrorInvalidValue;
-  return p.quant == Quant::Int4 ? launch_gemv_q<Quant::Int4>(p, s) : launch_gemv_q<Quant::Int8>(p, s);
+  switch (p.quant) {
+    case Quant::Int4: return launch_gemv_q<Quant::Int4>(p, s);
+    case Quant::Int4M: return launch_gemv_q<Quant::Int4M>(p, s);
+    case Quant::Int8: return launch_gemv_q<Quant::Int8>(p, s);
+    case Quant::Int8G: return launch_gemv_q<Quant::Int8G>(p, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace rlx

@@ -8,7 +8,12 @@
 namespace rlx {
 
 enum class DType : int { F32 = 0, BF16 = 1 };
-enum class Quant : int { None = 0, Int8 = 1, Int4 = 2 };
+// Weight layouts of the dequantising matmul: Int8 per-channel scales; Int4
+// group-32 scale and zero-point, W = (q - z) s; Int8G int8 codes with group-32
+// scales, W = q s; Int4M group-32 scale and min, W = q s + m.
+enum class Quant : int { None = 0, Int8 = 1, Int4 = 2, Int8G = 3, Int4M = 4 };
+__host__ __device__ constexpr bool quant_int8(Quant q) { return q == Quant::Int8 || q == Quant::Int8G; }
+__host__ __device__ constexpr bool quant_int4(Quant q) { return q == Quant::Int4 || q == Quant::Int4M; }
 enum class Epi : int { None = 0, Bias = 1, BiasGelu = 2, BiasResidual = 3 };
 
 struct GemmParams {
@@ -55,6 +60,11 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 // this path by itself whenever it applies.
 bool gemv_supported(const GemmParams& p);
 hipError_t launch_gemv(const GemmParams& p, hipStream_t s);
+
+// GGUF blocks (type 2 Q4_0, 3 Q4_1, 8 Q8_0) of an [N, K] tensor -> the Int4
+// (Q4_0, z = 8), Int4M (Q4_1) or Int8G (Q8_0) layout (gguf.hip).
+hipError_t launch_gguf_repack(const void* blocks, int type, int N, int K, void* codes, void* scales, void* zeros,
+                              hipStream_t s);
 
 hipError_t launch_dequant_unpack(const void* w, Quant q, const void* scales, const void* zeros, int N, int K,
                                  float* out, hipStream_t s);

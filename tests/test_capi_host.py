@@ -164,3 +164,30 @@ def test_scaled_matmul_argument_errors(L):
     assert b"aligned" in L.rlx_last_error()
     # M == 0: a no-op that succeeds without touching the device
     assert f(P, P, E4M3, P, P, E2M1, 0, 128, 128, P, None) == rlx.OK
+
+
+def test_gguf_repack_argument_errors(L):
+    """Rejected before any launch (fake, never dereferenced device addresses)."""
+    p16, p2 = 0x10000, 0x10002
+    st = L.rlx_gguf_repack(p16, 6, 64, 64, p16, p16, p16, None, None)  # Q5_0
+    assert st == rlx.ERR_UNSUPPORTED and b"Q4_0" in L.rlx_last_error()
+    assert L.rlx_gguf_repack(p16, 2, 64, 96, p16, p16, p16, None, None) == rlx.ERR_UNSUPPORTED  # K % 64
+    assert L.rlx_gguf_repack(p16, 2, -1, 64, p16, p16, p16, None, None) == rlx.ERR_INVALID_ARG
+    assert L.rlx_gguf_repack(p16, 2, 64, 64, p16, p16, None, None, None) == rlx.ERR_INVALID_ARG  # Q4_0 needs zeros
+    assert L.rlx_gguf_repack(None, 8, 64, 64, p16, p16, None, None, None) == rlx.ERR_INVALID_ARG
+    assert L.rlx_gguf_repack(p16 + 1, 2, 64, 64, p16, p16, p16, None, None) == rlx.ERR_UNSUPPORTED  # odd address
+    assert L.rlx_gguf_repack(p16, 8, 64, 64, p2, p16, None, None, None) == rlx.ERR_UNSUPPORTED  # codes not 16-aligned
+    assert L.rlx_gguf_repack(None, 2, 0, 64, None, None, None, None, None) == rlx.OK  # N == 0: nothing to do
+
+
+def test_new_schemes_argument_errors(L):
+    p16 = 0x10000
+    # int4 min needs mins in `zeros`; the group schemes need group_size 32
+    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, rlx.Q_INT4_GROUP_MIN, p16, None, 32, 64, None, None,
+                              rlx.EPI_NONE, p16, None)
+    assert st == rlx.ERR_INVALID_ARG
+    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, rlx.Q_INT8_GROUP, p16, None, 64, 64, None, None,
+                              rlx.EPI_NONE, p16, None)
+    assert st == rlx.ERR_UNSUPPORTED
+    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, 5, p16, p16, 32, 64, None, None, rlx.EPI_NONE, p16, None)
+    assert st == rlx.ERR_INVALID_ARG  # unknown scheme

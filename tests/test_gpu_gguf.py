@@ -1,0 +1,101 @@
+"""GPU parity of the GGUF path: rlx_gguf_repack rewrites Q4_0 / Q4_1 / Q8_0
+blocks into the int4 zero-point / int4 min / int8 group layouts, and
+rlx_dequant_matmul multiplies with them (the tiled path for many rows, the
+few-row path for 1..16), through the C ABI, against ``oracle.gguf``.
+
+* Repack + dequantisation alone is bit-exact: every weight of these blocks is
+  exact in fp32.
+* The matmul is bounded by fp32 accumulation, bf16 output rounding, the bf16
+  rounding of each weight on the tiled path (2^-9 of |W|), and the few-row
+  path's offset arithmetic: 2^-9 sum_k |x_k| (|s| + |m|) of the block's scale
+  and min (see test_gpu_gemv.py for the int4 derivation; int8 groups add
+  less).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_helpers import assert_within, gemm_tolerance, to_bf16_exact
+from workloads import gguf as wg
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+FMTS = ("q4_0", "q4_1", "q8_0")
+
+
+@pytest.fixture(scope="module")
+def rlx():
+    import paper_2609_37916_amd as m
+    m.lib()
+    return m
+
+
+def _dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    return t.to(device="cuda", dtype=dtype) if dtype is not None else t.to("cuda")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("N,K", [(64, 64), (256, 384), (384, 1536)])
+def test_repack_and_unpack_bit_exact(rlx, fmt, N, K):
+    blocks = wg.random_blocks(np.random.default_rng(700 + N + K), N, K, fmt)
+    scheme, codes, scales, zeros = rlx.gguf_repack(_dev(blocks), fmt, N=N, K=K)
+    assert scheme == {"q4_0": rlx.Q_INT4_GROUP_ZP, "q4_1": rlx.Q_INT4_GROUP_MIN, "q8_0": rlx.Q_INT8_GROUP}[fmt]
+    got = rlx.dequant_unpack(codes, scheme=scheme, scales=scales, zeros=zeros, N=N, K=K).cpu().numpy()
+    want = oracle.gguf.dequant(blocks, fmt, K).astype(np.float32)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def _case(rlx, fmt, M, N, K, epi, seed):
+    rng = np.random.default_rng(seed)
+    x = to_bf16_exact(rng.normal(0, 1, (M, K)))
+    blocks = wg.quantize(rng.normal(0, 0.02, (N, K)).astype(np.float32), fmt)
+    b = rng.normal(0, 0.5, N).astype(np.float32)
+    r = to_bf16_exact(rng.normal(0, 1, (M, N)))
+    scheme, codes, scales, zeros = rlx.gguf_repack(_dev(blocks), fmt, N=N, K=K)
+    code = {"none": rlx.EPI_NONE, "bias": rlx.EPI_BIAS, "gelu": rlx.EPI_BIAS_GELU, "residual": rlx.EPI_BIAS_RESIDUAL}[epi]
+    y = rlx.dequant_matmul(_dev(x, torch.bfloat16), codes, scheme=scheme, scales=scales, zeros=zeros, group_size=32,
+                           N=N, bias=_dev(b, torch.float32), residual=_dev(r, torch.bfloat16), epi=code)
+    torch.cuda.synchronize()
+    w = oracle.gguf.dequant(blocks, fmt, K)
+    ref = oracle.linear(x, w, None if epi == "none" else b)
+    pre = ref.copy() if epi == "gelu" else None
+    if epi == "gelu":
+        ref = oracle.gelu(ref)
+    if epi == "residual":
+        ref = ref + r
+    _, d, m = oracle.gguf.parse(blocks, fmt, K)
+    sm = np.abs(np.repeat(d, 32, axis=1)) + (np.abs(np.repeat(m, 32, axis=1)) if m is not None else 0.0)
+    tol = (gemm_tolerance(x, w, ref, out_bf16=True, weight_rel=2.0 ** -9, pre=pre) +
+           2.0 ** -9 * (np.abs(x.astype(np.float64)) @ sm.T) + 2.0 ** -24 * 4 * np.abs(ref))
+    return y.float().cpu().numpy(), ref, tol
+
+
+# few-row shapes (1..16 rows, K % 128 == 0) and tiled ones (more rows, K % 128 != 0, or 128 KB of x)
+SHAPES = [(1, 256, 1024), (5, 1152, 384), (16, 384, 1536), (3, 128, 192), (33, 384, 1536), (300, 1536, 384),
+          (16, 512, 4096)]
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("M,N,K", SHAPES)
+def test_gguf_matmul_parity(rlx, fmt, M, N, K):
+    epi = ("bias", "gelu", "residual", "none")[(M + N) % 4]
+    got, ref, tol = _case(rlx, fmt, M, N, K, epi, 900 + M + N + K)
+    assert_within(got, ref, tol, f"gguf {fmt} {epi} {M}x{N}x{K}")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_every_epilogue_few_rows(rlx, fmt):
+    for epi in ("none", "bias", "gelu", "residual"):
+        got, ref, tol = _case(rlx, fmt, 7, 256, 512, epi, 31)
+        assert_within(got, ref, tol, f"gguf {fmt} {epi}")
+
+
+def test_binding_rejects_a_short_block_tensor(rlx):
+    blocks = _dev(wg.random_blocks(np.random.default_rng(0), 64, 64, "q4_0"))
+    with pytest.raises(ValueError):
+        rlx.gguf_repack(blocks, "q4_0", N=64, K=128)  # block tensor too small for the shape
+    with pytest.raises(ValueError):
+        rlx.gguf_repack(blocks, 6, N=64, K=64)  # Q5_0 is not supported
