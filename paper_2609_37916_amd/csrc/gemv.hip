@@ -3,7 +3,8 @@
 //
 //   y[m, n] = epi( sum_k x[m, k] W[n, k] ),   1 <= M <= 16 bf16 rows,
 //
-// with W in the int8 per-channel or the int4 group-32 zero-point layout.
+// with W in the int8 per-channel, int4 group-32 zero-point, int8 group-32 or
+// int4 group-32 min layout (the last two also hold GGUF Q8_0 / Q4_1 weights).
 // With so few rows the product reads every weight byte once and does little
 // arithmetic per byte: it is bound by HBM bandwidth and by the vector-ALU
 // work of unpacking the codes, not by the matrix cores.
@@ -15,8 +16,8 @@
 //    the tile the 8 partial 16 x 16 tiles are added in LDS in wave order
 //    (deterministic) and the epilogue is applied.
 //  * Each wave streams its (tile, unit) items through a private ring of LDS
-//    slots with direct-to-LDS loads, four items in flight across tile
-//    boundaries; the only barrier is the one per tile that hands the wave
+//    slots with direct-to-LDS loads, two to four items in flight (per
+//    layout, measured) across tile boundaries; the only barrier is the one per tile that hands the wave
 //    partials to the epilogue (double-buffered).  A unit's 16 weight rows land
 //    group-major ([16-byte chunk][row][16 B]): lane (n, G) then reads the 4
 //    (int4) or 8 (int8) bytes of k-octet G of each group with conflict-free
@@ -35,10 +36,12 @@
 //    a lane; the s (128 + z) X terms of four groups are one
 //    v_mfma_f32_16x16x4_f32 (X as A, -s (128 + z) as B).  No weight is
 //    rounded: every rounding is an fp32 sum (the tiled path instead rounds
-//    each (q - z) s to bf16).
-//  * int8: codes convert exactly to bf16 and one accumulator takes every
-//    group; the per-channel scale multiplies the fp32 sum in the epilogue, as
-//    in the tiled path.
+//    each (q - z) s to bf16).  int4 min (W = q s + m) is the same with
+//    (m - 128 s) X in place of -s (128 + z) X.
+//  * int8 per-channel: codes convert exactly to bf16 and one accumulator
+//    takes every group; the per-channel scale multiplies the fp32 sum in the
+//    epilogue, as in the tiled path.  int8 group: each group's product is
+//    scaled by its s with four FMAs a lane, as for int4.
 #include "common.hpp"
 #include "kernels.hpp"
 
