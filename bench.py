@@ -140,6 +140,11 @@ def bench_scaled_matmul(args):
     tf = flops / (us * 1e-6) / 1e12
     peak = MX_PEAK_TFLOPS[fx]
     name = f"mx_{fx}_m{M}_n{N}_k{K}"
+    # algorithmic bytes: both operands' codes and scales once, the fp32 output once
+    nbytes = (M * K * wmx.BITS[fx] + N * K * wmx.BITS[fw]) // 8 + (M + N) * (K // 32) + 4 * M * N
+    gbs = nbytes / (us * 1e-6) / 1e9
+    # the binding roofline: below the ridge point (peak flops / peak bandwidth) it is HBM
+    hbm_bound = flops / nbytes < peak * 1e12 / (PEAK_HBM_GBS * 1e9)
     rec = {
         "metric": f"scaled matmul TFLOP/s (MX {fx} x {fw}, {M}x{N}x{K}, 1 MI355X)",
         "value": round(tf, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -148,9 +153,13 @@ def bench_scaled_matmul(args):
         "data": "synthetic (seeded finite codes, E8M0 scales 2^-7 .. 2^7)",
         "config": {"workload": name, "M": M, "N": N, "K": K, "format_x": fx, "format_w": fw,
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "mx_gemm_kernel", "achieved": round(tf, 2), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(tf / peak, 4), "traffic": committed_traffic("mx_gemm", name),
-                     "flops_per_launch": flops, "avg_launch_us": round(us, 3)},
+        "roofline": ({"bound": "hbm", "kernel": "mx_gemm_kernel", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)} if hbm_bound else
+                     {"bound": "mfma", "kernel": "mx_gemm_kernel", "achieved": round(tf, 2), "peak": peak,
+                      "unit": "TFLOP/s", "frac": round(tf / peak, 4)}) | {
+                     "traffic": committed_traffic("mx_gemm", name), "flops_per_launch": flops,
+                     "bytes_per_launch": nbytes, "mfma_frac": round(tf / peak, 4),
+                     "hbm_frac": round(gbs / PEAK_HBM_GBS, 4), "avg_launch_us": round(us, 3)},
     }
     if not args.no_cpu_baseline:
         import oracle
