@@ -71,6 +71,20 @@ __device__ __forceinline__ void int8x16_to_bf16(uint4 src, uint4& lo, uint4& hi)
   hi = make_uint4(o[4], o[5], o[6], o[7]);
 }
 
+// 8 int8 codes (k ascending) -> 8 bf16, exact.
+__device__ __forceinline__ bf16x8_t int8x8_to_bf16(uint2 c) {
+  const uint32_t w[2] = {c.x, c.y};
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float f0 = (float)(int8_t)(w[i] & 0xff), f1 = (float)(int8_t)((w[i] >> 8) & 0xff);
+    const float f2 = (float)(int8_t)((w[i] >> 16) & 0xff), f3 = (float)(int8_t)(w[i] >> 24);
+    o[2 * i] = __builtin_amdgcn_perm(__float_as_uint(f1), __float_as_uint(f0), 0x07060302u);
+    o[2 * i + 1] = __builtin_amdgcn_perm(__float_as_uint(f3), __float_as_uint(f2), 0x07060302u);
+  }
+  return as_bf16x8(make_uint4(o[0], o[1], o[2], o[3]));
+}
+
 // 16 int8 codes of one group -> 16 bf16 of q * s, RNE.
 __device__ __forceinline__ void int8x16_scaled_to_bf16(uint4 src, float s, uint4& lo, uint4& hi) {
   uint32_t w[4] = {src.x, src.y, src.z, src.w};
@@ -604,19 +618,29 @@ __device__ __forceinline__ void issue_epilogue_operands(const GemmParams& p, int
 // KS > 1 (bf16): 4*KS waves; wave group g multiplies chunks [g*CH/KS, (g+1)*CH/KS)
 // of every stage into its own accumulators, summed in the epilogue.  With one
 // block per CU this gives each SIMD KS waves to interleave.
-template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1, int LN = 0>
+//
+// Q == Quant::Int8 (bf16 activations, int8 per-channel weights): the codes
+// travel by DMA like dense weights, 64 bytes per weight row and stage (rows
+// at a 64-byte pitch, 16-byte chunks XOR-swizzled by (row / 4) mod 4, which
+// leaves the 8-byte fragment reads at the minimum two-way bank conflict), and
+// become bf16 exactly in registers as each fragment is read; the per-channel
+// scale multiplies the fp32 sum in the epilogue.
+template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1, int LN = 0, Quant Q = Quant::None>
 __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   static_assert(BM % 64 == 0 && BN % 64 == 0 && STAGES >= 2 && STAGES <= 6, "tile");
   static_assert(KS == 1 || (sizeof(T) == 2 && (BK_BF16 / 16) % KS == 0), "K split over bf16 chunks");
+  static_assert(Q == Quant::None || (Q == Quant::Int8 && sizeof(T) == 2 && LN == 0), "int8 weights: bf16, no LN");
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int ES = sizeof(T);
   constexpr int BK = kRowBytes / ES;
   constexpr int CH = BK / 16;
   constexpr int NW = 4 * KS;            // waves
-  constexpr int kStage = (BM + BN) * kRowBytes;
-  constexpr int LPS = (BM + BN) / (8 * NW);  // DMA instructions per thread per stage (8 rows each per wave)
-  static_assert((BM + BN) % (8 * NW) == 0, "DMA rows split evenly over the waves");
+  constexpr int WB = Q == Quant::Int8 ? 64 : kRowBytes;  // weight bytes per row per stage
+  constexpr int kStage = BM * kRowBytes + BN * WB;
+  constexpr int XI = BM * kRowBytes / 1024;               // 1 KB DMA instructions of activations per stage
+  constexpr int LPS = kStage / (1024 * NW);  // DMA instructions per thread per stage
+  static_assert(kStage % (1024 * NW) == 0, "DMA blocks split evenly over the waves");
   static_assert((STAGES - 2) * LPS < 64, "vmcnt range");
 
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * kStage];
@@ -647,9 +671,11 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   const int KT = K / BK;
   const size_t pitch = (size_t)K * ES;
 
-  // Per-lane source rows of the DMA: instruction i of this wave fills tile rows
-  // wave*8 + i*32 .. +7 (rows < BM are activations, the rest weights); lane
-  // lands at row (lane >> 3), physical chunk (lane & 7).
+  // Per-lane sources of the DMA: instruction i of this wave fills the stage's
+  // 1 KB block g = wave + i * NW.  Activation blocks (g < BM / 8) hold rows
+  // 8g .. 8g+7, lane at row (lane >> 3), physical chunk (lane & 7); weight
+  // blocks hold rows 8h .. +7 likewise (h = g - BM / 8), or for int8 codes
+  // rows 16h .. +15 at a 64-byte pitch, lane at row (lane >> 2), chunk (lane & 3).
   // Activations are row-major, or head-major ([K/32][x_head_rows][32], 64-byte
   // rows per head) when they come from the fused attention; a 64-k stage then
   // spans two heads, and logical chunk c sits in head c/4 at dims (c%4)*8.
@@ -659,15 +685,21 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   bool is_x[LPS];
 #pragma unroll
   for (int i = 0; i < LPS; ++i) {
-    const int row = wave * 8 + i * 8 * NW + (lane >> 3);
-    const int c = swz(row, lane & 7);
-    is_x[i] = row < BM;
-    if (row < BM) {
+    const int g = wave + i * NW;
+    is_x[i] = g < XI;
+    if (g < XI) {
+      const int row = 8 * g + (lane >> 3);
+      const int c = swz(row, lane & 7);
       const int m = min(m0 + row, M - 1);
       src[i] = head_major ? reinterpret_cast<const uint8_t*>(p.x) + ((size_t)(c >> 2) * p.x_head_rows + m) * 64 + (c & 3) * 16
                           : reinterpret_cast<const uint8_t*>(p.x) + (size_t)m * pitch + c * 16;
+    } else if constexpr (Q == Quant::Int8) {
+      const int row = 16 * (g - XI) + (lane >> 2);
+      const int c = (lane & 3) ^ ((row >> 2) & 3);
+      src[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row) * K + c * 16;
     } else {
-      src[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row - BM) * pitch + c * 16;
+      const int row = 8 * (g - XI) + (lane >> 3);
+      src[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row) * pitch + swz(row, lane & 7) * 16;
     }
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)smem;
@@ -675,8 +707,8 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   auto issue = [&](int kt, int buf) {
 #pragma unroll
     for (int i = 0; i < LPS; ++i) {
-      const uint32_t la = lds0 + buf * kStage + (wave * 8 + i * 8 * NW) * kRowBytes;
-      lds_dma16(src[i] + (size_t)kt * (is_x[i] ? x_stage : (size_t)kRowBytes), __builtin_amdgcn_readfirstlane(la));
+      const uint32_t la = lds0 + buf * kStage + (wave + i * NW) * 1024;
+      lds_dma16(src[i] + (size_t)kt * (is_x[i] ? x_stage : (size_t)WB), __builtin_amdgcn_readfirstlane(la));
     }
   };
 
@@ -715,7 +747,13 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) {
               const int r = wn * WN + tn * 32 + l32;
-              af[qq][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
+              if constexpr (Q == Quant::Int8) {
+                // k = 16q + 8 half .. +7: bytes 8 half.. of logical chunk q
+                const uint2 c8 = *reinterpret_cast<const uint2*>(ws + r * 64 + ((q ^ ((r >> 2) & 3)) * 16) + half * 8);
+                af[qq][tn] = int8x8_to_bf16(c8);
+              } else {
+                af[qq][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
+              }
             }
 #pragma unroll
             for (int tm = 0; tm < TM; ++tm) {
@@ -774,15 +812,33 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
 
   constexpr int NRB = BM * (BN * 4 + 16) <= (int)sizeof(smem) ? 1 : 2;
   static_assert(BM / NRB * (BN * 4 + 16) <= (int)sizeof(smem), "epilogue row block fits the stage memory");
-  store_tile<BM, BN, T, Quant::None, E, TM, TN, NRB, KS, LN, STAGED>(acc, smem, p, m0, n0, M, epi_lds);
+  store_tile<BM, BN, T, Q, E, TM, TN, NRB, KS, LN, STAGED>(acc, smem, p, m0, n0, M, epi_lds);
 }
 
-template <int BM, int BN, int STAGES, typename T, Epi E, int KS, int LN>
+template <int BM, int BN, int STAGES, typename T, Epi E, int KS, int LN, Quant Q = Quant::None>
 hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
   const dim3 grid((p.N / BN) * ((p.M + BM - 1) / BM));
   const size_t epi = sizeof(T) == 2 ? (size_t)epi_layout_of<BM, BN, E, LN>(p.K, p.N).bytes : 0;
-  hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, E, KS, LN>), grid, dim3(kThreads * KS), epi, s, p);
+  hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, E, KS, LN, Q>), grid, dim3(kThreads * KS), epi, s, p);
   return hipGetLastError();
+}
+
+// int8 per-channel weights through the DMA kernel (bf16 activations, no
+// deferred LayerNorm): 64 x 128 tiles for the wide projections, else 64 x 64.
+template <int BM, int BN, int STAGES>
+hipError_t launch_dma_int8_tile(const GemmParams& p, hipStream_t s) {
+  switch (p.epi) {
+    case Epi::None: return launch_dma<BM, BN, STAGES, bf16_t, Epi::None, 1, 0, Quant::Int8>(p, s);
+    case Epi::Bias: return launch_dma<BM, BN, STAGES, bf16_t, Epi::Bias, 1, 0, Quant::Int8>(p, s);
+    case Epi::BiasGelu: return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasGelu, 1, 0, Quant::Int8>(p, s);
+    case Epi::BiasResidual: return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasResidual, 1, 0, Quant::Int8>(p, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_dma_int8(const GemmParams& p, hipStream_t s) {
+  if (p.N % 128 == 0 && p.N >= 1024) return launch_dma_int8_tile<64, 128, 4>(p, s);
+  return launch_dma_int8_tile<64, 64, 5>(p, s);
 }
 
 template <int BM, int BN, int STAGES, typename T, int KS = 1>
@@ -953,7 +1009,7 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   if (p.dtype == DType::F32) return launch_dense<float>(p, s);
   switch (p.quant) {
     case Quant::None: return launch_dense<bf16_t>(p, s);
-    case Quant::Int8: return launch_typed<bf16_t, Quant::Int8>(p, s);
+    case Quant::Int8: return launch_dma_int8(p, s);
     case Quant::Int4: return launch_typed<bf16_t, Quant::Int4>(p, s);
     case Quant::Int8G: return launch_typed<bf16_t, Quant::Int8G>(p, s);
     case Quant::Int4M: return launch_typed<bf16_t, Quant::Int4M>(p, s);
