@@ -85,6 +85,32 @@ __device__ __forceinline__ bf16x8_t int8x8_to_bf16(uint2 c) {
   return as_bf16x8(make_uint4(o[0], o[1], o[2], o[3]));
 }
 
+// 8 int8 codes (k ascending) -> 8 bf16 of q * s, RNE.
+__device__ __forceinline__ bf16x8_t int8x8_scaled_to_bf16(uint2 c, float s) {
+  const uint32_t w[2] = {c.x, c.y};
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    o[2 * i] = pack_bf16x2((float)(int8_t)(w[i] & 0xff) * s, (float)(int8_t)((w[i] >> 8) & 0xff) * s);
+    o[2 * i + 1] = pack_bf16x2((float)(int8_t)((w[i] >> 16) & 0xff) * s, (float)(int8_t)(w[i] >> 24) * s);
+  }
+  return as_bf16x8(make_uint4(o[0], o[1], o[2], o[3]));
+}
+
+// 8 int4 codes (k ascending, low nibble first) -> 8 bf16 of (q - z) * s
+// (Int4) or fma(q, s, m) (Int4M, z holding m), RNE: the same arithmetic as
+// the whole-group conversions below.
+template <Quant Q>
+__device__ __forceinline__ bf16x8_t int4x8_to_bf16(uint32_t c, float s, float z) {
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float lo = (float)((c >> (8 * j)) & 0xfu), hi = (float)((c >> (8 * j + 4)) & 0xfu);
+    o[j] = Q == Quant::Int4 ? pack_bf16x2((lo - z) * s, (hi - z) * s) : pack_bf16x2(fmaf(lo, s, z), fmaf(hi, s, z));
+  }
+  return as_bf16x8(make_uint4(o[0], o[1], o[2], o[3]));
+}
+
 // 16 int8 codes of one group -> 16 bf16 of q * s, RNE.
 __device__ __forceinline__ void int8x16_scaled_to_bf16(uint4 src, float s, uint4& lo, uint4& hi) {
   uint32_t w[4] = {src.x, src.y, src.z, src.w};
@@ -619,28 +645,46 @@ __device__ __forceinline__ void issue_epilogue_operands(const GemmParams& p, int
 // of every stage into its own accumulators, summed in the epilogue.  With one
 // block per CU this gives each SIMD KS waves to interleave.
 //
-// Q == Quant::Int8 (bf16 activations, int8 per-channel weights): the codes
-// travel by DMA like dense weights, 64 bytes per weight row and stage (rows
-// at a 64-byte pitch, 16-byte chunks XOR-swizzled by (row / 4) mod 4, which
-// leaves the 8-byte fragment reads at the minimum two-way bank conflict), and
-// become bf16 exactly in registers as each fragment is read; the per-channel
-// scale multiplies the fp32 sum in the epilogue.
+// Quantised weights (bf16 activations, no deferred LayerNorm): the codes
+// travel by DMA like dense weights and become bf16 in registers as each MFMA
+// fragment is read.  int8 (per-channel or group): 64 bytes per row and stage
+// at a 64-byte pitch, 16-byte chunks XOR-swizzled by (row / 4) mod 4; int4:
+// 32 bytes at a 32-byte pitch, chunks swizzled by (row / 8) mod 2 -- both
+// leave the fragment reads at the minimum two-way bank conflict.  Group
+// scales (and zeros / mins) of the tile's rows for all of K are loaded into
+// LDS once, before the first stage (gq_lds_bytes).  Each weight is formed as
+// in the register-staged kernel: int8 per-channel codes exactly (scale on the
+// fp32 sum in the epilogue); int8 group q s, int4 (q - z) s, int4 min
+// fma(q, s, m) in fp32, rounded to bf16.
+__host__ __device__ constexpr bool dma_quant_ok(Quant q) {
+  return q == Quant::None || q == Quant::Int8 || q == Quant::Int8G || q == Quant::Int4 || q == Quant::Int4M;
+}
+__host__ __device__ constexpr bool quant_grouped(Quant q) {
+  return q == Quant::Int8G || q == Quant::Int4 || q == Quant::Int4M;
+}
+// LDS for the group scales (and zeros / mins) of BN rows over K.
+__host__ __device__ inline int gq_lds_bytes(Quant q, int BN, int K) {
+  return quant_grouped(q) ? (BN * (K / 32) * 2 * (q == Quant::Int8G ? 1 : 2) + 1023) / 1024 * 1024 : 0;
+}
+
 template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1, int LN = 0, Quant Q = Quant::None>
 __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   static_assert(BM % 64 == 0 && BN % 64 == 0 && STAGES >= 2 && STAGES <= 6, "tile");
   static_assert(KS == 1 || (sizeof(T) == 2 && (BK_BF16 / 16) % KS == 0), "K split over bf16 chunks");
-  static_assert(Q == Quant::None || (Q == Quant::Int8 && sizeof(T) == 2 && LN == 0), "int8 weights: bf16, no LN");
+  static_assert(dma_quant_ok(Q) && (Q == Quant::None || (sizeof(T) == 2 && LN == 0)), "quantised: bf16, no LN");
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int ES = sizeof(T);
   constexpr int BK = kRowBytes / ES;
   constexpr int CH = BK / 16;
   constexpr int NW = 4 * KS;            // waves
-  constexpr int WB = Q == Quant::Int8 ? 64 : kRowBytes;  // weight bytes per row per stage
+  constexpr int WB = Q == Quant::None ? kRowBytes : (quant_int8(Q) ? 64 : 32);  // weight bytes per row per stage
+  constexpr int WRPK = 1024 / WB;  // weight rows per 1 KB DMA block
   constexpr int kStage = BM * kRowBytes + BN * WB;
   constexpr int XI = BM * kRowBytes / 1024;               // 1 KB DMA instructions of activations per stage
-  constexpr int LPS = kStage / (1024 * NW);  // DMA instructions per thread per stage
-  static_assert(kStage % (1024 * NW) == 0, "DMA blocks split evenly over the waves");
+  constexpr int NI = kStage / 1024;                   // 1 KB DMA blocks per stage
+  constexpr int LPS = (NI + NW - 1) / NW;             // DMA instructions per thread per stage (at most)
+  static_assert(kStage % 1024 == 0, "whole 1 KB DMA blocks");
   static_assert((STAGES - 2) * LPS < 64, "vmcnt range");
 
   __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * kStage];
@@ -685,7 +729,7 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   bool is_x[LPS];
 #pragma unroll
   for (int i = 0; i < LPS; ++i) {
-    const int g = wave + i * NW;
+    const int g = min(wave + i * NW, NI - 1);  // (blocks past NI are not issued)
     is_x[i] = g < XI;
     if (g < XI) {
       const int row = 8 * g + (lane >> 3);
@@ -693,10 +737,14 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
       const int m = min(m0 + row, M - 1);
       src[i] = head_major ? reinterpret_cast<const uint8_t*>(p.x) + ((size_t)(c >> 2) * p.x_head_rows + m) * 64 + (c & 3) * 16
                           : reinterpret_cast<const uint8_t*>(p.x) + (size_t)m * pitch + c * 16;
-    } else if constexpr (Q == Quant::Int8) {
-      const int row = 16 * (g - XI) + (lane >> 2);
+    } else if constexpr (quant_int8(Q)) {
+      const int row = WRPK * (g - XI) + (lane >> 2);
       const int c = (lane & 3) ^ ((row >> 2) & 3);
       src[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row) * K + c * 16;
+    } else if constexpr (quant_int4(Q)) {
+      const int row = WRPK * (g - XI) + (lane >> 1);
+      const int c = (lane & 1) ^ ((row >> 3) & 1);
+      src[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row) * (K / 2) + c * 16;
     } else {
       const int row = 8 * (g - XI) + (lane >> 3);
       src[i] = reinterpret_cast<const uint8_t*>(p.w) + (size_t)(n0 + row) * pitch + swz(row, lane & 7) * 16;
@@ -707,10 +755,34 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   auto issue = [&](int kt, int buf) {
 #pragma unroll
     for (int i = 0; i < LPS; ++i) {
+      if (NI % NW != 0 && wave + i * NW >= NI) break;  // uneven split: this wave has one block fewer
       const uint32_t la = lds0 + buf * kStage + (wave + i * NW) * 1024;
       lds_dma16(src[i] + (size_t)kt * (is_x[i] ? x_stage : (size_t)WB), __builtin_amdgcn_readfirstlane(la));
     }
   };
+
+  // Group scales (then zeros / mins) of rows n0 .. n0+BN-1, [BN][K/32] f16
+  // each, into LDS after the epilogue operands: older than every stage load,
+  // so the first stage's wait covers them.
+  const int G = K / 32;
+  uint8_t* gq = epi_lds + (STAGED ? epi_layout_of<BM, BN, E, LN>(p.K, p.N).bytes : 0);
+  if constexpr (quant_grouped(Q)) {
+    const int dw = BN * G / 2;  // dwords per array (G is even)
+    const uint32_t gq0 = lds_addr_of(gq);
+    for (int a = 0; a < (Q == Quant::Int8G ? 1 : 2); ++a) {
+      const uint8_t* arr = reinterpret_cast<const uint8_t*>(a == 0 ? p.scales : p.zeros);
+      for (int j = wave; j * 64 < dw; j += NW) {
+        const int d = j * 64 + lane;
+        if (d < dw) {
+          const int row = d / (G / 2), col = d - row * (G / 2);
+          lds_dma4(arr + ((size_t)(n0 + row) * G + 2 * col) * 2,
+                   __builtin_amdgcn_readfirstlane(gq0 + (uint32_t)(a * dw + j * 64) * 4));
+        }
+      }
+    }
+  }
+  const uint16_t* gs = reinterpret_cast<const uint16_t*>(gq);           // [BN][G] scales
+  const uint16_t* gz = reinterpret_cast<const uint16_t*>(gq) + BN * G;  // [BN][G] zeros / mins
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -729,7 +801,10 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
     for (int u = 0; u < STAGES; ++u) {
       const int kt = kt0 + u;
       if (kt < KT) {
-        wait_stage<LPS, STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
+        if (NI % NW == 0 || wave < NI % NW)
+          wait_stage<LPS, STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
+        else
+          wait_stage<(NI % NW == 0 ? LPS : LPS - 1), STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
         __syncthreads();  // stage kt visible to all waves; buffer of stage kt-1 is free
         const bool prefetch = kt + STAGES - 1 < KT;
         const uint8_t* xs = smem + u * kStage;
@@ -747,10 +822,19 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) {
               const int r = wn * WN + tn * 32 + l32;
-              if constexpr (Q == Quant::Int8) {
+              if constexpr (quant_int8(Q)) {
                 // k = 16q + 8 half .. +7: bytes 8 half.. of logical chunk q
                 const uint2 c8 = *reinterpret_cast<const uint2*>(ws + r * 64 + ((q ^ ((r >> 2) & 3)) * 16) + half * 8);
-                af[qq][tn] = int8x8_to_bf16(c8);
+                if constexpr (Q == Quant::Int8)
+                  af[qq][tn] = int8x8_to_bf16(c8);
+                else
+                  af[qq][tn] = int8x8_scaled_to_bf16(c8, f16_bits_to_f32(gs[r * G + 2 * kt + (q >> 1)]));
+              } else if constexpr (quant_int4(Q)) {
+                // k = 16q + 8 half .. +7: nibbles of bytes 8q + 4 half .. +3, logical chunk q / 2
+                const uint32_t c4 = *reinterpret_cast<const uint32_t*>(
+                    ws + r * 32 + (((q >> 1) ^ ((r >> 3) & 1)) * 16) + (q & 1) * 8 + half * 4);
+                const int gi = r * G + 2 * kt + (q >> 1);
+                af[qq][tn] = int4x8_to_bf16<Q>(c4, f16_bits_to_f32(gs[gi]), f16_bits_to_f32(gz[gi]));
               } else {
                 af[qq][tn] = as_bf16x8(ld16(ws + r * kRowBytes + swz(r, 2 * q + half) * 16));
               }
@@ -818,27 +902,51 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
 template <int BM, int BN, int STAGES, typename T, Epi E, int KS, int LN, Quant Q = Quant::None>
 hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
   const dim3 grid((p.N / BN) * ((p.M + BM - 1) / BM));
-  const size_t epi = sizeof(T) == 2 ? (size_t)epi_layout_of<BM, BN, E, LN>(p.K, p.N).bytes : 0;
+  const size_t epi = (sizeof(T) == 2 ? (size_t)epi_layout_of<BM, BN, E, LN>(p.K, p.N).bytes : 0) +
+                     (size_t)gq_lds_bytes(Q, BN, p.K);
   hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, E, KS, LN, Q>), grid, dim3(kThreads * KS), epi, s, p);
   return hipGetLastError();
 }
 
-// int8 per-channel weights through the DMA kernel (bf16 activations, no
-// deferred LayerNorm): 64 x 128 tiles for the wide projections, else 64 x 64.
-template <int BM, int BN, int STAGES>
-hipError_t launch_dma_int8_tile(const GemmParams& p, hipStream_t s) {
+// Quantised weights through the DMA kernel (bf16 activations, no deferred
+// LayerNorm): 64 x 128 tiles for the wide projections, else 64 x 64.
+template <int BM, int BN, int STAGES, Quant Q>
+hipError_t launch_dma_q_tile(const GemmParams& p, hipStream_t s) {
   switch (p.epi) {
-    case Epi::None: return launch_dma<BM, BN, STAGES, bf16_t, Epi::None, 1, 0, Quant::Int8>(p, s);
-    case Epi::Bias: return launch_dma<BM, BN, STAGES, bf16_t, Epi::Bias, 1, 0, Quant::Int8>(p, s);
-    case Epi::BiasGelu: return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasGelu, 1, 0, Quant::Int8>(p, s);
-    case Epi::BiasResidual: return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasResidual, 1, 0, Quant::Int8>(p, s);
+    case Epi::None: return launch_dma<BM, BN, STAGES, bf16_t, Epi::None, 1, 0, Q>(p, s);
+    case Epi::Bias: return launch_dma<BM, BN, STAGES, bf16_t, Epi::Bias, 1, 0, Q>(p, s);
+    case Epi::BiasGelu: return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasGelu, 1, 0, Q>(p, s);
+    case Epi::BiasResidual: return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasResidual, 1, 0, Q>(p, s);
   }
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_dma_int8(const GemmParams& p, hipStream_t s) {
-  if (p.N % 128 == 0 && p.N >= 1024) return launch_dma_int8_tile<64, 128, 4>(p, s);
-  return launch_dma_int8_tile<64, 64, 5>(p, s);
+// The group scales of a tile's rows must fit the LDS next to the ring: up to
+// 32 KB (for example K <= 4096 with 64 weight rows of int4 scales and zeros),
+// and come by dword DMA, so 4-byte aligned; otherwise the register-staged
+// kernel runs.
+bool dma_q_fits(const GemmParams& p, int BN) {
+  auto a4 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 3) == 0; };
+  if (quant_grouped(p.quant) && (!a4(p.scales) || (p.quant != Quant::Int8G && !a4(p.zeros)))) return false;
+  return gq_lds_bytes(p.quant, BN, p.K) <= 32 * 1024;
+}
+
+template <typename T, Quant Q>
+hipError_t launch_typed(const GemmParams& p, hipStream_t s);
+
+// Measured on the quantised encoder (batch 32 x 128, per forward): the DMA
+// kernel wins where K is long -- FFN-down (K = 1536) 114 -> 71 us (int8),
+// 150 -> 133 us (int4) -- while at K = 384 the register-staged kernel, which
+// converts each weight once per block instead of once per wave that reads
+// it, is as fast for int8 and faster for int4 (FFN-up 84 vs 105 us, QKV 70
+// vs 92 us).
+template <Quant Q>
+hipError_t launch_dma_q(const GemmParams& p, hipStream_t s) {
+  if (p.K >= 1024) {
+    if (p.N % 128 == 0 && p.N >= 1024 && dma_q_fits(p, 128)) return launch_dma_q_tile<64, 128, 4, Q>(p, s);
+    if (dma_q_fits(p, 64)) return launch_dma_q_tile<64, 64, 5, Q>(p, s);
+  }
+  return launch_typed<bf16_t, Q>(p, s);
 }
 
 template <int BM, int BN, int STAGES, typename T, int KS = 1>
@@ -1009,10 +1117,10 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   if (p.dtype == DType::F32) return launch_dense<float>(p, s);
   switch (p.quant) {
     case Quant::None: return launch_dense<bf16_t>(p, s);
-    case Quant::Int8: return launch_dma_int8(p, s);
-    case Quant::Int4: return launch_typed<bf16_t, Quant::Int4>(p, s);
-    case Quant::Int8G: return launch_typed<bf16_t, Quant::Int8G>(p, s);
-    case Quant::Int4M: return launch_typed<bf16_t, Quant::Int4M>(p, s);
+    case Quant::Int8: return launch_dma_q<Quant::Int8>(p, s);
+    case Quant::Int4: return launch_dma_q<Quant::Int4>(p, s);
+    case Quant::Int8G: return launch_dma_q<Quant::Int8G>(p, s);
+    case Quant::Int4M: return launch_dma_q<Quant::Int4M>(p, s);
   }
   return hipErrorInvalidValue;
 }

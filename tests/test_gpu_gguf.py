@@ -73,9 +73,10 @@ def _case(rlx, fmt, M, N, K, epi, seed):
     return y.float().cpu().numpy(), ref, tol
 
 
-# few-row shapes (1..16 rows, K % 128 == 0) and tiled ones (more rows, K % 128 != 0, or 128 KB of x)
+# few-row shapes (1..16 rows, K % 128 == 0) and tiled ones (more rows, K % 128 != 0, or 128 KB of x;
+# K >= 1024 takes the LDS-DMA kernel, with 64 x 128 tiles from N = 1024)
 SHAPES = [(1, 256, 1024), (5, 1152, 384), (16, 384, 1536), (3, 128, 192), (33, 384, 1536), (300, 1536, 384),
-          (16, 512, 4096)]
+          (16, 512, 4096), (40, 1024, 1024)]
 
 
 @pytest.mark.parametrize("fmt", FMTS)

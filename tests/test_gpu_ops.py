@@ -112,7 +112,8 @@ def test_bf16_output_rounding_is_round_to_nearest_even(rlx, N):
 
 @pytest.mark.parametrize("scheme", ["int8", "int4"])
 @pytest.mark.parametrize("epi", EPIS)
-@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 1152, 384), (129, 1536, 384), (200, 384, 1536)])
+# (K >= 1024 takes the LDS-DMA kernel: 64 x 64 tiles, or 64 x 128 from N = 1024)
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 1152, 384), (129, 1536, 384), (200, 384, 1536), (100, 1024, 1024)])
 def test_gemm_dequant(rlx, scheme, epi, M, N, K):
     rng = np.random.default_rng(2000 + M + N + K)
     x = to_bf16_exact(rng.normal(0, 1, (M, K)))
