@@ -18,10 +18,10 @@
 //  * Each wave streams its (tile, unit) items through a private ring of LDS
 //    slots with direct-to-LDS loads, two to four items in flight (per
 //    layout, measured) across tile boundaries; the only barrier is the one
-//    per tile that hands the wave partials to the epilogue (double-buffered).  A unit's 16 weight rows land
-//    group-major ([16-byte chunk][row][16 B]): lane (n, G) then reads the 4
-//    (int4) or 8 (int8) bytes of k-octet G of each group with conflict-free
-//    ds_read2.
+//    per tile that hands the wave partials to the epilogue (double-buffered).
+//    A unit's 16 weight rows land group-major ([16-byte chunk][row][16 B]):
+//    lane (n, G) then reads the 4 (int4) or 8 (int8) bytes of k-octet G of
+//    each group with conflict-free ds_read2.
 //  * v_mfma_f32_16x16x32_bf16 takes the activations as the A operand (rows m;
 //    rows M..15 repeat row M-1 and their results are dropped) and the codes
 //    as B, one 32-k group per instruction.  Lane l supplies row / column
