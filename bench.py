@@ -183,6 +183,97 @@ def bench_scaled_matmul(args):
     print(json.dumps(rec), flush=True)
 
 
+def attention_pairs(kind, S, lens, window):
+    """Visible (query, key) pairs per head summed over the batch (every query row is computed)."""
+    if kind == "custom":
+        return sum(S * int(L) for L in lens)
+    if kind == "none":
+        return len(lens) * S * S
+    if kind == "causal":
+        return len(lens) * S * (S + 1) // 2
+    return len(lens) * sum(min(window, i + 1) for i in range(S))
+
+
+def bench_attention(args):
+    """rlx_masked_attention on the long-sequence shape: batch 8 x 512, 12 heads
+    x 32, bf16, Q / K / V as column views of one fused [B*S, 3H] buffer; key
+    lengths half U[64, 512], half 512 (custom mask) or the mask kind's own
+    visibility (none, causal, sliding window)."""
+    import numpy as np
+    import torch
+
+    import paper_2609_37916_amd as rlx
+
+    B, S, heads, d = 8, 512, 12, 32
+    H = heads * d
+    kind = args.attn_kind
+    code = {"none": rlx.MASK_NONE, "causal": rlx.MASK_CAUSAL, "sliding": rlx.MASK_SLIDING_WINDOW,
+            "custom": rlx.MASK_CUSTOM}[kind]
+    rng = np.random.default_rng(11)
+    lens = np.concatenate([rng.integers(64, S + 1, B // 2), np.full(B - B // 2, S)])
+    mask = (np.arange(S)[None, :] < lens[:, None]).astype(np.uint8)
+    qkv = torch.from_numpy(rng.normal(0, 1, (B * S, 3 * H)).astype(np.float32)).to("cuda", torch.bfloat16)
+    km = torch.from_numpy(mask).cuda() if kind == "custom" else None
+    out = torch.empty((B * S, H), dtype=torch.bfloat16, device="cuda")
+    window = args.attn_window
+
+    def launch():
+        rlx.masked_attention(qkv[:, :H], qkv[:, H:2 * H], qkv[:, 2 * H:], B=B, S=S, heads=heads, kind=code,
+                             key_mask=km, window=window, row_stride=3 * H, out=out)
+
+    for _ in range(args.warmup):
+        launch()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        launch()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = 1e3 * e0.elapsed_time(e1) / args.steps
+    pairs = attention_pairs(kind, S, lens, window) * heads
+    flops = 4.0 * d * pairs  # Q K^T and P V over the visible pairs
+    tf = flops / (us * 1e-6) / 1e12
+    name = f"attention_{kind}_b{B}_s{S}"
+    rec = {
+        "metric": f"masked attention TFLOP/s ({kind} mask, batch {B} x {S}, {heads} heads x {d}, bf16, 1 MI355X)",
+        "value": round(tf, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(us / 1e3, 5), "p50_ms": round(us / 1e3, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (N(0,1) Q / K / V; key lengths half U[64,512], half 512)",
+        "config": {"workload": name, "batch": B, "seq_len": S, "heads": heads, "head_dim": d, "mask": kind,
+                   "window": window if kind == "sliding" else None, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "flops_per_launch": flops, "avg_launch_us": round(us, 3)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        q4 = qkv.float().cpu().numpy().reshape(B, S, 3, heads, d)
+        okind = {"none": oracle.MASK_NONE, "causal": oracle.MASK_CAUSAL, "sliding": oracle.MASK_SLIDING_WINDOW,
+                 "custom": oracle.MASK_CUSTOM}[kind]
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            b = reps % B
+            oracle.masked_attention(q4[b:b + 1, :, 0], q4[b:b + 1, :, 1], q4[b:b + 1, :, 2], kind=okind,
+                                    key_mask=mask[b:b + 1] if kind == "custom" else None, window=window)
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= args.cpu_seconds or reps >= 1000:
+                break
+        done = sum(attention_pairs(kind, S, lens[[r % B]], window) for r in range(reps)) * heads * 4.0 * d
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+        except Exception:
+            threads = os.cpu_count() or 1
+        rec["cpu_baseline"] = {"value": round(done / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+                               "sample": f"{reps} single-sequence calls (all heads), float64 NumPy oracle, {dt:.1f} s"}
+    print(json.dumps(rec), flush=True)
+
+
 def gemv_bytes(scheme, M, N, K, epi_bias=True):
     """Algorithmic HBM bytes of one few-row dequantising matmul: every weight
     code, scale and zero-point (or min) once, the activations, the bias and the
@@ -299,9 +390,11 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=20, help="profiled forwards (per-kernel event times)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", choices=("encoder", "scaled_matmul", "dequant_gemv"), default="encoder",
+    ap.add_argument("--op", choices=("encoder", "scaled_matmul", "dequant_gemv", "attention"), default="encoder",
                     help="encoder: the encoder forward (default); scaled_matmul: the block-scaled minifloat matmul; "
-                         "dequant_gemv: the few-row dequantising matmul")
+                         "dequant_gemv: the few-row dequantising matmul; attention: rlx_masked_attention")
+    ap.add_argument("--attn-kind", default="causal", choices=("none", "causal", "sliding", "custom"))
+    ap.add_argument("--attn-window", type=int, default=128)
     ap.add_argument("--gemv-scheme", default="int4", choices=("int4", "int8", "q4_0", "q4_1", "q8_0"))
     ap.add_argument("--gemv-shape", type=int, nargs=3, default=(1, 14336, 4096), metavar=("M", "N", "K"))
     ap.add_argument("--mx-format", default="e4m3", choices=sorted(MX_PEAK_TFLOPS))
@@ -345,6 +438,9 @@ def main():
         return
     if args.op == "dequant_gemv":
         bench_dequant_gemv(args)
+        return
+    if args.op == "attention":
+        bench_attention(args)
         return
 
     sp = workloads.spec(args.workload)
