@@ -6,16 +6,20 @@
 // strided narrows of one buffer (Section III-B).  Here that is one kernel that
 // reads Q/K/V by row stride straight out of the fused QKV projection.
 //
-// bf16 kernel -- one block per (query block of 128, head, sequence), four
-// waves of 32 queries each:
+// bf16 kernel -- one block per (query block of 128, head, sequence), eight
+// waves: four query sub-tiles of 32, each walked by two waves that take one
+// half of its visible key tiles apiece and merge their softmax states (max,
+// denominator, unnormalised context) through LDS at the end:
 //  * K rows and V (transposed) for the block's key range are staged once in
-//    LDS; key tiles of 32 whose keys are all masked are skipped.
+//    LDS; key tiles of 32 whose keys are all masked are skipped, and tiles
+//    that every query of the sub-tile sees in full skip the mask arithmetic.
 //  * Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16
 //    (d = 32 is two k-steps), so each lane holds 16 keys of a single query:
 //    the softmax max / sum over keys is 15 in-lane steps plus one exchange
 //    with the partner lane 32 away.
-//  * Online softmax in fp32 in base 2 (scale * log2 e folded into one
-//    multiply), then P is rounded to bf16 and multiplied into ctx^T = V^T P^T,
+//  * Online softmax in fp32 in base 2 (p = 2^(s c - m c), c = scale log2 e, as one fma),
+//    the state rescaled only when some query's maximum grows), then P is
+//    rounded to bf16 and multiplied into ctx^T = V^T P^T,
 //    again on the matrix cores.  The probabilities stay in registers: their
 //    C-layout is used directly as the B operand, with the V^T operand read in
 //    the matching (permuted) key order.
@@ -61,52 +65,97 @@ __device__ __forceinline__ bool visible(int kind, int window, int qi, int key) {
   return true;
 }
 
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnParams p, int vt_stride) {
+// Whole 32-key tile [key0, key0 + 32) visible to every query of [q0, q0 + 32)
+// under the positional part of the mask (the key mask is checked separately).
+__device__ __forceinline__ bool tile_fully_visible(int kind, int window, int q0, int key0) {
+  if (kind == 1) return key0 + 31 <= q0;
+  if (kind == 2) return key0 + 31 <= q0 && key0 > q0 + 31 - window;
+  return true;
+}
+
+// Partial softmax state of one wave, handed to its partner wave through LDS:
+// [query sub-tile][m, l, acc[16]][lane].
+constexpr int kPartFloats = 18;
+constexpr size_t kPartBytes = (size_t)4 * kPartFloats * 64 * 4;
+
+__global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_stride, int gx) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  const int b = blockIdx.z, h = blockIdx.y;
+  // Block order: the blocks of one (head, sequence) sit on one XCD (workgroups
+  // go to the eight XCDs round-robin), so its K and V are fetched into one L2;
+  // within it the query tile with the most visible keys comes first.
+  const int total = (int)gridDim.x;
+  int lin = (int)blockIdx.x;
+  if ((total & 7) == 0) lin = (lin & 7) * (total >> 3) + (lin >> 3);
+  const int qt = gx - 1 - lin % gx;
+  const int h = (lin / gx) % p.heads, b = lin / gx / p.heads;
   const SeqRange sr = seq_range(p, b);
   const int n = sr.n;
-  const int q_begin = blockIdx.x * kQBlock;
+  const int q_begin = qt * kQBlock;
   if (q_begin >= n) return;
   const int q_end = min(n, q_begin + kQBlock);
 
   int klo, khi;
   key_bounds(p, n, q_begin, q_end, klo, khi);
   klo &= ~31;                                  // stage whole 32-key tiles
-  const int nk = ((khi - klo) + 31) & ~31;     // staged keys (>= 0)
+  const int nk = ((khi - klo) + 31) & ~31;     // staged keys (0..512)
   const int ntiles = nk >> 5;
 
-  uint8_t* k_lds = smem;                                               // [nk][80 B]
+  uint8_t* k_lds = smem;                                                  // [nk][80 B]
   bf16_t* vt_lds = reinterpret_cast<bf16_t*>(smem + (size_t)nk * kKRow);  // [32][vt_stride]
   uint32_t* kbits = reinterpret_cast<uint32_t*>(smem + (size_t)nk * kKRow + 32 * vt_stride * 2);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int sub = wave & 3, kh = wave >> 2;  // query sub-tile of 32, key half
   const bf16_t* kg = reinterpret_cast<const bf16_t*>(p.k);
   const bf16_t* vg = reinterpret_cast<const bf16_t*>(p.v);
   const bf16_t* qg = reinterpret_cast<const bf16_t*>(p.q);
   const size_t ld = (size_t)p.ld_qkv;
   const int col = h * 32;
 
-  // Stage K (row-major) and V (transposed); keys past the sequence are zero.
-  for (int idx = tid; idx < nk * 4; idx += 256) {
-    const int kr = idx >> 2, c = idx & 3;
-    const int key = klo + kr;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (key < n) {
-      const size_t off = (size_t)(sr.row0 + key) * ld + col + c * 8;
-      kv = *reinterpret_cast<const uint4*>(kg + off);
-      vv = *reinterpret_cast<const uint4*>(vg + off);
-    }
-    *reinterpret_cast<uint4*>(k_lds + kr * kKRow + c * 16) = kv;
-    const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+  const int q0 = q_begin + sub * 32;
+  const bool active = q0 < n;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int qi = q0 + l32;
+  const int qrow = sr.row0 + min(qi, n - 1);
+  uint4 qa = *reinterpret_cast<const uint4*>(qg + (size_t)qrow * ld + col + half * 8);
+  uint4 qb = *reinterpret_cast<const uint4*>(qg + (size_t)qrow * ld + col + 16 + half * 8);
+  if (p.scale < 0.0f) {  // fold the sign into Q (exact) so the running max is over raw scores
+    qa.x ^= 0x80008000u; qa.y ^= 0x80008000u; qa.z ^= 0x80008000u; qa.w ^= 0x80008000u;
+    qb.x ^= 0x80008000u; qb.y ^= 0x80008000u; qb.z ^= 0x80008000u; qb.w ^= 0x80008000u;
+  }
+
+  // Stage K (row-major) and V (transposed): thread t takes keys 4(t/4) .. +3,
+  // dimensions 8(t%4) .. +7; all eight 16-byte loads are issued before any
+  // store.  Keys past the sequence are zero.
+  if (tid < nk) {
+    const int kq = tid >> 2, c = tid & 3;
+    uint4 kv[4], vv[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      vt_lds[(c * 8 + 2 * e) * vt_stride + kr] = (bf16_t)(w4[e] & 0xffffu);
-      vt_lds[(c * 8 + 2 * e + 1) * vt_stride + kr] = (bf16_t)(w4[e] >> 16);
+    for (int j = 0; j < 4; ++j) {
+      const int key = klo + 4 * kq + j;
+      kv[j] = make_uint4(0, 0, 0, 0);
+      vv[j] = make_uint4(0, 0, 0, 0);
+      if (key < n) {
+        const size_t off = (size_t)(sr.row0 + key) * ld + col + c * 8;
+        kv[j] = *reinterpret_cast<const uint4*>(kg + off);
+        vv[j] = *reinterpret_cast<const uint4*>(vg + off);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4*>(k_lds + (4 * kq + j) * kKRow + c * 16) = kv[j];
+    // V^T row 8c + e, keys 4kq .. 4kq+3: one 8-byte store per dimension.
+    auto word = [](const uint4& u, int w) { return w == 0 ? u.x : (w == 1 ? u.y : (w == 2 ? u.z : u.w)); };
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t a0 = word(vv[0], w), a1 = word(vv[1], w), a2 = word(vv[2], w), a3 = word(vv[3], w);
+      bf16_t* dst = vt_lds + (size_t)(c * 8 + 2 * w) * vt_stride + 4 * kq;
+      *reinterpret_cast<uint2*>(dst) = make_uint2((a0 & 0xffffu) | (a1 << 16), (a2 & 0xffffu) | (a3 << 16));
+      *reinterpret_cast<uint2*>(dst + vt_stride) = make_uint2((a0 >> 16) | (a1 & 0xffff0000u),
+                                                                 (a2 >> 16) | (a3 & 0xffff0000u));
     }
   }
   // Per-tile validity bits (key inside the sequence and allowed by the key mask).
-  for (int t = wave; t < ntiles; t += 4) {
+  for (int t = wave; t < ntiles; t += 8) {
     const int key = klo + t * 32 + (lane & 31);
     bool ok = key < n;
     if (ok && p.key_mask) ok = p.key_mask[(size_t)b * p.S + key] != 0;
@@ -115,29 +164,35 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnParams p, int vt_str
   }
   __syncthreads();
 
-  const int q0 = q_begin + wave * 32;
-  if (q0 >= n) return;
-  const int l32 = lane & 31, half = lane >> 5;
-  const int qi = q0 + l32;
-  const int qrow = sr.row0 + min(qi, n - 1);
+  const bf16x8_t qf0 = as_bf16x8(qa), qf1 = as_bf16x8(qb);
+  // The sub-tile's tiles, split between its two waves at the point that gives
+  // the first wave half (rounded up) of the tiles holding a visible key.  The
+  // split depends only on those tiles, so appending masked keys to a sequence
+  // leaves every result bit-identical.
+  int t_begin = 0, t_end = 0;
+  if (active) {
+    int wlo, whi;
+    key_bounds(p, n, q0, min(n, q0 + 32), wlo, whi);
+    const int a = max(0, (wlo - klo) >> 5), e = min(ntiles, (whi - klo + 31) >> 5);
+    int live = 0;
+    for (int t = a; t < e; ++t) live += kbits[t] != 0u;
+    int mid = a;
+    for (int c = 0; mid < e && c < (live + 1) / 2; ++mid) c += kbits[mid] != 0u;
+    t_begin = kh ? mid : a;
+    t_end = kh ? max(mid, e) : mid;
+  }
 
-  const bf16x8_t qf0 = as_bf16x8(*reinterpret_cast<const uint4*>(qg + (size_t)qrow * ld + col + half * 8));
-  const bf16x8_t qf1 = as_bf16x8(*reinterpret_cast<const uint4*>(qg + (size_t)qrow * ld + col + 16 + half * 8));
-
-  // Tiles this wave needs.
-  int wlo, whi;
-  key_bounds(p, n, q0, min(n, q0 + 32), wlo, whi);
-  const int t_begin = max(0, (wlo - klo) >> 5);
-  const int t_end = min(ntiles, (whi - klo + 31) >> 5);
-
-  const float sl2 = p.scale * kLog2e;
-  float m_run = -INFINITY, l_run = 0.0f;
+  // Kept above zero so that masked scores (-inf) stay -inf after the scaling.
+  const float sl2 = fmaxf(fabsf(p.scale) * kLog2e, 1e-30f);
+  const int xor32 = (lane ^ 32) << 2;  // ds_bpermute address of the partner lane
+  float m_run = -INFINITY;  // running max of the raw scores of this query (both lanes agree)
+  float l_run = 0.0f;       // this lane's share of the running denominator, relative to m_run
   f32x16_t acc;
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
 
   for (int t = t_begin; t < t_end; ++t) {
-    const uint32_t bits = kbits[t];
+    const uint32_t bits = __builtin_amdgcn_readfirstlane(kbits[t]);
     if (bits == 0u) continue;
     const int kb = t * 32;
     const uint8_t* krow = k_lds + (kb + l32) * kKRow + half * 16;
@@ -148,37 +203,48 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnParams p, int vt_str
     s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(*reinterpret_cast<const uint4*>(krow + 32)), qf1, s, 0, 0,
                                                 0);
     // Register v holds key kb + 8*(v/4) + 4*half + (v%4) for query qi.
-    float tv[16];
     float tmax = -INFINITY;
-    const bool need_pos = p.kind == 1 || p.kind == 2;
+    if (bits == 0xffffffffu && tile_fully_visible(p.kind, p.window, q0, klo + kb)) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int kk = 8 * (v >> 2) + 4 * half + (v & 3);
-      bool ok = (bits >> kk) & 1u;
-      if (need_pos) ok = ok && visible(p.kind, p.window, qi, klo + kb + kk);
-      tv[v] = ok ? s[v] * sl2 : -INFINITY;
-      tmax = fmaxf(tmax, tv[v]);
-    }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float m_new = fmaxf(m_run, tmax);
-    float alpha, psum = 0.0f;
-    float pv[16];
-    if (m_new == -INFINITY) {
-      alpha = 1.0f;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) pv[v] = 0.0f;
+      for (int v = 0; v < 16; ++v) tmax = fmaxf(tmax, s[v]);
     } else {
-      alpha = exp2f(m_run - m_new);
+      // This lane's visible keys of the tile as a bit mask (bit kk = key
+      // klo + kb + kk), shifted so that register v tests a constant bit.
+      uint32_t vis = bits;
+      if (p.kind == 1 || p.kind == 2) {
+        const int rel = qi - (klo + kb);  // keys kk <= rel are not in the future
+        vis &= rel >= 31 ? ~0u : (rel < 0 ? 0u : (2u << rel) - 1u);
+        if (p.kind == 2) {
+          const int lo = rel - p.window + 1;  // keys kk >= lo are inside the window
+          vis &= lo <= 0 ? ~0u : (lo >= 32 ? 0u : ~0u << lo);
+        }
+      }
+      vis >>= 4 * half;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        pv[v] = exp2f(tv[v] - m_new);
-        psum += pv[v];
+        s[v] = (vis >> (8 * (v >> 2) + (v & 3))) & 1u ? s[v] : -INFINITY;
+        tmax = fmaxf(tmax, s[v]);
       }
     }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+    tmax = fmaxf(tmax, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(xor32, __builtin_bit_cast(int, tmax))));
+    if (__any(tmax > m_run)) {  // some query's maximum grew: rescale its state
+      const float alpha = tmax > m_run ? __builtin_amdgcn_exp2f((m_run - tmax) * sl2) : 1.0f;
+      l_run *= alpha;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[v] *= alpha;
+      for (int v = 0; v < 16; ++v) acc[v] *= alpha;
+      m_run = fmaxf(m_run, tmax);
+    }
+    // p = exp2(sl2 * (s - m)) with the bare hardware exp2 (results below
+    // 2^-126 flush to zero); a query with nothing visible yet has s = -inf
+    // everywhere and gets p = 0.
+    const float mb = m_run == -INFINITY ? 0.0f : m_run * sl2;
+    float pv[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) pv[v] = __builtin_amdgcn_exp2f(fmaf(s[v], sl2, -mb));
+    float psum = 0.0f;
+#pragma unroll
+    for (int v = 0; v < 16; v += 4) psum += (pv[v] + pv[v + 1]) + (pv[v + 2] + pv[v + 3]);
+    l_run += psum;
 
     const uint4 pb0 = make_uint4(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]), pack_bf16x2(pv[4], pv[5]),
                                  pack_bf16x2(pv[6], pv[7]));
@@ -196,16 +262,37 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnParams p, int vt_str
                                                   as_bf16x8(pb1), acc, 0, 0, 0);
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  // Merge the two key halves of each query sub-tile (the K / V staging area is
+  // free once every wave has passed the barrier).
+  __syncthreads();
+  float* part = reinterpret_cast<float*>(smem) + (size_t)sub * kPartFloats * 64 + lane;
+  if (kh == 1 && active) {
+    part[0] = m_run;
+    part[64] = l_run;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) part[(2 + v) * 64] = acc[v];
+  }
+  __syncthreads();
+  if (kh == 1 || !active) return;
+  const float m1 = part[0], l1 = part[64];
+  const float m = fmaxf(m_run, m1);
+  float a0 = 0.0f, a1 = 0.0f;
+  if (m != -INFINITY) {
+    a0 = exp2f((m_run - m) * sl2);
+    a1 = exp2f((m1 - m) * sl2);
+  }
+  const float l_lane = a0 * l_run + a1 * l1;
+  const float l_tot = l_lane + __shfl_xor(l_lane, 32, 64);
   if (qi >= n) return;
   const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
   bf16_t* og = reinterpret_cast<bf16_t*>(p.out) + (size_t)(sr.row0 + qi) * p.ld_out + col;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int d = 8 * i + 4 * half;
-    *reinterpret_cast<uint2*>(og + d) =
-        make_uint2(pack_bf16x2(acc[4 * i] * inv, acc[4 * i + 1] * inv),
-                   pack_bf16x2(acc[4 * i + 2] * inv, acc[4 * i + 3] * inv));
+    float o[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) o[r] = (a0 * acc[4 * i + r] + a1 * part[(2 + 4 * i + r) * 64]) * inv;
+    *reinterpret_cast<uint2*>(og + d) = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
   }
 }
 
@@ -608,13 +695,17 @@ hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
   if (p.B <= 0 || p.S <= 0) return hipSuccess;
   const hipError_t le = set_lds_limits();
   if (le != hipSuccess) return le;
-  const dim3 grid((p.S + kQBlock - 1) / kQBlock, p.heads, p.B);
+  const int gx = (p.S + kQBlock - 1) / kQBlock;
   if (p.dtype == DType::BF16) {
     const int nk_max = (p.S + 31) & ~31;  // staged keys never exceed the padded length
     const int vt_stride = ((nk_max + 127) & ~127) + 4;
-    const size_t lds = (size_t)nk_max * kKRow + 32 * (size_t)vt_stride * 2 + (size_t)(nk_max / 32) * 4;
-    hipLaunchKernelGGL(attn_bf16_kernel, grid, dim3(256), lds, s, p, vt_stride);
+    const size_t stage = (size_t)nk_max * kKRow + 32 * (size_t)vt_stride * 2 + (size_t)(nk_max / 32) * 4;
+    const size_t lds = stage > kPartBytes ? stage : kPartBytes;
+    const int64_t blocks = (int64_t)gx * p.heads * p.B;
+    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(512), lds, s, p, vt_stride, gx);
   } else {
+    const dim3 grid(gx, p.heads, p.B);
     const size_t lds = (size_t)p.S * 32 * 4 * 2 + (size_t)p.S;
     hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(128), lds, s, p);
   }
