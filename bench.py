@@ -245,7 +245,8 @@ def bench_attention(args):
         "config": {"workload": name, "batch": B, "seq_len": S, "heads": heads, "head_dim": d, "mask": kind,
                    "window": window if kind == "sliding" else None, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4),
+                     "traffic": committed_traffic("attention", f"{kind}_b{B}_s{S}"),
                      "flops_per_launch": flops, "avg_launch_us": round(us, 3)},
     }
     if not args.no_cpu_baseline:
