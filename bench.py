@@ -496,7 +496,8 @@ def main():
     mfma_util = mm_flops / (mm_us * 1e-6) / (PEAK_BF16_TFLOPS * 1e12)
 
     rec = {
-        "metric": "encoder fwd sequences/sec (b32, s128, bf16, 1 MI355X)",
+        "metric": f"encoder fwd sequences/sec (b{sp.batch}, s{sp.seq}, "
+                  f"{sp.quant if sp.quant != 'none' else sp.dtype}, 1 MI355X)",
         "value": round(seq_per_s, 1),
         "unit": "sequences/s",
         "n_gpus": 1,

@@ -264,3 +264,27 @@ def test_attention_identical_keys_mean_of_values(rlx):
         mean_v = v[b, :L].mean(axis=0)  # [heads, 32]
         assert_within(got[b], np.broadcast_to(mean_v, got[b].shape), BF16_REL * np.abs(mean_v) + 2.0 ** -7 *
                       np.abs(v[b, :L]).max(), "identical keys")
+
+
+@pytest.mark.parametrize("scale", [-0.3, 0.0, 2.5])
+@pytest.mark.parametrize("kind,window", [("custom", 0), ("causal", 0), ("sliding", 50)])
+def test_attention_scale_sign_and_zero(rlx, kind, window, scale):
+    """A negative scale (its sign folded into Q), a zero scale (uniform
+    weights over the visible keys) and a sharp one, over several query blocks
+    with a ragged sequence."""
+    rng = np.random.default_rng(4300 + KINDS[kind])
+    B, S, heads = 2, 300, 2
+    H = heads * 32
+    qkv, mask = _attention_case(rng, B, S, heads, [S, 77], holes=(kind == "custom"))
+    qkv = to_bf16_exact(qkv)
+    use_mask = kind == "custom"
+    buf = _dev(qkv, torch.bfloat16)
+    got = rlx.masked_attention(buf[:, 0:H], buf[:, H:2 * H], buf[:, 2 * H:], B=B, S=S, heads=heads, kind=KINDS[kind],
+                               key_mask=_dev(mask, torch.uint8) if use_mask else None, window=window, scale=scale,
+                               row_stride=3 * H).float().cpu().numpy().reshape(B, S, heads, 32)
+    q = qkv[:, :H].reshape(B, S, heads, 32)
+    k = qkv[:, H:2 * H].reshape(B, S, heads, 32)
+    v = qkv[:, 2 * H:].reshape(B, S, heads, 32)
+    ref = oracle.masked_attention(q, k, v, KINDS[kind], mask if use_mask else None, window, scale)
+    tol = BF16_REL * np.abs(ref) + 2.0 ** -7 * np.abs(v).max(axis=(1, 3), keepdims=True)
+    assert_within(got, ref, tol, f"attention {kind} scale={scale}")
