@@ -6,10 +6,12 @@
 // strided narrows of one buffer (Section III-B).  Here that is one kernel that
 // reads Q/K/V by row stride straight out of the fused QKV projection.
 //
-// bf16 kernel -- one block per (query block of 128, head, sequence), eight
-// waves: four query sub-tiles of 32, each walked by two waves that take one
-// half of its visible key tiles apiece and merge their softmax states (max,
-// denominator, unnormalised context) through LDS at the end:
+// bf16 kernel -- blocks of eight waves per (query tile of 128, head,
+// sequence): four query sub-tiles of 32, each walked by two waves that take
+// one half of its visible key tiles apiece and merge their softmax states
+// (max, denominator, unnormalised context) through LDS at the end.  When there
+// are fewer than two tiles per CU, some tiles are split into two half blocks
+// (64 queries, four waves per sub-tile) so that every CU holds the same work:
 //  * K rows and V (transposed) for the block's key range are staged once in
 //    LDS; key tiles of 32 whose keys are all masked are skipped, and tiles
 //    that every query of the sub-tile sees in full skip the mask arithmetic.
@@ -28,6 +30,8 @@
 //    the encoder uses after compacting away padded tokens.
 // fp32 kernel -- one thread per query, K/V staged in LDS, scalar online softmax.
 #include <math.h>
+
+#include <algorithm>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -73,26 +77,47 @@ __device__ __forceinline__ bool tile_fully_visible(int kind, int window, int q0,
   return true;
 }
 
-// Partial softmax state of one wave, handed to its partner wave through LDS:
-// [query sub-tile][m, l, acc[16]][lane].
+// Partial softmax states of the waves that hand theirs to a sub-tile's first
+// wave through LDS: [query sub-tile][key part - 1][m, l, acc[16]][lane]
+// (4 sub-tiles x 1 part, or 2 sub-tiles x 3 parts).
 constexpr int kPartFloats = 18;
-constexpr size_t kPartBytes = (size_t)4 * kPartFloats * 64 * 4;
+constexpr size_t kPartBytes = (size_t)6 * kPartFloats * 64 * 4;
 
-__global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_stride, int gx) {
+// Blocks of eight waves.  A whole block takes a query tile of 128: four
+// sub-tiles of 32, each walked by two waves that split its key tiles.  A half
+// block takes 64 queries of a tile: two sub-tiles, each split over four waves.
+// Block -> work: workgroups go to the eight XCDs round-robin (block i to XCD
+// i % 8), and each XCD is given a contiguous run of query tiles (tile index
+// fastest, the tile with the most visible keys first, then head, then
+// sequence), so the tiles of one (head, sequence) share one L2.  With
+// nfull >= 0 the first nfull / 8 tiles of each XCD's run are whole blocks and
+// the rest are split into two half blocks; with nfull < 0 every tile is a
+// whole block and the XCD runs apply when the block count is a multiple of 8.
+__global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_stride, int gx, int nfull) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  // Block order: the blocks of one (head, sequence) sit on one XCD (workgroups
-  // go to the eight XCDs round-robin), so its K and V are fetched into one L2;
-  // within it the query tile with the most visible keys comes first.
   const int total = (int)gridDim.x;
-  int lin = (int)blockIdx.x;
-  if ((total & 7) == 0) lin = (lin & 7) * (total >> 3) + (lin >> 3);
+  int lin, qhalf = -1;  // query tile, and which half of it (-1: the whole tile)
+  if (nfull >= 0) {
+    const int tq = gx * p.heads * p.B / 8, fx = nfull / 8;
+    const int x = (int)blockIdx.x & 7, j = (int)blockIdx.x >> 3;
+    if (j < fx) {
+      lin = x * tq + j;
+    } else {
+      lin = x * tq + fx + ((j - fx) >> 1);
+      qhalf = (j - fx) & 1;
+    }
+  } else {
+    lin = (int)blockIdx.x;
+    if ((total & 7) == 0) lin = (lin & 7) * (total >> 3) + (lin >> 3);
+  }
   const int qt = gx - 1 - lin % gx;
   const int h = (lin / gx) % p.heads, b = lin / gx / p.heads;
   const SeqRange sr = seq_range(p, b);
   const int n = sr.n;
-  const int q_begin = qt * kQBlock;
+  const int q_begin = qt * kQBlock + (qhalf > 0 ? kQBlock / 2 : 0);
   if (q_begin >= n) return;
-  const int q_end = min(n, q_begin + kQBlock);
+  const int q_end = min(n, q_begin + (qhalf >= 0 ? kQBlock / 2 : kQBlock));
+  const int nsub = qhalf >= 0 ? 2 : 4, nsplit = 8 / nsub;  // query sub-tiles, key parts per sub-tile
 
   int klo, khi;
   key_bounds(p, n, q_begin, q_end, klo, khi);
@@ -105,7 +130,7 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_str
   uint32_t* kbits = reinterpret_cast<uint32_t*>(smem + (size_t)nk * kKRow + 32 * vt_stride * 2);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int sub = wave & 3, kh = wave >> 2;  // query sub-tile of 32, key half
+  const int sub = wave & (nsub - 1), kp = wave / nsub;  // query sub-tile of 32, key part
   const bf16_t* kg = reinterpret_cast<const bf16_t*>(p.k);
   const bf16_t* vg = reinterpret_cast<const bf16_t*>(p.v);
   const bf16_t* qg = reinterpret_cast<const bf16_t*>(p.q);
@@ -165,10 +190,10 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_str
   __syncthreads();
 
   const bf16x8_t qf0 = as_bf16x8(qa), qf1 = as_bf16x8(qb);
-  // The sub-tile's tiles, split between its two waves at the point that gives
-  // the first wave half (rounded up) of the tiles holding a visible key.  The
-  // split depends only on those tiles, so appending masked keys to a sequence
-  // leaves every result bit-identical.
+  // The sub-tile's tiles holding a visible key, split between its waves in
+  // key order: part k takes ranks [ceil(k c / P), ceil((k + 1) c / P)) of the
+  // c such tiles (P parts).  The split depends only on those tiles, so
+  // appending masked keys to a sequence leaves every result bit-identical.
   int t_begin = 0, t_end = 0;
   if (active) {
     int wlo, whi;
@@ -176,10 +201,19 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_str
     const int a = max(0, (wlo - klo) >> 5), e = min(ntiles, (whi - klo + 31) >> 5);
     int live = 0;
     for (int t = a; t < e; ++t) live += kbits[t] != 0u;
-    int mid = a;
-    for (int c = 0; mid < e && c < (live + 1) / 2; ++mid) c += kbits[mid] != 0u;
-    t_begin = kh ? mid : a;
-    t_end = kh ? max(mid, e) : mid;
+    const int r0 = (kp * live + nsplit - 1) / nsplit, r1 = ((kp + 1) * live + nsplit - 1) / nsplit;
+    t_begin = e;
+    t_end = e;
+    for (int t = a, c = 0; t < e; ++t) {
+      if (kbits[t] == 0u) continue;
+      if (c == r0) t_begin = t;
+      if (c == r1) {
+        t_end = t;
+        break;
+      }
+      ++c;
+    }
+    t_begin = min(t_begin, t_end);
   }
 
   // Kept above zero so that masked scores (-inf) stay -inf after the scaling.
@@ -262,26 +296,34 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_str
                                                   as_bf16x8(pb1), acc, 0, 0, 0);
   }
 
-  // Merge the two key halves of each query sub-tile (the K / V staging area is
-  // free once every wave has passed the barrier).
+  // Merge the key parts of each query sub-tile into its first wave (the K / V
+  // staging area is free once every wave has passed the barrier).
   __syncthreads();
-  float* part = reinterpret_cast<float*>(smem) + (size_t)sub * kPartFloats * 64 + lane;
-  if (kh == 1 && active) {
-    part[0] = m_run;
-    part[64] = l_run;
+  float* part = reinterpret_cast<float*>(smem) + (size_t)sub * (nsplit - 1) * kPartFloats * 64 + lane;
+  if (kp > 0 && active) {
+    float* pp = part + (size_t)(kp - 1) * kPartFloats * 64;
+    pp[0] = m_run;
+    pp[64] = l_run;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) part[(2 + v) * 64] = acc[v];
+    for (int v = 0; v < 16; ++v) pp[(2 + v) * 64] = acc[v];
   }
   __syncthreads();
-  if (kh == 1 || !active) return;
-  const float m1 = part[0], l1 = part[64];
-  const float m = fmaxf(m_run, m1);
-  float a0 = 0.0f, a1 = 0.0f;
-  if (m != -INFINITY) {
-    a0 = exp2f((m_run - m) * sl2);
-    a1 = exp2f((m1 - m) * sl2);
+  if (kp > 0 || !active) return;
+  float m = m_run;
+  for (int k = 1; k < nsplit; ++k) m = fmaxf(m, part[(size_t)(k - 1) * kPartFloats * 64]);
+  // A part that saw no key has m = -inf and weight 0; so has every part of a
+  // query with no visible key (m = -inf), whose output is then zero.
+  const float a0 = m == -INFINITY ? 0.0f : exp2f((m_run - m) * sl2);
+  float l_lane = a0 * l_run;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] *= a0;
+  for (int k = 1; k < nsplit; ++k) {
+    const float* pp = part + (size_t)(k - 1) * kPartFloats * 64;
+    const float ak = m == -INFINITY ? 0.0f : exp2f((pp[0] - m) * sl2);
+    l_lane += ak * pp[64];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] += ak * pp[(2 + v) * 64];
   }
-  const float l_lane = a0 * l_run + a1 * l1;
   const float l_tot = l_lane + __shfl_xor(l_lane, 32, 64);
   if (qi >= n) return;
   const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
@@ -289,10 +331,9 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_str
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int d = 8 * i + 4 * half;
-    float o[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) o[r] = (a0 * acc[4 * i + r] + a1 * part[(2 + 4 * i + r) * 64]) * inv;
-    *reinterpret_cast<uint2*>(og + d) = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+    *reinterpret_cast<uint2*>(og + d) =
+        make_uint2(pack_bf16x2(acc[4 * i] * inv, acc[4 * i + 1] * inv),
+                   pack_bf16x2(acc[4 * i + 2] * inv, acc[4 * i + 3] * inv));
   }
 }
 
@@ -701,9 +742,22 @@ hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
     const int vt_stride = ((nk_max + 127) & ~127) + 4;
     const size_t stage = (size_t)nk_max * kKRow + 32 * (size_t)vt_stride * 2 + (size_t)(nk_max / 32) * 4;
     const size_t lds = stage > kPartBytes ? stage : kPartBytes;
-    const int64_t blocks = (int64_t)gx * p.heads * p.B;
-    if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(512), lds, s, p, vt_stride, gx);
+    const int64_t tiles = (int64_t)gx * p.heads * p.B;
+    if (tiles > 0x3fffffff) return hipErrorInvalidValue;
+    // Two blocks fit a CU.  With at most two tiles per CU, split tiles into
+    // half blocks until every CU holds one whole and one half block (or two
+    // halves); with fewer tiles than CUs, every tile is split.
+    int cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return hipErrorInvalidValue;
+    int nfull = -1;
+    int64_t blocks = tiles;
+    if (tiles % 8 == 0 && cus % 8 == 0 && tiles < 2 * (int64_t)cus) {
+      nfull = (int)std::max<int64_t>(0, 2 * tiles - 2 * (int64_t)cus);
+      blocks = 2 * tiles - nfull;
+    }
+    hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(512), lds, s, p, vt_stride, gx, nfull);
   } else {
     const dim3 grid(gx, p.heads, p.B);
     const size_t lds = (size_t)p.S * 32 * 4 * 2 + (size_t)p.S;

@@ -288,3 +288,25 @@ def test_attention_scale_sign_and_zero(rlx, kind, window, scale):
     ref = oracle.masked_attention(q, k, v, KINDS[kind], mask if use_mask else None, window, scale)
     tol = BF16_REL * np.abs(ref) + 2.0 ** -7 * np.abs(v).max(axis=(1, 3), keepdims=True)
     assert_within(got, ref, tol, f"attention {kind} scale={scale}")
+
+
+@pytest.mark.parametrize("kind,window", [("none", 0), ("causal", 0), ("sliding", 128), ("custom", 0)])
+def test_attention_benchmark_workload_full_size(rlx, kind, window):
+    """The attention benchmark's own shape and launch: batch 8 x 512, 12 heads
+    x 32, Q / K / V as column views of one fused [4096, 1152] bf16 buffer, key
+    lengths half U[64, 512] and half 512 (the key mask for the custom kind);
+    every output against the oracle."""
+    rng = np.random.default_rng(11)
+    B, S, heads = 8, 512, 12
+    H = heads * 32
+    lens = np.concatenate([rng.integers(64, S + 1, B // 2), np.full(B - B // 2, S)])
+    mask = (np.arange(S)[None, :] < lens[:, None]).astype(np.uint8)
+    qkv = to_bf16_exact(rng.normal(0, 1, (B * S, 3 * H)))
+    use_mask = kind == "custom"
+    got = _run_attention(rlx, qkv, mask, B, S, heads, "bf16", kind, window, use_mask)
+    q = qkv[:, :H].reshape(B, S, heads, 32)
+    k = qkv[:, H:2 * H].reshape(B, S, heads, 32)
+    v = qkv[:, 2 * H:].reshape(B, S, heads, 32)
+    ref = oracle.masked_attention(q, k, v, KINDS[kind], mask if use_mask else None, window, 1 / math.sqrt(32))
+    tol = BF16_REL * np.abs(ref) + 2.0 ** -7 * np.abs(v).max(axis=(1, 3), keepdims=True)
+    assert_within(got, ref, tol, f"attention {kind} batch 8 x 512")
