@@ -406,7 +406,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} (WORLD_SIZE {world}) is not supported; the encoder "
-              f"forward is data-parallel over sequences and this build runs on a single MI355X.", file=sys.stderr)
+              f"forward is data-parallel over sequences and this library runs it on a single MI355X.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

@@ -20,7 +20,7 @@ definitions taken here are those of the OCP Microscaling (MX) formats, v1.0:
   (-1)^s 2^(e - bias) (1 + m / 2^mbits).
 * value of element k of a row = X[k // 32] * decode(code[k]).
 
-Storage readings (this build's layout, the same on both sides): rows are
+Storage readings (the library's layout, the same on both sides): rows are
 row-major along K; FP8 codes take one byte each; FP4 codes two per byte, the
 lower k in the low nibble; FP6 codes four per three bytes as a little-endian
 bit stream (code i of a row occupies bits 6i .. 6i+5 of the row's bytes read
@@ -30,7 +30,7 @@ ScaledMatMul:  Y[m, n] = sum_k A(m, k) * B(n, k)  (B in the nn.Linear
 convention, one row per output column), computed here in float64 on the
 decoded values.  Every product of two decoded elements and two scales is a
 power-of-two multiple of a small integer, so the float64 sum is exact for
-every input this build tests, and equals any exactly rounded float32 result
+every input the tests use, and equals any exactly rounded float32 result
 whenever the float32 partial sums are exact.
 """
 from __future__ import annotations
