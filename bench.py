@@ -100,8 +100,38 @@ def cpu_baseline(workload_name, target_s):
         oracle.encoder_forward(sample)
     dt = time.perf_counter() - t0
     what = f"first {n} of {B} sequences" if reps == 1 else f"all {B} sequences, {reps} times"
-    return {"value": n * reps / dt, "unit": "sequences/s", "cores": threads, "kind": "oracle",
-            "sample": f"{what} of {workload_name}, float64 NumPy oracle, {dt:.1f} s"}
+    rec = {"value": n * reps / dt, "unit": "sequences/s", "cores": threads, "kind": "oracle",
+           "sample": f"{what} of {workload_name}, float64 NumPy oracle, {dt:.1f} s"}
+    # the same oracle on one thread, over a quarter of the time
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            n1 = max(1, min(B, round(target_s / 4 / max(per_seq, 1e-6))))
+            one = workloads.select_rows(wl, np.arange(n1))
+            t0 = time.perf_counter()
+            oracle.encoder_forward(one)
+            d1 = time.perf_counter() - t0
+        rec["one_thread"] = {"value": n1 / d1, "sample": f"first {n1} sequences, {d1:.1f} s"}
+    except Exception:
+        rec["one_thread"] = None
+    return rec
+
+
+def gpu_state():
+    """Shader clock and temperatures from rocm-smi after the timed region (run as a
+    child process), or None where it is unavailable."""
+    import shutil
+    import subprocess
+    exe = shutil.which("rocm-smi") or ("/opt/rocm/bin/rocm-smi" if os.path.exists("/opt/rocm/bin/rocm-smi") else None)
+    if exe is None:
+        return None
+    try:
+        r = subprocess.run([exe, "--showclocks", "--showtemp", "--json"], capture_output=True, text=True, timeout=30)
+        card = next(iter(json.loads(r.stdout[r.stdout.index("{"):]).values()))
+    except Exception:
+        return None
+    keep = {k: v for k, v in card.items() if "sclk" in k.lower() or "mclk" in k.lower() or "emperature" in k}
+    return keep or None
 
 
 MX_PEAK_TFLOPS = {"e4m3": 5000.0, "e5m2": 5000.0, "e2m3": 10100.0, "e3m2": 10100.0, "e2m1": 10100.0}
@@ -183,6 +213,12 @@ def bench_scaled_matmul(args):
     print(json.dumps(rec), flush=True)
 
 
+# Chip-wide rate of the bare exp2 instruction (v_exp_f32), measured on one MI355X
+# with independent exp2 chains against fma chains: ~17.0 T/s, a quarter of the
+# measured fp32 fma rate (63 T/s).
+EXP2_PEAK_G = 17000.0
+
+
 def attention_pairs(kind, S, lens, window):
     """Visible (query, key) pairs per head summed over the batch (every query row is computed)."""
     if kind == "custom":
@@ -247,7 +283,11 @@ def bench_attention(args):
         "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel", "achieved": round(tf, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(tf / PEAK_BF16_TFLOPS, 4),
                      "traffic": committed_traffic("attention", f"{kind}_b{B}_s{S}"),
-                     "flops_per_launch": flops, "avg_launch_us": round(us, 3)},
+                     "flops_per_launch": flops, "avg_launch_us": round(us, 3),
+                     # at head_dim 32 every score costs one exp2 against 64 MFMA flops: the exp pipe's
+                     # ceiling in visible scores per second (measured rate of the bare exp2 instruction)
+                     "exp_ceiling": {"achieved_g_per_s": round(pairs / us / 1e3, 1), "peak_g_per_s": EXP2_PEAK_G,
+                                     "frac": round(pairs / us / 1e3 / EXP2_PEAK_G, 4)}},
     }
     if not args.no_cpu_baseline:
         import oracle
@@ -391,6 +431,8 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=20, help="profiled forwards (per-kernel event times)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the encoder forward replayed from its HIP graph instead of launched kernel by kernel")
     ap.add_argument("--op", choices=("encoder", "scaled_matmul", "dequant_gemv", "attention"), default="encoder",
                     help="encoder: the encoder forward (default); scaled_matmul: the block-scaled minifloat matmul; "
                          "dequant_gemv: the few-row dequantising matmul; attention: rlx_masked_attention")
@@ -447,7 +489,7 @@ def main():
     sp = workloads.spec(args.workload)
     wl = workloads.make(sp)
     weights, inputs = to_device(wl)
-    enc = rlx.Encoder(**encoder_kwargs(sp), weights=weights)
+    enc = rlx.Encoder(**encoder_kwargs(sp, use_graph=args.graph), weights=weights)
     out = torch.empty((sp.batch, sp.hidden), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
 
@@ -515,7 +557,7 @@ def main():
         "data": "synthetic (seeded ids, N(0,0.02) weights, lengths U[%d,%d])" % (sp.len_lo, sp.len_hi),
         "config": {"workload": sp.name, "batch": sp.batch, "seq_len": sp.seq, "layers": sp.layers,
                    "hidden": sp.hidden, "heads": sp.heads, "ffn": sp.ffn, "real_tokens": tokens,
-                   "quant": sp.quant, "parallelism": "single GPU", "graph_replay": True},
+                   "quant": sp.quant, "parallelism": "single GPU", "graph_replay": args.graph},
         "mfma_util_pct": round(100 * mfma_util, 2),
         "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
@@ -524,6 +566,24 @@ def main():
         "kernel_us_per_forward": {k: round(v, 2) for k, v in sorted(per_fwd_us.items(), key=lambda kv: -kv[1])},
     }
     enc.close()
+
+    # the same forward in the other launch mode (HIP graph replay or kernel by kernel), a shorter sample
+    eager = rlx.Encoder(**encoder_kwargs(sp, use_graph=not args.graph), weights=weights)
+    for _ in range(5):
+        eager.forward(inputs["input"], inputs["mask"], out=out)
+    n_eager = max(10, args.steps // 4)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_eager + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for i in range(n_eager):
+        eager.forward(inputs["input"], inputs["mask"], out=out)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    eager_p50 = statistics.median([evs[i].elapsed_time(evs[i + 1]) for i in range(n_eager)])
+    eager.close()
+    rec["other_mode"] = {"graph_replay": not args.graph, "p50_ms": round(eager_p50, 5),
+                         "sequences_per_s": round(sp.batch / (eager_p50 / 1e3), 1), "steps": n_eager}
+    rec["gpu_state"] = gpu_state()
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_seconds)
     print(json.dumps(rec), flush=True)

@@ -259,7 +259,7 @@ class Encoder:
 
     def __init__(self, *, hidden=384, heads=12, head_dim=32, ffn=1536, layers=6, vocab=30522, max_pos=512,
                  type_vocab=2, ln_eps=1e-12, dtype="bf16", quant="none", group_size=32, input_kind="ids",
-                 output_kind="pooled", max_batch=32, max_seq=128, use_graph=True, weights: Dict = None):
+                 output_kind="pooled", max_batch=32, max_seq=128, use_graph=False, weights: Dict = None):
         self._keep: List = []
         cfg = EncoderConfig(hidden, heads, head_dim, ffn, layers, vocab, max_pos, type_vocab, ln_eps,
                             {"f32": F32, "bf16": BF16}[dtype],

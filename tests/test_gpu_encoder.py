@@ -33,7 +33,7 @@ def _tol(sp):
     return TOL[sp.quant] if sp.quant != "none" else TOL[sp.dtype]
 
 
-def _run(rlx, wl, use_graph=True, max_batch=None, max_seq=None):
+def _run(rlx, wl, use_graph=False, max_batch=None, max_seq=None):
     weights, inputs = to_device(wl)
     enc = rlx.Encoder(**encoder_kwargs(wl.spec, max_batch, max_seq, use_graph), weights=weights)
     out = enc.forward(inputs["input"], inputs["mask"])

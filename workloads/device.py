@@ -46,7 +46,7 @@ def to_device(wl, device="cuda"):
     return weights, inputs
 
 
-def encoder_kwargs(sp, max_batch=None, max_seq=None, use_graph=True):
+def encoder_kwargs(sp, max_batch=None, max_seq=None, use_graph=False):
     return dict(hidden=sp.hidden, heads=sp.heads, head_dim=sp.head_dim, ffn=sp.ffn, layers=sp.layers, vocab=sp.vocab,
                 max_pos=sp.max_pos, type_vocab=sp.type_vocab, ln_eps=sp.eps, dtype=sp.dtype, quant=sp.quant,
                 group_size=sp.group, input_kind=sp.input_kind, output_kind=sp.output_kind,
