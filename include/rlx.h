@@ -236,7 +236,9 @@ typedef struct {
   rlx_output_kind output_kind;
   int max_batch;     /* <= 8192; workspace is planned for max_batch * max_seq tokens */
   int max_seq;       /* <= 512                                           */
-  int use_graph;     /* 1: record each (B,S,buffers) forward once as a HIP graph and replay it */
+  int use_graph;     /* 1: record each (B,S,buffers) forward once as a HIP graph and replay it;
+                        0: launch the kernels one by one (measured 1-3% faster for this
+                        forward on MI355X: the launches hide behind the running kernels) */
 } rlx_encoder_config;
 
 /* One layer's weights.  Linear weights follow the nn.Linear convention
