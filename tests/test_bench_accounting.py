@@ -22,3 +22,27 @@ def test_attention_pairs_match_the_oracle_visibility(kind, S, window):
         row = (np.arange(S) < L).astype(np.uint8) if kind == "custom" else None
         want += int(visible_keys(S, KINDS[kind], row, window).sum())
     assert bench.attention_pairs(kind, S, lens, window) == want
+
+
+@pytest.mark.parametrize("scheme", ["int4", "int8", "q4_0", "q4_1", "q8_0"])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 128), (5, 192, 256)])
+def test_gemv_bytes_match_the_buffers(scheme, M, N, K):
+    """bench.py's algorithmic bytes of the few-row matmul equal the sizes of the
+    buffers one call reads and writes: the weight codes and their per-channel
+    or per-group metadata (GGUF schemes as their repacked layout: 4-bit codes
+    two per byte or int8 codes, one f16 scale per 32-weight block, and one f16
+    zero / min per block for the 4-bit ones), bf16 x and y, and the f32 bias."""
+    import workloads
+    from workloads import gguf as wg
+    rng = np.random.default_rng(N + K)
+    w = rng.normal(0, 0.02, (N, K)).astype(np.float32)
+    if scheme == "int4":
+        weight = sum(a.nbytes for a in workloads.quantize_int4_grouped(w, 32))
+    elif scheme == "int8":
+        weight = sum(a.nbytes for a in workloads.quantize_int8_per_channel(w))
+    else:
+        codes, d, m = oracle.gguf.parse(wg.quantize(w, scheme), scheme, K)
+        per_code = 0.5 if scheme != "q8_0" else 1.0
+        weight = int(codes.size * per_code) + 2 * d.size + (2 * d.size if scheme != "q8_0" else 0)
+    io = 2 * M * K + 2 * M * N + 4 * N
+    assert bench.gemv_bytes(scheme, M, N, K) == weight + io
