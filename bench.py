@@ -7,7 +7,8 @@ accumulation, seeded synthetic ids and N(0, 0.02) weights, valid lengths
 U[16, 128] -- the paper's inference measurement (p50 of the encoder forward
 at seq 128, batch up to 32) restated on this GPU.  One step is one whole
 forward (embedding, 6 layers, pooling) with the inputs resident in HBM,
-replayed from the encoder's recorded HIP graph.
+enqueued by rlx_encoder_forward in the encoder's default launch mode
+(--graph: replayed from its recorded HIP graph instead).
 
 Prints one JSON line: sequences/s, p50 ms, the roofline of the dominant
 kernel (algorithmic flops per launch / its event-timed average duration) and
@@ -83,7 +84,7 @@ def cpu_baseline(workload_name, target_s):
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     except Exception:
-        threads = os.cpu_count() or 1
+        threads = None
     wl = workloads.make(workload_name)
     B = wl.spec.batch
     probe = workloads.select_rows(wl, np.arange(min(2, B)))
@@ -100,7 +101,14 @@ def cpu_baseline(workload_name, target_s):
         oracle.encoder_forward(sample)
     dt = time.perf_counter() - t0
     what = f"first {n} of {B} sequences" if reps == 1 else f"all {B} sequences, {reps} times"
+    # cores: the threads the oracle used (its BLAS pool; the rest of NumPy runs on one);
+    # the host's CPU count and the CPUs this process may run on, beside it
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except Exception:
+        affinity = None
     rec = {"value": n * reps / dt, "unit": "sequences/s", "cores": threads, "kind": "oracle",
+           "blas_threads": threads, "host_cpu_count": os.cpu_count(), "affinity_cpus": affinity,
            "sample": f"{what} of {workload_name}, float64 NumPy oracle, {dt:.1f} s"}
     # the same oracle on one thread, over a quarter of the time
     try:

@@ -117,9 +117,10 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
  * x: [M,K] row-major, dtype x_dt (RLX_BF16 or RLX_F32; quantised schemes
  * need RLX_BF16).  W: [N,K] in the layout of `scheme` (nn.Linear
  * convention: one row per output feature).  bias: f32 [N] (needed by every
- * epilogue except RLX_EPI_NONE).  residual: [M,N] of dtype x_dt (only for
- * RLX_EPI_BIAS_RESIDUAL).  y: [M,N] of dtype x_dt.  Accumulation is fp32;
- * bf16 outputs are rounded once at the end.
+ * epilogue except RLX_EPI_NONE).  y: [M,N] of dtype y_dt: RLX_BF16 or
+ * RLX_F32 for bf16 x, RLX_F32 for f32 x.  residual: [M,N] of dtype y_dt
+ * (only for RLX_EPI_BIAS_RESIDUAL).  Accumulation is fp32; bf16 outputs are
+ * rounded once at the end, f32 outputs are the fp32 result of the epilogue.
  * int8: the integer codes enter the bf16 matrix cores exactly and the
  * per-channel scale is applied to the fp32 sum.  int4: each weight
  * (q - z) * s is formed in fp32 and rounded to bf16 before the product,
@@ -137,12 +138,13 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
  * (both except in the few-row path below).
  * Supported: M >= 0 (M == 0 is a no-op), N and K positive multiples of 64,
  * group_size == 32 for the group schemes (ignored for int8 per-channel),
- * 16-byte aligned x, w, residual and y.  Otherwise RLX_ERR_UNSUPPORTED.
+ * 16-byte aligned x, w, residual and y; y_dt as above.  Otherwise
+ * RLX_ERR_UNSUPPORTED.
  */
 rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const void* w, rlx_quant scheme,
                               const void* scales, const void* zeros, int group_size, int N,
                               const float* bias, const void* residual, rlx_epilogue epi, void* y,
-                              void* stream);
+                              rlx_dtype y_dt, void* stream);
 
 /* Test support for the dequantisation step alone: writes the dequantised
  * weights W[n,k] as f32 [N,K] (products of a code and an f16 scale are exact
@@ -300,7 +302,9 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
 rlx_status rlx_encoder_forward(rlx_encoder* enc, const void* input, const uint8_t* attention_mask, int B, int S,
                                void* output, void* stream);
 
-/* Frees the workspace and cached graphs (waits for the device first).  NULL is ignored. */
+/* Frees the workspace and cached graphs after waiting for the last forward
+ * enqueued through the handle (an event recorded on its stream) -- not for
+ * the rest of the device.  NULL is ignored. */
 void rlx_encoder_destroy(rlx_encoder* enc);
 
 /* Per-kernel timing of forward passes (a native counterpart of a per-operator

@@ -88,7 +88,7 @@ def lib() -> ctypes.CDLL:
     L = ctypes.CDLL(LIB_PATH)
     i64, i32, f32 = ctypes.c_int64, ctypes.c_int, ctypes.c_float
     L.rlx_masked_attention.argtypes = [_vp, _vp, _vp, i64, _vp, i64, i32, i32, i32, i32, i32, i32, _vp, i32, f32, _vp]
-    L.rlx_dequant_matmul.argtypes = [_vp, i32, i32, i32, _vp, i32, _vp, _vp, i32, i32, _vp, _vp, i32, _vp, _vp]
+    L.rlx_dequant_matmul.argtypes = [_vp, i32, i32, i32, _vp, i32, _vp, _vp, i32, i32, _vp, _vp, i32, _vp, i32, _vp]
     L.rlx_dequant_unpack.argtypes = [_vp, i32, _vp, _vp, i32, i32, i32, _vp, _vp]
     L.rlx_scaled_matmul.argtypes = [_vp, _vp, i32, _vp, _vp, i32, i32, i32, i32, _vp, _vp]
     L.rlx_gguf_repack.argtypes = [_vp, i32, i32, i32, _vp, _vp, _vp, ctypes.POINTER(i32), _vp]
@@ -176,16 +176,17 @@ def masked_attention(q, k, v, *, B: int, S: int, heads: int, head_dim: int = 32,
 
 
 def dequant_matmul(x, w, *, scheme: int = Q_NONE, scales=None, zeros=None, group_size: int = 32, N: Optional[int] = None,
-                   bias=None, residual=None, epi: int = EPI_NONE, out=None, stream=None):
-    """y = epi(x @ dequant(w)^T) (see rlx_dequant_matmul)."""
+                   bias=None, residual=None, epi: int = EPI_NONE, out=None, out_dtype=None, stream=None):
+    """y = epi(x @ dequant(w)^T) (see rlx_dequant_matmul); y has x's dtype
+    unless ``out_dtype`` (or ``out``) says float32."""
     torch = _torch()
     M, K = x.shape
     if N is None:
         N = w.shape[0]
     if out is None:
-        out = torch.empty((M, N), dtype=x.dtype, device=x.device)
+        out = torch.empty((M, N), dtype=out_dtype if out_dtype is not None else x.dtype, device=x.device)
     check(lib().rlx_dequant_matmul(_ptr(x), _dt(x), M, K, _ptr(w), scheme, _ptr(scales), _ptr(zeros), group_size, N,
-                                   _ptr(bias), _ptr(residual), epi, _ptr(out), _stream(stream)))
+                                   _ptr(bias), _ptr(residual), epi, _ptr(out), _dt(out), _stream(stream)))
     return out
 
 

@@ -192,6 +192,9 @@ struct rlx_encoder {
   std::vector<Folded> folded;
   void* fold_mem = nullptr;
   hipStream_t cap_stream = nullptr;
+  // recorded after every forward on the caller's stream: destroy and the graph
+  // cache wait for it (the handle's own work) instead of the whole device
+  hipEvent_t done_ev = nullptr;
   std::vector<GraphEntry> graphs;
   uint64_t use_clock = 0;
   bool profiling = false;
@@ -468,7 +471,7 @@ rlx_status profiled_forward(rlx_encoder* e, const void* input, const uint8_t* ma
     if (g.g.B == B && g.g.S == S && g.g.input == input && g.g.mask == mask && g.g.output == output) hit = &g;
   if (!hit) {
     if (e->prof_graphs.size() >= kMaxGraphs) {
-      RLX_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
+      RLX_HIP(hipEventSynchronize(e->done_ev), "hipEventSynchronize");
       for (auto x : e->prof_graphs.front().slot_exec) (void)hipGraphExecDestroy(x);
       e->prof_graphs.erase(e->prof_graphs.begin());
     }
@@ -523,7 +526,7 @@ rlx_status run_graph_forward(rlx_encoder* e, const void* input, const uint8_t* m
     if (e->graphs.size() >= kMaxGraphs) {
       auto lru = std::min_element(e->graphs.begin(), e->graphs.end(),
                                   [](const GraphEntry& a, const GraphEntry& b) { return a.last_use < b.last_use; });
-      RLX_HIP(hipDeviceSynchronize(), "hipDeviceSynchronize");
+      RLX_HIP(hipEventSynchronize(e->done_ev), "hipEventSynchronize");  // no replay of it is in flight
       (void)hipGraphExecDestroy(lru->exec);
       e->graphs.erase(lru);
     }
@@ -616,7 +619,7 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
 
 rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const void* w, rlx_quant scheme,
                               const void* scales, const void* zeros, int group_size, int N, const float* bias,
-                              const void* residual, rlx_epilogue epi, void* y, void* stream) {
+                              const void* residual, rlx_epilogue epi, void* y, rlx_dtype y_dt, void* stream) {
   if (M < 0 || N <= 0 || K <= 0)
     return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: M=%d must be >= 0, N=%d and K=%d positive", M, N, K);
   if (!x || !y) return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: x and y must be non-null");
@@ -628,6 +631,9 @@ rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const
   if (x_dt != RLX_BF16 && x_dt != RLX_F32)
     return fail(RLX_ERR_UNSUPPORTED, "dequant_matmul: activation dtype %s not supported (bf16, f32)",
                 dtype_name(x_dt));
+  if (y_dt != x_dt && !(x_dt == RLX_BF16 && y_dt == RLX_F32))
+    return fail(RLX_ERR_UNSUPPORTED, "dequant_matmul: output dtype %s with %s activations not supported "
+                "(bf16 -> bf16 or f32, f32 -> f32)", dtype_name(y_dt), dtype_name(x_dt));
   rlx_status st = check_quant_weights("dequant_matmul", scheme, w, scales, zeros, group_size, N, K);
   if (st != RLX_OK) return st;
   if (scheme != RLX_Q_NONE && x_dt != RLX_BF16)
@@ -641,6 +647,7 @@ rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const
   g.dtype = x_dt == RLX_BF16 ? DType::BF16 : DType::F32;
   g.quant = to_quant(scheme);
   g.epi = static_cast<Epi>(epi);
+  g.y_f32 = x_dt == RLX_BF16 && y_dt == RLX_F32;
   RLX_HIP(launch_gemm(g, static_cast<hipStream_t>(stream)), "gemm launch");
   return ok();
 }
@@ -752,10 +759,10 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
     e->S2 = reinterpret_cast<float2*>(base + o_S2);
   }
   he = hipStreamCreateWithFlags(&e->cap_stream, hipStreamNonBlocking);
+  if (he == hipSuccess) he = hipEventCreateWithFlags(&e->done_ev, hipEventDisableTiming);
   if (he != hipSuccess) {
-    (void)hipFree(e->ws);
-    delete e;
-    return hip_fail(he, "hipStreamCreateWithFlags");
+    rlx_encoder_destroy(e);
+    return hip_fail(he, "encoder_create: stream and event");
   }
   if (e->deferred) {
     st = fold_layer_norms(e);
@@ -783,24 +790,27 @@ rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t*
     return fail(RLX_ERR_INVALID_ARG, "encoder_forward: current device %d differs from the handle's device %d", dev,
                 e->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (e->profiling) {
-    rlx_status st = profiled_forward(e, input, attention_mask, B, S, output, s);
-    return st == RLX_OK ? ok() : st;
-  }
-  if (!e->cfg.use_graph) {
-    rlx_status st = enqueue_forward(e, input, attention_mask, B, S, output, s, nullptr);
-    return st == RLX_OK ? ok() : st;
-  }
-  rlx_status st = run_graph_forward(e, input, attention_mask, B, S, output, s);
-  return st == RLX_OK ? ok() : st;
+  rlx_status st;
+  if (e->profiling)
+    st = profiled_forward(e, input, attention_mask, B, S, output, s);
+  else if (!e->cfg.use_graph)
+    st = enqueue_forward(e, input, attention_mask, B, S, output, s, nullptr);
+  else
+    st = run_graph_forward(e, input, attention_mask, B, S, output, s);
+  if (st != RLX_OK) return st;
+  RLX_HIP(hipEventRecord(e->done_ev, s), "hipEventRecord");
+  return ok();
 }
 
 void rlx_encoder_destroy(rlx_encoder* e) {
   if (!e) return;
-  (void)hipDeviceSynchronize();
+  // the last forward enqueued through the handle, and the handle's own stream
+  if (e->done_ev) (void)hipEventSynchronize(e->done_ev);
+  if (e->cap_stream) (void)hipStreamSynchronize(e->cap_stream);
   destroy_graphs(e);
   for (auto ev : e->prof_ev)
     if (ev) (void)hipEventDestroy(ev);
+  if (e->done_ev) (void)hipEventDestroy(e->done_ev);
   if (e->cap_stream) (void)hipStreamDestroy(e->cap_stream);
   if (e->ws) (void)hipFree(e->ws);
   if (e->fold_mem) (void)hipFree(e->fold_mem);

@@ -282,6 +282,7 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
   static_assert(KS == 1 || NRB == 1, "split-K tiles stage all rows at once");
   static_assert(kThreads * KS >= BM, "one thread per row merges the row statistics");
   constexpr int NT = kThreads * KS;
+  constexpr int ES = sizeof(T);
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int PITCH = BN * 4 + 16;  // bytes; 16 rows of a column land on distinct banks
   constexpr int EPC = 16 / (int)sizeof(T);
@@ -375,10 +376,19 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
       }
       if constexpr (E == Epi::BiasResidual) {
         float rr[EPC];
-        if constexpr (STAGED)
+        if (ES == 2 && p.y_f32) {  // an f32 residual beside an f32 output: from global memory
+          const float4* rf = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(p.residual) +
+                                                             (size_t)m * N + n);
+#pragma unroll
+          for (int e = 0; e < EPC; e += 4) {
+            const float4 a = rf[e / 4];
+            rr[e] = a.x; rr[e + 1] = a.y; rr[e + 2] = a.z; rr[e + 3] = a.w;
+          }
+        } else if constexpr (STAGED) {
           Vec16<T>::load(reinterpret_cast<const T*>(epi + lay.res_off + rl * (BN * 2) + cc * 16), rr);
-        else
+        } else {
           Vec16<T>::load(res + (size_t)m * N + n, rr);
+        }
         if constexpr ((LN & kLnRes) != 0) {
           const float2 st = mrg[BM + rl];
 #pragma unroll
@@ -416,6 +426,10 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
         for (int e = 0; e < 8; ++e) m2 = fmaf(f[e] - mean, f[e] - mean, m2);
         m2 = dpp_sum8(m2);
         if ((cc & 7) == 0) p.y_stats[(size_t)m * (N >> 6) + (n >> 6)] = make_float2(mean, m2);
+      } else if (ES == 2 && p.y_f32) {
+        float4* yf = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.y) + (size_t)m * N + n);
+#pragma unroll
+        for (int e = 0; e < EPC; e += 4) yf[e / 4] = make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
       } else {
         Vec16<T>::store(y + (size_t)m * N + n, v);
       }
@@ -629,8 +643,10 @@ __device__ __forceinline__ void issue_epilogue_operands(const GemmParams& p, int
                                                  : ((LN & kLnRes) ? p.res_beta : nullptr);
       if (vp) src = reinterpret_cast<const uint8_t*>(vp + n0 + c);
     } else if (o < lay.xst_off) {
+      // (an f32 residual is read by the epilogue itself)
       const int b = o - lay.res_off, r = b / (BN * 2);
-      src = reinterpret_cast<const uint8_t*>(p.residual) + ((size_t)min(m0 + r, M - 1) * p.N + n0) * 2 + b % (BN * 2);
+      if (!p.y_f32)
+        src = reinterpret_cast<const uint8_t*>(p.residual) + ((size_t)min(m0 + r, M - 1) * p.N + n0) * 2 + b % (BN * 2);
     } else if (o < lay.mrg_off) {
       const bool xs = o < lay.rst_off;
       const int np = xs ? p.K >> 6 : p.N >> 6;
@@ -1110,6 +1126,7 @@ bool gemm_deferred_ln_supported(DType dt, Quant q, int H) {
 
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
+  if (p.y_f32 && (p.dtype != DType::BF16 || p.x_stats || p.res_stats || p.y_stats)) return hipErrorInvalidValue;
   if (gemv_supported(p)) return launch_gemv(p, s);
   if ((p.x_stats && !gemm_deferred_ln_supported(p.dtype, p.quant, p.K)) ||
       ((p.res_stats || p.y_stats) && !gemm_deferred_ln_supported(p.dtype, p.quant, p.N)))

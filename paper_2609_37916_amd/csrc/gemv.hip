@@ -109,7 +109,8 @@ struct GvEpiLayout {
   int bias, scale, res, res_pitch, bytes;
 };
 __host__ __device__ constexpr int gv_round(int v, int a) { return (v + a - 1) / a * a; }
-__host__ __device__ inline GvEpiLayout gv_epi_layout(Quant q, Epi e, int M, int tpb) {
+// (residual rows of y's element size: 2 bytes, or 4 for an f32 output)
+__host__ __device__ inline GvEpiLayout gv_epi_layout(Quant q, Epi e, int M, int tpb, bool y_f32) {
   GvEpiLayout l{};
   int off = 0;
   l.bias = off;
@@ -117,7 +118,7 @@ __host__ __device__ inline GvEpiLayout gv_epi_layout(Quant q, Epi e, int M, int 
   l.scale = off;
   if (q == Quant::Int8) off += gv_round(tpb * 16 * 2, 256);
   l.res = off;
-  l.res_pitch = gv_round(tpb * 16 * 2, 256);
+  l.res_pitch = gv_round(tpb * 16 * (y_f32 ? 4 : 2), 256);
   if (e == Epi::BiasResidual) off += M * l.res_pitch;
   l.bytes = gv_round(off, 1024);
   return l;
@@ -146,7 +147,7 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
   uint8_t* ring = gv_lds + wave * U::kDepth * U::kCodeBytes;
   uint8_t* meta = gv_lds + kGvWaves * U::kDepth * U::kCodeBytes + wave * U::kDepth * U::kMetaBytes;
   uint8_t* red = gv_lds + kGvWaves * U::kDepth * (U::kCodeBytes + U::kMetaBytes);
-  const GvEpiLayout el = gv_epi_layout(Q, E, M, tpb);
+  const GvEpiLayout el = gv_epi_layout(Q, E, M, tpb, p.y_f32);
   uint8_t* epi = red + 2 * kGvWaves * 1024;
   uint8_t* xl = epi + el.bytes;
   float* xs = reinterpret_cast<float*>(xl + (size_t)M * K * 2);
@@ -179,9 +180,14 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
   if constexpr (Q == Quant::Int8)
     if (wave == 1) dma_run(reinterpret_cast<const uint16_t*>(p.scales) + (size_t)t0 * 16, epi + el.scale, ncol / 2);
   if constexpr (E == Epi::BiasResidual)
-    for (int m = wave; m < M; m += kGvWaves)
-      dma_run(reinterpret_cast<const bf16_t*>(p.residual) + (size_t)m * N + (size_t)t0 * 16, epi + el.res + m * el.res_pitch,
-              ncol / 2);
+    for (int m = wave; m < M; m += kGvWaves) {
+      if (p.y_f32)
+        dma_run(reinterpret_cast<const float*>(p.residual) + (size_t)m * N + (size_t)t0 * 16,
+                epi + el.res + m * el.res_pitch, ncol);
+      else
+        dma_run(reinterpret_cast<const bf16_t*>(p.residual) + (size_t)m * N + (size_t)t0 * 16,
+                epi + el.res + m * el.res_pitch, ncol / 2);
+    }
 
   // 2. Item loads.  Item (tile t, unit u): lane (row l16, chunk G) of the
   //    wave moves 16 bytes of row 16 t + l16; slot layout [chunk][row][16 B].
@@ -328,8 +334,12 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
         if constexpr (E != Epi::None) v += reinterpret_cast<const float*>(epi + el.bias)[c];
         if constexpr (E == Epi::BiasGelu) v = gelu_erf(v);
         if constexpr (E == Epi::BiasResidual)
-          v += bf16_to_f32(reinterpret_cast<const bf16_t*>(epi + el.res + m * el.res_pitch)[c]);
-        reinterpret_cast<bf16_t*>(p.y)[(size_t)m * N + n] = f32_to_bf16(v);
+          v += p.y_f32 ? reinterpret_cast<const float*>(epi + el.res + m * el.res_pitch)[c]
+                       : bf16_to_f32(reinterpret_cast<const bf16_t*>(epi + el.res + m * el.res_pitch)[c]);
+        if (p.y_f32)
+          reinterpret_cast<float*>(p.y)[(size_t)m * N + n] = v;
+        else
+          reinterpret_cast<bf16_t*>(p.y)[(size_t)m * N + n] = f32_to_bf16(v);
       }
     }
   }
@@ -369,7 +379,7 @@ GvPlan gemv_plan(const GemmParams& p) {
   GvPlan g{};
   for (int per_cu = 2; per_cu >= 1; --per_cu) {
     g.tpb = (tiles + device_cus() * per_cu - 1) / (device_cus() * per_cu);
-    g.lds = base + gv_epi_layout(p.quant, p.epi, p.M, g.tpb).bytes;
+    g.lds = base + gv_epi_layout(p.quant, p.epi, p.M, g.tpb, p.y_f32).bytes;
     if (g.lds * per_cu <= 160 * 1024) break;
   }
   g.grid = (tiles + g.tpb - 1) / g.tpb;

@@ -22,8 +22,8 @@ struct GemmParams {
   const void* scales;    // f16 (int8: [N]; int4: [N,K/32])
   const void* zeros;     // f16 [N,K/32] (int4)
   const float* bias;     // f32 [N]
-  const void* residual;  // [M,N] (dtype)
-  void* y;               // [M,N] (dtype)
+  const void* residual;  // [M,N] (dtype, or f32 with y_f32)
+  void* y;               // [M,N] (dtype, or f32 with y_f32)
   int M, N, K;           // M is an upper bound when m_dev is set
   const int* m_dev;      // optional device-side row count (rows >= *m_dev are skipped)
   DType dtype;
@@ -48,6 +48,7 @@ struct GemmParams {
   const float* res_beta;
   float2* y_stats;
   float ln_eps;
+  bool y_f32;            // bf16 x with an f32 output (and residual); not with the deferred-LayerNorm fields
 };
 // True when the deferred-LayerNorm fields are implemented for rows of H columns.
 bool gemm_deferred_ln_supported(DType dt, Quant q, int H);

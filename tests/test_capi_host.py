@@ -64,23 +64,37 @@ def test_attention_argument_errors(L):
 def test_dequant_matmul_argument_errors(L):
     f = L.rlx_dequant_matmul
     P = 4096
-    # (x, x_dt, M, K, w, scheme, scales, zeros, group, N, bias, residual, epi, y, stream)
-    assert f(P, rlx.BF16, 8, 96, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.ERR_UNSUPPORTED
-    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, rlx.EPI_BIAS, P, None) == \
-        rlx.ERR_INVALID_ARG
-    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, P, None, rlx.EPI_BIAS_RESIDUAL, P, None) == \
-        rlx.ERR_INVALID_ARG
-    assert f(P, rlx.F32, 8, 64, P, rlx.Q_INT8_PER_CHANNEL, P, None, 32, 64, None, None, 0, P, None) == \
+    # (x, x_dt, M, K, w, scheme, scales, zeros, group, N, bias, residual, epi, y, y_dt, stream)
+    assert f(P, rlx.BF16, 8, 96, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.BF16, None) == \
         rlx.ERR_UNSUPPORTED
-    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT8_PER_CHANNEL, None, None, 32, 64, None, None, 0, P, None) == \
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, rlx.EPI_BIAS, P, rlx.BF16, None) == \
         rlx.ERR_INVALID_ARG
-    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT4_GROUP_ZP, P, P, 64, 64, None, None, 0, P, None) == rlx.ERR_UNSUPPORTED
-    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT4_GROUP_ZP, P, None, 32, 64, None, None, 0, P, None) == \
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, P,
+             None, rlx.EPI_BIAS_RESIDUAL, P, rlx.BF16, None) == \
         rlx.ERR_INVALID_ARG
-    assert f(P, rlx.F16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.ERR_UNSUPPORTED
-    assert f(None, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.ERR_INVALID_ARG
-    assert f(P, rlx.BF16, -1, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.ERR_INVALID_ARG
-    assert f(P, rlx.BF16, 0, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, None) == rlx.OK
+    assert f(P, rlx.F32, 8, 64, P, rlx.Q_INT8_PER_CHANNEL, P, None, 32, 64, None, None, 0, P, rlx.F32, None) == \
+        rlx.ERR_UNSUPPORTED
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT8_PER_CHANNEL, None, None, 32, 64, None, None, 0, P, rlx.BF16, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT4_GROUP_ZP, P, P, 64, 64, None, None, 0, P, rlx.BF16, None) == \
+        rlx.ERR_UNSUPPORTED
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_INT4_GROUP_ZP, P, None, 32, 64, None, None, 0, P, rlx.BF16, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, rlx.F16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.BF16, None) == \
+        rlx.ERR_UNSUPPORTED
+    assert f(None, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.BF16, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, rlx.BF16, -1, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.BF16, None) == \
+        rlx.ERR_INVALID_ARG
+    assert f(P, rlx.BF16, 0, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.BF16, None) == rlx.OK
+    # output dtype: bf16 x gives bf16 or f32, f32 x gives f32
+    assert f(P, rlx.BF16, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.F16, None) == \
+        rlx.ERR_UNSUPPORTED
+    assert f(P, rlx.F32, 8, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.BF16, None) == \
+        rlx.ERR_UNSUPPORTED
+    assert b"output dtype" in L.rlx_last_error()
+    assert f(P, rlx.BF16, 0, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.F32, None) == rlx.OK
+    assert f(P, rlx.F32, 0, 64, P, rlx.Q_NONE, None, None, 32, 64, None, None, 0, P, rlx.F32, None) == rlx.OK
     assert L.rlx_dequant_unpack(P, rlx.Q_NONE, P, None, 32, 64, 64, P, None) == rlx.ERR_INVALID_ARG
 
 
@@ -184,10 +198,11 @@ def test_new_schemes_argument_errors(L):
     p16 = 0x10000
     # int4 min needs mins in `zeros`; the group schemes need group_size 32
     st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, rlx.Q_INT4_GROUP_MIN, p16, None, 32, 64, None, None,
-                              rlx.EPI_NONE, p16, None)
+                              rlx.EPI_NONE, p16, rlx.BF16, None)
     assert st == rlx.ERR_INVALID_ARG
     st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, rlx.Q_INT8_GROUP, p16, None, 64, 64, None, None,
-                              rlx.EPI_NONE, p16, None)
+                              rlx.EPI_NONE, p16, rlx.BF16, None)
     assert st == rlx.ERR_UNSUPPORTED
-    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, 5, p16, p16, 32, 64, None, None, rlx.EPI_NONE, p16, None)
+    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, 5, p16, p16, 32, 64, None, None, rlx.EPI_NONE, p16, rlx.BF16,
+                              None)
     assert st == rlx.ERR_INVALID_ARG  # unknown scheme
