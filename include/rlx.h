@@ -302,6 +302,26 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
 rlx_status rlx_encoder_forward(rlx_encoder* enc, const void* input, const uint8_t* attention_mask, int B, int S,
                                void* output, void* stream);
 
+/* The same forward without a handle and without allocating anything, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  cfg and w are as for
+ * rlx_encoder_create (host pointers, read during the call; the weights are
+ * device pointers), input / attention_mask / output as for
+ * rlx_encoder_forward, with B and S the only size limits that apply
+ * (cfg->max_batch, max_seq and use_graph are ignored).  The workspace (token
+ * maps and activations) lives in a static 16 MiB array that the library holds
+ * on each GPU it runs on until the process ends: B * S tokens must fit it --
+ * about 1900 bf16 or 950 f32 tokens at hidden 384, ffn 1536 -- otherwise
+ * RLX_ERR_UNSUPPORTED.  The LayerNorms run as separate kernels (the handle's
+ * forward folds them into weights derived at create time), so results agree
+ * with rlx_encoder_forward up to rounding.  Every call on one GPU uses that
+ * GPU's one array: calls that overlap on one GPU (concurrent streams or host
+ * threads) race and must be serialised by the caller.  Errors as for
+ * rlx_encoder_create and rlx_encoder_forward. */
+rlx_status rlx_encoder_forward_noalloc(const rlx_encoder_config* cfg, const rlx_encoder_weights* w,
+                                       const void* input, const uint8_t* attention_mask, int B, int S, void* output,
+                                       void* stream);
+
 /* Frees the workspace and cached graphs after waiting for the last forward
  * enqueued through the handle (an event recorded on its stream) -- not for
  * the rest of the device.  NULL is ignored. */

@@ -35,8 +35,8 @@ STATUS_NAMES = {0: "RLX_OK", 1: "RLX_ERR_INVALID_ARG", 2: "RLX_ERR_UNSUPPORTED",
 # every symbol include/rlx.h declares
 EXPORTS = ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_gguf_repack", "rlx_scaled_matmul",
            "rlx_encoder_create",
-           "rlx_encoder_forward", "rlx_encoder_destroy", "rlx_encoder_set_profiling", "rlx_encoder_profile_read",
-           "rlx_last_error", "rlx_version")
+           "rlx_encoder_forward", "rlx_encoder_forward_noalloc", "rlx_encoder_destroy", "rlx_encoder_set_profiling",
+           "rlx_encoder_profile_read", "rlx_last_error", "rlx_version")
 
 
 class RlxError(RuntimeError):
@@ -95,14 +95,16 @@ def lib() -> ctypes.CDLL:
     L.rlx_encoder_create.argtypes = [ctypes.POINTER(EncoderConfig), ctypes.POINTER(EncoderWeights),
                                      ctypes.POINTER(_vp)]
     L.rlx_encoder_forward.argtypes = [_vp, _vp, _vp, i32, i32, _vp, _vp]
+    L.rlx_encoder_forward_noalloc.argtypes = [ctypes.POINTER(EncoderConfig), ctypes.POINTER(EncoderWeights), _vp, _vp,
+                                              i32, i32, _vp, _vp]
     L.rlx_encoder_destroy.argtypes = [_vp]
     L.rlx_encoder_destroy.restype = None
     L.rlx_encoder_set_profiling.argtypes = [_vp, i32]
     L.rlx_encoder_profile_read.argtypes = [_vp, i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(i32),
                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
     for nm in ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_gguf_repack", "rlx_scaled_matmul",
-               "rlx_encoder_create",
-               "rlx_encoder_forward", "rlx_encoder_set_profiling", "rlx_encoder_profile_read"):
+               "rlx_encoder_create", "rlx_encoder_forward", "rlx_encoder_forward_noalloc", "rlx_encoder_set_profiling",
+               "rlx_encoder_profile_read"):
         getattr(L, nm).restype = ctypes.c_int
     L.rlx_last_error.restype = ctypes.c_char_p
     L.rlx_last_error.argtypes = []
@@ -248,6 +250,59 @@ def gguf_repack(blocks, gguf_type, *, N: int, K: int, stream=None):
     return scheme.value, codes, scales, zeros
 
 
+def _encoder_structs(keep: List, weights: Dict, *, hidden=384, heads=12, head_dim=32, ffn=1536, layers=6, vocab=30522,
+                     max_pos=512, type_vocab=2, ln_eps=1e-12, dtype="bf16", quant="none", group_size=32,
+                     input_kind="ids", output_kind="pooled", max_batch=32, max_seq=128, use_graph=False):
+    """EncoderConfig, EncoderWeights and the per-layer array they point to,
+    from keyword settings and a dict of device tensors (see Encoder); every
+    tensor passed is appended to ``keep``."""
+    cfg = EncoderConfig(hidden, heads, head_dim, ffn, layers, vocab, max_pos, type_vocab, ln_eps,
+                        {"f32": F32, "bf16": BF16}[dtype],
+                        {"none": Q_NONE, "int8": Q_INT8_PER_CHANNEL, "int4": Q_INT4_GROUP_ZP}[quant], group_size,
+                        {"ids": INPUT_IDS, "hidden": INPUT_HIDDEN}[input_kind],
+                        {"pooled": OUTPUT_POOLED, "hidden": OUTPUT_HIDDEN}[output_kind], max_batch, max_seq,
+                        1 if use_graph else 0)
+
+    def p(t):
+        if t is None:
+            return None
+        keep.append(t)
+        return _ptr(t)
+
+    lw_arr = (LayerWeights * layers)()
+    for i, lw in enumerate(weights["layers"]):
+        L = lw_arr[i]
+        for nm in ("wqkv", "wo", "w1", "w2"):
+            setattr(L, nm, p(lw[nm]))
+            setattr(L, nm + "_scales", p(lw.get(nm + "_scales")))
+            setattr(L, nm + "_zeros", p(lw.get(nm + "_zeros")))
+        L.bqkv, L.bo, L.b1, L.b2 = p(lw["bqkv"]), p(lw["bo"]), p(lw["b1"]), p(lw["b2"])
+        L.ln1_gamma, L.ln1_beta = p(lw["ln1_g"]), p(lw["ln1_b"])
+        L.ln2_gamma, L.ln2_beta = p(lw["ln2_g"]), p(lw["ln2_b"])
+    w = EncoderWeights(p(weights.get("word")), p(weights.get("pos")), p(weights.get("type")),
+                       p(weights.get("emb_gamma")), p(weights.get("emb_beta")),
+                       ctypes.cast(lw_arr, ctypes.POINTER(LayerWeights)))
+    keep.append(lw_arr)
+    return cfg, w
+
+
+def encoder_forward_noalloc(inp, mask, *, weights: Dict, out=None, stream=None, **settings):
+    """One encoder forward without a handle and without any device allocation
+    by the library (see rlx_encoder_forward_noalloc); ``settings`` are the
+    Encoder keyword settings."""
+    torch = _torch()
+    keep: List = []
+    cfg, w = _encoder_structs(keep, weights, **settings)
+    B, S = mask.shape
+    hidden = settings.get("hidden", 384)
+    if out is None:
+        shape = (B, hidden) if settings.get("output_kind", "pooled") == "pooled" else (B, S, hidden)
+        out = torch.empty(shape, dtype=torch.float32, device=mask.device)
+    check(lib().rlx_encoder_forward_noalloc(ctypes.byref(cfg), ctypes.byref(w), _ptr(inp), _ptr(mask), B, S, _ptr(out),
+                                            _stream(stream)))
+    return out
+
+
 class Encoder:
     """A compiled encoder: weights bound once, forward run many times.
 
@@ -262,35 +317,13 @@ class Encoder:
                  type_vocab=2, ln_eps=1e-12, dtype="bf16", quant="none", group_size=32, input_kind="ids",
                  output_kind="pooled", max_batch=32, max_seq=128, use_graph=False, weights: Dict = None):
         self._keep: List = []
-        cfg = EncoderConfig(hidden, heads, head_dim, ffn, layers, vocab, max_pos, type_vocab, ln_eps,
-                            {"f32": F32, "bf16": BF16}[dtype],
-                            {"none": Q_NONE, "int8": Q_INT8_PER_CHANNEL, "int4": Q_INT4_GROUP_ZP}[quant], group_size,
-                            {"ids": INPUT_IDS, "hidden": INPUT_HIDDEN}[input_kind],
-                            {"pooled": OUTPUT_POOLED, "hidden": OUTPUT_HIDDEN}[output_kind], max_batch, max_seq,
-                            1 if use_graph else 0)
+        cfg, w = _encoder_structs(self._keep, weights, hidden=hidden, heads=heads, head_dim=head_dim, ffn=ffn,
+                                  layers=layers, vocab=vocab, max_pos=max_pos, type_vocab=type_vocab, ln_eps=ln_eps,
+                                  dtype=dtype, quant=quant, group_size=group_size, input_kind=input_kind,
+                                  output_kind=output_kind, max_batch=max_batch, max_seq=max_seq, use_graph=use_graph)
         self.cfg = cfg
         self.hidden = hidden
         self.output_kind = output_kind
-
-        def p(t):
-            if t is None:
-                return None
-            self._keep.append(t)
-            return _ptr(t)
-
-        lw_arr = (LayerWeights * layers)()
-        for i, lw in enumerate(weights["layers"]):
-            L = lw_arr[i]
-            for nm in ("wqkv", "wo", "w1", "w2"):
-                setattr(L, nm, p(lw[nm]))
-                setattr(L, nm + "_scales", p(lw.get(nm + "_scales")))
-                setattr(L, nm + "_zeros", p(lw.get(nm + "_zeros")))
-            L.bqkv, L.bo, L.b1, L.b2 = p(lw["bqkv"]), p(lw["bo"]), p(lw["b1"]), p(lw["b2"])
-            L.ln1_gamma, L.ln1_beta = p(lw["ln1_g"]), p(lw["ln1_b"])
-            L.ln2_gamma, L.ln2_beta = p(lw["ln2_g"]), p(lw["ln2_b"])
-        w = EncoderWeights(p(weights.get("word")), p(weights.get("pos")), p(weights.get("type")),
-                           p(weights.get("emb_gamma")), p(weights.get("emb_beta")),
-                           ctypes.cast(lw_arr, ctypes.POINTER(LayerWeights)))
         h = _vp()
         check(lib().rlx_encoder_create(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(h)))
         self._h = h

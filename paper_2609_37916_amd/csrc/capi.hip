@@ -15,6 +15,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -210,6 +211,58 @@ constexpr size_t kMaxGraphs = 16;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// What one forward reads: the configuration, the bound weights and a
+// workspace (token maps and activation buffers for up to B*S tokens).  The
+// encoder handle owns one; the handle-free forward builds one over the
+// library's static scratch.
+struct FwdCtx {
+  const rlx_encoder_config* cfg;
+  const rlx_encoder_weights* w;
+  const rlx_layer_weights* layers;
+  DType dt;
+  int *cu, *tok_src, *tok_dst, *order;
+  void *X, *X1, *A, *CTX, *QKV, *G;
+  bool deferred;  // dense bf16: LayerNorms applied by the kernels that read their outputs
+  float2 *S1, *S2;
+  const rlx_encoder::Folded* folded;
+};
+
+FwdCtx ctx_of(const rlx_encoder* e) {
+  return FwdCtx{&e->cfg, &e->w, e->layers.data(), e->dt, e->cu, e->tok_src, e->tok_dst, e->order,
+                e->X, e->X1, e->A, e->CTX, e->QKV, e->G, e->deferred, e->S1, e->S2, e->folded.data()};
+}
+
+// Workspace layout for max_batch sequences of max_seq tokens (256-byte aligned regions).
+struct WsPlan {
+  size_t cu, src, dst, ord, X, X1, A, C, Q, G, S1, S2, bytes;
+};
+WsPlan plan_workspace(size_t max_batch, size_t max_seq, size_t H, size_t F, size_t es, bool deferred) {
+  const size_t T = max_batch * max_seq;
+  WsPlan p{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+  p.cu = take((max_batch + 1) * sizeof(int));
+  p.src = take(T * sizeof(int));
+  p.dst = take(T * sizeof(int));
+  p.ord = take(max_batch * sizeof(int));
+  p.X = take(T * H * es); p.X1 = take(T * H * es); p.A = take(T * H * es); p.C = take(T * H * es);
+  p.Q = take(T * 3 * H * es); p.G = take(T * F * es);
+  const size_t stats_bytes = deferred ? T * (H / 64) * sizeof(float2) : 0;
+  p.S1 = take(stats_bytes); p.S2 = take(stats_bytes);
+  p.bytes = off;
+  return p;
+}
+
+void bind_workspace(FwdCtx& c, uint8_t* base, const WsPlan& p) {
+  c.cu = reinterpret_cast<int*>(base + p.cu);
+  c.tok_src = reinterpret_cast<int*>(base + p.src);
+  c.tok_dst = reinterpret_cast<int*>(base + p.dst);
+  c.order = reinterpret_cast<int*>(base + p.ord);
+  c.X = base + p.X; c.X1 = base + p.X1; c.A = base + p.A; c.CTX = base + p.C; c.QKV = base + p.Q; c.G = base + p.G;
+  c.S1 = c.deferred ? reinterpret_cast<float2*>(base + p.S1) : nullptr;
+  c.S2 = c.deferred ? reinterpret_cast<float2*>(base + p.S2) : nullptr;
+}
+
 rlx_status check_config(const rlx_encoder_config* c) {
   if (c->hidden <= 0 || c->heads <= 0 || c->head_dim <= 0 || c->ffn <= 0 || c->layers <= 0)
     return fail(RLX_ERR_INVALID_ARG, "encoder: hidden, heads, head_dim, ffn and layers must be positive");
@@ -279,137 +332,136 @@ rlx_status check_weights(const rlx_encoder_config* c, const rlx_encoder_weights*
 // Enqueue one forward on `s`.  With `slots` non-null every launch is also
 // recorded (kernel class + a closure holding a copy of its arguments) so that
 // the profiling mode can replay single kernels.
-rlx_status enqueue_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
+rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* mask, int B, int S, void* output,
                            hipStream_t s, std::vector<KernelSlot>* slots) {
-  const rlx_encoder_config& c = e->cfg;
+  // (held by value: a profiled forward's recorded launches copy it and outlive fc)
+  const FwdCtx E = fc;
+  const rlx_encoder_config& c = *E.cfg;
   const int H = c.hidden, F = c.ffn, T = B * S;
-  const int* n_dev = e->cu + B;  // number of real tokens, written by the mask scan
-  auto step = [&](int cls, std::function<hipError_t(hipStream_t)> fn) -> rlx_status {
-    hipError_t err = fn(s);
-    if (err != hipSuccess) return hip_fail(err, kClassNames[cls]);
-    if (slots) slots->push_back({cls, std::move(fn)});
-    return RLX_OK;
-  };
-#define STEP(cls, expr)                                                            \
-  do {                                                                             \
-    rlx_status st_ = step(cls, [=](hipStream_t ss) -> hipError_t { return (expr); }); \
-    if (st_ != RLX_OK) return st_;                                                 \
+  const int* n_dev = E.cu + B;  // number of real tokens, written by the mask scan
+  // Each launch runs at once; only a profiled forward also keeps a replayable
+  // closure of it (so a plain forward builds no std::function).
+#define STEP(cls, expr)                                                                    \
+  do {                                                                                     \
+    const hipError_t err_ = [&](hipStream_t ss) -> hipError_t { return (expr); }(s);     \
+    if (err_ != hipSuccess) return hip_fail(err_, kClassNames[cls]);                       \
+    if (slots) slots->push_back({cls, [=](hipStream_t ss) -> hipError_t { return (expr); }}); \
   } while (0)
 
   if (c.input_kind == RLX_INPUT_IDS && embed_scan_supported(B, S)) {
     // small masks: the scan runs inside the embedding kernel
-    STEP(K_EMBED_LN, launch_embed_scan(mask, static_cast<const int*>(input), B, S, e->w.word_emb, e->w.pos_emb,
-                                       e->w.type_emb, e->w.emb_ln_gamma, e->w.emb_ln_beta, c.ln_eps, c.vocab, H,
-                                       e->cu, e->tok_src, e->tok_dst, e->order, e->X, e->dt, ss));
+    STEP(K_EMBED_LN, launch_embed_scan(mask, static_cast<const int*>(input), B, S, E.w->word_emb, E.w->pos_emb,
+                                       E.w->type_emb, E.w->emb_ln_gamma, E.w->emb_ln_beta, c.ln_eps, c.vocab, H,
+                                       E.cu, E.tok_src, E.tok_dst, E.order, E.X, E.dt, ss));
   } else {
-    STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, e->cu, e->tok_src, e->tok_dst, e->order, ss));
+    STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, E.cu, E.tok_src, E.tok_dst, E.order, ss));
     if (c.input_kind == RLX_INPUT_IDS) {
-      STEP(K_EMBED_LN, launch_embed_ln(static_cast<const int*>(input), e->w.word_emb, e->w.pos_emb, e->w.type_emb,
-                                       e->w.emb_ln_gamma, e->w.emb_ln_beta, c.ln_eps, c.vocab, S, H, e->tok_src,
-                                       n_dev, T, e->X, e->dt, ss));
+      STEP(K_EMBED_LN, launch_embed_ln(static_cast<const int*>(input), E.w->word_emb, E.w->pos_emb, E.w->type_emb,
+                                       E.w->emb_ln_gamma, E.w->emb_ln_beta, c.ln_eps, c.vocab, S, H, E.tok_src,
+                                       n_dev, T, E.X, E.dt, ss));
     } else {
-      STEP(K_GATHER_ROWS, launch_gather_rows(input, H, e->tok_src, n_dev, T, e->X, e->dt, ss));
+      STEP(K_GATHER_ROWS, launch_gather_rows(input, H, E.tok_src, n_dev, T, E.X, E.dt, ss));
     }
   }
   const Quant q = to_quant(c.quant);
   for (int l = 0; l < c.layers; ++l) {
-    const rlx_layer_weights& L = e->layers[l];
+    const rlx_layer_weights& L = E.layers[l];
     // From the second layer on, a deferred-LayerNorm forward's layer input X
     // holds the previous layer's LN2 input, normalised by its readers.
-    const bool x_def = e->deferred && l > 0;
-    const rlx_layer_weights* prev = l > 0 ? &e->layers[l - 1] : nullptr;
-    const void* wqkv = x_def ? e->folded[l].wqkv : L.wqkv;
-    const float* bqkv = x_def ? e->folded[l].vq : L.bqkv;
-    const float* uqkv = x_def ? e->folded[l].uq : nullptr;
+    const bool x_def = E.deferred && l > 0;
+    const rlx_layer_weights* prev = l > 0 ? &E.layers[l - 1] : nullptr;
+    const void* wqkv = x_def ? E.folded[l].wqkv : L.wqkv;
+    const float* bqkv = x_def ? E.folded[l].vq : L.bqkv;
+    const float* uqkv = x_def ? E.folded[l].uq : nullptr;
     GemmParams g{};
     g.m_dev = n_dev;
     g.M = T;
-    g.dtype = e->dt;
+    g.dtype = E.dt;
     g.quant = q;
     g.ln_eps = c.ln_eps;
 
-    const bool fused_attn = e->dt == DType::BF16 && q == Quant::None && S <= 128;
+    const bool fused_attn = E.dt == DType::BF16 && q == Quant::None && S <= 128;
     if (fused_attn) {
       FusedAttnParams fa{};
-      fa.x = e->X; fa.wqkv = wqkv; fa.bqkv = bqkv; fa.cu_seqlens = e->cu; fa.out = e->CTX; fa.out_rows = T;
+      fa.x = E.X; fa.wqkv = wqkv; fa.bqkv = bqkv; fa.cu_seqlens = E.cu; fa.out = E.CTX; fa.out_rows = T;
       fa.B = B; fa.H = H; fa.heads = c.heads; fa.scale = 1.0f / std::sqrt((float)c.head_dim);
-      fa.seq_order = B <= kMaxOrderedBatch ? e->order : nullptr;  // written by the mask scan
-      fa.x_stats = x_def ? e->S2 : nullptr; fa.fold_u = uqkv; fa.ln_eps = c.ln_eps;
+      fa.seq_order = B <= kMaxOrderedBatch ? E.order : nullptr;  // written by the mask scan
+      fa.x_stats = x_def ? E.S2 : nullptr; fa.fold_u = uqkv; fa.ln_eps = c.ln_eps;
       STEP(K_QKV_ATTENTION, launch_qkv_attention(fa, ss));
     } else {
-      g.x = e->X; g.w = wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = bqkv;
-      g.residual = nullptr; g.y = e->QKV; g.N = 3 * H; g.K = H; g.epi = Epi::Bias;
-      g.x_stats = x_def ? e->S2 : nullptr; g.fold_u = uqkv;
+      g.x = E.X; g.w = wqkv; g.scales = L.wqkv_scales; g.zeros = L.wqkv_zeros; g.bias = bqkv;
+      g.residual = nullptr; g.y = E.QKV; g.N = 3 * H; g.K = H; g.epi = Epi::Bias;
+      g.x_stats = x_def ? E.S2 : nullptr; g.fold_u = uqkv;
       STEP(K_GEMM_QKV, launch_gemm(g, ss));
       g.x_stats = nullptr; g.fold_u = nullptr;
 
       AttnParams a{};
-      const size_t es = e->dt == DType::BF16 ? 2 : 4;
-      a.q = e->QKV;
-      a.k = static_cast<const uint8_t*>(e->QKV) + (size_t)H * es;
-      a.v = static_cast<const uint8_t*>(e->QKV) + (size_t)2 * H * es;
+      const size_t es = E.dt == DType::BF16 ? 2 : 4;
+      a.q = E.QKV;
+      a.k = static_cast<const uint8_t*>(E.QKV) + (size_t)H * es;
+      a.v = static_cast<const uint8_t*>(E.QKV) + (size_t)2 * H * es;
       a.ld_qkv = 3 * H;
-      a.out = e->CTX; a.ld_out = H;
+      a.out = E.CTX; a.ld_out = H;
       a.B = B; a.S = S; a.heads = c.heads; a.kind = 0; a.key_mask = nullptr; a.window = 0;
       a.scale = 1.0f / std::sqrt((float)c.head_dim);
-      a.cu_seqlens = e->cu;
-      a.dtype = e->dt;
+      a.cu_seqlens = E.cu;
+      a.dtype = E.dt;
       STEP(K_ATTENTION, launch_attention(a, ss));
     }
 
-    g.x = e->CTX; g.w = L.wo; g.scales = L.wo_scales; g.zeros = L.wo_zeros; g.bias = L.bo;
-    g.residual = e->X; g.y = e->A; g.N = H; g.K = H; g.epi = Epi::BiasResidual;
+    g.x = E.CTX; g.w = L.wo; g.scales = L.wo_scales; g.zeros = L.wo_zeros; g.bias = L.bo;
+    g.residual = E.X; g.y = E.A; g.N = H; g.K = H; g.epi = Epi::BiasResidual;
     g.x_head_rows = fused_attn ? T : 0;  // the fused attention writes the context head-major
     if (x_def) {
-      g.res_stats = e->S2; g.res_gamma = prev->ln2_gamma; g.res_beta = prev->ln2_beta;
+      g.res_stats = E.S2; g.res_gamma = prev->ln2_gamma; g.res_beta = prev->ln2_beta;
     }
-    g.y_stats = e->deferred ? e->S1 : nullptr;
+    g.y_stats = E.deferred ? E.S1 : nullptr;
     STEP(K_GEMM_ATTN_OUT, launch_gemm(g, ss));
     g.x_head_rows = 0;
     g.res_stats = nullptr; g.res_gamma = g.res_beta = nullptr; g.y_stats = nullptr;
 
-    if (e->deferred) {
+    if (E.deferred) {
       // FFN-up on LN1(A) with LN1 folded into W1; FFN-down's residual LN1(A)
       // is normalised in its epilogue, and its output is LN2's input
-      g.x = e->A; g.x_stats = e->S1; g.fold_u = e->folded[l].u1;
-      g.w = e->folded[l].w1; g.scales = nullptr; g.zeros = nullptr; g.bias = e->folded[l].v1;
-      g.residual = nullptr; g.y = e->G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
+      g.x = E.A; g.x_stats = E.S1; g.fold_u = E.folded[l].u1;
+      g.w = E.folded[l].w1; g.scales = nullptr; g.zeros = nullptr; g.bias = E.folded[l].v1;
+      g.residual = nullptr; g.y = E.G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
       STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
       g.x_stats = nullptr; g.fold_u = nullptr;
 
-      g.x = e->G; g.w = L.w2; g.scales = nullptr; g.zeros = nullptr; g.bias = L.b2;
-      g.residual = e->A; g.res_stats = e->S1; g.res_gamma = L.ln1_gamma; g.res_beta = L.ln1_beta;
-      g.y = e->X; g.y_stats = e->S2; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
+      g.x = E.G; g.w = L.w2; g.scales = nullptr; g.zeros = nullptr; g.bias = L.b2;
+      g.residual = E.A; g.res_stats = E.S1; g.res_gamma = L.ln1_gamma; g.res_beta = L.ln1_beta;
+      g.y = E.X; g.y_stats = E.S2; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
       STEP(K_GEMM_FFN_DOWN, launch_gemm(g, ss));
       continue;
     }
 
     // LN1 feeds the FFN-up projection and, as the residual, the FFN-down one.
-    STEP(K_LN1, launch_layer_norm(e->A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, ss));
-    g.x = e->X1; g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;
-    g.residual = nullptr; g.y = e->G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
+    STEP(K_LN1, launch_layer_norm(E.A, L.ln1_gamma, L.ln1_beta, c.ln_eps, H, n_dev, T, E.X1, E.dt, ss));
+    g.x = E.X1; g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros; g.bias = L.b1;
+    g.residual = nullptr; g.y = E.G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
     STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
 
-    g.x = e->G; g.w = L.w2; g.scales = L.w2_scales; g.zeros = L.w2_zeros; g.bias = L.b2;
-    g.residual = e->X1; g.y = e->A; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
+    g.x = E.G; g.w = L.w2; g.scales = L.w2_scales; g.zeros = L.w2_zeros; g.bias = L.b2;
+    g.residual = E.X1; g.y = E.A; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
     STEP(K_GEMM_FFN_DOWN, launch_gemm(g, ss));
-    STEP(K_LN2, launch_layer_norm(e->A, L.ln2_gamma, L.ln2_beta, c.ln_eps, H, n_dev, T, e->X, e->dt, ss));
+    STEP(K_LN2, launch_layer_norm(E.A, L.ln2_gamma, L.ln2_beta, c.ln_eps, H, n_dev, T, E.X, E.dt, ss));
   }
-  const rlx_layer_weights& last = e->layers[c.layers - 1];
+  const rlx_layer_weights& last = E.layers[c.layers - 1];
   if (c.output_kind == RLX_OUTPUT_POOLED) {
-    if (e->deferred) {
-      STEP(K_POOL, launch_pool_l2(e->X, H, e->cu, B, static_cast<float*>(output), e->dt, ss, e->S2,
+    if (E.deferred) {
+      STEP(K_POOL, launch_pool_l2(E.X, H, E.cu, B, static_cast<float*>(output), E.dt, ss, E.S2,
                                   last.ln2_gamma, last.ln2_beta, c.ln_eps));
     } else {
-      STEP(K_POOL, launch_pool_l2(e->X, H, e->cu, B, static_cast<float*>(output), e->dt, ss));
+      STEP(K_POOL, launch_pool_l2(E.X, H, E.cu, B, static_cast<float*>(output), E.dt, ss));
     }
   } else {
-    const void* hid = e->X;
-    if (e->deferred) {  // the hidden states are LN2's output: materialise it once
-      STEP(K_LN2, launch_layer_norm(e->X, last.ln2_gamma, last.ln2_beta, c.ln_eps, H, n_dev, T, e->X1, e->dt, ss));
-      hid = e->X1;
+    const void* hid = E.X;
+    if (E.deferred) {  // the hidden states are LN2's output: materialise it once
+      STEP(K_LN2, launch_layer_norm(E.X, last.ln2_gamma, last.ln2_beta, c.ln_eps, H, n_dev, T, E.X1, E.dt, ss));
+      hid = E.X1;
     }
-    STEP(K_SCATTER, launch_scatter_hidden(hid, H, e->tok_dst, T, static_cast<float*>(output), e->dt, ss));
+    STEP(K_SCATTER, launch_scatter_hidden(hid, H, E.tok_dst, T, static_cast<float*>(output), E.dt, ss));
   }
 #undef STEP
   return RLX_OK;
@@ -434,7 +486,7 @@ void clear_profile(rlx_encoder* e) {
 rlx_status capture_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
                            std::vector<KernelSlot>* slots, hipGraphExec_t* exec) {
   RLX_HIP(hipStreamBeginCapture(e->cap_stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
-  rlx_status st = enqueue_forward(e, input, mask, B, S, output, e->cap_stream, slots);
+  rlx_status st = enqueue_forward(ctx_of(e), input, mask, B, S, output, e->cap_stream, slots);
   hipGraph_t graph = nullptr;
   hipError_t he = hipStreamEndCapture(e->cap_stream, &graph);
   if (st != RLX_OK) {
@@ -478,7 +530,7 @@ rlx_status profiled_forward(rlx_encoder* e, const void* input, const uint8_t* ma
     // record the launches of one forward (also a real forward on the capture stream)
     std::vector<KernelSlot> slots;
     RLX_HIP(hipStreamSynchronize(s), "hipStreamSynchronize");
-    st = enqueue_forward(e, input, mask, B, S, output, e->cap_stream, &slots);
+    st = enqueue_forward(ctx_of(e), input, mask, B, S, output, e->cap_stream, &slots);
     if (st != RLX_OK) return st;
     RLX_HIP(hipStreamSynchronize(e->cap_stream), "hipStreamSynchronize");
     ProfGraph pg;
@@ -588,6 +640,37 @@ rlx_status fold_layer_norms(rlx_encoder* e) {
             "encoder_create: fold LN1 into W1");
   }
   RLX_HIP(hipStreamSynchronize(e->cap_stream), "encoder_create: fold LayerNorms");
+  return RLX_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch of the allocation-free forward
+// ---------------------------------------------------------------------------
+// One array per GPU, part of the library's code object: it exists from the
+// first use of the library on that GPU until the process ends.  In host code
+// `scratch` is only a host-side stand-in for the symbol; its device address is
+// looked up once per device with hipGetSymbolAddress and used everywhere.
+constexpr size_t kScratchBytes = (size_t)16 << 20;  // 16 MiB
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch_ptr[kMaxScratchDevices] = {nullptr};
+
+// Device address of this device's scratch (looked up on the first call with
+// the device current).
+rlx_status scratch_on_device(int dev, uint8_t** out) {
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder_forward_noalloc: device %d beyond the %d supported", dev,
+                kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t he = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (he != hipSuccess || !ptr) return hip_fail(he, "encoder_forward_noalloc: hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[dev] = static_cast<uint8_t*>(ptr);
+  }
+  *out = g_scratch_ptr[dev];
   return RLX_OK;
 }
 
@@ -728,35 +811,21 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
   }
 
   // Workspace plan: token maps, then six activation buffers for T_max tokens.
-  const size_t T = (size_t)cfg->max_batch * cfg->max_seq;
   const size_t es = e->dt == DType::BF16 ? 2 : 4;
-  const size_t H = cfg->hidden, F = cfg->ffn;
-  size_t off = 0;
-  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
-  const size_t o_cu = take((cfg->max_batch + 1) * sizeof(int));
-  const size_t o_src = take(T * sizeof(int));
-  const size_t o_dst = take(T * sizeof(int));
-  const size_t o_ord = take((size_t)cfg->max_batch * sizeof(int));
-  const size_t o_X = take(T * H * es), o_X1 = take(T * H * es), o_A = take(T * H * es), o_C = take(T * H * es);
-  const size_t o_Q = take(T * 3 * H * es), o_G = take(T * F * es);
   e->deferred = gemm_deferred_ln_supported(e->dt, to_quant(cfg->quant), cfg->hidden);
-  const size_t stats_bytes = e->deferred ? T * (H / 64) * sizeof(float2) : 0;
-  const size_t o_S1 = take(stats_bytes), o_S2 = take(stats_bytes);
-  he = hipMalloc(&e->ws, off);
+  const WsPlan plan = plan_workspace(cfg->max_batch, cfg->max_seq, cfg->hidden, cfg->ffn, es, e->deferred);
+  he = hipMalloc(&e->ws, plan.bytes);
   if (he != hipSuccess) {
     delete e;
-    return fail(RLX_ERR_OOM, "encoder_create: workspace of %zu bytes: %s", off, hipGetErrorString(he));
+    return fail(RLX_ERR_OOM, "encoder_create: workspace of %zu bytes: %s", plan.bytes, hipGetErrorString(he));
   }
-  uint8_t* base = static_cast<uint8_t*>(e->ws);
-  e->cu = reinterpret_cast<int*>(base + o_cu);
-  e->tok_src = reinterpret_cast<int*>(base + o_src);
-  e->tok_dst = reinterpret_cast<int*>(base + o_dst);
-  e->order = reinterpret_cast<int*>(base + o_ord);
-  e->X = base + o_X; e->X1 = base + o_X1; e->A = base + o_A; e->CTX = base + o_C; e->QKV = base + o_Q;
-  e->G = base + o_G;
-  if (e->deferred) {
-    e->S1 = reinterpret_cast<float2*>(base + o_S1);
-    e->S2 = reinterpret_cast<float2*>(base + o_S2);
+  {
+    FwdCtx view{};
+    view.deferred = e->deferred;
+    bind_workspace(view, static_cast<uint8_t*>(e->ws), plan);
+    e->cu = view.cu; e->tok_src = view.tok_src; e->tok_dst = view.tok_dst; e->order = view.order;
+    e->X = view.X; e->X1 = view.X1; e->A = view.A; e->CTX = view.CTX; e->QKV = view.QKV; e->G = view.G;
+    e->S1 = view.S1; e->S2 = view.S2;
   }
   he = hipStreamCreateWithFlags(&e->cap_stream, hipStreamNonBlocking);
   if (he == hipSuccess) he = hipEventCreateWithFlags(&e->done_ev, hipEventDisableTiming);
@@ -794,12 +863,52 @@ rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t*
   if (e->profiling)
     st = profiled_forward(e, input, attention_mask, B, S, output, s);
   else if (!e->cfg.use_graph)
-    st = enqueue_forward(e, input, attention_mask, B, S, output, s, nullptr);
+    st = enqueue_forward(ctx_of(e), input, attention_mask, B, S, output, s, nullptr);
   else
     st = run_graph_forward(e, input, attention_mask, B, S, output, s);
   if (st != RLX_OK) return st;
   RLX_HIP(hipEventRecord(e->done_ev, s), "hipEventRecord");
   return ok();
+}
+
+rlx_status rlx_encoder_forward_noalloc(const rlx_encoder_config* cfg, const rlx_encoder_weights* w,
+                                       const void* input, const uint8_t* attention_mask, int B, int S, void* output,
+                                       void* stream) {
+  if (!cfg || !w) return fail(RLX_ERR_INVALID_ARG, "encoder_forward_noalloc: cfg and weights must be non-null");
+  rlx_status st = check_config(cfg);
+  if (st != RLX_OK) return st;
+  st = check_weights(cfg, w);
+  if (st != RLX_OK) return st;
+  if (!input || !attention_mask || !output)
+    return fail(RLX_ERR_INVALID_ARG, "encoder_forward_noalloc: input, attention_mask and output must be non-null");
+  if (B < 1 || S < 1) return fail(RLX_ERR_INVALID_ARG, "encoder_forward_noalloc: B=%d and S=%d must be >= 1", B, S);
+  if (S > 512) return fail(RLX_ERR_UNSUPPORTED, "encoder_forward_noalloc: S=%d exceeds 512", S);
+  if (cfg->input_kind == RLX_INPUT_IDS && S > cfg->max_pos)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder_forward_noalloc: S=%d exceeds max_pos=%d", S, cfg->max_pos);
+  const DType dt = cfg->dtype == RLX_BF16 ? DType::BF16 : DType::F32;
+  const size_t es = dt == DType::BF16 ? 2 : 4;
+  // the plain-LayerNorm kernel sequence: no LayerNorm-folded weights to allocate
+  const WsPlan plan = plan_workspace((size_t)B, (size_t)S, cfg->hidden, cfg->ffn, es, false);
+  if (plan.bytes > kScratchBytes)
+    return fail(RLX_ERR_UNSUPPORTED,
+                "encoder_forward_noalloc: B=%d x S=%d needs %zu bytes of workspace, the static scratch holds %zu",
+                B, S, plan.bytes, kScratchBytes);
+  int dev = -1;
+  RLX_HIP(hipGetDevice(&dev), "hipGetDevice");
+  uint8_t* base = nullptr;
+  st = scratch_on_device(dev, &base);
+  if (st != RLX_OK) return st;
+  RLX_HIP(init_kernel_attributes(), "encoder_forward_noalloc: kernel attributes");
+  FwdCtx c{};
+  c.cfg = cfg;
+  c.w = w;
+  c.layers = w->layers;
+  c.dt = dt;
+  c.deferred = false;
+  c.folded = nullptr;
+  bind_workspace(c, base, plan);
+  st = enqueue_forward(c, input, attention_mask, B, S, output, static_cast<hipStream_t>(stream), nullptr);
+  return st == RLX_OK ? ok() : st;
 }
 
 void rlx_encoder_destroy(rlx_encoder* e) {

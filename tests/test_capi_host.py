@@ -206,3 +206,26 @@ def test_new_schemes_argument_errors(L):
     st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, 5, p16, p16, 32, 64, None, None, rlx.EPI_NONE, p16, rlx.BF16,
                               None)
     assert st == rlx.ERR_INVALID_ARG  # unknown scheme
+
+
+def test_encoder_forward_noalloc_argument_errors(L):
+    """The allocation-free forward validates like create and forward, and
+    rejects a batch whose workspace does not fit its static scratch, all
+    before any HIP call."""
+    f = L.rlx_encoder_forward_noalloc
+    P = 4096
+    w, _arr = _weights()
+    cfg = _cfg()
+    assert f(None, ctypes.byref(w), P, P, 4, 128, P, None) == rlx.ERR_INVALID_ARG
+    assert f(ctypes.byref(_cfg(head_dim=64, heads=6)), ctypes.byref(w), P, P, 4, 128, P, None) == \
+        rlx.ERR_UNSUPPORTED
+    assert f(ctypes.byref(cfg), ctypes.byref(w), None, P, 4, 128, P, None) == rlx.ERR_INVALID_ARG
+    assert f(ctypes.byref(cfg), ctypes.byref(w), P, P, 0, 128, P, None) == rlx.ERR_INVALID_ARG
+    assert f(ctypes.byref(cfg), ctypes.byref(w), P, P, 1, 1024, P, None) == rlx.ERR_UNSUPPORTED
+    # 64 x 512 bf16 tokens need far more than the 16 MiB scratch
+    assert f(ctypes.byref(cfg), ctypes.byref(w), P, P, 64, 512, P, None) == rlx.ERR_UNSUPPORTED
+    assert b"static scratch" in L.rlx_last_error()
+    # max_batch / max_seq of the config do not limit it (only the scratch does)
+    assert f(ctypes.byref(_cfg(max_batch=1, max_seq=8)), ctypes.byref(w), P, P, 64, 512, P, None) == \
+        rlx.ERR_UNSUPPORTED
+    assert b"static scratch" in L.rlx_last_error()
