@@ -327,6 +327,24 @@ rlx_status rlx_encoder_forward_noalloc(const rlx_encoder_config* cfg, const rlx_
  * the rest of the device.  NULL is ignored. */
 void rlx_encoder_destroy(rlx_encoder* enc);
 
+/* Forward passes with dense bf16 weights, id input, pooled output, hidden
+ * 384 (heads of 32), FFN a multiple of 128, at most 12 layers, and per call
+ * B <= 256, S <= 128, B * S <= 32768, run as one persistent launch: resident
+ * blocks, each XCD working on its own run of sequences, every tile starting
+ * when the tiles it reads are done.  rlx_encoder_create selects it when
+ * RLX_PIPELINE=1 is set in the environment (otherwise forwards launch one
+ * kernel per step).  Same results up to rounding.
+ * Returns 1 when the handle's supported forwards take the persistent launch. */
+int rlx_encoder_uses_persistent_forward(const rlx_encoder* enc);
+
+/* Waits for the last forward enqueued through the handle, then reports
+ * whether a wait inside the persistent launch of it or of an earlier forward
+ * gave up (bounded waits: after ~0.5 s without progress the launch finishes
+ * with invalid outputs instead of hanging): RLX_ERR_HIP with a message, after
+ * which the report is cleared.  RLX_OK otherwise (always for handles without
+ * the persistent launch). */
+rlx_status rlx_encoder_check(rlx_encoder* enc);
+
 /* Per-kernel timing of forward passes (a native counterpart of a per-operator
  * dispatch report).  While enabled, each forward runs normally, then replays,
  * kernel by kernel in forward order, a HIP graph holding 8 back-to-back

@@ -36,7 +36,8 @@ STATUS_NAMES = {0: "RLX_OK", 1: "RLX_ERR_INVALID_ARG", 2: "RLX_ERR_UNSUPPORTED",
 EXPORTS = ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_gguf_repack", "rlx_scaled_matmul",
            "rlx_encoder_create",
            "rlx_encoder_forward", "rlx_encoder_forward_noalloc", "rlx_encoder_destroy", "rlx_encoder_set_profiling",
-           "rlx_encoder_profile_read", "rlx_last_error", "rlx_version")
+           "rlx_encoder_profile_read", "rlx_encoder_check", "rlx_encoder_uses_persistent_forward", "rlx_last_error",
+           "rlx_version")
 
 
 class RlxError(RuntimeError):
@@ -97,6 +98,9 @@ def lib() -> ctypes.CDLL:
     L.rlx_encoder_forward.argtypes = [_vp, _vp, _vp, i32, i32, _vp, _vp]
     L.rlx_encoder_forward_noalloc.argtypes = [ctypes.POINTER(EncoderConfig), ctypes.POINTER(EncoderWeights), _vp, _vp,
                                               i32, i32, _vp, _vp]
+    L.rlx_encoder_check.argtypes = [_vp]
+    L.rlx_encoder_uses_persistent_forward.argtypes = [_vp]
+    L.rlx_encoder_uses_persistent_forward.restype = ctypes.c_int
     L.rlx_encoder_destroy.argtypes = [_vp]
     L.rlx_encoder_destroy.restype = None
     L.rlx_encoder_set_profiling.argtypes = [_vp, i32]
@@ -104,7 +108,7 @@ def lib() -> ctypes.CDLL:
                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
     for nm in ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_gguf_repack", "rlx_scaled_matmul",
                "rlx_encoder_create", "rlx_encoder_forward", "rlx_encoder_forward_noalloc", "rlx_encoder_set_profiling",
-               "rlx_encoder_profile_read"):
+               "rlx_encoder_profile_read", "rlx_encoder_check"):
         getattr(L, nm).restype = ctypes.c_int
     L.rlx_last_error.restype = ctypes.c_char_p
     L.rlx_last_error.argtypes = []
@@ -338,6 +342,15 @@ class Encoder:
         return out
 
     __call__ = forward
+
+    @property
+    def persistent(self) -> bool:
+        """True when supported forwards run as one persistent launch."""
+        return bool(lib().rlx_encoder_uses_persistent_forward(self._h))
+
+    def check(self) -> None:
+        """Waits for the last forward; raises if a wait of the persistent launch gave up."""
+        check(lib().rlx_encoder_check(self._h))
 
     def set_profiling(self, enable: bool) -> None:
         check(lib().rlx_encoder_set_profiling(self._h, 1 if enable else 0))

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG_DIR)
 CSRC = os.path.join(PKG_DIR, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "librlx.so")
-SOURCES = ("gemm.hip", "gemv.hip", "gguf.hip", "attention.hip", "rowops.hip", "mx_gemm.hip", "capi.hip")
+SOURCES = ("gemm.hip", "gemv.hip", "gguf.hip", "attention.hip", "rowops.hip", "mx_gemm.hip", "pipe.hip", "capi.hip")
 ARCH = "gfx950"
 
 

@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <functional>
 #include <mutex>
@@ -135,12 +136,12 @@ namespace {
 
 enum KernelClass {
   K_MASK_SCAN = 0, K_EMBED_LN, K_GATHER_ROWS, K_GEMM_QKV, K_ATTENTION, K_GEMM_ATTN_OUT, K_LN1, K_GEMM_FFN_UP,
-  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_NUM_CLASSES
+  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_PIPE, K_NUM_CLASSES
 };
 const char* kClassNames[K_NUM_CLASSES] = {"mask_scan",     "embed_ln",    "gather_rows", "gemm_qkv",
                                           "attention",     "gemm_attn_out", "layer_norm_1", "gemm_ffn_up",
                                           "gemm_ffn_down", "layer_norm_2", "pool_l2",     "scatter_hidden",
-                                          "qkv_attention"};
+                                          "qkv_attention", "encoder_pipe"};
 
 struct GraphEntry {
   int B, S;
@@ -192,6 +193,14 @@ struct rlx_encoder {
   };
   std::vector<Folded> folded;
   void* fold_mem = nullptr;
+  // Persistent forward (pipe.hip): chosen at create for the shapes it
+  // supports; its per-layer pointer table and per-XCD sync words live in
+  // pipe_mem.
+  bool pipe = false;
+  int pipe_grid = 0;
+  void* pipe_mem = nullptr;
+  PipeLayer* pipe_layers = nullptr;
+  int* pipe_sync = nullptr;
   hipStream_t cap_stream = nullptr;
   // recorded after every forward on the caller's stream: destroy and the graph
   // cache wait for it (the handle's own work) instead of the whole device
@@ -225,11 +234,16 @@ struct FwdCtx {
   bool deferred;  // dense bf16: LayerNorms applied by the kernels that read their outputs
   float2 *S1, *S2;
   const rlx_encoder::Folded* folded;
+  // the persistent forward, when the handle has it (else pipe_grid == 0)
+  int pipe_grid;
+  const PipeLayer* pipe_layers;
+  int* pipe_sync;
 };
 
 FwdCtx ctx_of(const rlx_encoder* e) {
   return FwdCtx{&e->cfg, &e->w, e->layers.data(), e->dt, e->cu, e->tok_src, e->tok_dst, e->order,
-                e->X, e->X1, e->A, e->CTX, e->QKV, e->G, e->deferred, e->S1, e->S2, e->folded.data()};
+                e->X, e->X1, e->A, e->CTX, e->QKV, e->G, e->deferred, e->S1, e->S2, e->folded.data(),
+                e->pipe ? e->pipe_grid : 0, e->pipe_layers, e->pipe_sync};
 }
 
 // Workspace layout for max_batch sequences of max_seq tokens (256-byte aligned regions).
@@ -348,6 +362,22 @@ rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* m
     if (slots) slots->push_back({cls, [=](hipStream_t ss) -> hipError_t { return (expr); }}); \
   } while (0)
 
+  if (E.pipe_grid > 0 && pipe_supported(PipeShape{B, S, H, F, c.heads, c.layers})) {
+    // the whole forward in one persistent launch (pipe.hip)
+    PipeParams pp{};
+    pp.mask = mask; pp.ids = static_cast<const int*>(input); pp.B = B; pp.S = S;
+    pp.word = static_cast<const bf16_t*>(E.w->word_emb); pp.pos = static_cast<const bf16_t*>(E.w->pos_emb);
+    pp.type = static_cast<const bf16_t*>(E.w->type_emb); pp.emb_g = E.w->emb_ln_gamma; pp.emb_b = E.w->emb_ln_beta;
+    pp.vocab = c.vocab; pp.eps = c.ln_eps; pp.scale = 1.0f / std::sqrt((float)c.head_dim);
+    pp.layers = E.pipe_layers; pp.L = c.layers; pp.H = H; pp.F = F; pp.heads = c.heads;
+    pp.X = static_cast<bf16_t*>(E.X); pp.A = static_cast<bf16_t*>(E.A); pp.CTX = static_cast<bf16_t*>(E.CTX);
+    pp.G = static_cast<bf16_t*>(E.G); pp.S1 = E.S1; pp.S2 = E.S2; pp.ctx_rows = T;
+    pp.last_g = E.layers[c.layers - 1].ln2_gamma; pp.last_b = E.layers[c.layers - 1].ln2_beta;
+    pp.out = static_cast<float*>(output); pp.sync = E.pipe_sync;
+    const int grid = E.pipe_grid;
+    STEP(K_PIPE, launch_encoder_pipe(pp, grid, ss));
+    return RLX_OK;
+  }
   if (c.input_kind == RLX_INPUT_IDS && embed_scan_supported(B, S)) {
     // small masks: the scan runs inside the embedding kernel
     STEP(K_EMBED_LN, launch_embed_scan(mask, static_cast<const int*>(input), B, S, E.w->word_emb, E.w->pos_emb,
@@ -643,6 +673,55 @@ rlx_status fold_layer_norms(rlx_encoder* e) {
   return RLX_OK;
 }
 
+// Persistent forward: usable for a handle with dense bf16 weights, id input,
+// pooled output and the hidden size its LDS plan is made for (the batch and
+// sequence limits are checked per forward); selected when RLX_PIPELINE=1 is
+// set in the environment.  Two blocks per CU.
+rlx_status setup_pipeline(rlx_encoder* e) {
+  const rlx_encoder_config& c = e->cfg;
+  const char* env = std::getenv("RLX_PIPELINE");
+  if (!env || env[0] != '1' || !e->deferred || c.input_kind != RLX_INPUT_IDS || c.output_kind != RLX_OUTPUT_POOLED ||
+      !pipe_supported(PipeShape{1, 16, c.hidden, c.ffn, c.heads, c.layers}) || c.layers > kPipeMaxLayers)
+    return RLX_OK;
+  int cus = 0;
+  RLX_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, e->device), "hipDeviceGetAttribute");
+  const int grid = 2 * cus;  // two blocks per CU
+  if (grid <= 0) return RLX_OK;
+  RLX_HIP(init_pipe_attributes(), "encoder_create: persistent-forward attributes");
+  const size_t layer_bytes = align_up((size_t)c.layers * sizeof(PipeLayer), 256);
+  const size_t bytes = layer_bytes + pipe_sync_bytes();
+  hipError_t he = hipMalloc(&e->pipe_mem, bytes);
+  if (he != hipSuccess) {
+    e->pipe_mem = nullptr;
+    return fail(RLX_ERR_OOM, "encoder_create: persistent-forward tables of %zu bytes: %s", bytes, hipGetErrorString(he));
+  }
+  uint8_t* base = static_cast<uint8_t*>(e->pipe_mem);
+  e->pipe_layers = reinterpret_cast<PipeLayer*>(base);
+  e->pipe_sync = reinterpret_cast<int*>(base + layer_bytes);
+  std::vector<PipeLayer> host(c.layers);
+  for (int l = 0; l < c.layers; ++l) {
+    const rlx_layer_weights& L = e->layers[l];
+    const rlx_encoder::Folded& f = e->folded[l];
+    PipeLayer& P = host[l];
+    P.wqkv = static_cast<const bf16_t*>(l > 0 ? f.wqkv : L.wqkv);
+    P.bqkv = l > 0 ? f.vq : L.bqkv;
+    P.uq = l > 0 ? f.uq : nullptr;
+    P.wo = static_cast<const bf16_t*>(L.wo); P.bo = L.bo;
+    P.res_g = l > 0 ? e->layers[l - 1].ln2_gamma : nullptr;
+    P.res_b = l > 0 ? e->layers[l - 1].ln2_beta : nullptr;
+    P.w1 = static_cast<const bf16_t*>(f.w1); P.v1 = f.v1; P.u1 = f.u1;
+    P.w2 = static_cast<const bf16_t*>(L.w2); P.b2 = L.b2;
+    P.ln1_g = L.ln1_gamma; P.ln1_b = L.ln1_beta;
+  }
+  RLX_HIP(hipMemcpyAsync(e->pipe_layers, host.data(), c.layers * sizeof(PipeLayer), hipMemcpyHostToDevice,
+                         e->cap_stream), "encoder_create: persistent-forward layer table");
+  RLX_HIP(hipMemsetAsync(e->pipe_sync, 0, pipe_sync_bytes(), e->cap_stream), "encoder_create: sync words");
+  RLX_HIP(hipStreamSynchronize(e->cap_stream), "encoder_create: persistent-forward tables");
+  e->pipe = true;
+  e->pipe_grid = grid;
+  return RLX_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Static scratch of the allocation-free forward
 // ---------------------------------------------------------------------------
@@ -835,6 +914,7 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
   }
   if (e->deferred) {
     st = fold_layer_norms(e);
+    if (st == RLX_OK) st = setup_pipeline(e);
     if (st != RLX_OK) {
       rlx_encoder_destroy(e);
       return st;
@@ -923,8 +1003,34 @@ void rlx_encoder_destroy(rlx_encoder* e) {
   if (e->cap_stream) (void)hipStreamDestroy(e->cap_stream);
   if (e->ws) (void)hipFree(e->ws);
   if (e->fold_mem) (void)hipFree(e->fold_mem);
+  if (e->pipe_mem) (void)hipFree(e->pipe_mem);
   delete e;
 }
+
+rlx_status rlx_encoder_check(rlx_encoder* e) {
+  if (!e) return fail(RLX_ERR_INVALID_ARG, "encoder_check: null handle");
+  RLX_HIP(hipEventSynchronize(e->done_ev), "hipEventSynchronize");
+  if (!e->pipe) return ok();
+  // the sticky error word of each XCD (word 3 of its sync block)
+  int err[8] = {0};
+  for (int x = 0; x < 8; ++x)
+    RLX_HIP(hipMemcpyAsync(&err[x], e->pipe_sync + (size_t)x * kPipeSyncStride + 3, sizeof(int),
+                           hipMemcpyDeviceToHost, e->cap_stream), "encoder_check: read");
+  RLX_HIP(hipStreamSynchronize(e->cap_stream), "encoder_check: read");
+  int all = 0;
+  for (int x = 0; x < 8; ++x) {
+    if (err[x])
+      RLX_HIP(hipMemsetAsync(e->pipe_sync + (size_t)x * kPipeSyncStride + 3, 0, sizeof(int), e->cap_stream),
+              "encoder_check: clear");
+    all |= err[x];
+  }
+  RLX_HIP(hipStreamSynchronize(e->cap_stream), "encoder_check: clear");
+  if (all)
+    return fail(RLX_ERR_HIP, "encoder_check: a wait of the persistent forward gave up; its outputs are not valid");
+  return ok();
+}
+
+int rlx_encoder_uses_persistent_forward(const rlx_encoder* e) { return e && e->pipe ? 1 : 0; }
 
 rlx_status rlx_encoder_set_profiling(rlx_encoder* e, int enable) {
   if (!e) return fail(RLX_ERR_INVALID_ARG, "encoder_set_profiling: null handle");

@@ -154,17 +154,20 @@ __device__ __forceinline__ float dpp_sum8(float v) {
 // inserting a full vmcnt wait before every later LDS read (it cannot tell
 // which LDS bytes the load writes); the kernels place their own waits.  M0 is
 // used by nothing else in these kernels.
+__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds_addr) {
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void lds_dma16(const void* g, uint32_t lds_addr) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
                : "memory", "m0");
+#pragma clang diagnostic pop
 }
 __device__ __forceinline__ void lds_dma4(const void* g, uint32_t lds_addr) {
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(lds_addr)
                : "memory", "m0");
-}
 #pragma clang diagnostic pop
+}
 
 // Wait until at most N vector-memory operations of this wave are outstanding.
 template <int N>

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "common.hpp"
+
 namespace rlx {
 
 enum class DType : int { F32 = 0, BF16 = 1 };
@@ -124,6 +126,47 @@ hipError_t launch_mx_gemm(const MxGemmParams& p, hipStream_t s);
 // (sums in fp64).  w: bf16 [N,K].
 hipError_t launch_fold_ln_weights(const void* w, int N, int K, const float* gamma, const float* beta,
                                   const float* bias, void* w_out, float* u_out, float* v_out, hipStream_t s);
+
+// Persistent encoder forward (pipe.hip): the whole bf16 forward (embedding,
+// `L` post-LN layers with the LayerNorms deferred as in the GEMM kernels,
+// pooling) in one launch of resident blocks, each XCD working on its own run
+// of sequences.  Shapes it supports: pipe_supported.
+constexpr int kPipeHidden = 384;         // hidden size the LDS plan is made for
+constexpr int kPipeMaxBatch = 256;
+constexpr int kPipeMaxTokens = 32768;    // B * S
+constexpr int kPipeMaxRowTiles = kPipeMaxTokens / 64;
+constexpr int kPipeMaxLayers = 12;
+constexpr int kPipeLdsBytes = 80 * 1024;  // two blocks per CU
+// ints of sync words per XCD (a whole number of 4 KB pages)
+constexpr int kPipeSyncStride =
+    ((64 + kPipeMaxLayers * (kPipeMaxBatch + 3 * kPipeMaxRowTiles)) + 1023) / 1024 * 1024;
+struct PipeLayer {
+  const bf16_t* wqkv; const float* bqkv; const float* uq;  // layer 0: as given, uq null; later: LN2 folded in
+  const bf16_t* wo; const float* bo;
+  const float* res_g; const float* res_b;                  // LN2 of the previous layer (the residual); layer 0 null
+  const bf16_t* w1; const float* v1; const float* u1;      // LN1 folded in
+  const bf16_t* w2; const float* b2;
+  const float* ln1_g; const float* ln1_b;
+};
+struct PipeParams {
+  const uint8_t* mask; const int* ids; int B, S;           // mask rows 16-byte aligned, S % 16 == 0
+  const bf16_t* word; const bf16_t* pos; const bf16_t* type; const float* emb_g; const float* emb_b; int vocab;
+  float eps, scale;
+  const PipeLayer* layers; int L;                          // device array
+  int H, F, heads;
+  bf16_t* X; bf16_t* A; bf16_t* CTX; bf16_t* G; float2* S1; float2* S2; int ctx_rows;
+  const float* last_g; const float* last_b;                // LN2 of the last layer
+  float* out;                                              // f32 [B, H] pooled
+  int* sync;                                               // pipe_sync_bytes(), zero before the first launch
+};
+struct PipeShape {
+  int B, S, H, F, heads, L;
+};
+bool pipe_supported(const PipeShape& s);
+size_t pipe_sync_bytes();
+// Clears the sync words, then launches the forward on `grid` blocks.
+hipError_t launch_encoder_pipe(const PipeParams& p, int grid, hipStream_t s);
+hipError_t init_pipe_attributes();  // raises the kernel's LDS limit (idempotent)
 
 // Raises per-kernel dynamic-LDS limits once per process (idempotent).
 hipError_t init_kernel_attributes();
