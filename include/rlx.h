@@ -33,11 +33,21 @@
 #include <stddef.h>
 #include <stdint.h>
 
+/* The enumerations are int-sized in C and C++ alike.  In C++ they carry the
+ * fixed underlying type int32_t, so any int a C caller passes is a value of
+ * the enumeration type (an unknown one is rejected by the callee's checks,
+ * never undefined behaviour). */
+#ifdef __cplusplus
+#define RLX_ENUM enum : int32_t
+#else
+#define RLX_ENUM enum
+#endif
+
 #ifdef __cplusplus
 extern "C" {
 #endif
 
-typedef enum {
+typedef RLX_ENUM {
   RLX_OK = 0,
   RLX_ERR_INVALID_ARG = 1,  /* null pointer, negative size, inconsistent shapes     */
   RLX_ERR_UNSUPPORTED = 2,  /* well-formed request outside what the kernels implement */
@@ -45,13 +55,13 @@ typedef enum {
   RLX_ERR_OOM = 4           /* device allocation failed (encoder workspace)        */
 } rlx_status;
 
-typedef enum {
+typedef RLX_ENUM {
   RLX_F32 = 0, RLX_BF16 = 1, RLX_F16 = 2, RLX_I8 = 3, RLX_U4X2 = 4, RLX_I32 = 5, RLX_U8 = 6
 } rlx_dtype;
 
 /* The masked-attention primitive's MaskKind (Section III-A): None, Causal,
  * SlidingWindow(w), Custom (an explicit mask). */
-typedef enum {
+typedef RLX_ENUM {
   RLX_MASK_NONE = 0,
   RLX_MASK_CAUSAL = 1,          /* key j visible to query i iff j <= i                */
   RLX_MASK_SLIDING_WINDOW = 2,  /* iff i - window < j <= i                            */
@@ -59,7 +69,7 @@ typedef enum {
 } rlx_mask_kind;
 
 /* Weight-only quantisation schemes of Op::DequantMatMul (Sections III-A, VI). */
-typedef enum {
+typedef RLX_ENUM {
   RLX_Q_NONE = 0,              /* w has the activation dtype (f32 or bf16), [N,K]      */
   RLX_Q_INT8_PER_CHANNEL = 1,  /* w int8 [N,K]; scales f16 [N]; W = q * s[n]          */
   RLX_Q_INT4_GROUP_ZP = 2,     /* w u8 [N,K/2], two codes per byte (k = 2j in the low
@@ -73,7 +83,7 @@ typedef enum {
                                   (GGUF Q4_1 after rlx_gguf_repack)                  */
 } rlx_quant;
 
-typedef enum {
+typedef RLX_ENUM {
   RLX_EPI_NONE = 0,           /* y = acc                                   */
   RLX_EPI_BIAS = 1,           /* y = acc + bias[n]                         */
   RLX_EPI_BIAS_GELU = 2,      /* y = GELU(acc + bias[n]), erf form         */
@@ -175,7 +185,7 @@ rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scale
  * K a positive multiple of 64, N >= 0 (N == 0 is a no-op).  Otherwise
  * RLX_ERR_UNSUPPORTED (type, alignment, K) or RLX_ERR_INVALID_ARG.
  */
-typedef enum { RLX_GGUF_Q4_0 = 2, RLX_GGUF_Q4_1 = 3, RLX_GGUF_Q8_0 = 8 } rlx_gguf_type;
+typedef RLX_ENUM { RLX_GGUF_Q4_0 = 2, RLX_GGUF_Q4_1 = 3, RLX_GGUF_Q8_0 = 8 } rlx_gguf_type;
 
 rlx_status rlx_gguf_repack(const void* blocks, rlx_gguf_type type, int N, int K, void* codes, void* scales,
                            void* zeros, rlx_quant* scheme, void* stream);
@@ -207,7 +217,7 @@ rlx_status rlx_gguf_repack(const void* blocks, rlx_gguf_type type, int N, int K,
  * Otherwise RLX_ERR_UNSUPPORTED (alignment, sizes) or RLX_ERR_INVALID_ARG.
  * All pointers are device pointers owned by the caller.
  */
-typedef enum { RLX_MX_E4M3 = 0, RLX_MX_E5M2 = 1, RLX_MX_E2M3 = 2, RLX_MX_E3M2 = 3, RLX_MX_E2M1 = 4 } rlx_mx_format;
+typedef RLX_ENUM { RLX_MX_E4M3 = 0, RLX_MX_E5M2 = 1, RLX_MX_E2M3 = 2, RLX_MX_E3M2 = 3, RLX_MX_E2M1 = 4 } rlx_mx_format;
 
 rlx_status rlx_scaled_matmul(const void* x, const uint8_t* x_scales, rlx_mx_format fx, const void* w,
                              const uint8_t* w_scales, rlx_mx_format fw, int M, int N, int K, float* y,
@@ -218,8 +228,8 @@ rlx_status rlx_scaled_matmul(const void* x, const uint8_t* x_scales, rlx_mx_form
  * (the paper's Session::compile -> CompiledGraph executed with bound inputs,
  * Section III-C).
  */
-typedef enum { RLX_INPUT_IDS = 0, RLX_INPUT_HIDDEN = 1 } rlx_input_kind;
-typedef enum { RLX_OUTPUT_POOLED = 0, RLX_OUTPUT_HIDDEN = 1 } rlx_output_kind;
+typedef RLX_ENUM { RLX_INPUT_IDS = 0, RLX_INPUT_HIDDEN = 1 } rlx_input_kind;
+typedef RLX_ENUM { RLX_OUTPUT_POOLED = 0, RLX_OUTPUT_HIDDEN = 1 } rlx_output_kind;
 
 typedef struct {
   int hidden;        /* H = heads * head_dim (384)                        */
