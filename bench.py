@@ -43,35 +43,63 @@ def attention_flops(sp, lengths):
     return sum(4 * sp.head_dim * sp.heads * int(L) ** 2 for L in lengths)
 
 
-# the source file that holds each measured kernel class (with the shared device helpers)
-KERNEL_SOURCES = {"qkv_attention": "attention.hip", "attention": "attention.hip", "mx_gemm": "mx_gemm.hip",
-                  "gemv": "gemv.hip"}
+# the sources of each measured kernel class (with the shared device headers)
+_SHARED = ("common.hpp", "kernels.hpp")
+KERNEL_SOURCES = {
+    "qkv_attention": ("attention.hip", "qkv_attention.hpp"),
+    "attention": ("attention.hip", "qkv_attention.hpp"),
+    "mx_gemm": ("mx_gemm.hip",),
+    "gemv": ("gemv.hip",),
+    "encoder_pipe": ("pipe.hip", "gemm_tile.hpp", "qkv_attention.hpp"),
+    # every kernel of an encoder forward (the counter summaries of a whole forward)
+    "encoder": ("attention.hip", "qkv_attention.hpp", "gemm.hip", "gemm_tile.hpp", "rowops.hip", "pipe.hip"),
+}
 
 
 def kernel_source_digest(kernel_class="gemm"):
-    """Digest of the sources of one kernel class (its .hip file and the shared
-    device helpers): counter figures taken before a change to them are no
+    """Digest of the sources of one kernel class (its .hip files and the shared
+    device headers): counter figures taken before a change to them are no
     longer reported."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_37916_amd", "csrc")
-    for f in sorted({KERNEL_SOURCES.get(kernel_class, "gemm.hip"), "common.hpp"}):
+    for f in sorted(set(KERNEL_SOURCES.get(kernel_class, ("gemm.hip", "gemm_tile.hpp"))) | set(_SHARED)):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
 
 
-def committed_traffic(kernel_class, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when no summary exists or the kernel's sources changed since it was taken."""
+def _committed_summary(kernel_class, workload, digest_class=None):
     path = os.path.join(ROOT, "profiles", f"{kernel_class}_{workload}_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m_b = re.search(r"^hbm_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
     m_h = re.search(r"^kernel_source_digest:\s*([0-9a-f]+)", text, re.M)
-    if not m_b or not m_h or m_h.group(1) != kernel_source_digest(kernel_class):
+    if not m_h or m_h.group(1) != kernel_source_digest(digest_class or kernel_class):
         return None
-    return float(m_b.group(1))
+    return text
+
+
+def committed_traffic(kernel_class, workload, digest_class=None):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when no summary exists or the kernel's sources changed since it was taken."""
+    text = _committed_summary(kernel_class, workload, digest_class)
+    m_b = re.search(r"^hbm_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M) if text else None
+    return float(m_b.group(1)) if m_b else None
+
+
+def committed_forward_counters(workload):
+    """Per kernel class of a forward, from the committed counter summary of that
+    forward: calibrated HBM bytes per launch (FETCH_SIZE, WRITE_SIZE) and
+    executed matrix flops per launch (SQ_INSTS_VALU_MFMA_MOPS_* x 512); None
+    when no summary exists or the encoder's kernel sources changed since."""
+    text = _committed_summary("encoder_forward", workload, "encoder")
+    if text is None:
+        return None
+    out = {}
+    for key in ("hbm_bytes_per_launch", "mfma_flops_per_launch"):
+        m = re.search(r"^%s:\s*(\{.*\})\s*$" % key, text, re.M)
+        out[key] = json.loads(m.group(1)) if m else {}
+    return out
 
 
 def cpu_baseline(workload_name, target_s):
@@ -544,11 +572,24 @@ def main():
     per_layer = {k for k in flops_launch if k != "encoder_pipe"}
     matrix_classes = [k for k in flops_launch if k in per_fwd_us]
     dominant = max(matrix_classes, key=lambda k: per_fwd_us.get(k, 0.0))
+    counters = committed_forward_counters(args.workload)
+    traffic = counters["hbm_bytes_per_launch"].get(dominant) if counters else None
+    peak = PEAK_BF16_TFLOPS if sp.dtype == "bf16" else PEAK_F32_TFLOPS  # quantised weights: bf16 products
     achieved = flops_launch[dominant] / (per_launch_us[dominant] * 1e-6) / 1e12
-    traffic = committed_traffic(dominant, args.workload)
     mm_flops = sum(flops_launch[k] * (sp.layers if k in per_layer else 1) for k in matrix_classes)
     mm_us = sum(per_fwd_us.get(k, 0.0) for k in matrix_classes)
-    mfma_util = mm_flops / (mm_us * 1e-6) / (PEAK_BF16_TFLOPS * 1e12)
+    mfma_util = mm_flops / (mm_us * 1e-6) / (peak * 1e12)
+    # the same from the matrix cores' own count: executed flops per launch (counter summary of this
+    # workload's forward, padding included) over this run's per-launch times
+    mfma_counter = None
+    executed = counters["mfma_flops_per_launch"] if counters else {}
+    if executed and all(k in executed for k in matrix_classes):
+        launches = {k: per_fwd_us[k] / per_launch_us[k] for k in matrix_classes}
+        mfma_counter = {
+            "per_kernel": {k: round(executed[k] / (per_launch_us[k] * 1e-6) / (peak * 1e12), 4) for k in matrix_classes},
+            "aggregate": round(sum(executed[k] * launches[k] for k in matrix_classes) / (mm_us * 1e-6) / (peak * 1e12), 4),
+            "source": f"profiles/encoder_forward_{args.workload}_counters.md",
+        }
 
     rec = {
         "metric": f"encoder fwd sequences/sec (b{sp.batch}, s{sp.seq}, "
@@ -573,8 +614,9 @@ def main():
                    "quant": sp.quant, "parallelism": "single GPU", "graph_replay": args.graph,
                    "persistent_forward": persistent},
         "mfma_util_pct": round(100 * mfma_util, 2),
-        "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+        "mfma_util_counter": mfma_counter,
+        "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                      "traffic": traffic, "flops_per_launch": flops_launch[dominant],
                      "avg_launch_us": round(per_launch_us[dominant], 3)},
         "kernel_us_per_forward": {k: round(v, 2) for k, v in sorted(per_fwd_us.items(), key=lambda kv: -kv[1])},
