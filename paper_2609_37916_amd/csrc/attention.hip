@@ -338,8 +338,27 @@ __global__ __launch_bounds__(512) void attn_bf16_kernel(AttnParams p, int vt_str
   }
 }
 
-__global__ __launch_bounds__(128) void attn_f32_kernel(AttnParams p) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+// fp32 attention on the matrix cores (head_dim 32): a block of four waves
+// takes 128 queries of one (sequence, head); wave w owns queries
+// q0 + 32w .. q0 + 32w + 31.  Keys are staged into LDS 64 at a time (rows
+// padded so the fragment reads are bank-conflict free, rows past the key
+// range zeroed) and every wave walks the staged 32-key tiles with
+//   S^T = K Q^T   16 x v_mfma_f32_32x32x2_f32  (step t contracts d = t and
+//                 d = t + 16, one per lane half; Q stays in registers,
+//                 pre-scaled by scale * log2 e)
+//   O^T += V^T P^T 16 x v_mfma_f32_32x32x2_f32 (step s contracts the keys
+//                 the two lane halves hold in score register s)
+// so lane l holds query l % 32 in both products: its running max, sum and
+// output rescale are lane-local, the two halves (16 keys each) combine with
+// one exchange, and P goes from the score registers straight into P V.
+constexpr int kF32KeyChunk = 64;
+constexpr int kF32KPitch = 36;  // floats per staged K row: 16-byte reads of 16 lanes hit distinct banks
+constexpr int kF32VPitch = 40;  // floats per staged V row: the two lane halves' rows are 32 banks apart
+
+__global__ __launch_bounds__(256) void attn_f32_kernel(AttnParams p) {
+  __shared__ __attribute__((aligned(16))) float k_lds[kF32KeyChunk * kF32KPitch];
+  __shared__ __attribute__((aligned(16))) float v_lds[kF32KeyChunk * kF32VPitch];
+  __shared__ uint8_t ok_lds[kF32KeyChunk];
   const int b = blockIdx.z, h = blockIdx.y;
   const SeqRange sr = seq_range(p, b);
   const int n = sr.n;
@@ -348,62 +367,115 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnParams p) {
   const int q_end = min(n, q_begin + kQBlock);
   int klo, khi;
   key_bounds(p, n, q_begin, q_end, klo, khi);
-  const int nk = khi - klo;
-
-  float* k_lds = reinterpret_cast<float*>(smem);   // [nk][32]
-  float* v_lds = k_lds + (size_t)nk * 32;           // [nk][32]
-  uint8_t* ok_lds = reinterpret_cast<uint8_t*>(v_lds + (size_t)nk * 32);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int qw0 = q_begin + 32 * wave;
+  const bool active = qw0 < q_end;           // wave-uniform
+  const int qi = min(qw0 + l32, q_end - 1);  // this lane's query (clamped for the loads)
   const float* kg = reinterpret_cast<const float*>(p.k);
   const float* vg = reinterpret_cast<const float*>(p.v);
   const float* qg = reinterpret_cast<const float*>(p.q);
   const size_t ld = (size_t)p.ld_qkv;
   const int col = h * 32;
-  for (int idx = threadIdx.x; idx < nk * 8; idx += blockDim.x) {
-    const int kr = idx >> 3, c = idx & 7;
-    const size_t off = (size_t)(sr.row0 + klo + kr) * ld + col + c * 4;
-    *reinterpret_cast<float4*>(k_lds + kr * 32 + c * 4) = *reinterpret_cast<const float4*>(kg + off);
-    *reinterpret_cast<float4*>(v_lds + kr * 32 + c * 4) = *reinterpret_cast<const float4*>(vg + off);
-  }
-  for (int kr = threadIdx.x; kr < nk; kr += blockDim.x)
-    ok_lds[kr] = p.key_mask ? (p.key_mask[(size_t)b * p.S + klo + kr] != 0) : 1;
-  __syncthreads();
 
-  const int qi = q_begin + threadIdx.x;
-  if (qi >= n) return;
-  const float sl2 = p.scale * kLog2e;
-  float qv[32], acc[32];
-  const float* qrow = qg + (size_t)(sr.row0 + qi) * ld + col;
+  float qv[16];
+  {
+    const float sl2 = p.scale * kLog2e;
+    const float4* qr = reinterpret_cast<const float4*>(qg + (size_t)(sr.row0 + qi) * ld + col + 16 * half);
 #pragma unroll
-  for (int d = 0; d < 32; ++d) {
-    qv[d] = qrow[d] * sl2;
-    acc[d] = 0.0f;
-  }
-  float m_run = -INFINITY, l_run = 0.0f;
-  for (int kr = 0; kr < nk; ++kr) {
-    const int key = klo + kr;
-    if (!ok_lds[kr] || !visible(p.kind, p.window, qi, key)) continue;
-    const float* kk = k_lds + kr * 32;
-    float s = 0.0f;
-#pragma unroll
-    for (int d = 0; d < 32; ++d) s = fmaf(qv[d], kk[d], s);
-    if (s > m_run) {
-      const float alpha = exp2f(m_run - s);
-      l_run *= alpha;
-#pragma unroll
-      for (int d = 0; d < 32; ++d) acc[d] *= alpha;
-      m_run = s;
+    for (int i = 0; i < 4; ++i) {
+      const float4 v = qr[i];
+      qv[4 * i] = v.x * sl2; qv[4 * i + 1] = v.y * sl2; qv[4 * i + 2] = v.z * sl2; qv[4 * i + 3] = v.w * sl2;
     }
-    const float pr = exp2f(s - m_run);
-    l_run += pr;
-    const float* vv = v_lds + kr * 32;
-#pragma unroll
-    for (int d = 0; d < 32; ++d) acc[d] = fmaf(pr, vv[d], acc[d]);
   }
-  const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
-  float* og = reinterpret_cast<float*>(p.out) + (size_t)(sr.row0 + qi) * p.ld_out + col;
+  f32x16_t acc;
 #pragma unroll
-  for (int d = 0; d < 32; d += 4)
-    *reinterpret_cast<float4*>(og + d) = make_float4(acc[d] * inv, acc[d + 1] * inv, acc[d + 2] * inv, acc[d + 3] * inv);
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  for (int c0 = klo; c0 < khi; c0 += kF32KeyChunk) {
+    // stage keys c0 .. c0 + 63: two 16-byte pieces of K and of V per thread
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int idx = tid + 256 * i, kr = idx >> 3, c = idx & 7;
+      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
+      if (c0 + kr < khi) {
+        const size_t off = (size_t)(sr.row0 + c0 + kr) * ld + col + c * 4;
+        kv = *reinterpret_cast<const float4*>(kg + off);
+        vv = *reinterpret_cast<const float4*>(vg + off);
+      }
+      *reinterpret_cast<float4*>(k_lds + kr * kF32KPitch + c * 4) = kv;
+      *reinterpret_cast<float4*>(v_lds + kr * kF32VPitch + c * 4) = vv;
+    }
+    if (tid < kF32KeyChunk) {
+      const int key = c0 + tid;
+      ok_lds[tid] = key < khi && (!p.key_mask || p.key_mask[(size_t)b * p.S + key] != 0);
+    }
+    __syncthreads();
+    if (active) {
+#pragma unroll 1
+      for (int t0 = 0; t0 < kF32KeyChunk; t0 += 32) {
+        const int key0 = c0 + t0;
+        if (key0 >= khi) break;
+        // the whole tile hidden from every query of this wave by position: skip
+        if ((p.kind == 1 || p.kind == 2) && key0 > min(qw0 + 31, q_end - 1)) break;
+        if (p.kind == 2 && key0 + 31 <= qw0 - p.window) continue;
+        // S^T tile: keys key0 + 8(r/4) + 4 half + r%4 (register r) of query qi
+        f32x16_t st;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+        const float* kr = k_lds + (t0 + l32) * kF32KPitch + 16 * half;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float4 kf = *reinterpret_cast<const float4*>(kr + 4 * i);
+          st = __builtin_amdgcn_mfma_f32_32x32x2f32(kf.x, qv[4 * i], st, 0, 0, 0);
+          st = __builtin_amdgcn_mfma_f32_32x32x2f32(kf.y, qv[4 * i + 1], st, 0, 0, 0);
+          st = __builtin_amdgcn_mfma_f32_32x32x2f32(kf.z, qv[4 * i + 2], st, 0, 0, 0);
+          st = __builtin_amdgcn_mfma_f32_32x32x2f32(kf.w, qv[4 * i + 3], st, 0, 0, 0);
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kk = t0 + 8 * (r >> 2) + 4 * half + (r & 3);
+          const bool vis = ok_lds[kk] && visible(p.kind, p.window, qi, c0 + kk);
+          st[r] = vis ? st[r] : -INFINITY;
+          mx = fmaxf(mx, st[r]);
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = fmaxf(m_run, mx);
+        // nothing visible to this query yet: p = 0 and alpha = 0 (acc and l
+        // are still 0) with a finite reference, no divergence around the MFMAs
+        const float m_ref = m_new == -INFINITY ? 0.0f : m_new;
+        const float alpha = exp2f(m_run - m_ref);
+        float sum = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          st[r] = exp2f(st[r] - m_ref);
+          sum += st[r];
+        }
+        sum += __shfl_xor(sum, 32, 64);
+        l_run = l_run * alpha + sum;
+        m_run = m_new;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] *= alpha;
+        // O^T += V^T P^T: step r takes key t0 + 8(r/4) + 4 half + r%4 in each half
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float va = v_lds[(t0 + 8 * (r >> 2) + 4 * half + (r & 3)) * kF32VPitch + l32];
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(va, st[r], acc, 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // lane: query qw0 + l32, dims 8j + 4 half .. +3 in registers 4j .. 4j+3
+  if (!active || qw0 + l32 >= q_end) return;
+  const float inv = l_run > 0.0f ? 1.0f / l_run : 0.0f;
+  float* og = reinterpret_cast<float*>(p.out) + (size_t)(sr.row0 + qw0 + l32) * p.ld_out + col + 4 * half;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    *reinterpret_cast<float4*>(og + 8 * j) =
+        make_float4(acc[4 * j] * inv, acc[4 * j + 1] * inv, acc[4 * j + 2] * inv, acc[4 * j + 3] * inv);
 }
 
 }  // namespace
@@ -447,16 +519,12 @@ hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Raise the dynamic-LDS limit of both kernels once (S = 512 needs ~74 KB for
-// bf16 and ~128 KB for f32; gfx950 has 160 KB per workgroup).
+// Raise the dynamic-LDS limit of the bf16 kernel once (S = 512 needs ~74 KB;
+// gfx950 has 160 KB per workgroup).  The fp32 kernel stages 64 keys at a
+// time in static LDS.
 hipError_t set_lds_limits() {
-  static const hipError_t once = [] {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(attn_bf16_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    if (e != hipSuccess) return e;
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(attn_f32_kernel),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-  }();
+  static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(attn_bf16_kernel),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
   return once;
 }
 
@@ -490,8 +558,7 @@ hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
     hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(512), lds, s, p, vt_stride, gx, nfull);
   } else {
     const dim3 grid(gx, p.heads, p.B);
-    const size_t lds = (size_t)p.S * 32 * 4 * 2 + (size_t)p.S;
-    hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(128), lds, s, p);
+    hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(256), 0, s, p);
   }
   return hipGetLastError();
 }

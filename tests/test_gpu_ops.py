@@ -266,9 +266,10 @@ def test_attention_identical_keys_mean_of_values(rlx):
                       np.abs(v[b, :L]).max(), "identical keys")
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
 @pytest.mark.parametrize("scale", [-0.3, 0.0, 2.5])
 @pytest.mark.parametrize("kind,window", [("custom", 0), ("causal", 0), ("sliding", 50)])
-def test_attention_scale_sign_and_zero(rlx, kind, window, scale):
+def test_attention_scale_sign_and_zero(rlx, kind, window, scale, dt):
     """A negative scale (its sign folded into Q), a zero scale (uniform
     weights over the visible keys) and a sharp one, over several query blocks
     with a ragged sequence."""
@@ -276,9 +277,10 @@ def test_attention_scale_sign_and_zero(rlx, kind, window, scale):
     B, S, heads = 2, 300, 2
     H = heads * 32
     qkv, mask = _attention_case(rng, B, S, heads, [S, 77], holes=(kind == "custom"))
-    qkv = to_bf16_exact(qkv)
+    if dt == "bf16":
+        qkv = to_bf16_exact(qkv)
     use_mask = kind == "custom"
-    buf = _dev(qkv, torch.bfloat16)
+    buf = _dev(qkv, torch.bfloat16 if dt == "bf16" else torch.float32)
     got = rlx.masked_attention(buf[:, 0:H], buf[:, H:2 * H], buf[:, 2 * H:], B=B, S=S, heads=heads, kind=KINDS[kind],
                                key_mask=_dev(mask, torch.uint8) if use_mask else None, window=window, scale=scale,
                                row_stride=3 * H).float().cpu().numpy().reshape(B, S, heads, 32)
@@ -286,8 +288,9 @@ def test_attention_scale_sign_and_zero(rlx, kind, window, scale):
     k = qkv[:, H:2 * H].reshape(B, S, heads, 32)
     v = qkv[:, 2 * H:].reshape(B, S, heads, 32)
     ref = oracle.masked_attention(q, k, v, KINDS[kind], mask if use_mask else None, window, scale)
-    tol = BF16_REL * np.abs(ref) + 2.0 ** -7 * np.abs(v).max(axis=(1, 3), keepdims=True)
-    assert_within(got, ref, tol, f"attention {kind} scale={scale}")
+    vmax = np.abs(v).max(axis=(1, 3), keepdims=True)
+    tol = BF16_REL * np.abs(ref) + 2.0 ** -7 * vmax if dt == "bf16" else 1e-5 * np.abs(ref) + 1e-5 * vmax
+    assert_within(got, ref, tol, f"attention {dt} {kind} scale={scale}")
 
 
 @pytest.mark.parametrize("kind,window", [("none", 0), ("causal", 0), ("sliding", 128), ("custom", 0)])
