@@ -20,19 +20,47 @@
 namespace rlx {
 namespace {
 
+constexpr int kScanSeqs = 4;    // sequences per wave whose mask loads are in flight together
+constexpr int kScanChunks = 8;  // 64-position loads per sequence (S <= 512)
+
+// Mask bytes of sequences b0 .. b0 + kScanSeqs - 1 at positions 64 c + lane,
+// 0 past the batch or the row.  Every load is issued unconditionally at an
+// in-bounds (clamped) address and selected afterwards: a load under a
+// per-lane condition gets its own wait for the data, which serialises them.
+// Needs B >= 1 and 1 <= S <= 64 * kScanChunks.
+__device__ __forceinline__ void load_mask_group(const uint8_t* mask, int B, int S, int b0, int lane,
+                                                uint8_t (&mb)[kScanSeqs][kScanChunks]) {
+  uint8_t raw[kScanSeqs][kScanChunks];
+#pragma unroll
+  for (int g = 0; g < kScanSeqs; ++g)
+#pragma unroll
+    for (int c = 0; c < kScanChunks; ++c)
+      raw[g][c] = mask[(size_t)min(b0 + g, B - 1) * S + min(64 * c + lane, S - 1)];
+#pragma unroll
+  for (int g = 0; g < kScanSeqs; ++g)
+#pragma unroll
+    for (int c = 0; c < kScanChunks; ++c) mb[g][c] = (b0 + g < B && 64 * c + lane < S) ? raw[g][c] : 0;
+}
+
 __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, int B, int S, int* cu, int* tok_src,
                                                          int* tok_dst, int* order) {
   extern __shared__ int offs[];  // [B+1]: token counts, then their exclusive prefix; then [B] ranks
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-  for (int b = wave; b < B; b += nw) {
-    int cnt = 0;
-    for (int s0 = 0; s0 < S; s0 += 64) {
-      const int s = s0 + lane;
-      const bool v = s < S && mask[(size_t)b * S + s] != 0;
-      cnt += __popcll(__ballot(v));
+  // each wave takes kScanSeqs sequences at a time and requests all their mask
+  // bytes (64 positions per load, up to 8 per sequence) before the first
+  // ballot: one memory round trip per group instead of one per 64 positions
+  const int nch = (S + 63) / 64;
+  for (int b0 = wave * kScanSeqs; b0 < B; b0 += nw * kScanSeqs) {
+    uint8_t mb[kScanSeqs][kScanChunks];
+    load_mask_group(mask, B, S, b0, lane, mb);
+#pragma unroll
+    for (int g = 0; g < kScanSeqs; ++g) {
+      int cnt = 0;
+#pragma unroll
+      for (int c = 0; c < kScanChunks; ++c) cnt += __popcll(__ballot(mb[g][c] != 0));
+      if (lane == 0 && b0 + g < B) offs[b0 + g] = cnt;
     }
-    if (lane == 0) offs[b] = cnt;
   }
   __syncthreads();
   // Sequences by token count, longest first (ties by index), for kernels that
@@ -75,19 +103,28 @@ __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, in
   }
   __syncthreads();
   for (int i = threadIdx.x; i <= B; i += blockDim.x) cu[i] = offs[i];
-  for (int b = wave; b < B; b += nw) {
-    int base = offs[b];
-    for (int s0 = 0; s0 < S; s0 += 64) {
-      const int s = s0 + lane;
-      const bool v = s < S && mask[(size_t)b * S + s] != 0;
-      const uint64_t bal = __ballot(v);
-      const int rank = __popcll(bal & below);
-      if (s < S) {
-        const int src = b * S + s;
-        if (v) tok_src[base + rank] = src;
-        tok_dst[src] = v ? base + rank : -1;
+  for (int b0 = wave * kScanSeqs; b0 < B; b0 += nw * kScanSeqs) {
+    uint8_t mb[kScanSeqs][kScanChunks];
+    load_mask_group(mask, B, S, b0, lane, mb);
+#pragma unroll
+    for (int g = 0; g < kScanSeqs; ++g) {
+      const int b = b0 + g;
+      if (b >= B) break;  // wave-uniform
+      int base = offs[b];
+#pragma unroll
+      for (int c = 0; c < kScanChunks; ++c) {
+        if (c >= nch) break;
+        const int s = 64 * c + lane;
+        const bool v = mb[g][c] != 0;
+        const uint64_t bal = __ballot(v);
+        const int rank = __popcll(bal & below);
+        if (s < S) {
+          const int src = b * S + s;
+          if (v) tok_src[base + rank] = src;
+          tok_dst[src] = v ? base + rank : -1;
+        }
+        base += __popcll(bal);
       }
-      base += __popcll(bal);
     }
   }
 }
@@ -480,6 +517,7 @@ inline int blocks_for_rows(int rows) { return (rows + 3) / 4; }
 
 hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, int* order,
                             hipStream_t s) {
+  if (B < 1 || S < 1 || S > 64 * kScanChunks) return hipErrorInvalidValue;
   hipLaunchKernelGGL(mask_scan_kernel, dim3(1), dim3(1024), (size_t)(2 * B + 1) * sizeof(int), s, mask, B, S, cu,
                      tok_src, tok_dst, B <= kMaxOrderedBatch ? order : nullptr);
   return hipGetLastError();

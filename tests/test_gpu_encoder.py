@@ -107,6 +107,27 @@ def test_encoder_mask_with_holes_and_empty_row(rlx):
     _compare(got, ref, wl, TOL["bf16"], "mask with holes")
 
 
+def test_encoder_hidden_input_large_ragged_mask_f32(rlx):
+    """Hidden-state input always takes the separate mask scan (counts, prefix,
+    compaction maps): 136 sequences of up to 136 positions (more than 128
+    sequences, a length that is not a multiple of 64), holes, empty sequences
+    at both ends and in the middle, full-length ones; one fp32 layer."""
+    sp = workloads.spec("layer_f32_b2_s16", batch=136, seq=136, layers=1, len_lo=1, len_hi=136)
+    wl = workloads.make(sp, affine=True)
+    rng = np.random.default_rng(21)
+    wl.mask = (wl.mask & (rng.random(wl.mask.shape) < 0.7)).astype(np.uint8)
+    wl.mask[[0, 77, 135]] = 0
+    wl.mask[[5, 100]] = 1
+    wl.lengths = wl.mask.sum(axis=1)
+    got = _run(rlx, wl)
+    ref = oracle.encoder_forward(wl)
+    m = wl.mask.astype(bool)
+    assert np.all(np.isfinite(got)) and np.all(got[~m] == 0), "masked positions must be zero rows"
+    err = float(np.abs(got[m] - ref[m]).max())
+    print(f"hidden input, large ragged mask: max-abs error {err:.3g}", flush=True)
+    assert err <= TOL["f32"]
+
+
 def test_encoder_hidden_output_f32(rlx):
     sp = workloads.spec("minilm_b4_s128_f32", batch=3, seq=40, layers=2, output_kind="hidden", len_lo=1, len_hi=40)
     wl = workloads.make(sp, affine=True)
