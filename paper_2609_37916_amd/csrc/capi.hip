@@ -393,14 +393,16 @@ rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* m
       STEP(K_GATHER_ROWS, launch_gather_rows(input, H, E.tok_src, n_dev, T, E.X, E.dt, ss));
     }
   }
-  const Quant q = to_quant(c.quant);
   for (int l = 0; l < c.layers; ++l) {
     const rlx_layer_weights& L = E.layers[l];
     // From the second layer on, a deferred-LayerNorm forward's layer input X
     // holds the previous layer's LN2 input, normalised by its readers.
     const bool x_def = E.deferred && l > 0;
     const rlx_layer_weights* prev = l > 0 ? &E.layers[l - 1] : nullptr;
-    const void* wqkv = x_def ? E.folded[l].wqkv : L.wqkv;
+    const Quant q = to_quant(c.quant);
+    // quantised weights keep their codes; their deferred LN inputs are gamma-scaled
+    const bool gsc = E.deferred && q != Quant::None;
+    const void* wqkv = x_def && !gsc ? E.folded[l].wqkv : L.wqkv;
     const float* bqkv = x_def ? E.folded[l].vq : L.bqkv;
     const float* uqkv = x_def ? E.folded[l].uq : nullptr;
     GemmParams g{};
@@ -443,26 +445,35 @@ rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* m
     g.residual = E.X; g.y = E.A; g.N = H; g.K = H; g.epi = Epi::BiasResidual;
     g.x_head_rows = fused_attn ? T : 0;  // the fused attention writes the context head-major
     if (x_def) {
-      g.res_stats = E.S2; g.res_gamma = prev->ln2_gamma; g.res_beta = prev->ln2_beta;
+      g.res_stats = E.S2; g.res_gamma = prev->ln2_gamma; g.res_beta = prev->ln2_beta; g.res_scaled = gsc;
     }
     g.y_stats = E.deferred ? E.S1 : nullptr;
+    g.y_gamma = gsc ? L.ln1_gamma : nullptr;
     STEP(K_GEMM_ATTN_OUT, launch_gemm(g, ss));
     g.x_head_rows = 0;
     g.res_stats = nullptr; g.res_gamma = g.res_beta = nullptr; g.y_stats = nullptr;
+    g.res_scaled = false; g.y_gamma = nullptr;
 
     if (E.deferred) {
       // FFN-up on LN1(A) with LN1 folded into W1; FFN-down's residual LN1(A)
       // is normalised in its epilogue, and its output is LN2's input
       g.x = E.A; g.x_stats = E.S1; g.fold_u = E.folded[l].u1;
-      g.w = E.folded[l].w1; g.scales = nullptr; g.zeros = nullptr; g.bias = E.folded[l].v1;
+      if (gsc) {
+        g.w = L.w1; g.scales = L.w1_scales; g.zeros = L.w1_zeros;
+      } else {
+        g.w = E.folded[l].w1; g.scales = nullptr; g.zeros = nullptr;
+      }
+      g.bias = E.folded[l].v1;
       g.residual = nullptr; g.y = E.G; g.N = F; g.K = H; g.epi = Epi::BiasGelu;
       STEP(K_GEMM_FFN_UP, launch_gemm(g, ss));
       g.x_stats = nullptr; g.fold_u = nullptr;
 
-      g.x = E.G; g.w = L.w2; g.scales = nullptr; g.zeros = nullptr; g.bias = L.b2;
-      g.residual = E.A; g.res_stats = E.S1; g.res_gamma = L.ln1_gamma; g.res_beta = L.ln1_beta;
-      g.y = E.X; g.y_stats = E.S2; g.N = H; g.K = F; g.epi = Epi::BiasResidual;
+      g.x = E.G; g.w = L.w2; g.scales = L.w2_scales; g.zeros = L.w2_zeros; g.bias = L.b2;
+      g.residual = E.A; g.res_stats = E.S1; g.res_gamma = L.ln1_gamma; g.res_beta = L.ln1_beta; g.res_scaled = gsc;
+      g.y = E.X; g.y_stats = E.S2; g.y_gamma = gsc ? L.ln2_gamma : nullptr; g.N = H; g.K = F;
+      g.epi = Epi::BiasResidual;
       STEP(K_GEMM_FFN_DOWN, launch_gemm(g, ss));
+      g.res_scaled = false; g.y_gamma = nullptr;
       continue;
     }
 
@@ -481,7 +492,7 @@ rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* m
   if (c.output_kind == RLX_OUTPUT_POOLED) {
     if (E.deferred) {
       STEP(K_POOL, launch_pool_l2(E.X, H, E.cu, B, static_cast<float*>(output), E.dt, ss, E.S2,
-                                  last.ln2_gamma, last.ln2_beta, c.ln_eps));
+                                  last.ln2_gamma, last.ln2_beta, c.ln_eps, c.quant != RLX_Q_NONE));
     } else {
       STEP(K_POOL, launch_pool_l2(E.X, H, E.cu, B, static_cast<float*>(output), E.dt, ss));
     }
@@ -633,13 +644,16 @@ rlx_status fold_layer_norms(rlx_encoder* e) {
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
   struct Offs { size_t wqkv, uq, vq, w1, u1, v1; };
   std::vector<Offs> offs(c.layers);
+  // dense weights get gamma-scaled copies; quantised ones only the vectors
+  // (their LN inputs travel gamma-scaled instead)
+  const bool quant = c.quant != RLX_Q_NONE;
   for (int l = 0; l < c.layers; ++l) {
     if (l > 0) {
-      offs[l].wqkv = take(3 * H * H * 2);
+      if (!quant) offs[l].wqkv = take(3 * H * H * 2);
       offs[l].uq = take(3 * H * sizeof(float));
       offs[l].vq = take(3 * H * sizeof(float));
     }
-    offs[l].w1 = take(F * H * 2);
+    if (!quant) offs[l].w1 = take(F * H * 2);
     offs[l].u1 = take(F * sizeof(float));
     offs[l].v1 = take(F * sizeof(float));
   }
@@ -653,21 +667,34 @@ rlx_status fold_layer_norms(rlx_encoder* e) {
   for (int l = 0; l < c.layers; ++l) {
     const rlx_layer_weights& L = e->layers[l];
     rlx_encoder::Folded& f = e->folded[l];
+    const Quant q = to_quant(c.quant);
     if (l > 0) {
       const rlx_layer_weights& P = e->layers[l - 1];
-      f.wqkv = base + offs[l].wqkv;
       f.uq = reinterpret_cast<float*>(base + offs[l].uq);
       f.vq = reinterpret_cast<float*>(base + offs[l].vq);
-      RLX_HIP(launch_fold_ln_weights(L.wqkv, 3 * c.hidden, c.hidden, P.ln2_gamma, P.ln2_beta, L.bqkv, f.wqkv, f.uq,
-                                     f.vq, e->cap_stream),
-              "encoder_create: fold LN2 into Wqkv");
+      if (quant) {
+        RLX_HIP(launch_fold_ln_quant(L.wqkv, q, L.wqkv_scales, L.wqkv_zeros, 3 * c.hidden, c.hidden, P.ln2_gamma,
+                                     P.ln2_beta, L.bqkv, f.uq, f.vq, e->cap_stream),
+                "encoder_create: fold LN2 into the QKV vectors");
+      } else {
+        f.wqkv = base + offs[l].wqkv;
+        RLX_HIP(launch_fold_ln_weights(L.wqkv, 3 * c.hidden, c.hidden, P.ln2_gamma, P.ln2_beta, L.bqkv, f.wqkv,
+                                       f.uq, f.vq, e->cap_stream),
+                "encoder_create: fold LN2 into Wqkv");
+      }
     }
-    f.w1 = base + offs[l].w1;
     f.u1 = reinterpret_cast<float*>(base + offs[l].u1);
     f.v1 = reinterpret_cast<float*>(base + offs[l].v1);
-    RLX_HIP(launch_fold_ln_weights(L.w1, c.ffn, c.hidden, L.ln1_gamma, L.ln1_beta, L.b1, f.w1, f.u1, f.v1,
-                                   e->cap_stream),
-            "encoder_create: fold LN1 into W1");
+    if (quant) {
+      RLX_HIP(launch_fold_ln_quant(L.w1, q, L.w1_scales, L.w1_zeros, c.ffn, c.hidden, L.ln1_gamma, L.ln1_beta, L.b1,
+                                   f.u1, f.v1, e->cap_stream),
+              "encoder_create: fold LN1 into the FFN-up vectors");
+    } else {
+      f.w1 = base + offs[l].w1;
+      RLX_HIP(launch_fold_ln_weights(L.w1, c.ffn, c.hidden, L.ln1_gamma, L.ln1_beta, L.b1, f.w1, f.u1, f.v1,
+                                     e->cap_stream),
+              "encoder_create: fold LN1 into W1");
+    }
   }
   RLX_HIP(hipStreamSynchronize(e->cap_stream), "encoder_create: fold LayerNorms");
   return RLX_OK;
@@ -680,7 +707,8 @@ rlx_status fold_layer_norms(rlx_encoder* e) {
 rlx_status setup_pipeline(rlx_encoder* e) {
   const rlx_encoder_config& c = e->cfg;
   const char* env = std::getenv("RLX_PIPELINE");
-  if (!env || env[0] != '1' || !e->deferred || c.input_kind != RLX_INPUT_IDS || c.output_kind != RLX_OUTPUT_POOLED ||
+  if (!env || env[0] != '1' || !e->deferred || c.quant != RLX_Q_NONE || c.input_kind != RLX_INPUT_IDS ||
+      c.output_kind != RLX_OUTPUT_POOLED ||
       !pipe_supported(PipeShape{1, 16, c.hidden, c.ffn, c.heads, c.layers}) || c.layers > kPipeMaxLayers)
     return RLX_OK;
   int cus = 0;
@@ -891,7 +919,11 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
 
   // Workspace plan: token maps, then six activation buffers for T_max tokens.
   const size_t es = e->dt == DType::BF16 ? 2 : 4;
-  e->deferred = gemm_deferred_ln_supported(e->dt, to_quant(cfg->quant), cfg->hidden);
+  // Quantised weights: the deferred LayerNorm stores LN inputs gamma-scaled,
+  // so the final hidden states would need their own normalisation kernel;
+  // pooled outputs only.
+  e->deferred = gemm_deferred_ln_supported(e->dt, to_quant(cfg->quant), cfg->hidden) &&
+                (cfg->quant == RLX_Q_NONE || cfg->output_kind == RLX_OUTPUT_POOLED);
   const WsPlan plan = plan_workspace(cfg->max_batch, cfg->max_seq, cfg->hidden, cfg->ffn, es, e->deferred);
   he = hipMalloc(&e->ws, plan.bytes);
   if (he != hipSuccess) {

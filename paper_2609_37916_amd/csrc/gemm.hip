@@ -93,13 +93,20 @@ __device__ __forceinline__ bf16x8_t int8x8_scaled_to_bf16(uint2 c, float s) {
 // 8 int4 codes (k ascending, low nibble first) -> 8 bf16 of (q - z) * s
 // (Int4) or fma(q, s, m) (Int4M, z holding m), RNE: the same arithmetic as
 // the whole-group conversions below.
+// The low and the high nibbles go to the bytes of two words, each byte to
+// fp32 with v_cvt_f32_ubyte; (q - z) * s is formed as fma(q, s, -z s), exact
+// in the same way: z s (two f16 significands) needs at most 22 bits, so it is
+// exact in fp32 and the fma rounds (q - z) s once, like the product of the
+// exact difference.
 template <Quant Q>
 __device__ __forceinline__ bf16x8_t int4x8_to_bf16(uint32_t c, float s, float z) {
+  const uint32_t lo = c & 0x0f0f0f0fu, hi = (c >> 4) & 0x0f0f0f0fu;
+  const float zs = Q == Quant::Int4 ? -z * s : z;
   uint32_t o[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const float lo = (float)((c >> (8 * j)) & 0xfu), hi = (float)((c >> (8 * j + 4)) & 0xfu);
-    o[j] = Q == Quant::Int4 ? pack_bf16x2((lo - z) * s, (hi - z) * s) : pack_bf16x2(fmaf(lo, s, z), fmaf(hi, s, z));
+    const float a = (float)((lo >> (8 * j)) & 0xffu), b = (float)((hi >> (8 * j)) & 0xffu);
+    o[j] = pack_bf16x2(fmaf(a, s, zs), fmaf(b, s, zs));
   }
   return as_bf16x8(make_uint4(o[0], o[1], o[2], o[3]));
 }
@@ -364,7 +371,7 @@ template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1, int LN = 0,
 __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   static_assert(BM % 64 == 0 && BN % 64 == 0 && STAGES >= 2 && STAGES <= 6, "tile");
   static_assert(KS == 1 || (sizeof(T) == 2 && (BK_BF16 / 16) % KS == 0), "K split over bf16 chunks");
-  static_assert(dma_quant_ok(Q) && (Q == Quant::None || (sizeof(T) == 2 && LN == 0)), "quantised: bf16, no LN");
+  static_assert(dma_quant_ok(Q) && (Q == Quant::None || sizeof(T) == 2), "quantised: bf16 activations");
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int ES = sizeof(T);
@@ -601,15 +608,39 @@ hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Quantised weights through the DMA kernel (bf16 activations, no deferred
-// LayerNorm): 64 x 128 tiles for the wide projections, else 64 x 64.
+// Deferred-LayerNorm role bits of a call (gemm_tile.hpp).
+int ln_roles(const GemmParams& p) {
+  return (p.x_stats ? kLnX : 0) | (p.res_stats ? kLnRes | (p.res_scaled ? kLnResG : 0) : 0) |
+         (p.y_stats ? kLnOut | (p.y_gamma ? kLnOutG : 0) : 0);
+}
+
+// Quantised weights through the DMA kernel (bf16 activations): 64 x 128 tiles
+// for the wide projections, else 64 x 64.  The deferred-LayerNorm roles of
+// the quantised encoder layer: the QKV and FFN-up projections read a
+// gamma-scaled deferred input; the output projection and FFN-down write a
+// gamma-scaled LN input, the output projection's residual being the plain
+// embedding output in the first layer and a gamma-scaled one after it.
 template <int BM, int BN, int STAGES, Quant Q>
 hipError_t launch_dma_q_tile(const GemmParams& p, hipStream_t s) {
+  constexpr int kOutG = kLnOut | kLnOutG, kResG = kLnRes | kLnResG;
+  const int ln = ln_roles(p);
   switch (p.epi) {
-    case Epi::None: return launch_dma<BM, BN, STAGES, bf16_t, Epi::None, 1, 0, Q>(p, s);
-    case Epi::Bias: return launch_dma<BM, BN, STAGES, bf16_t, Epi::Bias, 1, 0, Q>(p, s);
-    case Epi::BiasGelu: return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasGelu, 1, 0, Q>(p, s);
-    case Epi::BiasResidual: return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasResidual, 1, 0, Q>(p, s);
+    case Epi::None:
+      if (ln == 0) return launch_dma<BM, BN, STAGES, bf16_t, Epi::None, 1, 0, Q>(p, s);
+      break;
+    case Epi::Bias:
+      if (ln == 0) return launch_dma<BM, BN, STAGES, bf16_t, Epi::Bias, 1, 0, Q>(p, s);
+      if (ln == kLnX) return launch_dma<BM, BN, STAGES, bf16_t, Epi::Bias, 1, kLnX, Q>(p, s);
+      break;
+    case Epi::BiasGelu:
+      if (ln == 0) return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasGelu, 1, 0, Q>(p, s);
+      if (ln == kLnX) return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasGelu, 1, kLnX, Q>(p, s);
+      break;
+    case Epi::BiasResidual:
+      if (ln == 0) return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasResidual, 1, 0, Q>(p, s);
+      if (ln == kOutG) return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasResidual, 1, kOutG, Q>(p, s);
+      if (ln == (kResG | kOutG)) return launch_dma<BM, BN, STAGES, bf16_t, Epi::BiasResidual, 1, kResG | kOutG, Q>(p, s);
+      break;
   }
   return hipErrorInvalidValue;
 }
@@ -633,18 +664,22 @@ hipError_t launch_typed(const GemmParams& p, hipStream_t s);
 // converts each weight once per block instead of once per wave that reads
 // it, is as fast for int8 and faster for int4 (FFN-up 84 vs 105 us, QKV 70
 // vs 92 us).
+// With a deferred LayerNorm role the DMA kernel runs at every K: its
+// epilogue operands are staged in LDS, which the roles need.
 template <Quant Q>
 hipError_t launch_dma_q(const GemmParams& p, hipStream_t s) {
-  if (p.K >= 1024) {
+  const bool ln = ln_roles(p) != 0;
+  if (p.K >= 1024 || ln) {
     if (p.N % 128 == 0 && p.N >= 1024 && dma_q_fits(p, 128)) return launch_dma_q_tile<64, 128, 4, Q>(p, s);
     if (dma_q_fits(p, 64)) return launch_dma_q_tile<64, 64, 5, Q>(p, s);
+    if (ln) return hipErrorInvalidValue;
   }
   return launch_typed<bf16_t, Q>(p, s);
 }
 
 template <int BM, int BN, int STAGES, typename T, int KS = 1>
 hipError_t launch_dma_tile(const GemmParams& p, hipStream_t s) {
-  const int ln = (p.x_stats ? kLnX : 0) | (p.res_stats ? kLnRes : 0) | (p.y_stats ? kLnOut : 0);
+  const int ln = ln_roles(p);  // (the gamma-scaled roles are for quantised weights: rejected here)
   if constexpr (sizeof(T) == 2) {
     // the deferred-LayerNorm combinations of the encoder layer: the QKV and
     // FFN-up projections read a deferred input; the output projection writes
@@ -786,6 +821,51 @@ __global__ __launch_bounds__(256) void fold_ln_weights_kernel(const bf16_t* w, i
   }
 }
 
+// Effective weight of row n, column k of quantised weights: the value the
+// matrix cores multiply (q * s for int8 per channel, whose scale multiplies
+// the fp32 sum; otherwise the bf16 rounding of the same fp32 arithmetic as
+// the GEMM's code conversions).
+__device__ __forceinline__ float effective_weight(const uint8_t* w, Quant q, const uint16_t* scales,
+                                                  const uint16_t* zeros, int n, int k, int K) {
+  const int gi = n * (K / 32) + k / 32;
+  if (q == Quant::Int8) return (float)(int8_t)w[(size_t)n * K + k] * f16_bits_to_f32(scales[n]);
+  if (q == Quant::Int8G) return bf16_to_f32(f32_to_bf16((float)(int8_t)w[(size_t)n * K + k] * f16_bits_to_f32(scales[gi])));
+  const uint32_t byte = w[(size_t)n * (K / 2) + k / 2];
+  const float c = (float)((k & 1) ? byte >> 4 : byte & 0xfu);
+  const float sc = f16_bits_to_f32(scales[gi]), z = f16_bits_to_f32(zeros[gi]);
+  return bf16_to_f32(f32_to_bf16(q == Quant::Int4 ? (c - z) * sc : fmaf(c, sc, z)));
+}
+
+// One block per weight row n (256 threads over k): u[n] = sum_k gamma_k W_nk,
+// v[n] = bias[n] + sum_k beta_k W_nk over the effective weights.
+__global__ __launch_bounds__(256) void fold_ln_quant_kernel(const uint8_t* w, Quant q, const uint16_t* scales,
+                                                             const uint16_t* zeros, int K, const float* gamma,
+                                                             const float* beta, const float* bias, float* u_out,
+                                                             float* v_out) {
+  const int n = blockIdx.x, tid = threadIdx.x;
+  double u = 0.0, v = 0.0;
+  for (int k = tid; k < K; k += 256) {
+    const double wk = effective_weight(w, q, scales, zeros, n, k, K);
+    u += (double)gamma[k] * wk;
+    v += (double)beta[k] * wk;
+  }
+  __shared__ double red[2][4];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    u += __shfl_xor(u, o, 64);
+    v += __shfl_xor(v, o, 64);
+  }
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = u;
+    red[1][tid >> 6] = v;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    u_out[n] = (float)(red[0][0] + red[0][1] + red[0][2] + red[0][3]);
+    v_out[n] = (float)(red[1][0] + red[1][1] + red[1][2] + red[1][3] + (bias ? (double)bias[n] : 0.0));
+  }
+}
+
 }  // namespace
 
 hipError_t launch_fold_ln_weights(const void* w, int N, int K, const float* gamma, const float* beta,
@@ -796,9 +876,20 @@ hipError_t launch_fold_ln_weights(const void* w, int N, int K, const float* gamm
   return hipGetLastError();
 }
 
+hipError_t launch_fold_ln_quant(const void* w, Quant q, const void* scales, const void* zeros, int N, int K,
+                                const float* gamma, const float* beta, const float* bias, float* u_out, float* v_out,
+                                hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  if (!dma_quant_ok(q) || q == Quant::None || K % 32 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(fold_ln_quant_kernel, dim3(N), dim3(256), 0, s, reinterpret_cast<const uint8_t*>(w), q,
+                     reinterpret_cast<const uint16_t*>(scales), reinterpret_cast<const uint16_t*>(zeros), K, gamma,
+                     beta, bias, u_out, v_out);
+  return hipGetLastError();
+}
+
 bool gemm_deferred_ln_supported(DType dt, Quant q, int H) {
   // rows of an even number of 64-column parts (whole 16-byte statistics runs), up to 1024 columns
-  return dt == DType::BF16 && q == Quant::None && H % 128 == 0 && H <= 64 * kLnMaxParts;
+  return dt == DType::BF16 && (q == Quant::None || dma_quant_ok(q)) && H % 128 == 0 && H <= 64 * kLnMaxParts;
 }
 
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {

@@ -75,13 +75,16 @@ template <> struct OutVec<float> {
 // of the K range for the same 64-row tile layout; the staging sums the groups'
 // partials (group 0 writes, the others add in turn) before the epilogue, which
 // then runs on all 256*KS threads.
-// Deferred-LayerNorm roles of a dense bf16 GEMM (the GemmParams fields):
+// Deferred-LayerNorm roles of a bf16-activation GEMM (the GemmParams fields):
 // normalise the product of a deferred input, normalise a deferred residual,
-// write the partial statistics of the output.
-constexpr int kLnX = 1, kLnRes = 2, kLnOut = 4;
+// write the partial statistics of the output.  With quantised weights, where
+// gamma cannot be folded into the codes, the LayerNorm input travels
+// gamma-scaled: kLnOutG stores gamma[n] * y (statistics still of y) and
+// kLnResG takes a residual stored that way.
+constexpr int kLnX = 1, kLnRes = 2, kLnOut = 4, kLnOutG = 8, kLnResG = 16;
 
-// Epilogue operands staged in LDS (dense bf16 kernels): the block's per-column
-// vectors [bias, fold_u, res_gamma, res_beta][BN] (f32), its residual tile
+// Epilogue operands staged in LDS (bf16-activation kernels): the block's per-column
+// vectors [bias, fold_u, res_gamma, res_beta(, y_gamma)][BN] (f32), its residual tile
 // [BM][BN] (bf16) and the partial statistics of its rows ([BM][K/64] for x,
 // [BM][N/64] for the residual).  Every region is a whole number of 1 KB DMA
 // blocks.  They are requested before the first operand stage, so by the
@@ -94,9 +97,10 @@ constexpr int kLnX = 1, kLnRes = 2, kLnOut = 4;
 struct EpiLayout {
   int res_off, xst_off, rst_off, mrg_off, bytes;
 };
-__host__ __device__ constexpr EpiLayout epi_layout(int BM, int BN, bool res, bool xst, bool rst, int K, int N) {
+__host__ __device__ constexpr EpiLayout epi_layout(int BM, int BN, bool res, bool xst, bool rst, int K, int N,
+                                                   bool out_gamma = false) {
   EpiLayout L{};
-  int off = 16 * BN;  // four f32 vectors of BN
+  int off = out_gamma ? (20 * BN + 1023) / 1024 * 1024 : 16 * BN;  // four (five) f32 vectors of BN
   L.res_off = off;
   if (res) off += BM * BN * 2;
   L.xst_off = off;
@@ -110,7 +114,8 @@ __host__ __device__ constexpr EpiLayout epi_layout(int BM, int BN, bool res, boo
 }
 template <int BM, int BN, Epi E, int LN>
 __host__ __device__ constexpr EpiLayout epi_layout_of(int K, int N) {
-  return epi_layout(BM, BN, E == Epi::BiasResidual, (LN & kLnX) != 0, (LN & kLnRes) != 0, K, N);
+  return epi_layout(BM, BN, E == Epi::BiasResidual, (LN & kLnX) != 0, (LN & kLnRes) != 0, K, N,
+                    (LN & kLnOutG) != 0);
 }
 
 // Merges the partial statistics staged at `epi` into each row's (mean, rstd)
@@ -139,7 +144,9 @@ template <int BM, int BN, typename T, Quant Q, Epi E, int TM, int TN, int NRB, i
 __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_t* lds, const GemmParams& p, int m0,
                                            int n0, int M, uint8_t* epi = nullptr) {
   static_assert(NRB == 1 || NRB == 2, "row blocks follow the 2 wave rows");
-  static_assert(LN == 0 || (sizeof(T) == 2 && Q == Quant::None && STAGED), "deferred LayerNorm: dense bf16");
+  static_assert(LN == 0 || (sizeof(T) == 2 && STAGED), "deferred LayerNorm: bf16 activations, staged operands");
+  static_assert(!(LN & kLnOutG) || (LN & kLnOut), "gamma-scaled output: with its statistics");
+  static_assert(!(LN & kLnResG) || (LN & kLnRes), "gamma-scaled residual: a deferred residual");
   static_assert(!STAGED || sizeof(T) == 2, "staged epilogue operands: bf16");
   static_assert(!(LN & kLnRes) || E == Epi::BiasResidual, "a deferred residual needs the residual epilogue");
   static_assert(KS == 1 || NRB == 1, "split-K tiles stage all rows at once");
@@ -159,7 +166,7 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
   const T* res = reinterpret_cast<const T*>(p.residual);
   const uint16_t* qs = reinterpret_cast<const uint16_t*>(p.scales);
   const EpiLayout lay = epi_layout_of<BM, BN, E, LN>(p.K, N);
-  const float* vec = reinterpret_cast<const float*>(epi);  // [4][BN]: bias, fold_u, res_gamma, res_beta
+  const float* vec = reinterpret_cast<const float*>(epi);  // [4 or 5][BN]: bias, fold_u, res_gamma, res_beta, y_gamma
   float2* mrg = reinterpret_cast<float2*>(epi + lay.mrg_off);  // [2][BM]: (mean, rstd) of x rows, residual rows
   // one thread per row merges the rows' statistics while the others stage
   // their accumulators; the barrier after the staging publishes them
@@ -258,10 +265,17 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
           for (int e = 0; e < EPC; e += 4) {
             const float4 g = *reinterpret_cast<const float4*>(vec + 2 * BN + cl + e);
             const float4 b = *reinterpret_cast<const float4*>(vec + 3 * BN + cl + e);
-            rr[e] = fmaf((rr[e] - st.x) * st.y, g.x, b.x);
-            rr[e + 1] = fmaf((rr[e + 1] - st.x) * st.y, g.y, b.y);
-            rr[e + 2] = fmaf((rr[e + 2] - st.x) * st.y, g.z, b.z);
-            rr[e + 3] = fmaf((rr[e + 3] - st.x) * st.y, g.w, b.w);
+            if constexpr ((LN & kLnResG) != 0) {  // stored gamma * a: rstd * (r - mean * gamma) + beta
+              rr[e] = fmaf(fmaf(-st.x, g.x, rr[e]), st.y, b.x);
+              rr[e + 1] = fmaf(fmaf(-st.x, g.y, rr[e + 1]), st.y, b.y);
+              rr[e + 2] = fmaf(fmaf(-st.x, g.z, rr[e + 2]), st.y, b.z);
+              rr[e + 3] = fmaf(fmaf(-st.x, g.w, rr[e + 3]), st.y, b.w);
+            } else {
+              rr[e] = fmaf((rr[e] - st.x) * st.y, g.x, b.x);
+              rr[e + 1] = fmaf((rr[e + 1] - st.x) * st.y, g.y, b.y);
+              rr[e + 2] = fmaf((rr[e + 2] - st.x) * st.y, g.z, b.z);
+              rr[e + 3] = fmaf((rr[e + 3] - st.x) * st.y, g.w, b.w);
+            }
           }
         }
 #pragma unroll
@@ -273,7 +287,15 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
         // consecutive 16-byte chunks of one row; a group is all in or all out).
         const uint4 w = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                                    pack_bf16x2(v[6], v[7]));
-        *reinterpret_cast<uint4*>(y + (size_t)m * N + n) = w;
+        if constexpr ((LN & kLnOutG) != 0) {  // stored: gamma * y, each rounded once
+          const float4 g0 = *reinterpret_cast<const float4*>(vec + 4 * BN + cl);
+          const float4 g1 = *reinterpret_cast<const float4*>(vec + 4 * BN + cl + 4);
+          *reinterpret_cast<uint4*>(y + (size_t)m * N + n) =
+              make_uint4(pack_bf16x2(g0.x * v[0], g0.y * v[1]), pack_bf16x2(g0.z * v[2], g0.w * v[3]),
+                         pack_bf16x2(g1.x * v[4], g1.y * v[5]), pack_bf16x2(g1.z * v[6], g1.w * v[7]));
+        } else {
+          *reinterpret_cast<uint4*>(y + (size_t)m * N + n) = w;
+        }
         const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
         float f[8], sum = 0.0f;
 #pragma unroll
@@ -317,8 +339,10 @@ __device__ __forceinline__ void issue_epilogue_operands(const GemmParams& p, int
       const int v = o / (BN * 4), c = (o % (BN * 4)) / 4;
       const float* vp = v == 0 ? (E != Epi::None ? p.bias : nullptr)
                                : v == 1 ? ((LN & kLnX) ? p.fold_u : nullptr)
-                                        : v == 2 ? ((LN & kLnRes) ? p.res_gamma : nullptr)
-                                                 : ((LN & kLnRes) ? p.res_beta : nullptr);
+                               : v == 2 ? ((LN & kLnRes) ? p.res_gamma : nullptr)
+                               : v == 3 ? ((LN & kLnRes) ? p.res_beta : nullptr)
+                               : v == 4 ? ((LN & kLnOutG) ? p.y_gamma : nullptr)
+                                        : nullptr;  // (the padding of the vector region)
       if (vp) src = reinterpret_cast<const uint8_t*>(vp + n0 + c);
     } else if (o < lay.xst_off) {
       // (an f32 residual is read by the epilogue itself)

@@ -34,26 +34,40 @@ struct GemmParams {
   int tile;              // 0: choose automatically; otherwise a GemmTile value (tuning)
   int x_head_rows;       // 0: x is row-major [M,K]; > 0: x is head-major [K/32][x_head_rows][32]
                          // (dense bf16 only), as written by the fused attention
-  // Deferred LayerNorm (dense bf16 only).  A post-LN activation can travel as
-  // its pre-norm rows a plus, per row and per 64 columns, the mean and the
+  // Deferred LayerNorm (bf16 activations).  A post-LN activation can travel
+  // as its pre-norm rows a plus, per row and per 64 columns, the mean and the
   // centred sum of squares of the stored values (float2 [rows][cols/64],
-  // "partial statistics"); whoever reads it applies the norm.
-  //  x_stats: x is such an activation and W holds gamma-scaled weights:
-  //           y = rstd[m] * (acc - mean[m] * fold_u[n]) + bias[n], then the epilogue
+  // "partial statistics"); whoever reads it applies the norm.  Dense weights
+  // take gamma folded into W; quantised weights cannot, so their activation
+  // travels gamma-scaled (gamma[k] * a[k]) instead.
+  //  x_stats: x is such an activation and the product carries gamma (in W or in x):
+  //           y = rstd[m] * (acc - mean[m] * fold_u[n]) + bias[n], then the epilogue,
+  //           fold_u[n] = sum_k gamma_k W_nk
   //  res_stats: the residual is such an activation:
   //           residual[m,n] = (a[m,n] - mean[m]) * rstd[m] * res_gamma[n] + res_beta[n]
+  //           (res_scaled: stored as gamma * a, so rstd[m] * (r - mean[m] * res_gamma[n]) + res_beta[n])
   //  y_stats: also write the partial statistics of the stored y
+  //           (y_gamma: store y_gamma[n] * y; the statistics stay those of y)
   const float2* x_stats;
   const float* fold_u;
   const float2* res_stats;
   const float* res_gamma;
   const float* res_beta;
   float2* y_stats;
+  const float* y_gamma;
+  bool res_scaled;
   float ln_eps;
   bool y_f32;            // bf16 x with an f32 output (and residual); not with the deferred-LayerNorm fields
 };
 // True when the deferred-LayerNorm fields are implemented for rows of H columns.
 bool gemm_deferred_ln_supported(DType dt, Quant q, int H);
+// Deferred LayerNorm with quantised weights: per row n of the effective
+// weights W (the values the matrix cores multiply: q * s for int8 per
+// channel, the bf16 rounding of the scheme's dequantisation otherwise),
+// u[n] = sum_k gamma_k W_nk and v[n] = bias[n] + sum_k beta_k W_nk.
+hipError_t launch_fold_ln_quant(const void* w, Quant q, const void* scales, const void* zeros, int N, int K,
+                                const float* gamma, const float* beta, const float* bias, float* u_out, float* v_out,
+                                hipStream_t s);
 enum GemmTile : int { kTileAuto = 0, kTile128x128 = 1, kTile64x128 = 2, kTile64x64 = 3, kTile128x64 = 4 };
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 
@@ -207,10 +221,11 @@ hipError_t launch_layer_norm(const void* a, const float* gamma, const float* bet
 
 // out[b] = normalize(mean over the sequence's compact rows) (f32 [B,H]).
 // With x_stats (bf16), x is a deferred-LayerNorm activation (see GemmParams)
-// and the rows are normalised with gamma, beta and eps first.
+// and the rows are normalised with gamma, beta and eps first; gamma_scaled:
+// the rows are stored gamma-scaled (quantised-weight encoders).
 hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s,
                           const float2* x_stats = nullptr, const float* gamma = nullptr,
-                          const float* beta = nullptr, float eps = 0.0f);
+                          const float* beta = nullptr, float eps = 0.0f, bool gamma_scaled = false);
 
 // out[b,s,:] = x[tok_dst[b*S+s]] or 0 (f32 [B,S,H]).
 hipError_t launch_scatter_hidden(const void* x, int H, const int* tok_dst, int n_tok, float* out, DType dt,

@@ -420,7 +420,7 @@ constexpr int kMaxPoolRows = 512;  // the longest sequence
 template <typename T>
 __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const int* cu, float* out,
                                                        const float2* x_stats, const float* gamma, const float* beta,
-                                                       float eps) {
+                                                       float eps, bool gamma_scaled) {
   constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
   constexpr int kPoolBatch = 16 / CPL;  // rows per wave in flight
   extern __shared__ float part[];  // [16][H]
@@ -452,6 +452,15 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
     for (int r = threadIdx.x; r < L; r += 1024) row_st[r] = row_ln_stats(x_stats + (size_t)(r0 + r) * (H >> 6), H >> 6, eps);
     __syncthreads();
   }
+  // a gamma-scaled row holds gamma * a: (r - mean * gamma) * rstd = gamma * LN's centred, scaled a
+  float gsc[CPL][EPC];
+#pragma unroll
+  for (int i = 0; i < CPL; ++i)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+      const int c = min(lane + 64 * i, nch - 1) * EPC + e;
+      gsc[i][e] = gamma_scaled ? gamma[c] : 1.0f;
+    }
   for (int rb = wave; rb < L; rb += 16 * kPoolBatch) {
     if (rb != wave) load_batch(rb);
 #pragma unroll
@@ -467,7 +476,7 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
           float v[EPC];
           Chunk<T>::from_raw(raw[k][i], v);
 #pragma unroll
-          for (int e = 0; e < EPC; ++e) acc[i][e] += (v[e] - st.x) * st.y;
+          for (int e = 0; e < EPC; ++e) acc[i][e] += fmaf(-st.x, gsc[i][e], v[e]) * st.y;
         }
       }
     }
@@ -488,7 +497,7 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
 #pragma unroll
     for (int w = 0; w < 16; ++w) sum += part[w * H + c];
     mean = sum / denom;
-    if (x_stats) mean = L > 0 ? fmaf(gamma[c], mean, beta[c]) : 0.0f;
+    if (x_stats) mean = L > 0 ? (gamma_scaled ? mean + beta[c] : fmaf(gamma[c], mean, beta[c])) : 0.0f;
   }
   const float ss = wave_sum(mean * mean);
   if (lane == 0) red[wave] = ss;
@@ -580,17 +589,18 @@ hipError_t launch_layer_norm(const void* a, const float* gamma, const float* bet
 }
 
 hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s,
-                          const float2* x_stats, const float* gamma, const float* beta, float eps) {
+                          const float2* x_stats, const float* gamma, const float* beta, float eps, bool gamma_scaled) {
   if (B <= 0) return hipSuccess;
+  if (gamma_scaled && !x_stats) return hipErrorInvalidValue;
   const size_t lds = (size_t)16 * H * sizeof(float);
   if (dt == DType::BF16)
     hipLaunchKernelGGL(pool_l2_kernel<bf16_t>, dim3(B), dim3(1024), lds, s, (const bf16_t*)x, H, cu, out, x_stats,
-                       gamma, beta, eps);
+                       gamma, beta, eps, gamma_scaled);
   else if (x_stats)
     return hipErrorInvalidValue;
   else
     hipLaunchKernelGGL(pool_l2_kernel<float>, dim3(B), dim3(1024), lds, s, (const float*)x, H, cu, out, nullptr,
-                       nullptr, nullptr, 0.0f);
+                       nullptr, nullptr, 0.0f, false);
   return hipGetLastError();
 }
 
