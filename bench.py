@@ -612,7 +612,10 @@ def main():
         "config": {"workload": sp.name, "batch": sp.batch, "seq_len": sp.seq, "layers": sp.layers,
                    "hidden": sp.hidden, "heads": sp.heads, "ffn": sp.ffn, "real_tokens": tokens,
                    "quant": sp.quant, "parallelism": "single GPU", "graph_replay": args.graph,
-                   "persistent_forward": persistent},
+                   "persistent_forward": persistent,
+                   # quantised weights: dequantised to bf16 by the forward's first kernel (large calls)
+                   # or inside the GEMMs
+                   "dequant_prologue": "dequant_weights" in per_fwd_us},
         "mfma_util_pct": round(100 * mfma_util, 2),
         "mfma_util_counter": mfma_counter,
         "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(achieved, 2), "peak": peak,

@@ -291,6 +291,17 @@ typedef struct rlx_encoder rlx_encoder;
  * 1.. with the preceding LayerNorm's gamma folded in, and folded biases from
  * beta, bqkv and b1; later changes to those arrays, the LayerNorm parameters
  * or bqkv/b1 are not seen by the handle.
+ * With quantised weights (bf16 activations) and pooled output, the handle
+ * also holds bf16 copies of every layer's matrices (Section VI's
+ * DequantMatMul, taken once per forward): the first kernel of each forward
+ * dequantises all layers into them, with the gamma fold above, and the rest
+ * of the forward runs the dense bf16 kernels (the folded vectors come from
+ * the codes, scales and LayerNorm parameters at create, so the weights must
+ * keep their values).  RLX_DEQUANT_PROLOGUE_MIN_TOKENS=<n> in the environment at
+ * create makes only calls with B * S >= n take it and the others run the
+ * dequantising GEMMs (n < 0: never); by default every call takes it.
+ * Quantised weights with hidden-state output run the dequantising GEMMs with
+ * LayerNorm kernels.
  * Errors: RLX_ERR_INVALID_ARG (nulls, non-positive sizes, H != heads*head_dim),
  * RLX_ERR_UNSUPPORTED (head_dim != 32, H or F not a multiple of 64,
  * max_seq > 512 or > max_pos, quantised weights with f32 activations,

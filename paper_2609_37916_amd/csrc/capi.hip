@@ -136,12 +136,12 @@ namespace {
 
 enum KernelClass {
   K_MASK_SCAN = 0, K_EMBED_LN, K_GATHER_ROWS, K_GEMM_QKV, K_ATTENTION, K_GEMM_ATTN_OUT, K_LN1, K_GEMM_FFN_UP,
-  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_PIPE, K_NUM_CLASSES
+  K_GEMM_FFN_DOWN, K_LN2, K_POOL, K_SCATTER, K_QKV_ATTENTION, K_PIPE, K_DEQUANT, K_NUM_CLASSES
 };
 const char* kClassNames[K_NUM_CLASSES] = {"mask_scan",     "embed_ln",    "gather_rows", "gemm_qkv",
                                           "attention",     "gemm_attn_out", "layer_norm_1", "gemm_ffn_up",
                                           "gemm_ffn_down", "layer_norm_2", "pool_l2",     "scatter_hidden",
-                                          "qkv_attention", "encoder_pipe"};
+                                          "qkv_attention", "encoder_pipe", "dequant_weights"};
 
 struct GraphEntry {
   int B, S;
@@ -193,6 +193,18 @@ struct rlx_encoder {
   };
   std::vector<Folded> folded;
   void* fold_mem = nullptr;
+  // Quantised weights, calls of at least dq_min_tokens = B*S positions: one
+  // kernel at the start of the forward dequantises every layer to bf16
+  // (gamma folded in where the dense deferred LayerNorm wants it) and the
+  // forward runs the bf16 kernels on them (dq_cfg, dq_layers, dq_folded).
+  // Smaller calls run the dequantising GEMMs.
+  int dq_min_tokens = -1;  // < 0: never
+  void* dq_mem = nullptr;  // bf16 weights, folded vectors, then the job table
+  const DequantJob* dq_jobs = nullptr;
+  int dq_njobs = 0, dq_max_elems = 0;
+  rlx_encoder_config dq_cfg{};
+  std::vector<rlx_layer_weights> dq_layers;
+  std::vector<Folded> dq_folded;
   // Persistent forward (pipe.hip): chosen at create for the shapes it
   // supports; its per-layer pointer table and per-XCD sync words live in
   // pipe_mem.
@@ -238,12 +250,19 @@ struct FwdCtx {
   int pipe_grid;
   const PipeLayer* pipe_layers;
   int* pipe_sync;
+  // the weight dequantisation that starts the forward (dq_njobs == 0: none)
+  const DequantJob* dq_jobs;
+  int dq_njobs, dq_max_elems;
 };
 
-FwdCtx ctx_of(const rlx_encoder* e) {
-  return FwdCtx{&e->cfg, &e->w, e->layers.data(), e->dt, e->cu, e->tok_src, e->tok_dst, e->order,
-                e->X, e->X1, e->A, e->CTX, e->QKV, e->G, e->deferred, e->S1, e->S2, e->folded.data(),
-                e->pipe ? e->pipe_grid : 0, e->pipe_layers, e->pipe_sync};
+// The forward of B sequences of S positions: with the dequantisation prologue
+// when the handle has one and the call is large enough (cfg then says dense).
+FwdCtx ctx_of(const rlx_encoder* e, int B, int S) {
+  const bool dq = e->dq_mem && e->dq_min_tokens >= 0 && (long long)B * S >= e->dq_min_tokens;
+  return FwdCtx{dq ? &e->dq_cfg : &e->cfg, &e->w, dq ? e->dq_layers.data() : e->layers.data(), e->dt, e->cu,
+                e->tok_src, e->tok_dst, e->order, e->X, e->X1, e->A, e->CTX, e->QKV, e->G, e->deferred, e->S1,
+                e->S2, dq ? e->dq_folded.data() : e->folded.data(), e->pipe ? e->pipe_grid : 0, e->pipe_layers,
+                e->pipe_sync, dq ? e->dq_jobs : nullptr, dq ? e->dq_njobs : 0, dq ? e->dq_max_elems : 0};
 }
 
 // Workspace layout for max_batch sequences of max_seq tokens (256-byte aligned regions).
@@ -362,6 +381,8 @@ rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* m
     if (slots) slots->push_back({cls, [=](hipStream_t ss) -> hipError_t { return (expr); }}); \
   } while (0)
 
+  if (E.dq_njobs > 0)  // quantised weights of every layer to bf16 (the rest of the forward is dense)
+    STEP(K_DEQUANT, launch_dequant_jobs(E.dq_jobs, E.dq_njobs, E.dq_max_elems, ss));
   if (E.pipe_grid > 0 && pipe_supported(PipeShape{B, S, H, F, c.heads, c.layers})) {
     // the whole forward in one persistent launch (pipe.hip)
     PipeParams pp{};
@@ -527,7 +548,7 @@ void clear_profile(rlx_encoder* e) {
 rlx_status capture_forward(rlx_encoder* e, const void* input, const uint8_t* mask, int B, int S, void* output,
                            std::vector<KernelSlot>* slots, hipGraphExec_t* exec) {
   RLX_HIP(hipStreamBeginCapture(e->cap_stream, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
-  rlx_status st = enqueue_forward(ctx_of(e), input, mask, B, S, output, e->cap_stream, slots);
+  rlx_status st = enqueue_forward(ctx_of(e, B, S), input, mask, B, S, output, e->cap_stream, slots);
   hipGraph_t graph = nullptr;
   hipError_t he = hipStreamEndCapture(e->cap_stream, &graph);
   if (st != RLX_OK) {
@@ -571,7 +592,7 @@ rlx_status profiled_forward(rlx_encoder* e, const void* input, const uint8_t* ma
     // record the launches of one forward (also a real forward on the capture stream)
     std::vector<KernelSlot> slots;
     RLX_HIP(hipStreamSynchronize(s), "hipStreamSynchronize");
-    st = enqueue_forward(ctx_of(e), input, mask, B, S, output, e->cap_stream, &slots);
+    st = enqueue_forward(ctx_of(e, B, S), input, mask, B, S, output, e->cap_stream, &slots);
     if (st != RLX_OK) return st;
     RLX_HIP(hipStreamSynchronize(e->cap_stream), "hipStreamSynchronize");
     ProfGraph pg;
@@ -674,7 +695,7 @@ rlx_status fold_layer_norms(rlx_encoder* e) {
       f.vq = reinterpret_cast<float*>(base + offs[l].vq);
       if (quant) {
         RLX_HIP(launch_fold_ln_quant(L.wqkv, q, L.wqkv_scales, L.wqkv_zeros, 3 * c.hidden, c.hidden, P.ln2_gamma,
-                                     P.ln2_beta, L.bqkv, f.uq, f.vq, e->cap_stream),
+                                     P.ln2_beta, L.bqkv, false, f.uq, f.vq, e->cap_stream),
                 "encoder_create: fold LN2 into the QKV vectors");
       } else {
         f.wqkv = base + offs[l].wqkv;
@@ -687,7 +708,7 @@ rlx_status fold_layer_norms(rlx_encoder* e) {
     f.v1 = reinterpret_cast<float*>(base + offs[l].v1);
     if (quant) {
       RLX_HIP(launch_fold_ln_quant(L.w1, q, L.w1_scales, L.w1_zeros, c.ffn, c.hidden, L.ln1_gamma, L.ln1_beta, L.b1,
-                                   f.u1, f.v1, e->cap_stream),
+                                   false, f.u1, f.v1, e->cap_stream),
               "encoder_create: fold LN1 into the FFN-up vectors");
     } else {
       f.w1 = base + offs[l].w1;
@@ -697,6 +718,94 @@ rlx_status fold_layer_norms(rlx_encoder* e) {
     }
   }
   RLX_HIP(hipStreamSynchronize(e->cap_stream), "encoder_create: fold LayerNorms");
+  return RLX_OK;
+}
+
+// Dequantisation prologue for a handle with quantised weights and the
+// deferred LayerNorm: bf16 copies of every layer's matrices (refreshed by the
+// first kernel of each large forward), with LN2 of layer l-1 folded into the
+// QKV weights of layer l and LN1 into W1 as the dense path has them, their
+// u / v vectors (over the same bf16(gamma * d) values), and the job table.
+// RLX_DEQUANT_PROLOGUE_MIN_TOKENS overrides the size (B*S) from which a
+// forward takes it; a negative value turns it off.  Measured on MiniLM-L6
+// (per forward, dequantising GEMMs -> prologue): b1 int8 0.258 -> 0.197 ms,
+// int4 0.356 -> 0.198; b4 0.281 -> 0.215, 0.375 -> 0.216; b32 0.331 -> 0.237,
+// 0.437 -> 0.237.  The bf16 weights are converted once per forward instead of
+// once per tile and wave that reads them, and the forward keeps the fused
+// attention; so every size takes it.
+constexpr int kDequantPrologueMinTokens = 0;
+
+rlx_status setup_dequant_prologue(rlx_encoder* e) {
+  const rlx_encoder_config& c = e->cfg;
+  if (c.quant == RLX_Q_NONE || !e->deferred) return RLX_OK;
+  int min_tokens = kDequantPrologueMinTokens;
+  if (const char* env = std::getenv("RLX_DEQUANT_PROLOGUE_MIN_TOKENS")) min_tokens = std::atoi(env);
+  if (min_tokens < 0) return RLX_OK;
+  const size_t H = c.hidden, F = c.ffn, L = c.layers;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+  struct Offs { size_t wqkv, wo, w1, w2, uq, vq, u1, v1; };
+  std::vector<Offs> offs(L);
+  for (size_t l = 0; l < L; ++l) {
+    offs[l].wqkv = take(3 * H * H * 2);
+    offs[l].wo = take(H * H * 2);
+    offs[l].w1 = take(F * H * 2);
+    offs[l].w2 = take(H * F * 2);
+    offs[l].uq = take(3 * H * sizeof(float));
+    offs[l].vq = take(3 * H * sizeof(float));
+    offs[l].u1 = take(F * sizeof(float));
+    offs[l].v1 = take(F * sizeof(float));
+  }
+  const size_t jobs_off = take(4 * L * sizeof(DequantJob));
+  RLX_HIP(hipMalloc(&e->dq_mem, off), "encoder_create: bf16 weight copies");
+  uint8_t* base = static_cast<uint8_t*>(e->dq_mem);
+  const Quant q = to_quant(c.quant);
+  std::vector<DequantJob> jobs;
+  e->dq_layers = e->layers;
+  e->dq_folded.assign(L, rlx_encoder::Folded{});
+  int max_elems = 0;
+  auto job = [&](const void* w, const void* sc, const void* z, const float* gamma, void* out, int N, int K) {
+    jobs.push_back(DequantJob{w, sc, z, gamma, out, N, K, q});
+    max_elems = std::max(max_elems, N * K);
+  };
+  for (size_t l = 0; l < L; ++l) {
+    const rlx_layer_weights& W = e->layers[l];
+    rlx_layer_weights& D = e->dq_layers[l];
+    rlx_encoder::Folded& f = e->dq_folded[l];
+    void* wqkv = base + offs[l].wqkv;
+    job(W.wqkv, W.wqkv_scales, W.wqkv_zeros, l > 0 ? e->layers[l - 1].ln2_gamma : nullptr, wqkv, 3 * H, H);
+    job(W.wo, W.wo_scales, W.wo_zeros, nullptr, base + offs[l].wo, H, H);
+    job(W.w1, W.w1_scales, W.w1_zeros, W.ln1_gamma, base + offs[l].w1, F, H);
+    job(W.w2, W.w2_scales, W.w2_zeros, nullptr, base + offs[l].w2, H, F);
+    D.wqkv = wqkv; D.wo = base + offs[l].wo; D.w1 = base + offs[l].w1; D.w2 = base + offs[l].w2;
+    D.wqkv_scales = D.wqkv_zeros = D.wo_scales = D.wo_zeros = nullptr;
+    D.w1_scales = D.w1_zeros = D.w2_scales = D.w2_zeros = nullptr;
+    f.w1 = base + offs[l].w1;
+    f.u1 = reinterpret_cast<float*>(base + offs[l].u1);
+    f.v1 = reinterpret_cast<float*>(base + offs[l].v1);
+    RLX_HIP(launch_fold_ln_quant(W.w1, q, W.w1_scales, W.w1_zeros, c.ffn, c.hidden, W.ln1_gamma, W.ln1_beta, W.b1, true,
+                                 f.u1, f.v1, e->cap_stream),
+            "encoder_create: fold LN1 (bf16 copies)");
+    if (l > 0) {
+      const rlx_layer_weights& P = e->layers[l - 1];
+      f.wqkv = wqkv;
+      f.uq = reinterpret_cast<float*>(base + offs[l].uq);
+      f.vq = reinterpret_cast<float*>(base + offs[l].vq);
+      RLX_HIP(launch_fold_ln_quant(W.wqkv, q, W.wqkv_scales, W.wqkv_zeros, 3 * c.hidden, c.hidden, P.ln2_gamma,
+                                   P.ln2_beta, W.bqkv, true, f.uq, f.vq, e->cap_stream),
+              "encoder_create: fold LN2 (bf16 copies)");
+    }
+  }
+  RLX_HIP(hipMemcpyAsync(base + jobs_off, jobs.data(), jobs.size() * sizeof(DequantJob), hipMemcpyHostToDevice,
+                         e->cap_stream),
+          "encoder_create: dequantisation jobs");
+  RLX_HIP(hipStreamSynchronize(e->cap_stream), "encoder_create: dequantisation setup");
+  e->dq_jobs = reinterpret_cast<const DequantJob*>(base + jobs_off);
+  e->dq_njobs = (int)jobs.size();
+  e->dq_max_elems = max_elems;
+  e->dq_cfg = c;
+  e->dq_cfg.quant = RLX_Q_NONE;
+  e->dq_min_tokens = min_tokens;
   return RLX_OK;
 }
 
@@ -946,6 +1055,7 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
   }
   if (e->deferred) {
     st = fold_layer_norms(e);
+    if (st == RLX_OK) st = setup_dequant_prologue(e);
     if (st == RLX_OK) st = setup_pipeline(e);
     if (st != RLX_OK) {
       rlx_encoder_destroy(e);
@@ -975,7 +1085,7 @@ rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t*
   if (e->profiling)
     st = profiled_forward(e, input, attention_mask, B, S, output, s);
   else if (!e->cfg.use_graph)
-    st = enqueue_forward(ctx_of(e), input, attention_mask, B, S, output, s, nullptr);
+    st = enqueue_forward(ctx_of(e, B, S), input, attention_mask, B, S, output, s, nullptr);
   else
     st = run_graph_forward(e, input, attention_mask, B, S, output, s);
   if (st != RLX_OK) return st;
@@ -1035,6 +1145,7 @@ void rlx_encoder_destroy(rlx_encoder* e) {
   if (e->cap_stream) (void)hipStreamDestroy(e->cap_stream);
   if (e->ws) (void)hipFree(e->ws);
   if (e->fold_mem) (void)hipFree(e->fold_mem);
+  if (e->dq_mem) (void)hipFree(e->dq_mem);
   if (e->pipe_mem) (void)hipFree(e->pipe_mem);
   delete e;
 }

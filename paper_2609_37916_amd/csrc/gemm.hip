@@ -821,33 +821,51 @@ __global__ __launch_bounds__(256) void fold_ln_weights_kernel(const bf16_t* w, i
   }
 }
 
-// Effective weight of row n, column k of quantised weights: the value the
-// matrix cores multiply (q * s for int8 per channel, whose scale multiplies
-// the fp32 sum; otherwise the bf16 rounding of the same fp32 arithmetic as
-// the GEMM's code conversions).
-__device__ __forceinline__ float effective_weight(const uint8_t* w, Quant q, const uint16_t* scales,
-                                                  const uint16_t* zeros, int n, int k, int K) {
+// The fp32 dequantisation of row n, column k of quantised weights, with the
+// same arithmetic as the GEMM's code conversions before their bf16 rounding:
+// q * s (int8, per channel or per group), fma(q, s, -z s) = (q - z) s rounded
+// once (int4 with zero points), fma(q, s, m) (int4 with mins).
+__device__ __forceinline__ float deq32(const uint8_t* w, Quant q, const uint16_t* scales, const uint16_t* zeros,
+                                       int n, int k, int K) {
   const int gi = n * (K / 32) + k / 32;
   if (q == Quant::Int8) return (float)(int8_t)w[(size_t)n * K + k] * f16_bits_to_f32(scales[n]);
-  if (q == Quant::Int8G) return bf16_to_f32(f32_to_bf16((float)(int8_t)w[(size_t)n * K + k] * f16_bits_to_f32(scales[gi])));
+  if (q == Quant::Int8G) return (float)(int8_t)w[(size_t)n * K + k] * f16_bits_to_f32(scales[gi]);
   const uint32_t byte = w[(size_t)n * (K / 2) + k / 2];
   const float c = (float)((k & 1) ? byte >> 4 : byte & 0xfu);
   const float sc = f16_bits_to_f32(scales[gi]), z = f16_bits_to_f32(zeros[gi]);
-  return bf16_to_f32(f32_to_bf16(q == Quant::Int4 ? (c - z) * sc : fmaf(c, sc, z)));
+  return q == Quant::Int4 ? fmaf(c, sc, -z * sc) : fmaf(c, sc, z);
 }
 
-// One block per weight row n (256 threads over k): u[n] = sum_k gamma_k W_nk,
-// v[n] = bias[n] + sum_k beta_k W_nk over the effective weights.
+// Effective weight in the dequantising GEMMs: the value the matrix cores
+// multiply (q * s for int8 per channel, whose scale multiplies the fp32 sum;
+// the bf16 rounding of the dequantisation otherwise).
+__device__ __forceinline__ float effective_weight(const uint8_t* w, Quant q, const uint16_t* scales,
+                                                  const uint16_t* zeros, int n, int k, int K) {
+  const float d = deq32(w, q, scales, zeros, n, k, K);
+  return q == Quant::Int8 ? d : bf16_to_f32(f32_to_bf16(d));
+}
+
+// One block per weight row n (256 threads over k).  dense_fold = false (the
+// dequantising GEMMs, gamma-scaled inputs): u[n] = sum_k gamma_k W_nk over the
+// effective weights.  dense_fold = true (weights dequantised to bf16 with gamma
+// folded in, W'_nk = bf16(gamma_k * deq32)): u[n] = sum_k W'_nk.  Both:
+// v[n] = bias[n] + sum_k beta_k W_nk.
 __global__ __launch_bounds__(256) void fold_ln_quant_kernel(const uint8_t* w, Quant q, const uint16_t* scales,
                                                              const uint16_t* zeros, int K, const float* gamma,
-                                                             const float* beta, const float* bias, float* u_out,
-                                                             float* v_out) {
+                                                             const float* beta, const float* bias, bool dense_fold,
+                                                             float* u_out, float* v_out) {
   const int n = blockIdx.x, tid = threadIdx.x;
   double u = 0.0, v = 0.0;
   for (int k = tid; k < K; k += 256) {
-    const double wk = effective_weight(w, q, scales, zeros, n, k, K);
-    u += (double)gamma[k] * wk;
-    v += (double)beta[k] * wk;
+    if (dense_fold) {
+      const float d = deq32(w, q, scales, zeros, n, k, K);
+      u += (double)bf16_to_f32(f32_to_bf16(gamma[k] * d));
+      v += (double)beta[k] * (double)d;
+    } else {
+      const double wk = effective_weight(w, q, scales, zeros, n, k, K);
+      u += (double)gamma[k] * wk;
+      v += (double)beta[k] * wk;
+    }
   }
   __shared__ double red[2][4];
 #pragma unroll
@@ -866,6 +884,49 @@ __global__ __launch_bounds__(256) void fold_ln_quant_kernel(const uint8_t* w, Qu
   }
 }
 
+// Weights of every layer to bf16 in one launch: job blockIdx.y, 16
+// consecutive elements of a row per thread (a whole half group of 32), the
+// same fp32 dequantisation as deq32, then bf16(gamma_k * d) for a job with a
+// LayerNorm gamma to fold, else bf16(d).
+__global__ __launch_bounds__(256) void dequant_jobs_kernel(const DequantJob* jobs) {
+  const DequantJob& j = jobs[blockIdx.y];
+  const int K = j.K;
+  const int64_t e0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 16;
+  if (e0 >= (int64_t)j.N * K) return;
+  const int n = (int)(e0 / K), k = (int)(e0 % K);
+  const Quant q = j.quant;
+  const uint16_t* sc = reinterpret_cast<const uint16_t*>(j.scales);
+  float d[16];
+  if (q == Quant::Int8 || q == Quant::Int8G) {
+    const uint4 c = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(j.w) + (size_t)n * K + k);
+    const float s = f16_bits_to_f32(q == Quant::Int8 ? sc[n] : sc[n * (K / 32) + k / 32]);
+    const uint32_t cw[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) d[i] = (float)(int8_t)((cw[i >> 2] >> (8 * (i & 3))) & 0xffu) * s;
+  } else {
+    const uint2 c = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint8_t*>(j.w) + (size_t)n * (K / 2) + k / 2);
+    const int gi = n * (K / 32) + k / 32;
+    const float s = f16_bits_to_f32(sc[gi]), z = f16_bits_to_f32(reinterpret_cast<const uint16_t*>(j.zeros)[gi]);
+    const float zs = q == Quant::Int4 ? -z * s : z;
+    const uint32_t cw[2] = {c.x, c.y};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint32_t byte = (cw[i >> 3] >> (8 * ((i >> 1) & 3))) & 0xffu;
+      d[i] = fmaf((float)((i & 1) ? byte >> 4 : byte & 0xfu), s, zs);
+    }
+  }
+  if (j.gamma) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) d[i] *= j.gamma[k + i];
+  }
+  uint32_t o[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = pack_bf16x2(d[2 * i], d[2 * i + 1]);
+  uint4* dst = reinterpret_cast<uint4*>(reinterpret_cast<bf16_t*>(j.out) + e0);
+  dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+  dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+}
+
 }  // namespace
 
 hipError_t launch_fold_ln_weights(const void* w, int N, int K, const float* gamma, const float* beta,
@@ -877,13 +938,19 @@ hipError_t launch_fold_ln_weights(const void* w, int N, int K, const float* gamm
 }
 
 hipError_t launch_fold_ln_quant(const void* w, Quant q, const void* scales, const void* zeros, int N, int K,
-                                const float* gamma, const float* beta, const float* bias, float* u_out, float* v_out,
-                                hipStream_t s) {
+                                const float* gamma, const float* beta, const float* bias, bool dense_fold,
+                                float* u_out, float* v_out, hipStream_t s) {
   if (N <= 0) return hipSuccess;
   if (!dma_quant_ok(q) || q == Quant::None || K % 32 != 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(fold_ln_quant_kernel, dim3(N), dim3(256), 0, s, reinterpret_cast<const uint8_t*>(w), q,
                      reinterpret_cast<const uint16_t*>(scales), reinterpret_cast<const uint16_t*>(zeros), K, gamma,
-                     beta, bias, u_out, v_out);
+                     beta, bias, dense_fold, u_out, v_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_dequant_jobs(const DequantJob* jobs, int njobs, int max_elems, hipStream_t s) {
+  if (njobs <= 0 || max_elems <= 0) return hipSuccess;
+  hipLaunchKernelGGL(dequant_jobs_kernel, dim3((max_elems + 4095) / 4096, njobs), dim3(256), 0, s, jobs);
   return hipGetLastError();
 }
 

@@ -61,13 +61,30 @@ struct GemmParams {
 };
 // True when the deferred-LayerNorm fields are implemented for rows of H columns.
 bool gemm_deferred_ln_supported(DType dt, Quant q, int H);
-// Deferred LayerNorm with quantised weights: per row n of the effective
-// weights W (the values the matrix cores multiply: q * s for int8 per
-// channel, the bf16 rounding of the scheme's dequantisation otherwise),
-// u[n] = sum_k gamma_k W_nk and v[n] = bias[n] + sum_k beta_k W_nk.
+// Deferred LayerNorm with quantised weights, per row n:
+//  dense_fold = false (dequantising GEMMs, gamma-scaled inputs): over the
+//    effective weights W (the values the matrix cores multiply: q * s for int8
+//    per channel, the bf16 rounding of the scheme's dequantisation otherwise)
+//    u[n] = sum_k gamma_k W_nk;
+//  dense_fold = true (weights dequantised to bf16 with gamma folded in,
+//    W'_nk = bf16(gamma_k * d_nk), d the fp32 dequantisation): u[n] = sum_k W'_nk;
+//  both: v[n] = bias[n] + sum_k beta_k W_nk.
 hipError_t launch_fold_ln_quant(const void* w, Quant q, const void* scales, const void* zeros, int N, int K,
-                                const float* gamma, const float* beta, const float* bias, float* u_out, float* v_out,
-                                hipStream_t s);
+                                const float* gamma, const float* beta, const float* bias, bool dense_fold,
+                                float* u_out, float* v_out, hipStream_t s);
+
+// One matrix for launch_dequant_jobs: quantised weights [N,K] (K a multiple
+// of 32) to bf16 [N,K] at `out`, each element bf16(gamma[k] * d) when gamma
+// is given, else bf16(d), d the fp32 dequantisation (as the GEMM's code
+// conversions compute it).
+struct DequantJob {
+  const void* w; const void* scales; const void* zeros; const float* gamma;
+  void* out;
+  int N, K;
+  Quant quant;
+};
+// Every job of the device array `jobs` in one launch; max_elems bounds N*K.
+hipError_t launch_dequant_jobs(const DequantJob* jobs, int njobs, int max_elems, hipStream_t s);
 enum GemmTile : int { kTileAuto = 0, kTile128x128 = 1, kTile64x128 = 2, kTile64x64 = 3, kTile128x64 = 4 };
 hipError_t launch_gemm(const GemmParams& p, hipStream_t s);
 

@@ -8,6 +8,9 @@ Tolerances (max-abs on the final output): fp32 1e-4, bf16 2e-2, int8/int4
 largest sweep batches the oracle is run on a sample of sequences (they are
 independent), at the full launch configuration on the GPU.
 """
+import contextlib
+import os
+
 import numpy as np
 import pytest
 
@@ -86,11 +89,42 @@ def test_encoder_parity_affine(rlx, name):
     _compare(_run(rlx, wl), oracle.encoder_forward(wl), wl, _tol(wl.spec), name + " affine")
 
 
+@contextlib.contextmanager
+def _dequant_mode(mode):
+    """Which quantised path an encoder created inside takes: "prologue" (every
+    layer dequantised to bf16 by the first kernel of the forward, then the
+    bf16 kernels) or "in_gemm" (the dequantising GEMMs)."""
+    old = os.environ.get("RLX_DEQUANT_PROLOGUE_MIN_TOKENS")
+    os.environ["RLX_DEQUANT_PROLOGUE_MIN_TOKENS"] = "0" if mode == "prologue" else "-1"
+    try:
+        yield
+    finally:
+        if old is None:
+            del os.environ["RLX_DEQUANT_PROLOGUE_MIN_TOKENS"]
+        else:
+            os.environ["RLX_DEQUANT_PROLOGUE_MIN_TOKENS"] = old
+
+
+@pytest.mark.parametrize("mode", ["prologue", "in_gemm"])
 @pytest.mark.parametrize("quant", ["int8", "int4"])
-def test_encoder_parity_quant_affine(rlx, quant):
+def test_encoder_parity_quant_affine(rlx, quant, mode):
     sp = workloads.spec(f"minilm_b32_s128_{quant}", batch=6)
     wl = workloads.make(sp, affine=True)
-    _compare(_run(rlx, wl), oracle.encoder_forward(wl), wl, _tol(sp), sp.name + " affine")
+    with _dequant_mode(mode):
+        got = _run(rlx, wl)
+    _compare(got, oracle.encoder_forward(wl), wl, _tol(sp), f"{sp.name} affine, {mode}")
+
+
+@pytest.mark.parametrize("mode", ["prologue", "in_gemm"])
+@pytest.mark.parametrize("quant,batch", [("int8", 1), ("int4", 1), ("int8", 4), ("int4", 4)])
+def test_encoder_parity_quant_small_batch(rlx, quant, batch, mode):
+    """Batches 1 and 4 of the quantised encoder (lengths U[8, 128]) on both
+    paths, with affine LayerNorms and biases."""
+    sp = workloads.spec(f"minilm_b32_s128_{quant}", batch=batch, len_lo=8, len_hi=128)
+    wl = workloads.make(sp, affine=True)
+    with _dequant_mode(mode):
+        got = _run(rlx, wl)
+    _compare(got, oracle.encoder_forward(wl), wl, _tol(sp), f"{sp.name} b{batch}, {mode}")
 
 
 def test_encoder_mask_with_holes_and_empty_row(rlx):

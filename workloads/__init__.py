@@ -95,6 +95,10 @@ def _registry() -> Dict[str, Spec]:
     for q in ("int8", "int4"):
         n = f"minilm_b32_s128_{q}"
         r[n] = Spec(n, 32, 128, LAYERS, "bf16", "ids", "pooled", 16, 128, seed=5, quant=q)
+        # the small-batch regime of the quantised encoder (lengths as the batch sweep)
+        for b in (1, 4):
+            n = f"minilm_b{b}_s128_{q}"
+            r[n] = Spec(n, b, 128, LAYERS, "bf16", "ids", "pooled", 8, 128, seed=3000 + b, quant=q)
     return r
 
 
