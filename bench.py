@@ -161,8 +161,16 @@ def gpu_state():
     exe = shutil.which("rocm-smi") or ("/opt/rocm/bin/rocm-smi" if os.path.exists("/opt/rocm/bin/rocm-smi") else None)
     if exe is None:
         return None
+    # Under a profiler its preloaded library would follow the child (and
+    # initialise the GPU there); not needed for a profile.
+    if "rocprof" in os.environ.get("LD_PRELOAD", ""):
+        return {"skipped": "run under a profiler"}
     try:
-        r = subprocess.run([exe, "--showclocks", "--showtemp", "--json"], capture_output=True, text=True, timeout=30)
+        # a Python script runs under this interpreter directly: no '/usr/bin/env python3' hop
+        with open(exe, "rb") as fh:
+            first = fh.readline()
+        cmd = [sys.executable, exe] if first.startswith(b"#!") and b"python" in first else [exe]
+        r = subprocess.run(cmd + ["--showclocks", "--showtemp", "--json"], capture_output=True, text=True, timeout=30)
         card = next(iter(json.loads(r.stdout[r.stdout.index("{"):]).values()))
     except Exception:
         return None

@@ -249,8 +249,9 @@ typedef struct {
   int max_batch;     /* <= 8192; workspace is planned for max_batch * max_seq tokens */
   int max_seq;       /* <= 512                                           */
   int use_graph;     /* 1: record each (B,S,buffers) forward once as a HIP graph and replay it;
-                        0: launch the kernels one by one (measured 1-3% faster for this
-                        forward on MI355X: the launches hide behind the running kernels) */
+                        0: launch the kernels one by one.  On MI355X the two measure within
+                        about 2% of each other for this forward, either one ahead from run
+                        to run (the launches hide behind the running kernels) */
 } rlx_encoder_config;
 
 /* One layer's weights.  Linear weights follow the nn.Linear convention
