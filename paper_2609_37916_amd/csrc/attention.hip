@@ -515,6 +515,9 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
 
 hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s) {
   if (p.B <= 0) return hipSuccess;
+  RLX_LOG_LAUNCH("qkv_attn_bf16_kernel", dim3(((p.B + 7) / 8) * 8 * p.heads), dim3(256), 0,
+                 "fused QKV projection + attention, stages=2 B=%d heads=%d H=%d%s", p.B, p.heads, p.H,
+                 p.x_stats ? " deferred-LN input" : "");
   hipLaunchKernelGGL(qkv_attn_bf16_kernel<2>, dim3(((p.B + 7) / 8) * 8 * p.heads), dim3(256), 0, s, p);
   return hipGetLastError();
 }
@@ -555,9 +558,14 @@ hipError_t launch_attention(const AttnParams& p, hipStream_t s) {
       nfull = (int)std::max<int64_t>(0, 2 * tiles - 2 * (int64_t)cus);
       blocks = 2 * tiles - nfull;
     }
+    RLX_LOG_LAUNCH("attn_bf16_kernel", dim3((unsigned)blocks), dim3(512), lds,
+                   "B=%d S=%d heads=%d kind=%d query tiles=%lld whole blocks=%d%s", p.B, p.S, p.heads, p.kind,
+                   (long long)tiles, nfull < 0 ? (int)tiles : nfull, p.cu_seqlens ? " varlen" : "");
     hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(512), lds, s, p, vt_stride, gx, nfull);
   } else {
     const dim3 grid(gx, p.heads, p.B);
+    RLX_LOG_LAUNCH("attn_f32_kernel", grid, dim3(256), 0, "B=%d S=%d heads=%d kind=%d%s", p.B, p.S, p.heads, p.kind,
+                   p.cu_seqlens ? " varlen" : "");
     hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(256), 0, s, p);
   }
   return hipGetLastError();

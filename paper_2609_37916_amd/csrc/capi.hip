@@ -892,6 +892,27 @@ rlx_status scratch_on_device(int dev, uint8_t** out) {
 
 }  // namespace
 
+bool rlx::g_log_launches = false;
+
+void rlx::log_launch(const char* kernel, dim3 grid, dim3 block, size_t lds, const char* fmt, ...) {
+  char detail[256];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(detail, sizeof(detail), fmt, ap);
+  va_end(ap);
+  std::fprintf(stderr, "[rlx] %s %s grid=(%u,%u,%u) block=%u lds=%zu\n", kernel, detail, grid.x, grid.y, grid.z,
+               block.x, lds);
+}
+
+namespace {
+// Every entry point re-reads RLX_LOG, so a caller can switch the log on or off
+// between calls.
+void log_refresh() {
+  const char* v = std::getenv("RLX_LOG");
+  g_log_launches = v && v[0] == '1';
+}
+}  // namespace
+
 extern "C" {
 
 const char* rlx_last_error(void) { return g_last_error.c_str(); }
@@ -902,6 +923,7 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
                                 int64_t out_row_stride, int B, int S, int num_heads, int head_dim, rlx_dtype dt,
                                 rlx_mask_kind kind, const uint8_t* key_mask, int window, float scale,
                                 void* stream) {
+  log_refresh();
   rlx_status st = check_attention_args(q, k, v, qkv_row_stride, out, out_row_stride, B, S, num_heads, head_dim, dt,
                                        kind, key_mask, window, scale);
   if (st != RLX_OK) return st;
@@ -919,6 +941,7 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
 rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const void* w, rlx_quant scheme,
                               const void* scales, const void* zeros, int group_size, int N, const float* bias,
                               const void* residual, rlx_epilogue epi, void* y, rlx_dtype y_dt, void* stream) {
+  log_refresh();
   if (M < 0 || N <= 0 || K <= 0)
     return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: M=%d must be >= 0, N=%d and K=%d positive", M, N, K);
   if (!x || !y) return fail(RLX_ERR_INVALID_ARG, "dequant_matmul: x and y must be non-null");
@@ -954,6 +977,7 @@ rlx_status rlx_dequant_matmul(const void* x, rlx_dtype x_dt, int M, int K, const
 rlx_status rlx_scaled_matmul(const void* x, const uint8_t* x_scales, rlx_mx_format fx, const void* w,
                              const uint8_t* w_scales, rlx_mx_format fw, int M, int N, int K, float* y,
                              void* stream) {
+  log_refresh();
   if (M < 0 || N <= 0 || K <= 0)
     return fail(RLX_ERR_INVALID_ARG, "scaled_matmul: M=%d must be >= 0, N=%d and K=%d positive", M, N, K);
   if (fx < RLX_MX_E4M3 || fx > RLX_MX_E2M1 || fw < RLX_MX_E4M3 || fw > RLX_MX_E2M1)
@@ -976,6 +1000,7 @@ rlx_status rlx_scaled_matmul(const void* x, const uint8_t* x_scales, rlx_mx_form
 
 rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scales, const void* zeros, int group_size,
                               int N, int K, float* w_out, void* stream) {
+  log_refresh();
   if (N <= 0 || K <= 0) return fail(RLX_ERR_INVALID_ARG, "dequant_unpack: N=%d and K=%d must be positive", N, K);
   if (!w_out) return fail(RLX_ERR_INVALID_ARG, "dequant_unpack: w_out must be non-null");
   if (scheme == RLX_Q_NONE) return fail(RLX_ERR_INVALID_ARG, "dequant_unpack: scheme must be a quantised one");
@@ -988,6 +1013,7 @@ rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scale
 
 rlx_status rlx_gguf_repack(const void* blocks, rlx_gguf_type type, int N, int K, void* codes, void* scales,
                            void* zeros, rlx_quant* scheme, void* stream) {
+  log_refresh();
   if (type != RLX_GGUF_Q4_0 && type != RLX_GGUF_Q4_1 && type != RLX_GGUF_Q8_0)
     return fail(RLX_ERR_UNSUPPORTED, "gguf_repack: tensor type %d not supported (Q4_0 2, Q4_1 3, Q8_0 8)", (int)type);
   if (N < 0 || K <= 0) return fail(RLX_ERR_INVALID_ARG, "gguf_repack: N=%d must be >= 0 and K=%d positive", N, K);
@@ -1006,6 +1032,7 @@ rlx_status rlx_gguf_repack(const void* blocks, rlx_gguf_type type, int N, int K,
 }
 
 rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_weights* w, rlx_encoder** out) {
+  log_refresh();
   if (!cfg || !w || !out) return fail(RLX_ERR_INVALID_ARG, "encoder_create: cfg, weights and out must be non-null");
   *out = nullptr;
   rlx_status st = check_config(cfg);
@@ -1068,6 +1095,7 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
 
 rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t* attention_mask, int B, int S,
                                void* output, void* stream) {
+  log_refresh();
   if (!e) return fail(RLX_ERR_INVALID_ARG, "encoder_forward: null handle");
   if (!input || !attention_mask || !output)
     return fail(RLX_ERR_INVALID_ARG, "encoder_forward: input, attention_mask and output must be non-null");
@@ -1081,6 +1109,13 @@ rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t*
     return fail(RLX_ERR_INVALID_ARG, "encoder_forward: current device %d differs from the handle's device %d", dev,
                 e->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (g_log_launches) {
+    const FwdCtx c = ctx_of(e, B, S);
+    std::fprintf(stderr, "[rlx] encoder_forward B=%d S=%d layers=%d %s%s%s%s\n", B, S, e->cfg.layers,
+                 e->dt == DType::BF16 ? "bf16" : "f32", c.dq_njobs ? ", dequantisation prologue" : "",
+                 c.pipe_grid > 0 ? ", persistent" : "",
+                 e->profiling ? ", profiled" : e->cfg.use_graph ? ", graph (launches below only when recorded)" : "");
+  }
   rlx_status st;
   if (e->profiling)
     st = profiled_forward(e, input, attention_mask, B, S, output, s);
@@ -1096,6 +1131,7 @@ rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t*
 rlx_status rlx_encoder_forward_noalloc(const rlx_encoder_config* cfg, const rlx_encoder_weights* w,
                                        const void* input, const uint8_t* attention_mask, int B, int S, void* output,
                                        void* stream) {
+  log_refresh();
   if (!cfg || !w) return fail(RLX_ERR_INVALID_ARG, "encoder_forward_noalloc: cfg and weights must be non-null");
   rlx_status st = check_config(cfg);
   if (st != RLX_OK) return st;

@@ -6,6 +6,18 @@
 
 namespace rlx {
 
+// Launch log (RLX_LOG=1 in the environment, read again at every C-ABI entry
+// point): each launch prints its kernel with the parameters that chose it,
+// its grid, block and dynamic LDS, to stderr.  Launches recorded into a HIP
+// graph print once, when recorded.
+extern bool g_log_launches;
+void log_launch(const char* kernel, dim3 grid, dim3 block, size_t lds, const char* fmt, ...)
+    __attribute__((format(printf, 5, 6)));
+#define RLX_LOG_LAUNCH(kernel, grid, block, lds, ...)                      \
+  do {                                                                     \
+    if (::rlx::g_log_launches) ::rlx::log_launch(kernel, grid, block, lds, __VA_ARGS__); \
+  } while (0)
+
 typedef uint16_t bf16_t;  // bfloat16 storage (upper half of an IEEE binary32)
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));

@@ -604,6 +604,10 @@ hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
   const dim3 grid((p.N / BN) * ((p.M + BM - 1) / BM));
   const size_t epi = (sizeof(T) == 2 ? (size_t)epi_layout_of<BM, BN, E, LN>(p.K, p.N).bytes : 0) +
                      (size_t)gq_lds_bytes(Q, BN, p.K);
+  RLX_LOG_LAUNCH("gemm_dma_kernel", grid, dim3(kThreads * KS), epi,
+                 "tile=%dx%d stages=%d %s %s ksplit=%d ln=%d epi=%s M=%d%s N=%d K=%d", BM, BN, STAGES,
+                 sizeof(T) == 2 ? "bf16" : "f32", quant_name(Q), KS, LN, epi_name(E), p.M, p.m_dev ? "(device)" : "",
+                 p.N, p.K);
   hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, E, KS, LN, Q>), grid, dim3(kThreads * KS), epi, s, p);
   return hipGetLastError();
 }
@@ -744,6 +748,9 @@ hipError_t launch_dense(const GemmParams& p, hipStream_t s) {
 template <int BM, int BN, typename T, Quant Q>
 hipError_t launch_tile(const GemmParams& p, hipStream_t s) {
   dim3 grid(p.N / BN, (p.M + BM - 1) / BM);
+  RLX_LOG_LAUNCH("gemm_kernel", grid, dim3(kThreads), 0, "tile=%dx%d register-staged %s %s epi=%s M=%d%s N=%d K=%d",
+                 BM, BN, sizeof(T) == 2 ? "bf16" : "f32", quant_name(Q), epi_name(p.epi), p.M,
+                 p.m_dev ? "(device)" : "", p.N, p.K);
   switch (p.epi) {
     case Epi::None: hipLaunchKernelGGL((gemm_kernel<BM, BN, T, Q, Epi::None>), grid, dim3(kThreads), 0, s, p); break;
     case Epi::Bias: hipLaunchKernelGGL((gemm_kernel<BM, BN, T, Q, Epi::Bias>), grid, dim3(kThreads), 0, s, p); break;
@@ -932,6 +939,7 @@ __global__ __launch_bounds__(256) void dequant_jobs_kernel(const DequantJob* job
 hipError_t launch_fold_ln_weights(const void* w, int N, int K, const float* gamma, const float* beta,
                                   const float* bias, void* w_out, float* u_out, float* v_out, hipStream_t s) {
   if (N <= 0) return hipSuccess;
+  RLX_LOG_LAUNCH("fold_ln_weights_kernel", dim3(N), dim3(256), 0, "N=%d K=%d", N, K);
   hipLaunchKernelGGL(fold_ln_weights_kernel, dim3(N), dim3(256), 0, s, reinterpret_cast<const bf16_t*>(w), K, gamma,
                      beta, bias, reinterpret_cast<bf16_t*>(w_out), u_out, v_out);
   return hipGetLastError();
@@ -942,6 +950,8 @@ hipError_t launch_fold_ln_quant(const void* w, Quant q, const void* scales, cons
                                 float* u_out, float* v_out, hipStream_t s) {
   if (N <= 0) return hipSuccess;
   if (!dma_quant_ok(q) || q == Quant::None || K % 32 != 0) return hipErrorInvalidValue;
+  RLX_LOG_LAUNCH("fold_ln_quant_kernel", dim3(N), dim3(256), 0, "%s N=%d K=%d %s", quant_name(q), N, K,
+                 dense_fold ? "bf16 fold" : "gamma-scaled inputs");
   hipLaunchKernelGGL(fold_ln_quant_kernel, dim3(N), dim3(256), 0, s, reinterpret_cast<const uint8_t*>(w), q,
                      reinterpret_cast<const uint16_t*>(scales), reinterpret_cast<const uint16_t*>(zeros), K, gamma,
                      beta, bias, dense_fold, u_out, v_out);
@@ -950,6 +960,8 @@ hipError_t launch_fold_ln_quant(const void* w, Quant q, const void* scales, cons
 
 hipError_t launch_dequant_jobs(const DequantJob* jobs, int njobs, int max_elems, hipStream_t s) {
   if (njobs <= 0 || max_elems <= 0) return hipSuccess;
+  RLX_LOG_LAUNCH("dequant_jobs_kernel", dim3((max_elems + 4095) / 4096, njobs), dim3(256), 0,
+                 "jobs=%d max N*K=%d", njobs, max_elems);
   hipLaunchKernelGGL(dequant_jobs_kernel, dim3((max_elems + 4095) / 4096, njobs), dim3(256), 0, s, jobs);
   return hipGetLastError();
 }
@@ -981,6 +993,7 @@ hipError_t launch_dequant_unpack(const void* w, Quant q, const void* scales, con
                                  float* out, hipStream_t s) {
   const size_t total = (size_t)N * K;
   const int blocks = (int)std::min<size_t>((total + 255) / 256, 4096);
+  RLX_LOG_LAUNCH("dequant_unpack_kernel", dim3(blocks), dim3(256), 0, "%s N=%d K=%d", quant_name(q), N, K);
   hipLaunchKernelGGL(dequant_unpack_kernel, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const uint8_t*>(w), q,
                      reinterpret_cast<const uint16_t*>(scales), reinterpret_cast<const uint16_t*>(zeros), N, K, out);
   return hipGetLastError();

@@ -392,6 +392,8 @@ hipError_t launch_gemv_typed(const GemmParams& p, hipStream_t s) {
   static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(gemv_q_kernel<Q, E>),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
   if (attr != hipSuccess) return attr;
+  RLX_LOG_LAUNCH("gemv_q_kernel", dim3(g.grid), dim3(kGvThreads), g.lds, "few-row %s epi=%s M=%d N=%d K=%d",
+                 quant_name(Q), epi_name(E), p.M, p.N, p.K);
   hipLaunchKernelGGL((gemv_q_kernel<Q, E>), dim3(g.grid), dim3(kGvThreads), g.lds, s, p);
   return hipGetLastError();
 }

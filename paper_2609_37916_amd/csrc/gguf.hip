@@ -70,6 +70,7 @@ template <int TYPE>
 hipError_t launch_repack(const void* blocks, int N, int K, void* codes, void* scales, void* zeros, hipStream_t s) {
   const size_t total = (size_t)N * (K / 32);
   const int grid = (int)std::min<size_t>((total + 255) / 256, 4096);
+  RLX_LOG_LAUNCH("gguf_repack_kernel", dim3(grid), dim3(256), 0, "type=%d", (int)TYPE);
   hipLaunchKernelGGL(gguf_repack_kernel<TYPE>, dim3(grid), dim3(256), 0, s, reinterpret_cast<const uint16_t*>(blocks),
                      N, K, reinterpret_cast<uint8_t*>(codes), reinterpret_cast<uint16_t*>(scales),
                      reinterpret_cast<uint16_t*>(zeros));

@@ -59,6 +59,14 @@ struct GemmParams {
   float ln_eps;
   bool y_f32;            // bf16 x with an f32 output (and residual); not with the deferred-LayerNorm fields
 };
+// Names for the launch log.
+inline const char* epi_name(Epi e) {
+  return e == Epi::None ? "none" : e == Epi::Bias ? "bias" : e == Epi::BiasGelu ? "bias+gelu" : "bias+residual";
+}
+inline const char* quant_name(Quant q) {
+  return q == Quant::None ? "dense" : q == Quant::Int8 ? "int8" : q == Quant::Int4 ? "int4-zp"
+         : q == Quant::Int8G ? "int8-group" : "int4-min";
+}
 // True when the deferred-LayerNorm fields are implemented for rows of H columns.
 bool gemm_deferred_ln_supported(DType dt, Quant q, int H);
 // Deferred LayerNorm with quantised weights, per row n:

@@ -198,6 +198,8 @@ __global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
 template <int FX, int FW>
 hipError_t launch_mx_typed(const MxGemmParams& p, hipStream_t s) {
   const int tiles = (p.N / kMxBN) * ((p.M + kMxBM - 1) / kMxBM);
+  RLX_LOG_LAUNCH("mx_gemm_kernel", dim3(tiles), dim3(256), 0, "formats=%d,%d M=%d N=%d K=%d", (int)FX, (int)FW, p.M,
+                 p.N, p.K);
   hipLaunchKernelGGL((mx_gemm_kernel<FX, FW>), dim3(tiles), dim3(256), 0, s, p);
   return hipGetLastError();
 }

@@ -707,6 +707,8 @@ hipError_t launch_encoder_pipe(const PipeParams& p, int grid, hipStream_t s) {
   hipLaunchKernelGGL(pipe_clear_kernel, dim3(8), dim3(256), 0, s, p.sync, p.L, p.B, rts);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  RLX_LOG_LAUNCH("encoder_pipe_kernel", dim3(grid), dim3(kPThreads), kPipeLdsBytes, "persistent B=%d S=%d layers=%d",
+                 p.B, p.S, p.L);
   hipLaunchKernelGGL(encoder_pipe_kernel, dim3(grid), dim3(kPThreads), kPipeLdsBytes, s, p);
   return hipGetLastError();
 }

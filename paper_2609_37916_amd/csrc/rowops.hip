@@ -527,6 +527,7 @@ inline int blocks_for_rows(int rows) { return (rows + 3) / 4; }
 hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, int* order,
                             hipStream_t s) {
   if (B < 1 || S < 1 || S > 64 * kScanChunks) return hipErrorInvalidValue;
+  RLX_LOG_LAUNCH("mask_scan_kernel", dim3(1), dim3(1024), (size_t)(2 * B + 1) * sizeof(int), "B=%d S=%d", B, S);
   hipLaunchKernelGGL(mask_scan_kernel, dim3(1), dim3(1024), (size_t)(2 * B + 1) * sizeof(int), s, mask, B, S, cu,
                      tok_src, tok_dst, B <= kMaxOrderedBatch ? order : nullptr);
   return hipGetLastError();
@@ -536,6 +537,7 @@ hipError_t launch_embed_ln(const int* ids, const void* word, const void* pos, co
                            const float* beta, float eps, int vocab, int S, int H, const int* tok_src,
                            const int* n_dev, int n_max, void* x, DType dt, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
+  RLX_LOG_LAUNCH("embed_ln_kernel", dim3(blocks_for_rows(n_max)), dim3(256), 0, "%s rows<=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", n_max, H);
   if (dt == DType::BF16)
     hipLaunchKernelGGL(embed_ln_kernel<bf16_t>, dim3(blocks_for_rows(n_max)), dim3(256), 0, s, ids,
                        (const bf16_t*)word, (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, S, H,
@@ -553,6 +555,7 @@ hipError_t launch_embed_scan(const uint8_t* mask, const int* ids, int B, int S, 
   if (B <= 0 || S <= 0) return hipSuccess;
   if (!embed_scan_supported(B, S)) return hipErrorInvalidValue;
   const dim3 grid(B, (S + kEmbedScanTokens - 1) / kEmbedScanTokens);
+  RLX_LOG_LAUNCH("embed_scan_kernel", grid, dim3(256), 0, "mask scan + embedding %s B=%d S=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", B, S, H);
   if (dt == DType::BF16)
     hipLaunchKernelGGL(embed_scan_kernel<bf16_t>, grid, dim3(256), 0, s, mask, ids, B, S, (const bf16_t*)word,
                        (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
@@ -567,6 +570,7 @@ hipError_t launch_embed_scan(const uint8_t* mask, const int* ids, int B, int S, 
 hipError_t launch_gather_rows(const void* hidden, int H, const int* tok_src, const int* n_dev, int n_max, void* x,
                               DType dt, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
+  RLX_LOG_LAUNCH("gather_rows_kernel", dim3(blocks_for_rows(n_max)), dim3(256), 0, "%s rows<=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", n_max, H);
   if (dt == DType::BF16)
     hipLaunchKernelGGL(gather_rows_kernel<bf16_t>, dim3(blocks_for_rows(n_max)), dim3(256), 0, s,
                        (const bf16_t*)hidden, H, tok_src, n_dev, n_max, (bf16_t*)x);
@@ -579,6 +583,7 @@ hipError_t launch_gather_rows(const void* hidden, int H, const int* tok_src, con
 hipError_t launch_layer_norm(const void* a, const float* gamma, const float* beta, float eps, int H,
                              const int* n_dev, int n_max, void* y, DType dt, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
+  RLX_LOG_LAUNCH("layer_norm_kernel", dim3(blocks_for_rows(n_max)), dim3(256), 0, "%s rows<=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", n_max, H);
   if (dt == DType::BF16)
     hipLaunchKernelGGL(layer_norm_kernel<bf16_t>, dim3(blocks_for_rows(n_max)), dim3(256), 0, s, (const bf16_t*)a,
                        gamma, beta, eps, H, n_dev, n_max, (bf16_t*)y);
@@ -593,6 +598,8 @@ hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out
   if (B <= 0) return hipSuccess;
   if (gamma_scaled && !x_stats) return hipErrorInvalidValue;
   const size_t lds = (size_t)16 * H * sizeof(float);
+  RLX_LOG_LAUNCH("pool_l2_kernel", dim3(B), dim3(1024), lds, "%s B=%d H=%d%s", dt == DType::BF16 ? "bf16" : "f32", B, H,
+                 x_stats ? (gamma_scaled ? " deferred-LN input (gamma-scaled)" : " deferred-LN input") : "");
   if (dt == DType::BF16)
     hipLaunchKernelGGL(pool_l2_kernel<bf16_t>, dim3(B), dim3(1024), lds, s, (const bf16_t*)x, H, cu, out, x_stats,
                        gamma, beta, eps, gamma_scaled);
@@ -607,6 +614,7 @@ hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out
 hipError_t launch_scatter_hidden(const void* x, int H, const int* tok_dst, int n_tok, float* out, DType dt,
                                  hipStream_t s) {
   if (n_tok <= 0) return hipSuccess;
+  RLX_LOG_LAUNCH("scatter_hidden_kernel", dim3(blocks_for_rows(n_tok)), dim3(256), 0, "%s positions=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", n_tok, H);
   if (dt == DType::BF16)
     hipLaunchKernelGGL(scatter_hidden_kernel<bf16_t>, dim3(blocks_for_rows(n_tok)), dim3(256), 0, s,
                        (const bf16_t*)x, H, tok_dst, n_tok, out);
