@@ -116,3 +116,127 @@ def test_formats_equal_their_internal_layouts():
             else:
                 got = og.dequant_int4_min(packed, s16, m.astype(np.float16))
         assert np.array_equal(got, want), fmt
+
+
+# --- K-quants (256-weight super-blocks) --------------------------------------
+
+KFMTS = ("q4_k", "q6_k")
+
+
+def test_kquant_block_sizes_and_bits_per_weight():
+    # the published sizes: 4.5 and 6.5625 bits per weight for 256-weight super-blocks
+    assert {f: og.KQ_BLOCK_BYTES[f] * 8 / 256 for f in KFMTS} == {"q4_k": 4.5, "q6_k": 6.5625}
+    assert og.KQ_TYPE_ID == {"q4_k": 12, "q6_k": 14}
+    rng = np.random.default_rng(1)
+    for f in KFMTS:
+        assert wg.random_kquant_blocks(rng, 2, 512, f).shape == (2, 2 * og.KQ_BLOCK_BYTES[f])
+
+
+def test_hand_built_q4_k_super_block():
+    """d = 1, dmin = 0.5; scale bytes written out by hand: sub-blocks 0-3 take
+    scales 1..4 / mins 5..8 from the low six bits of bytes 0-7, sub-blocks 4-7
+    scales 1, 3, 5, 7 / mins 2, 4, 6, 8 from the nibbles of bytes 8-11, plus
+    top bits: byte 0 = 0xC1 adds 3 << 4 to sub-block 4's scale, byte 4 = 0x85
+    adds 2 << 4 to its min.  Byte l of run c: l % 16 low, 15 - l % 16 high."""
+    S = [0xC1, 2, 3, 4, 0x85, 6, 7, 8, 0x21, 0x43, 0x65, 0x87]
+    sc = [1, 2, 3, 4, 1 | 3 << 4, 3, 5, 7]
+    mn = [5, 6, 7, 8, 2 | 2 << 4, 4, 6, 8]
+    qs = [(l % 16) | ((15 - l % 16) << 4) for l in range(32)] * 4
+    blk = np.array([[0x00, 0x3C, 0x00, 0x38] + S + qs], dtype=np.uint8)
+    got = og.dequant_k(blk, "q4_k", 256)[0]
+    want = []
+    for c in range(4):
+        want += [sc[2 * c] * (l % 16) - 0.5 * mn[2 * c] for l in range(32)]
+        want += [sc[2 * c + 1] * (15 - l % 16) - 0.5 * mn[2 * c + 1] for l in range(32)]
+    assert got.tolist() == want
+
+
+def test_hand_built_q6_k_super_block():
+    """d = 0.25; every ql byte 0x21 (low nibble 1, high 2), every qh byte 0xE4
+    (bit pairs 0, 1, 2, 3 from the bottom): the four quarters of each half get
+    the 6-bit values 1, 17, 34, 50, i.e. codes -31, -15, 2, 18; scales
+    1, -1, 2, -2, ... per 16 weights."""
+    scales = [(s // 2 + 1) * (1 if s % 2 == 0 else -1) for s in range(16)]
+    blk = np.array([[0x21] * 128 + [0xE4] * 64 + list(np.array(scales, np.int8).view(np.uint8)) + [0x00, 0x34]],
+                   dtype=np.uint8)
+    got = og.dequant_k(blk, "q6_k", 256)[0]
+    quarter = [-31, -15, 2, 18]
+    want = [0.25 * scales[i // 16] * quarter[(i % 128) // 32] for i in range(256)]
+    assert got.tolist() == want
+
+
+def _q4_k_bit_address(raw, i):
+    """Weight i of one Q4_K super-block, read by its bit address."""
+    f16 = lambda o: float(np.frombuffer(raw[o:o + 2], dtype=np.float16)[0])
+    d, dmin, S = f16(0), f16(2), raw[4:16]
+    j = i // 32
+    if j < 4:
+        sc, mn = S[j] % 64, S[j + 4] % 64
+    else:
+        sc = S[j + 4] % 16 + (S[j - 4] // 64) * 16
+        mn = S[j + 4] // 16 + (S[j] // 64) * 16
+    c, r = divmod(i, 64)
+    byte = raw[16 + 32 * c + r % 32]
+    q = byte % 16 if r < 32 else byte // 16
+    return d * sc * q - dmin * mn
+
+
+def _q6_k_bit_address(raw, i):
+    """Weight i of one Q6_K super-block, read by its bit address."""
+    d = float(np.frombuffer(raw[208:210], dtype=np.float16)[0])
+    sc = int(np.frombuffer(raw[192 + i // 16:193 + i // 16], dtype=np.int8)[0])
+    h, r = divmod(i, 128)
+    quarter, l = divmod(r, 32)
+    lo_byte = raw[64 * h + l + (32 if quarter in (1, 3) else 0)]
+    lo = lo_byte % 16 if quarter < 2 else lo_byte // 16
+    hi = (raw[128 + 32 * h + l] >> (2 * quarter)) % 4
+    return d * sc * (lo + 16 * hi - 32)
+
+
+@pytest.mark.parametrize("fmt", KFMTS)
+def test_kquant_element_order_matches_bit_addresses(fmt):
+    rng = np.random.default_rng(5)
+    K = 512
+    b = wg.random_kquant_blocks(rng, 2, K, fmt)
+    B = og.KQ_BLOCK_BYTES[fmt]
+    read = _q4_k_bit_address if fmt == "q4_k" else _q6_k_bit_address
+    want = np.array([[read(bytes(b[r, (i // 256) * B:(i // 256 + 1) * B]), i % 256) for i in range(K)]
+                     for r in range(2)])
+    assert np.array_equal(og.dequant_k(b, fmt, K), want)
+
+
+@pytest.mark.parametrize("fmt", KFMTS)
+def test_kquant_internal_layouts(fmt):
+    """With d and dmin powers of two the composed scales are exact in f16 and
+    the repacked layout holds the same numbers; with any d they are within
+    2^-11 (|s q| + |m|) (one f16 rounding of each composed value)."""
+    rng = np.random.default_rng(13)
+    K, N = 512, 4
+    nb = K // 256
+    if fmt == "q4_k":
+        codes = rng.integers(0, 16, (N, K))
+        sc, mn = rng.integers(0, 64, (N, K // 32)), rng.integers(0, 64, (N, K // 32))
+        exact = wg.pack_q4_k(codes, np.exp2(rng.integers(-14, -6, (N, nb))), np.exp2(rng.integers(-14, -6, (N, nb))),
+                             sc, mn)
+        general = wg.random_kquant_blocks(rng, N, K, fmt)
+    else:
+        codes = rng.integers(-32, 32, (N, K))
+        exact = wg.pack_q6_k(codes, -np.exp2(rng.integers(-14, -6, (N, nb))), rng.integers(-128, 128, (N, K // 16)))
+        general = wg.random_kquant_blocks(rng, N, K, fmt)
+
+    def internal(b):
+        kind, c, s, m = og.kquant_internal(b, fmt, K)
+        if kind == "int4_min":
+            return og.dequant_int4_min(c, s, m), s, m
+        return og.dequant_int8_group16(c, s), s, None
+
+    got, _, _ = internal(exact)
+    assert np.array_equal(got, og.dequant_k(exact, fmt, K))
+    got, s, m = internal(general)
+    want = og.dequant_k(general, fmt, K)
+    gs = 32 if fmt == "q4_k" else 16
+    qmax = 15 if fmt == "q4_k" else 32
+    bound = 2.0 ** -11 * 1.001 * (np.repeat(np.abs(s.astype(np.float64)), gs, axis=1) * qmax +
+                          (np.repeat(np.abs(m.astype(np.float64)), gs, axis=1) if m is not None else 0.0))
+    assert np.all(np.abs(got - want) <= bound)
+    assert np.any(got != want)  # the rounding is real for general scales

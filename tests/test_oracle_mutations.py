@@ -405,3 +405,73 @@ def test_planted_gguf_mistake_fails_a_pin(name, monkeypatch):
         except Exception as e:
             failed.append(type(e).__name__)
     assert failed, f"no pin caught the planted mistake '{name}'"
+
+
+# --- planted mistakes in the K-quant part of the GGUF oracle ---
+
+KQ_ORIG = {n: getattr(ogg, n) for n in ("parse_q4_k", "parse_q6_k", "dequant_k")}
+
+
+def _kquant_pin_calls():
+    calls = [ggpins.test_kquant_block_sizes_and_bits_per_weight, ggpins.test_hand_built_q4_k_super_block,
+             ggpins.test_hand_built_q6_k_super_block]
+    for fmt in ggpins.KFMTS:
+        calls.append(lambda fmt=fmt: ggpins.test_kquant_element_order_matches_bit_addresses(fmt))
+        calls.append(lambda fmt=fmt: ggpins.test_kquant_internal_layouts(fmt))
+    return calls
+
+
+def kq_scale_min_swapped_high(blocks, K):
+    codes, d, dmin, sc, mn = KQ_ORIG["parse_q4_k"](blocks, K)
+    s, m = sc.reshape(sc.shape[0], -1, 8).copy(), mn.reshape(mn.shape[0], -1, 8).copy()
+    s[:, :, 4:], m[:, :, 4:] = m[:, :, 4:].copy(), s[:, :, 4:].copy()  # sub-blocks 4-7: scale and min exchanged
+    return codes, d, dmin, s.reshape(sc.shape), m.reshape(mn.shape)
+
+
+def kq_q4_k_runs_interleaved(blocks, K):
+    codes, d, dmin, sc, mn = KQ_ORIG["parse_q4_k"](blocks, K)
+    r = codes.reshape(codes.shape[0], -1, 2, 32)  # low / high nibbles as weights 2l / 2l+1
+    return np.stack([r[:, :, 0], r[:, :, 1]], axis=3).reshape(codes.shape), d, dmin, sc, mn
+
+
+def kq_q6_k_no_offset(blocks, K):
+    codes, d, sc = KQ_ORIG["parse_q6_k"](blocks, K)
+    return codes + 32, d, sc
+
+
+def kq_q6_k_high_bits_reversed(blocks, K):
+    codes, d, sc = KQ_ORIG["parse_q6_k"](blocks, K)
+    u = (codes + 32).reshape(codes.shape[0], -1, 2, 4, 32)
+    lo, hi = u & 15, u >> 4
+    u = lo | (hi[:, :, :, ::-1, :] << 4)  # quarter k takes the bit pair of quarter 3 - k
+    return u.reshape(codes.shape) - 32, d, sc
+
+
+def kq_q4_k_min_added(blocks, fmt, K):
+    w = KQ_ORIG["dequant_k"](blocks, fmt, K)
+    if fmt == "q4_k":
+        _, _, dmin, _, mn = ogg.parse_q4_k(blocks, K)
+        w = w + 2.0 * dmin[:, np.arange(K) // 256] * mn[:, np.arange(K) // 32]
+    return w
+
+
+KQ_MUTANTS = {
+    "q4_k: scale and min of sub-blocks 4-7 exchanged": ("parse_q4_k", kq_scale_min_swapped_high),
+    "q4_k: nibbles of a run interleaved": ("parse_q4_k", kq_q4_k_runs_interleaved),
+    "q6_k: codes without the -32": ("parse_q6_k", kq_q6_k_no_offset),
+    "q6_k: high bit pairs in reverse order": ("parse_q6_k", kq_q6_k_high_bits_reversed),
+    "q4_k: min added instead of subtracted": ("dequant_k", kq_q4_k_min_added),
+}
+
+
+@pytest.mark.parametrize("name", list(KQ_MUTANTS))
+def test_planted_kquant_mistake_fails_a_pin(name, monkeypatch):
+    attr, fake = KQ_MUTANTS[name]
+    monkeypatch.setattr(ogg, attr, fake)
+    failed = []
+    for call in _kquant_pin_calls():
+        try:
+            call()
+        except Exception as e:
+            failed.append(type(e).__name__)
+    assert failed, f"no pin caught the planted mistake '{name}'"

@@ -79,3 +79,68 @@ def random_blocks(rng, N: int, K: int, fmt: str) -> np.ndarray:
          (1 + rng.random((N, nb))))
     m = rng.normal(0, 0.05, size=(N, nb)) if fmt == "q4_1" else None
     return pack_blocks(codes, d, m, fmt)
+
+
+# --- K-quants: 256-weight super-blocks -------------------------------------
+
+QK_K = 256
+KQ_BLOCK_BYTES = {"q4_k": 144, "q6_k": 210}
+
+
+def pack_q4_k(codes, d, dmin, sc, mn) -> np.ndarray:
+    """codes [N, K] 0..15, d / dmin [N, K/256], sc / mn [N, K/32] in 0..63 ->
+    Q4_K super-blocks [N, K/256*144]: f16 d, f16 dmin, the twelve scale bytes
+    (sub-blocks 0-3: scale and min in the low six bits of bytes 0-3 / 4-7;
+    sub-blocks 4-7: low four bits of scale and min in bytes 8-11, their top
+    two bits in the top bits of bytes 0-3 / 4-7), then four runs of 32 bytes,
+    byte l of run c holding weights 64c + l (low nibble) and 64c + 32 + l."""
+    q = np.asarray(codes, dtype=np.int64)
+    N, K = q.shape
+    nb = K // QK_K
+    out = np.zeros((N, nb, 144), dtype=np.uint8)
+    out[:, :, 0:2] = np.asarray(d, dtype=np.float16).reshape(N, nb, 1).view(np.uint8)
+    out[:, :, 2:4] = np.asarray(dmin, dtype=np.float16).reshape(N, nb, 1).view(np.uint8)
+    s = np.asarray(sc, dtype=np.int64).reshape(N, nb, 8)
+    m = np.asarray(mn, dtype=np.int64).reshape(N, nb, 8)
+    out[:, :, 4:8] = (s[:, :, 0:4] | ((s[:, :, 4:8] >> 4) << 6)).astype(np.uint8)
+    out[:, :, 8:12] = (m[:, :, 0:4] | ((m[:, :, 4:8] >> 4) << 6)).astype(np.uint8)
+    out[:, :, 12:16] = ((s[:, :, 4:8] & 15) | ((m[:, :, 4:8] & 15) << 4)).astype(np.uint8)
+    runs = q.reshape(N, nb, 4, 64)
+    out[:, :, 16:144] = (runs[..., 0:32] | (runs[..., 32:64] << 4)).reshape(N, nb, 128).astype(np.uint8)
+    return out.reshape(N, nb * 144)
+
+
+def pack_q6_k(codes, d, sc) -> np.ndarray:
+    """codes [N, K] in -32..31, d [N, K/256], sc [N, K/16] int8 -> Q6_K
+    super-blocks [N, K/256*210]: ql, qh, the sixteen scales, f16 d.  With
+    u = code + 32, per half h and l < 32: ql[64h + l] = low four bits of
+    u[128h + l] | those of u[128h + 64 + l] << 4; ql[64h + 32 + l] likewise
+    for u[128h + 32 + l] and u[128h + 96 + l]; qh[32h + l] = the top two bits
+    of u[128h + l], u[128h + 32 + l], u[128h + 64 + l], u[128h + 96 + l] at
+    bits 0, 2, 4, 6."""
+    u = np.asarray(codes, dtype=np.int64) + 32
+    N, K = u.shape
+    nb = K // QK_K
+    out = np.zeros((N, nb, 210), dtype=np.uint8)
+    h = u.reshape(N, nb, 2, 4, 32)  # [.., half, quarter, l]
+    ql = np.concatenate([(h[..., 0, :] & 15) | ((h[..., 2, :] & 15) << 4),
+                         (h[..., 1, :] & 15) | ((h[..., 3, :] & 15) << 4)], axis=3)  # [.., half, 64]
+    qh = (h[..., 0, :] >> 4) | ((h[..., 1, :] >> 4) << 2) | ((h[..., 2, :] >> 4) << 4) | ((h[..., 3, :] >> 4) << 6)
+    out[:, :, 0:128] = ql.reshape(N, nb, 128).astype(np.uint8)
+    out[:, :, 128:192] = qh.reshape(N, nb, 64).astype(np.uint8)
+    out[:, :, 192:208] = np.asarray(sc, dtype=np.int8).reshape(N, nb, 16).view(np.uint8)
+    out[:, :, 208:210] = np.asarray(d, dtype=np.float16).reshape(N, nb, 1).view(np.uint8)
+    return out.reshape(N, nb * 210)
+
+
+def random_kquant_blocks(rng, N: int, K: int, fmt: str) -> np.ndarray:
+    """Every code, scale and min value with equal probability; d, dmin =
+    2^U(-12, -8) * (1 + U(0,1)) stored as f16 (d negative half the time for Q6_K)."""
+    nb = K // QK_K
+    d = np.exp2(rng.uniform(-12, -8, size=(N, nb))) * (1 + rng.random((N, nb)))
+    if fmt == "q4_k":
+        dmin = np.exp2(rng.uniform(-12, -8, size=(N, nb))) * (1 + rng.random((N, nb)))
+        return pack_q4_k(rng.integers(0, 16, size=(N, K)), d, dmin, rng.integers(0, 64, size=(N, K // 32)),
+                         rng.integers(0, 64, size=(N, K // 32)))
+    d = d * rng.choice([-1.0, 1.0], size=(N, nb))
+    return pack_q6_k(rng.integers(-32, 32, size=(N, K)), d, rng.integers(-128, 128, size=(N, K // 16)))
