@@ -78,9 +78,12 @@ typedef RLX_ENUM {
                                   g = k / group                                       */
   RLX_Q_INT8_GROUP = 3,        /* w int8 [N,K]; scales f16 [N, K/group];
                                   W = q * s[n,g] (GGUF Q8_0 after rlx_gguf_repack)    */
-  RLX_Q_INT4_GROUP_MIN = 4     /* w as RLX_Q_INT4_GROUP_ZP; `zeros` holds mins m, f16
+  RLX_Q_INT4_GROUP_MIN = 4,    /* w as RLX_Q_INT4_GROUP_ZP; `zeros` holds mins m, f16
                                   [N, K/group]; W = q * s[n,g] + m[n,g]
-                                  (GGUF Q4_1 after rlx_gguf_repack)                  */
+                                  (GGUF Q4_1 and Q4_K after rlx_gguf_repack)         */
+  RLX_Q_INT8_GROUP16 = 5       /* w int8 [N,K]; scales f16 [N, K/16]; group_size 16;
+                                  W = q * s[n, k/16] (GGUF Q6_K after rlx_gguf_repack).
+                                  Tiled matmul path only (no few-row kernel)          */
 } rlx_quant;
 
 typedef RLX_ENUM {
@@ -167,25 +170,43 @@ rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scale
 
 /* GGUF weight blocks (the llama.cpp scheme set of Op::DequantMatMul, Section
  * VI).  A tensor of N rows of K weights is N * K/32 consecutive 32-weight
- * blocks, row-major; the tensor type ids and blocks are GGUF's:
+ * blocks (K-quants: N * K/256 super-blocks of 256 weights), row-major; the
+ * tensor type ids and blocks are GGUF's:
  *   RLX_GGUF_Q4_0  18 bytes: f16 d, 16 bytes of nibbles   W = (q - 8) * d
  *   RLX_GGUF_Q4_1  20 bytes: f16 d, f16 m, 16 bytes        W = q * d + m
  *   RLX_GGUF_Q8_0  34 bytes: f16 d, 32 int8                W = q * d
+ *   RLX_GGUF_Q4_K 144 bytes: f16 d, f16 dmin, 12 bytes of 6-bit sub-block
+ *                  scales sc_j and mins mn_j, 128 bytes of nibbles
+ *                                                          W = d sc_j q - dmin mn_j
+ *   RLX_GGUF_Q6_K 210 bytes: 128 bytes of low nibbles, 64 bytes of high bit
+ *                  pairs, 16 int8 sub-block scales sc_i, f16 d
+ *                                                          W = d sc_i (q - 32)
  * (4-bit blocks: element j < 16 in the low nibble of byte j, element j + 16
- * in its high nibble; f16 little-endian).
+ * in its high nibble; Q4_K / Q6_K: sub-blocks of 32 / 16 weights in the
+ * published bit layouts; f16 little-endian).
  * rlx_gguf_repack rewrites such a tensor, once, into the layout of an
- * rlx_quant scheme that represents the same weights exactly, and stores that
- * scheme in *scheme (if non-NULL):
+ * rlx_quant scheme, and stores that scheme in *scheme (if non-NULL):
  *   Q4_0 -> RLX_Q_INT4_GROUP_ZP  (codes [N,K/2], scales = d, zeros = 8)
  *   Q4_1 -> RLX_Q_INT4_GROUP_MIN (codes [N,K/2], scales = d, zeros = m)
  *   Q8_0 -> RLX_Q_INT8_GROUP     (codes [N,K] int8, scales = d; zeros unused)
- * scales and zeros are f16 [N, K/32].  Pass the results to
- * rlx_dequant_matmul with group_size 32.  Device pointers owned by the
- * caller; blocks, scales and zeros 2-byte aligned, codes 16-byte aligned;
- * K a positive multiple of 64, N >= 0 (N == 0 is a no-op).  Otherwise
- * RLX_ERR_UNSUPPORTED (type, alignment, K) or RLX_ERR_INVALID_ARG.
+ *   Q4_K -> RLX_Q_INT4_GROUP_MIN (codes [N,K/2], scales = f16(d sc_j),
+ *                                 zeros = f16(0 - dmin mn_j))
+ *   Q6_K -> RLX_Q_INT8_GROUP16   (codes [N,K] int8 = q - 32, scales =
+ *                                 f16(d sc_i) [N, K/16]; zeros unused)
+ * The basic blocks map exactly.  A K-quant's composed sub-block scales and
+ * mins have up to 17 (Q4_K) / 19 (Q6_K) significant bits and are rounded once
+ * to f16 (nearest even): the repacked weights are within 2^-11 (|s q| + |m|)
+ * of the format's values, and the composed values must be finite in f16.
+ * scales and zeros are f16 [N, K/32] (Q6_K: scales [N, K/16]).  Pass the
+ * results to rlx_dequant_matmul with group_size 32 (Q6_K: 16).  Device
+ * pointers owned by the caller; blocks, scales and zeros 2-byte aligned,
+ * codes 16-byte aligned; K a positive multiple of 64 (K-quants: of 256),
+ * N >= 0 (N == 0 is a no-op).  Otherwise RLX_ERR_UNSUPPORTED (type,
+ * alignment, K) or RLX_ERR_INVALID_ARG.
  */
-typedef RLX_ENUM { RLX_GGUF_Q4_0 = 2, RLX_GGUF_Q4_1 = 3, RLX_GGUF_Q8_0 = 8 } rlx_gguf_type;
+typedef RLX_ENUM {
+  RLX_GGUF_Q4_0 = 2, RLX_GGUF_Q4_1 = 3, RLX_GGUF_Q8_0 = 8, RLX_GGUF_Q4_K = 12, RLX_GGUF_Q6_K = 14
+} rlx_gguf_type;
 
 rlx_status rlx_gguf_repack(const void* blocks, rlx_gguf_type type, int N, int K, void* codes, void* scales,
                            void* zeros, rlx_quant* scheme, void* stream);

@@ -195,14 +195,14 @@ def dequant_int8_group16(q, scales):
 def kquant_internal(blocks, fmt: str, K: int):
     """The internal layout a K-quant tensor is repacked into, as arrays:
     Q4_K -> ("int4_min", packed codes [N, K/2] (k = 2j low nibble), f16
-    scales d * sc_j, f16 mins -dmin * mn_j, each [N, K/32]);
+    scales d * sc_j, f16 mins 0 - dmin * mn_j (a zero min is +0), each [N, K/32]);
     Q6_K -> ("int8_group16", int8 codes [N, K], f16 scales d * sc_i [N, K/16], None).
     The composed scales are rounded once to f16 (nearest even)."""
     if fmt == "q4_k":
         codes, d, dmin, sc, mn = parse_q4_k(blocks, K)
         sb = np.arange(K // 32) // 8
         s = (d[:, sb] * sc).astype(np.float16)
-        m = (-(dmin[:, sb] * mn)).astype(np.float16)
+        m = (0.0 - dmin[:, sb] * mn).astype(np.float16)  # 0 - x: a zero min is +0
         packed = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
         return "int4_min", packed, s, m
     codes, d, sc = parse_q6_k(blocks, K)

@@ -20,10 +20,12 @@ LIB_PATH = os.path.join(PKG_DIR, "librlx.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_OOM = range(5)
 F32, BF16, F16, I8, U4X2, I32, U8 = range(7)
 MASK_NONE, MASK_CAUSAL, MASK_SLIDING_WINDOW, MASK_CUSTOM = range(4)
-Q_NONE, Q_INT8_PER_CHANNEL, Q_INT4_GROUP_ZP, Q_INT8_GROUP, Q_INT4_GROUP_MIN = range(5)
-GGUF_Q4_0, GGUF_Q4_1, GGUF_Q8_0 = 2, 3, 8
-GGUF_TYPES = {"q4_0": GGUF_Q4_0, "q4_1": GGUF_Q4_1, "q8_0": GGUF_Q8_0}
-GGUF_BLOCK_BYTES = {GGUF_Q4_0: 18, GGUF_Q4_1: 20, GGUF_Q8_0: 34}
+Q_NONE, Q_INT8_PER_CHANNEL, Q_INT4_GROUP_ZP, Q_INT8_GROUP, Q_INT4_GROUP_MIN, Q_INT8_GROUP16 = range(6)
+GGUF_Q4_0, GGUF_Q4_1, GGUF_Q8_0, GGUF_Q4_K, GGUF_Q6_K = 2, 3, 8, 12, 14
+GGUF_TYPES = {"q4_0": GGUF_Q4_0, "q4_1": GGUF_Q4_1, "q8_0": GGUF_Q8_0, "q4_k": GGUF_Q4_K, "q6_k": GGUF_Q6_K}
+# bytes per block and weights per block
+GGUF_BLOCK_BYTES = {GGUF_Q4_0: 18, GGUF_Q4_1: 20, GGUF_Q8_0: 34, GGUF_Q4_K: 144, GGUF_Q6_K: 210}
+GGUF_BLOCK_WEIGHTS = {GGUF_Q4_0: 32, GGUF_Q4_1: 32, GGUF_Q8_0: 32, GGUF_Q4_K: 256, GGUF_Q6_K: 256}
 EPI_NONE, EPI_BIAS, EPI_BIAS_GELU, EPI_BIAS_RESIDUAL = range(4)
 MX_E4M3, MX_E5M2, MX_E2M3, MX_E3M2, MX_E2M1 = range(5)
 MX_FORMAT_CODES = {"e4m3": MX_E4M3, "e5m2": MX_E5M2, "e2m3": MX_E2M3, "e3m2": MX_E3M2, "e2m1": MX_E2M1}
@@ -232,22 +234,25 @@ def dequant_unpack(w, *, scheme: int, scales, zeros=None, group_size: int = 32, 
 
 
 def gguf_repack(blocks, gguf_type, *, N: int, K: int, stream=None):
-    """GGUF blocks (uint8 device tensor of N * K/32 blocks) -> (scheme, codes,
-    scales, zeros) for dequant_matmul (see rlx_gguf_repack); zeros is None for Q8_0."""
+    """GGUF blocks (uint8 device tensor of N * K/32 blocks, or N * K/256 for the
+    K-quants) -> (scheme, codes, scales, zeros) for dequant_matmul (see
+    rlx_gguf_repack); zeros is None for Q8_0 and Q6_K, whose group size is 32
+    and 16."""
     torch = _torch()
     t = GGUF_TYPES.get(gguf_type, gguf_type)
     if t not in GGUF_BLOCK_BYTES:
         raise ValueError(f"unknown GGUF type {gguf_type!r}")
     # the C ABI cannot see buffer sizes: check the block tensor here so no kernel reads past it
-    want = N * (K // 32) * GGUF_BLOCK_BYTES[t]
-    if blocks.dtype != torch.uint8 or not blocks.is_contiguous() or blocks.numel() != want or K % 32:
+    bw = GGUF_BLOCK_WEIGHTS[t]
+    want = N * (K // bw) * GGUF_BLOCK_BYTES[t]
+    if blocks.dtype != torch.uint8 or not blocks.is_contiguous() or blocks.numel() != want or K % bw:
         raise ValueError(f"blocks: expected a contiguous uint8 tensor of {want} bytes, got {blocks.dtype} "
                          f"{tuple(blocks.shape)}")
     dev = blocks.device
-    codes = torch.empty((N, K // 2 if t != GGUF_Q8_0 else K), dtype=torch.uint8 if t != GGUF_Q8_0 else torch.int8,
-                        device=dev)
-    scales = torch.empty((N, K // 32), dtype=torch.float16, device=dev)
-    zeros = torch.empty((N, K // 32), dtype=torch.float16, device=dev) if t != GGUF_Q8_0 else None
+    int8_codes = t in (GGUF_Q8_0, GGUF_Q6_K)
+    codes = torch.empty((N, K if int8_codes else K // 2), dtype=torch.int8 if int8_codes else torch.uint8, device=dev)
+    scales = torch.empty((N, K // (16 if t == GGUF_Q6_K else 32)), dtype=torch.float16, device=dev)
+    zeros = None if int8_codes else torch.empty((N, K // 32), dtype=torch.float16, device=dev)
     scheme = ctypes.c_int(-1)
     check(lib().rlx_gguf_repack(_ptr(blocks), t, N, K, _ptr(codes), _ptr(scales), _ptr(zeros), ctypes.byref(scheme),
                                 _stream(stream)))

@@ -102,16 +102,18 @@ rlx_status check_attention_args(const void* q, const void* k, const void* v, int
 rlx_status check_quant_weights(const char* who, rlx_quant scheme, const void* w, const void* scales,
                                const void* zeros, int group_size, int N, int K) {
   if (!w) return fail(RLX_ERR_INVALID_ARG, "%s: weight pointer is null", who);
-  if (scheme < RLX_Q_NONE || scheme > RLX_Q_INT4_GROUP_MIN)
+  if (scheme < RLX_Q_NONE || scheme > RLX_Q_INT8_GROUP16)
     return fail(RLX_ERR_INVALID_ARG, "%s: unknown quantisation scheme %d", who, (int)scheme);
   if (N % 64 || K % 64)
     return fail(RLX_ERR_UNSUPPORTED, "%s: N=%d and K=%d must be multiples of 64", who, N, K);
   if (!aligned16(w)) return fail(RLX_ERR_UNSUPPORTED, "%s: weights must be 16-byte aligned", who);
-  if ((scheme == RLX_Q_INT8_PER_CHANNEL || scheme == RLX_Q_INT8_GROUP) && !scales)
+  if ((scheme == RLX_Q_INT8_PER_CHANNEL || scheme == RLX_Q_INT8_GROUP || scheme == RLX_Q_INT8_GROUP16) && !scales)
     return fail(RLX_ERR_INVALID_ARG, "%s: int8 weights need scales", who);
   if ((scheme == RLX_Q_INT4_GROUP_ZP || scheme == RLX_Q_INT4_GROUP_MIN) && (!scales || !zeros))
     return fail(RLX_ERR_INVALID_ARG, "%s: int4 weights need scales and zeros (or mins)", who);
-  if (scheme >= RLX_Q_INT4_GROUP_ZP && group_size != 32)
+  if (scheme == RLX_Q_INT8_GROUP16 && group_size != 16)
+    return fail(RLX_ERR_UNSUPPORTED, "%s: RLX_Q_INT8_GROUP16 takes group size 16, not %d", who, group_size);
+  if (scheme >= RLX_Q_INT4_GROUP_ZP && scheme != RLX_Q_INT8_GROUP16 && group_size != 32)
     return fail(RLX_ERR_UNSUPPORTED, "%s: group size %d not supported (32)", who, group_size);
   return RLX_OK;
 }
@@ -122,6 +124,7 @@ Quant to_quant(rlx_quant q) {
     case RLX_Q_INT4_GROUP_ZP: return Quant::Int4;
     case RLX_Q_INT8_GROUP: return Quant::Int8G;
     case RLX_Q_INT4_GROUP_MIN: return Quant::Int4M;
+    case RLX_Q_INT8_GROUP16: return Quant::Int8G16;
     default: return Quant::None;
   }
 }
@@ -314,11 +317,13 @@ rlx_status check_config(const rlx_encoder_config* c) {
     return fail(RLX_ERR_INVALID_ARG, "encoder: vocab, max_pos and type_vocab must be positive for id input");
   if (c->dtype != RLX_F32 && c->dtype != RLX_BF16)
     return fail(RLX_ERR_UNSUPPORTED, "encoder: dtype %s not supported (f32, bf16)", dtype_name(c->dtype));
-  if (c->quant < RLX_Q_NONE || c->quant > RLX_Q_INT4_GROUP_MIN)
+  if (c->quant < RLX_Q_NONE || c->quant > RLX_Q_INT8_GROUP16)
     return fail(RLX_ERR_INVALID_ARG, "encoder: unknown quantisation scheme %d", (int)c->quant);
   if (c->quant != RLX_Q_NONE && c->dtype != RLX_BF16)
     return fail(RLX_ERR_UNSUPPORTED, "encoder: quantised weights need bf16 activations");
-  if (c->quant >= RLX_Q_INT4_GROUP_ZP && c->group_size != 32)
+  if (c->quant == RLX_Q_INT8_GROUP16 && c->group_size != 16)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder: RLX_Q_INT8_GROUP16 takes group size 16, not %d", c->group_size);
+  if (c->quant >= RLX_Q_INT4_GROUP_ZP && c->quant != RLX_Q_INT8_GROUP16 && c->group_size != 32)
     return fail(RLX_ERR_UNSUPPORTED, "encoder: group size %d not supported (32)", c->group_size);
   if (c->head_dim != 32) return fail(RLX_ERR_UNSUPPORTED, "encoder: head_dim %d not supported (32)", c->head_dim);
   if (c->hidden % 64 || c->ffn % 64 || c->hidden > 1024)
@@ -1014,18 +1019,25 @@ rlx_status rlx_dequant_unpack(const void* w, rlx_quant scheme, const void* scale
 rlx_status rlx_gguf_repack(const void* blocks, rlx_gguf_type type, int N, int K, void* codes, void* scales,
                            void* zeros, rlx_quant* scheme, void* stream) {
   log_refresh();
-  if (type != RLX_GGUF_Q4_0 && type != RLX_GGUF_Q4_1 && type != RLX_GGUF_Q8_0)
-    return fail(RLX_ERR_UNSUPPORTED, "gguf_repack: tensor type %d not supported (Q4_0 2, Q4_1 3, Q8_0 8)", (int)type);
+  if (type != RLX_GGUF_Q4_0 && type != RLX_GGUF_Q4_1 && type != RLX_GGUF_Q8_0 && type != RLX_GGUF_Q4_K &&
+      type != RLX_GGUF_Q6_K)
+    return fail(RLX_ERR_UNSUPPORTED,
+                "gguf_repack: tensor type %d not supported (Q4_0 2, Q4_1 3, Q8_0 8, Q4_K 12, Q6_K 14)", (int)type);
   if (N < 0 || K <= 0) return fail(RLX_ERR_INVALID_ARG, "gguf_repack: N=%d must be >= 0 and K=%d positive", N, K);
-  if (K % 64) return fail(RLX_ERR_UNSUPPORTED, "gguf_repack: K=%d must be a multiple of 64", K);
-  const bool four = type != RLX_GGUF_Q8_0;
+  const bool kquant = type == RLX_GGUF_Q4_K || type == RLX_GGUF_Q6_K;
+  if (K % (kquant ? 256 : 64))
+    return fail(RLX_ERR_UNSUPPORTED, "gguf_repack: K=%d must be a multiple of %d", K, kquant ? 256 : 64);
+  const bool four = type != RLX_GGUF_Q8_0 && type != RLX_GGUF_Q6_K;  // a zeros / mins array
   if (N > 0 && (!blocks || !codes || !scales || (four && !zeros)))
     return fail(RLX_ERR_INVALID_ARG, "gguf_repack: blocks, codes, scales%s must be non-null", four ? " and zeros" : "");
   if ((reinterpret_cast<uintptr_t>(blocks) & 1) || !aligned16(codes) || (reinterpret_cast<uintptr_t>(scales) & 1) ||
       (four && (reinterpret_cast<uintptr_t>(zeros) & 1)))
     return fail(RLX_ERR_UNSUPPORTED, "gguf_repack: blocks, scales and zeros must be 2-byte, codes 16-byte aligned");
   if (scheme)
-    *scheme = type == RLX_GGUF_Q4_0 ? RLX_Q_INT4_GROUP_ZP : (type == RLX_GGUF_Q4_1 ? RLX_Q_INT4_GROUP_MIN : RLX_Q_INT8_GROUP);
+    *scheme = type == RLX_GGUF_Q4_0                            ? RLX_Q_INT4_GROUP_ZP
+              : (type == RLX_GGUF_Q4_1 || type == RLX_GGUF_Q4_K) ? RLX_Q_INT4_GROUP_MIN
+              : type == RLX_GGUF_Q6_K                          ? RLX_Q_INT8_GROUP16
+                                                               : RLX_Q_INT8_GROUP;
   RLX_HIP(launch_gguf_repack(blocks, (int)type, N, K, codes, scales, zeros, static_cast<hipStream_t>(stream)),
           "gguf repack launch");
   return ok();

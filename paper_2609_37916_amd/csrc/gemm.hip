@@ -237,6 +237,13 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
           int8x16_to_bf16(wr[i], lo, hi);
           st16(dst, lo);
           st16(dst + 16, hi);
+        } else if constexpr (Q == Quant::Int8G16) {
+          const int g = kt * 4 + c;  // 16 codes per chunk, one group per chunk
+          const float sg = f16_bits_to_f32(reinterpret_cast<const uint16_t*>(p.scales)[(size_t)(n0 + r) * (K / 16) + g]);
+          uint4 lo, hi;
+          int8x16_scaled_to_bf16(wr[i], sg, lo, hi);
+          st16(dst, lo);
+          st16(dst + 16, hi);
         } else if constexpr (Q == Quant::Int8G) {
           const int g = kt * 2 + (c >> 1);  // 16 codes per chunk, two chunks per group
           const float sg = f16_bits_to_f32(reinterpret_cast<const uint16_t*>(p.scales)[(size_t)(n0 + r) * (K / 32) + g]);
@@ -357,14 +364,18 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
 // fp32 sum in the epilogue); int8 group q s, int4 (q - z) s, int4 min
 // fma(q, s, m) in fp32, rounded to bf16.
 __host__ __device__ constexpr bool dma_quant_ok(Quant q) {
-  return q == Quant::None || q == Quant::Int8 || q == Quant::Int8G || q == Quant::Int4 || q == Quant::Int4M;
+  return q == Quant::None || q == Quant::Int8 || q == Quant::Int8G || q == Quant::Int4 || q == Quant::Int4M ||
+         q == Quant::Int8G16;
 }
 __host__ __device__ constexpr bool quant_grouped(Quant q) {
-  return q == Quant::Int8G || q == Quant::Int4 || q == Quant::Int4M;
+  return q == Quant::Int8G || q == Quant::Int4 || q == Quant::Int4M || q == Quant::Int8G16;
 }
+// Layouts with scales only (no zero-point / min array).
+__host__ __device__ constexpr bool quant_scales_only(Quant q) { return q == Quant::Int8G || q == Quant::Int8G16; }
 // LDS for the group scales (and zeros / mins) of BN rows over K.
 __host__ __device__ inline int gq_lds_bytes(Quant q, int BN, int K) {
-  return quant_grouped(q) ? (BN * (K / 32) * 2 * (q == Quant::Int8G ? 1 : 2) + 1023) / 1024 * 1024 : 0;
+  return quant_grouped(q) ? (BN * (K / quant_group_size(q)) * 2 * (quant_scales_only(q) ? 1 : 2) + 1023) / 1024 * 1024
+                          : 0;
 }
 
 template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1, int LN = 0, Quant Q = Quant::None>
@@ -461,15 +472,15 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
     }
   };
 
-  // Group scales (then zeros / mins) of rows n0 .. n0+BN-1, [BN][K/32] f16
-  // each, into LDS after the epilogue operands: older than every stage load,
-  // so the first stage's wait covers them.
-  const int G = K / 32;
+  // Group scales (then zeros / mins) of rows n0 .. n0+BN-1, [BN][G] f16
+  // each (G = K / group size), into LDS after the epilogue operands: older
+  // than every stage load, so the first stage's wait covers them.
+  const int G = K / quant_group_size(Q);
   uint8_t* gq = epi_lds + (STAGED ? epi_layout_of<BM, BN, E, LN>(p.K, p.N).bytes : 0);
   if constexpr (quant_grouped(Q)) {
     const int dw = BN * G / 2;  // dwords per array (G is even)
     const uint32_t gq0 = lds_addr_of(gq);
-    for (int a = 0; a < (Q == Quant::Int8G ? 1 : 2); ++a) {
+    for (int a = 0; a < (quant_scales_only(Q) ? 1 : 2); ++a) {
       const uint8_t* arr = reinterpret_cast<const uint8_t*>(a == 0 ? p.scales : p.zeros);
       for (int j = wave; j * 64 < dw; j += NW) {
         const int d = j * 64 + lane;
@@ -527,6 +538,8 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
                 const uint2 c8 = *reinterpret_cast<const uint2*>(ws + r * 64 + ((q ^ ((r >> 2) & 3)) * 16) + half * 8);
                 if constexpr (Q == Quant::Int8)
                   af[qq][tn] = int8x8_to_bf16(c8);
+                else if constexpr (Q == Quant::Int8G16)  // one group of 16 per 16-k chunk
+                  af[qq][tn] = int8x8_scaled_to_bf16(c8, f16_bits_to_f32(gs[r * G + 4 * kt + q]));
                 else
                   af[qq][tn] = int8x8_scaled_to_bf16(c8, f16_bits_to_f32(gs[r * G + 2 * kt + (q >> 1)]));
               } else if constexpr (quant_int4(Q)) {
@@ -655,7 +668,7 @@ hipError_t launch_dma_q_tile(const GemmParams& p, hipStream_t s) {
 // kernel runs.
 bool dma_q_fits(const GemmParams& p, int BN) {
   auto a4 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 3) == 0; };
-  if (quant_grouped(p.quant) && (!a4(p.scales) || (p.quant != Quant::Int8G && !a4(p.zeros)))) return false;
+  if (quant_grouped(p.quant) && (!a4(p.scales) || (!quant_scales_only(p.quant) && !a4(p.zeros)))) return false;
   return gq_lds_bytes(p.quant, BN, p.K) <= 32 * 1024;
 }
 
@@ -782,6 +795,8 @@ __global__ void dequant_unpack_kernel(const uint8_t* w, Quant q, const uint16_t*
       out[i] = (float)(int8_t)w[i] * f16_bits_to_f32(scales[n]);
     } else if (q == Quant::Int8G) {
       out[i] = (float)(int8_t)w[i] * f16_bits_to_f32(scales[(size_t)n * (K / 32) + k / 32]);
+    } else if (q == Quant::Int8G16) {
+      out[i] = (float)(int8_t)w[i] * f16_bits_to_f32(scales[(size_t)n * (K / 16) + k / 16]);
     } else if (q == Quant::Int4M) {
       const uint8_t byte = w[(size_t)n * (K / 2) + k / 2];
       const float code = (float)((k & 1) ? (byte >> 4) : (byte & 0xf));
@@ -837,6 +852,8 @@ __device__ __forceinline__ float deq32(const uint8_t* w, Quant q, const uint16_t
   const int gi = n * (K / 32) + k / 32;
   if (q == Quant::Int8) return (float)(int8_t)w[(size_t)n * K + k] * f16_bits_to_f32(scales[n]);
   if (q == Quant::Int8G) return (float)(int8_t)w[(size_t)n * K + k] * f16_bits_to_f32(scales[gi]);
+  if (q == Quant::Int8G16)
+    return (float)(int8_t)w[(size_t)n * K + k] * f16_bits_to_f32(scales[n * (K / 16) + k / 16]);
   const uint32_t byte = w[(size_t)n * (K / 2) + k / 2];
   const float c = (float)((k & 1) ? byte >> 4 : byte & 0xfu);
   const float sc = f16_bits_to_f32(scales[gi]), z = f16_bits_to_f32(zeros[gi]);
@@ -904,9 +921,11 @@ __global__ __launch_bounds__(256) void dequant_jobs_kernel(const DequantJob* job
   const Quant q = j.quant;
   const uint16_t* sc = reinterpret_cast<const uint16_t*>(j.scales);
   float d[16];
-  if (q == Quant::Int8 || q == Quant::Int8G) {
+  if (quant_int8(q)) {
     const uint4 c = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint8_t*>(j.w) + (size_t)n * K + k);
-    const float s = f16_bits_to_f32(q == Quant::Int8 ? sc[n] : sc[n * (K / 32) + k / 32]);
+    const float s = f16_bits_to_f32(q == Quant::Int8    ? sc[n]
+                                    : q == Quant::Int8G ? sc[n * (K / 32) + k / 32]
+                                                        : sc[n * (K / 16) + k / 16]);
     const uint32_t cw[4] = {c.x, c.y, c.z, c.w};
 #pragma unroll
     for (int i = 0; i < 16; ++i) d[i] = (float)(int8_t)((cw[i >> 2] >> (8 * (i & 3))) & 0xffu) * s;
@@ -984,6 +1003,7 @@ hipError_t launch_gemm(const GemmParams& p, hipStream_t s) {
     case Quant::Int8: return launch_dma_q<Quant::Int8>(p, s);
     case Quant::Int4: return launch_dma_q<Quant::Int4>(p, s);
     case Quant::Int8G: return launch_dma_q<Quant::Int8G>(p, s);
+    case Quant::Int8G16: return launch_dma_q<Quant::Int8G16>(p, s);
     case Quant::Int4M: return launch_dma_q<Quant::Int4M>(p, s);
   }
   return hipErrorInvalidValue;

@@ -413,7 +413,7 @@ hipError_t launch_gemv_q(const GemmParams& p, hipStream_t s) {
 
 bool gemv_supported(const GemmParams& p) {
   auto a4 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 3) == 0; };
-  return p.quant != Quant::None && p.dtype == DType::BF16 && p.m_dev == nullptr &&
+  return p.quant != Quant::None && p.quant != Quant::Int8G16 && p.dtype == DType::BF16 && p.m_dev == nullptr &&
          p.x_head_rows == 0 && !p.x_stats && !p.res_stats && !p.y_stats && p.M >= 1 && p.M <= kGvMaxRows &&
          p.N % 16 == 0 && p.K % kGvUnitK == 0 && (size_t)p.M * p.K * 2 <= (size_t)kGvMaxXBytes &&
          a4(p.scales) && (!quant_int4(p.quant) || a4(p.zeros)) && gemv_plan(p).lds <= 160 * 1024;

@@ -12,9 +12,14 @@ namespace rlx {
 enum class DType : int { F32 = 0, BF16 = 1 };
 // Weight layouts of the dequantising matmul: Int8 per-channel scales; Int4
 // group-32 scale and zero-point, W = (q - z) s; Int8G int8 codes with group-32
-// scales, W = q s; Int4M group-32 scale and min, W = q s + m.
-enum class Quant : int { None = 0, Int8 = 1, Int4 = 2, Int8G = 3, Int4M = 4 };
-__host__ __device__ constexpr bool quant_int8(Quant q) { return q == Quant::Int8 || q == Quant::Int8G; }
+// scales, W = q s; Int4M group-32 scale and min, W = q s + m; Int8G16 int8
+// codes with group-16 scales, W = q s.
+enum class Quant : int { None = 0, Int8 = 1, Int4 = 2, Int8G = 3, Int4M = 4, Int8G16 = 5 };
+__host__ __device__ constexpr bool quant_int8(Quant q) {
+  return q == Quant::Int8 || q == Quant::Int8G || q == Quant::Int8G16;
+}
+// Weights per scale of a grouped layout.
+__host__ __device__ constexpr int quant_group_size(Quant q) { return q == Quant::Int8G16 ? 16 : 32; }
 __host__ __device__ constexpr bool quant_int4(Quant q) { return q == Quant::Int4 || q == Quant::Int4M; }
 enum class Epi : int { None = 0, Bias = 1, BiasGelu = 2, BiasResidual = 3 };
 
@@ -65,7 +70,7 @@ inline const char* epi_name(Epi e) {
 }
 inline const char* quant_name(Quant q) {
   return q == Quant::None ? "dense" : q == Quant::Int8 ? "int8" : q == Quant::Int4 ? "int4-zp"
-         : q == Quant::Int8G ? "int8-group" : "int4-min";
+         : q == Quant::Int8G ? "int8-group" : q == Quant::Int8G16 ? "int8-group16" : "int4-min";
 }
 // True when the deferred-LayerNorm fields are implemented for rows of H columns.
 bool gemm_deferred_ln_supported(DType dt, Quant q, int H);

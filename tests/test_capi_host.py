@@ -203,9 +203,21 @@ def test_new_schemes_argument_errors(L):
     st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, rlx.Q_INT8_GROUP, p16, None, 64, 64, None, None,
                               rlx.EPI_NONE, p16, rlx.BF16, None)
     assert st == rlx.ERR_UNSUPPORTED
-    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, 5, p16, p16, 32, 64, None, None, rlx.EPI_NONE, p16, rlx.BF16,
+    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, 6, p16, p16, 32, 64, None, None, rlx.EPI_NONE, p16, rlx.BF16,
                               None)
     assert st == rlx.ERR_INVALID_ARG  # unknown scheme
+    # int8 with a scale per 16 (GGUF Q6_K's layout): scales required, group size 16 only
+    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, rlx.Q_INT8_GROUP16, None, None, 16, 64, None, None,
+                              rlx.EPI_NONE, p16, rlx.BF16, None)
+    assert st == rlx.ERR_INVALID_ARG
+    st = L.rlx_dequant_matmul(p16, rlx.BF16, 4, 64, p16, rlx.Q_INT8_GROUP16, p16, None, 32, 64, None, None,
+                              rlx.EPI_NONE, p16, rlx.BF16, None)
+    assert st == rlx.ERR_UNSUPPORTED and b"group size 16" in L.rlx_last_error()
+    # K-quant repack: K a multiple of 256; Q4_K needs the mins array
+    assert L.rlx_gguf_repack(p16, rlx.GGUF_Q4_K, 64, 128, p16, p16, p16, None, None) == rlx.ERR_UNSUPPORTED
+    assert L.rlx_gguf_repack(p16, rlx.GGUF_Q4_K, 64, 256, p16, p16, None, None, None) == rlx.ERR_INVALID_ARG
+    assert L.rlx_gguf_repack(p16, rlx.GGUF_Q6_K, 64, 320, p16, p16, None, None, None) == rlx.ERR_UNSUPPORTED
+    assert L.rlx_gguf_repack(p16, 13, 64, 256, p16, p16, p16, None, None) == rlx.ERR_UNSUPPORTED  # Q5_K
 
 
 def test_encoder_forward_noalloc_argument_errors(L):

@@ -42,7 +42,7 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-SCHEMES = ["int8", "int4", "int8g", "int4m"]
+SCHEMES = ["int8", "int4", "int8g", "int4m", "int8g16"]
 EPIS = ["none", "bias", "gelu", "residual"]
 
 # path -> (M, N, K): the dispatch rule that selects it is stated beside each
@@ -97,6 +97,11 @@ class Weights:
             self.q = rng.integers(-127, 128, (N, K)).astype(np.int8)
             self.scales = (rng.uniform(0.5, 2.0, (N, K // 32)) * 2e-4).astype(np.float16)
             self.w = dequant_int8_group(self.q, self.scales)
+        elif scheme == "int8g16":  # GGUF Q6_K's layout: a scale per 16 weights
+            self.q = rng.integers(-32, 32, (N, K)).astype(np.int8)
+            self.scales = (rng.choice([-1.0, 1.0], (N, K // 16)) * rng.uniform(0.5, 2.0, (N, K // 16)) *
+                           5e-4).astype(np.float16)
+            self.w = oracle.gguf.dequant_int8_group16(self.q, self.scales)
         else:
             codes = rng.integers(0, 16, (N, K)).astype(np.uint8)
             self.q = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
@@ -106,11 +111,12 @@ class Weights:
 
     def run(self, rlx, x, *, bias=None, residual=None, epi="none", out_dtype=None):
         scheme = {"int8": rlx.Q_INT8_PER_CHANNEL, "int4": rlx.Q_INT4_GROUP_ZP, "int8g": rlx.Q_INT8_GROUP,
-                  "int4m": rlx.Q_INT4_GROUP_MIN}[self.scheme]
-        qd = _dev(self.q, torch.int8 if self.scheme in ("int8", "int8g") else torch.uint8)
+                  "int4m": rlx.Q_INT4_GROUP_MIN, "int8g16": rlx.Q_INT8_GROUP16}[self.scheme]
+        qd = _dev(self.q, torch.int8 if self.scheme in ("int8", "int8g", "int8g16") else torch.uint8)
         rdt = torch.float32 if out_dtype == torch.float32 else torch.bfloat16
         y = rlx.dequant_matmul(_dev(x, torch.bfloat16), qd, scheme=scheme, scales=_dev(self.scales, torch.float16),
-                               zeros=None if self.zeros is None else _dev(self.zeros, torch.float16), group_size=32,
+                               zeros=None if self.zeros is None else _dev(self.zeros, torch.float16),
+                               group_size=16 if self.scheme == "int8g16" else 32,
                                N=self.w.shape[0], bias=None if bias is None else _dev(bias, torch.float32),
                                residual=None if residual is None else _dev(residual, rdt), epi=_epi_code(rlx, epi),
                                out_dtype=out_dtype)
@@ -137,7 +143,9 @@ def test_one_hot_unpack_bit_exact(rlx, scheme, path):
     for off in offsets:
         x, k = _one_hot_rows(M, K, off)
         got = W.run(rlx, x).view(torch.int16).cpu().numpy().view(np.uint16)
-        want = _rne_bf16_bits(W.w[:, k].T.astype(np.float32))
+        # + 0.0: the dot product's accumulator starts at +0, so a -0 weight (q = 0 under a
+        # negative scale) gives +0 (IEEE: +0 + -0 = +0)
+        want = _rne_bf16_bits((W.w[:, k].T + 0.0).astype(np.float32))
         if ulp_ok:
             diff = np.abs(got.astype(np.int32) - want.astype(np.int32))
             assert diff.max() <= 1, f"{scheme} {path}: {np.count_nonzero(diff > 1)} outputs off by more than 1 ulp"

@@ -100,3 +100,70 @@ def test_binding_rejects_a_short_block_tensor(rlx):
         rlx.gguf_repack(blocks, "q4_0", N=64, K=128)  # block tensor too small for the shape
     with pytest.raises(ValueError):
         rlx.gguf_repack(blocks, 6, N=64, K=64)  # Q5_0 is not supported
+
+
+# --- K-quants -----------------------------------------------------------------
+
+KFMTS = ("q4_k", "q6_k")
+
+
+def _kq_internal_w(blocks, fmt, K):
+    kind, c, s, m = oracle.gguf.kquant_internal(blocks, fmt, K)
+    if kind == "int4_min":
+        return kind, c, s, m, oracle.gguf.dequant_int4_min(c, s, m)
+    return kind, c, s, m, oracle.gguf.dequant_int8_group16(c, s)
+
+
+@pytest.mark.parametrize("fmt", KFMTS)
+@pytest.mark.parametrize("N,K", [(64, 256), (256, 512), (384, 1536)])
+def test_kquant_repack_matches_the_oracle(rlx, fmt, N, K):
+    """Q4_K -> int4 with mins, Q6_K -> int8 with a scale per 16: codes,
+    f16 scales and mins bit for bit as the oracle composes and rounds them;
+    the unpacked weights bit for bit as the oracle's layout values, and
+    within 2^-11 (|s q| + |m|) of the format's own values."""
+    blocks = wg.random_kquant_blocks(np.random.default_rng(810 + N + K), N, K, fmt)
+    scheme, codes, scales, zeros = rlx.gguf_repack(_dev(blocks), fmt, N=N, K=K)
+    kind, c, s, m, w = _kq_internal_w(blocks, fmt, K)
+    assert scheme == (rlx.Q_INT4_GROUP_MIN if fmt == "q4_k" else rlx.Q_INT8_GROUP16)
+    assert np.array_equal(codes.cpu().numpy().view(np.uint8), c.view(np.uint8))
+    assert np.array_equal(scales.cpu().numpy().view(np.uint16), s.view(np.uint16))
+    if m is not None:
+        assert np.array_equal(zeros.cpu().numpy().view(np.uint16), m.view(np.uint16))
+    else:
+        assert zeros is None
+    got = rlx.dequant_unpack(codes, scheme=scheme, scales=scales, zeros=zeros, group_size=16 if fmt == "q6_k" else 32,
+                             N=N, K=K).cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), w.astype(np.float32).view(np.uint32))
+    gs, qmax = (32, 15) if fmt == "q4_k" else (16, 32)
+    bound = 2.0 ** -11 * 1.001 * (np.repeat(np.abs(s.astype(np.float64)), gs, axis=1) * qmax +
+                                  (np.repeat(np.abs(m.astype(np.float64)), gs, axis=1) if m is not None else 0.0))
+    assert np.all(np.abs(got - oracle.gguf.dequant_k(blocks, fmt, K)) <= bound)
+
+
+# rows 1..300; the int8 group-16 layout has no few-row kernel (tiled at every M); K >= 1024 takes the LDS-DMA kernel
+KSHAPES = [(1, 256, 512), (7, 384, 512), (40, 1024, 1024), (300, 384, 1536), (16, 512, 4096)]
+
+
+@pytest.mark.parametrize("fmt", KFMTS)
+@pytest.mark.parametrize("M,N,K", KSHAPES)
+def test_kquant_matmul_parity(rlx, fmt, M, N, K):
+    """Against the oracle on the repacked layout's weights (whose distance to
+    the format's values is the repack test's bound): fp32 accumulation, bf16
+    output rounding and the tiled path's bf16 rounding of each weight."""
+    rng = np.random.default_rng(1200 + M + N + K)
+    x = to_bf16_exact(rng.normal(0, 1, (M, K)))
+    blocks = wg.random_kquant_blocks(rng, N, K, fmt)
+    b = rng.normal(0, 0.5, N).astype(np.float32)
+    epi = ("bias", "gelu", "none")[(M + K) % 3]
+    scheme, codes, scales, zeros = rlx.gguf_repack(_dev(blocks), fmt, N=N, K=K)
+    code = {"none": rlx.EPI_NONE, "bias": rlx.EPI_BIAS, "gelu": rlx.EPI_BIAS_GELU}[epi]
+    y = rlx.dequant_matmul(_dev(x, torch.bfloat16), codes, scheme=scheme, scales=scales, zeros=zeros,
+                           group_size=16 if fmt == "q6_k" else 32, N=N, bias=_dev(b, torch.float32), epi=code)
+    torch.cuda.synchronize()
+    w = _kq_internal_w(blocks, fmt, K)[-1]
+    ref = oracle.linear(x, w, None if epi == "none" else b)
+    pre = None
+    if epi == "gelu":
+        pre, ref = ref, oracle.gelu(ref)
+    tol = gemm_tolerance(x, w, ref, out_bf16=True, weight_rel=2.0 ** -9, pre=pre) + 2.0 ** -24 * 4 * np.abs(ref)
+    assert_within(y.float().cpu().numpy(), ref, tol, f"gguf {fmt} {epi} {M}x{N}x{K}")
