@@ -363,10 +363,15 @@ def gemv_bytes(scheme, M, N, K, epi_bias=True):
     """Algorithmic HBM bytes of one few-row dequantising matmul: every weight
     code, scale and zero-point (or min) once, the activations, the bias and the
     output.  GGUF schemes count their repacked layout (Q4_0 and Q4_1: int4
-    codes, f16 scales and f16 zeros / mins; Q8_0: int8 codes and f16 scales)."""
-    four = scheme in ("int4", "q4_0", "q4_1")
+    codes, f16 scales and f16 zeros / mins; Q8_0: int8 codes and f16 scales;
+    Q4_K: as Q4_1, a composed f16 scale and min per 32 weights; Q6_K: int8
+    codes and a composed f16 scale per 16 weights)."""
+    four = scheme in ("int4", "q4_0", "q4_1", "q4_k")
     codes = N * K // 2 if four else N * K
-    meta = 2 * N * (K // 32) * 2 if four else (2 * N * (K // 32) if scheme == "q8_0" else 2 * N)
+    if four:
+        meta = 2 * N * (K // 32) * 2
+    else:
+        meta = {"q8_0": 2 * N * (K // 32), "q6_k": 2 * N * (K // 16)}.get(scheme, 2 * N)
     return codes + meta + 2 * M * K + 2 * M * N + (4 * N if epi_bias else 0)
 
 
@@ -388,12 +393,16 @@ def bench_dequant_gemv(args):
     wf = rng.normal(0, 0.02, (N, K)).astype(np.float32)
     b = rng.normal(0, 0.5, N).astype(np.float32)
     dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=dt)
-    if scheme in ("q4_0", "q4_1", "q8_0"):
+    if scheme in ("q4_0", "q4_1", "q8_0", "q4_k", "q6_k"):
         from workloads import gguf as wg
-        blocks = wg.quantize(wf, scheme)
+        if scheme in ("q4_k", "q6_k"):
+            # no K-quant quantiser here: random super-blocks stream the same bytes
+            blocks = wg.random_kquant_blocks(rng, N, K, scheme)
+        else:
+            blocks = wg.quantize(wf, scheme)
         sch, codes, scl, zr = rlx.gguf_repack(dev(blocks, torch.uint8), scheme, N=N, K=K)
         one = (codes, scl, zr)
-        kw = dict(scheme=sch, group_size=32)
+        kw = dict(scheme=sch, group_size=16 if scheme == "q6_k" else 32)
     elif scheme == "int8":
         q, s = workloads.quantize_int8_per_channel(wf)
         one = (dev(q, torch.int8), dev(s, torch.float16), None)
@@ -430,8 +439,10 @@ def bench_dequant_gemv(args):
         "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(us / 1e3, 5), "p50_ms": round(us / 1e3, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": f"synthetic (N(0,0.02) weights quantised {scheme}{' (GGUF blocks, repacked)' if scheme.startswith('q') else ''}, "
-                f"N(0,1) bf16 activations), {copies} weight copies",
+        "data": (f"synthetic (random {scheme} super-blocks: uniform codes, scales and mins, repacked"
+                 if scheme in ("q4_k", "q6_k") else
+                 f"synthetic (N(0,0.02) weights quantised {scheme}{' (GGUF blocks, repacked)' if scheme.startswith('q') else ''}")
+                + f", N(0,1) bf16 activations), {copies} weight copies",
         "config": {"workload": name, "M": M, "N": N, "K": K, "scheme": scheme, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "gemv_q_kernel", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
@@ -444,7 +455,9 @@ def bench_dequant_gemv(args):
         t0 = time.perf_counter()
         reps = 0
         while True:
-            if scheme in ("q4_0", "q4_1", "q8_0"):
+            if scheme in ("q4_k", "q6_k"):
+                wd = oracle.gguf.dequant_k(blocks[:cols], scheme, K)
+            elif scheme in ("q4_0", "q4_1", "q8_0"):
                 wd = oracle.gguf.dequant(blocks[:cols], scheme, K)
             elif scheme == "int8":
                 wd = oracle.dequant_int8(q[:cols], s[:cols])
@@ -482,7 +495,7 @@ def main():
                          "dequant_gemv: the few-row dequantising matmul; attention: rlx_masked_attention")
     ap.add_argument("--attn-kind", default="causal", choices=("none", "causal", "sliding", "custom"))
     ap.add_argument("--attn-window", type=int, default=128)
-    ap.add_argument("--gemv-scheme", default="int4", choices=("int4", "int8", "q4_0", "q4_1", "q8_0"))
+    ap.add_argument("--gemv-scheme", default="int4", choices=("int4", "int8", "q4_0", "q4_1", "q8_0", "q4_k", "q6_k"))
     ap.add_argument("--gemv-shape", type=int, nargs=3, default=(1, 14336, 4096), metavar=("M", "N", "K"))
     ap.add_argument("--mx-format", default="e4m3", choices=sorted(MX_PEAK_TFLOPS))
     ap.add_argument("--mx-shape", type=int, nargs=3, default=(18048, 384, 1536), metavar=("M", "N", "K"))

@@ -82,8 +82,7 @@ typedef RLX_ENUM {
                                   [N, K/group]; W = q * s[n,g] + m[n,g]
                                   (GGUF Q4_1 and Q4_K after rlx_gguf_repack)         */
   RLX_Q_INT8_GROUP16 = 5       /* w int8 [N,K]; scales f16 [N, K/16]; group_size 16;
-                                  W = q * s[n, k/16] (GGUF Q6_K after rlx_gguf_repack).
-                                  Tiled matmul path only (no few-row kernel)          */
+                                  W = q * s[n, k/16] (GGUF Q6_K after rlx_gguf_repack) */
 } rlx_quant;
 
 typedef RLX_ENUM {
@@ -141,8 +140,8 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
  * Few rows (the GEMV regime: 1 <= M <= 16, quantised weights, K a multiple
  * of 128, M * K * 2 <= 65536, scales and zeros 4-byte aligned) take a
  * dedicated kernel that streams the weights once: int8 per-channel as above;
- * no group-scheme weight is rounded: per 32-k group, int8 group gives
- * s * sum_k x_k q_k, int4 s * (sum_k x_k (128 + q_k) - (128 + z) sum_k x_k),
+ * no group-scheme weight is rounded: per group, int8 group (32 or 16 k)
+ * gives s * sum_k x_k q_k, int4 s * (sum_k x_k (128 + q_k) - (128 + z) sum_k x_k),
  * int4 min s * sum_k x_k (128 + q_k) + (m - 128 s) sum_k x_k, all in fp32.  Results of both paths are deterministic (the same
  * inputs give the same bits), and a row's result does not depend on the
  * other rows of the call.
@@ -150,7 +149,8 @@ rlx_status rlx_masked_attention(const void* q, const void* k, const void* v, int
  * int4 min: q * s + m formed in fp32 (one rounding) and rounded to bf16
  * (both except in the few-row path below).
  * Supported: M >= 0 (M == 0 is a no-op), N and K positive multiples of 64,
- * group_size == 32 for the group schemes (ignored for int8 per-channel),
+ * group_size == 32 for the group schemes (16 for RLX_Q_INT8_GROUP16;
+ * ignored for int8 per-channel),
  * 16-byte aligned x, w, residual and y; y_dt as above.  Otherwise
  * RLX_ERR_UNSUPPORTED.
  */

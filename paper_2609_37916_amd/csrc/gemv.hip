@@ -3,8 +3,9 @@
 //
 //   y[m, n] = epi( sum_k x[m, k] W[n, k] ),   1 <= M <= 16 bf16 rows,
 //
-// with W in the int8 per-channel, int4 group-32 zero-point, int8 group-32 or
-// int4 group-32 min layout (the last two also hold GGUF Q8_0 / Q4_1 weights).
+// with W in the int8 per-channel, int4 group-32 zero-point, int8 group-32,
+// int8 group-16 or int4 group-32 min layout (the last three also hold GGUF
+// Q8_0, Q6_K and Q4_1 / Q4_K weights).
 // With so few rows the product reads every weight byte once and does little
 // arithmetic per byte: it is bound by HBM bandwidth and by the vector-ALU
 // work of unpacking the codes, not by the matrix cores.
@@ -41,7 +42,11 @@
 //  * int8 per-channel: codes convert exactly to bf16 and one accumulator
 //    takes every group; the per-channel scale multiplies the fp32 sum in the
 //    epilogue, as in the tiled path.  int8 group: each group's product is
-//    scaled by its s with four FMAs a lane, as for int4.
+//    scaled by its s with four FMAs a lane, as for int4.  int8 group-16: a
+//    32-k instruction would add two groups of different scale, so each group
+//    of 32 takes two instructions, the lanes of the other half (k-octets 2, 3
+//    for the first, 0, 1 for the second) supplying zero codes; each product is
+//    scaled by its own s, as for group 32.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -68,6 +73,11 @@ struct GvUnit<Quant::Int4M> : GvUnit<Quant::Int4> {};  // zeros hold the mins
 template <>
 struct GvUnit<Quant::Int8G> {
   // codes: 16 rows x 128 bytes; meta: 16 rows x 4 f16 scales (then a copy)
+  static constexpr int kCodeBytes = 2048, kMetaBytes = 256, kLoads = 3, kDepth = 3;
+};
+template <>
+struct GvUnit<Quant::Int8G16> {
+  // codes: 16 rows x 128 bytes; meta: 16 rows x 8 f16 scales
   static constexpr int kCodeBytes = 2048, kMetaBytes = 256, kLoads = 3, kDepth = 3;
 };
 template <>
@@ -195,12 +205,15 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
   const uint8_t* wlane = reinterpret_cast<const uint8_t*>(p.w) + (size_t)l16 * wpitch + G * 16;
   // int4 scales and zeros ([N][K/32] f16): lanes < 32 move the scales of row
   // lane/2, the others the zeros of row (lane-32)/2, two groups (4 bytes) each
-  const size_t gpitch = (size_t)K / 32 * 2;
-  // (int8 group scales: every lane moves scales, lanes >= 32 a second copy)
+  // (int8 group scales: every lane moves scales, lanes >= 32 a second copy;
+  // group 16 ([N][K/16] f16): lane moves two of the eight scales of row lane/4)
+  constexpr bool kG16 = Q == Quant::Int8G16;
+  const size_t gpitch = (size_t)K / (kG16 ? 16 : 32) * 2;
   const uint8_t* mlane =
       U::kMetaBytes == 0 ? nullptr
-                         : reinterpret_cast<const uint8_t*>(lane < 32 || Q == Quant::Int8G ? p.scales : p.zeros) +
-                               (size_t)((lane & 31) >> 1) * gpitch + (lane & 1) * 4;
+      : kG16 ? reinterpret_cast<const uint8_t*>(p.scales) + (size_t)(lane >> 2) * gpitch + (lane & 3) * 4
+             : reinterpret_cast<const uint8_t*>(lane < 32 || Q == Quant::Int8G ? p.scales : p.zeros) +
+                   (size_t)((lane & 31) >> 1) * gpitch + (lane & 1) * 4;
   const uint32_t ring_addr = lds_addr_of(ring), meta_addr = lds_addr_of(meta);
   auto issue = [&](int i) {
     const int tt = i / nu, u = wave + (i - tt * nu) * kGvWaves;
@@ -213,7 +226,7 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
       lds_dma16(wlane + row0 * wpitch + (size_t)u * 128 + 64, __builtin_amdgcn_readfirstlane(slot + 1024));
     }
     if constexpr (U::kMetaBytes > 0)
-      lds_dma4(mlane + row0 * gpitch + (size_t)u * 8,
+      lds_dma4(mlane + row0 * gpitch + (size_t)u * (kG16 ? 16 : 8),
                __builtin_amdgcn_readfirstlane(meta_addr + (uint32_t)((i % U::kDepth) * U::kMetaBytes)));
   };
   // The activations are waited for before any item load goes out.  (Issuing
@@ -306,6 +319,26 @@ __global__ __launch_bounds__(kGvThreads) void gemv_q_kernel(GemmParams p) {
         const float s0 = f16_lo(sv.x), s1 = f16_hi(sv.x), s2 = f16_lo(sv.y), s3 = f16_hi(sv.y);
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[r] = fmaf(s0, v0[r], fmaf(s1, v1[r], fmaf(s2, v2[r], fmaf(s3, v3[r], acc[r]))));
+      } else if constexpr (Q == Quant::Int8G16) {
+        const uint2* cw = reinterpret_cast<const uint2*>(slot + (G >> 1) * 256 + l16 * 16 + (G & 1) * 8);
+        const uint2 c0 = cw[0], c1 = cw[64], c2 = cw[128], c3 = cw[192];
+        const uint4 sv = *reinterpret_cast<const uint4*>(mslot + l16 * 16);
+        wait_lgkmcnt0();
+        if (i + U::kDepth < items) issue(i + U::kDepth);
+        // group 2q (k 32q .. 32q + 15) is k-octets 0, 1 of instruction q, group 2q + 1 octets 2, 3
+        const bool first = G < 2;
+        const bf16x8_t zb = as_bf16x8(make_uint4(0u, 0u, 0u, 0u));
+        const uint2 cc[4] = {c0, c1, c2, c3};
+        const uint32_t sw[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const bf16x8_t b = int8_octet_as_bf16(cc[q].x, cc[q].y);
+          const f32x4_t va = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[q], first ? b : zb, zero4, 0, 0, 0);
+          const f32x4_t vb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[q], first ? zb : b, zero4, 0, 0, 0);
+          const float sa = f16_lo(sw[q]), sb = f16_hi(sw[q]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[r] = fmaf(sa, va[r], fmaf(sb, vb[r], acc[r]));
+        }
       } else {
         const uint2* cw = reinterpret_cast<const uint2*>(slot + (G >> 1) * 256 + l16 * 16 + (G & 1) * 8);
         const uint2 c0 = cw[0], c1 = cw[64], c2 = cw[128], c3 = cw[192];
@@ -370,9 +403,11 @@ GvPlan gemv_plan(const GemmParams& p) {
   using U4 = GvUnit<Quant::Int4>;
   using U8 = GvUnit<Quant::Int8>;
   using U8G = GvUnit<Quant::Int8G>;
-  const int ring = quant_int4(p.quant) ? U4::kDepth * (U4::kCodeBytes + U4::kMetaBytes)
-                   : p.quant == Quant::Int8G ? U8G::kDepth * (U8G::kCodeBytes + U8G::kMetaBytes)
-                                             : U8::kDepth * (U8::kCodeBytes + U8::kMetaBytes);
+  using U8G16 = GvUnit<Quant::Int8G16>;
+  const int ring = quant_int4(p.quant)            ? U4::kDepth * (U4::kCodeBytes + U4::kMetaBytes)
+                   : p.quant == Quant::Int8G     ? U8G::kDepth * (U8G::kCodeBytes + U8G::kMetaBytes)
+                   : p.quant == Quant::Int8G16   ? U8G16::kDepth * (U8G16::kCodeBytes + U8G16::kMetaBytes)
+                                                 : U8::kDepth * (U8::kCodeBytes + U8::kMetaBytes);
   const size_t base = (size_t)kGvWaves * ring + 2 * kGvWaves * 1024 + (size_t)p.M * p.K * 2 +
                       (size_t)p.M * (p.K / 32) * 4;
   const int tiles = p.N / 16;
@@ -413,7 +448,7 @@ hipError_t launch_gemv_q(const GemmParams& p, hipStream_t s) {
 
 bool gemv_supported(const GemmParams& p) {
   auto a4 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 3) == 0; };
-  return p.quant != Quant::None && p.quant != Quant::Int8G16 && p.dtype == DType::BF16 && p.m_dev == nullptr &&
+  return p.quant != Quant::None && p.dtype == DType::BF16 && p.m_dev == nullptr &&
          p.x_head_rows == 0 && !p.x_stats && !p.res_stats && !p.y_stats && p.M >= 1 && p.M <= kGvMaxRows &&
          p.N % 16 == 0 && p.K % kGvUnitK == 0 && (size_t)p.M * p.K * 2 <= (size_t)kGvMaxXBytes &&
          a4(p.scales) && (!quant_int4(p.quant) || a4(p.zeros)) && gemv_plan(p).lds <= 160 * 1024;
@@ -426,6 +461,7 @@ hipError_t launch_gemv(const GemmParams& p, hipStream_t s) {
     case Quant::Int4M: return launch_gemv_q<Quant::Int4M>(p, s);
     case Quant::Int8: return launch_gemv_q<Quant::Int8>(p, s);
     case Quant::Int8G: return launch_gemv_q<Quant::Int8G>(p, s);
+    case Quant::Int8G16: return launch_gemv_q<Quant::Int8G16>(p, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -1,5 +1,6 @@
 """GPU parity of the GGUF path: rlx_gguf_repack rewrites Q4_0 / Q4_1 / Q8_0
-blocks into the int4 zero-point / int4 min / int8 group layouts, and
+blocks into the int4 zero-point / int4 min / int8 group layouts (and the
+K-quants Q4_K / Q6_K into int4 min / int8 group-16), and
 rlx_dequant_matmul multiplies with them (the tiled path for many rows, the
 few-row path for 1..16), through the C ABI, against ``oracle.gguf``.
 
@@ -140,8 +141,26 @@ def test_kquant_repack_matches_the_oracle(rlx, fmt, N, K):
     assert np.all(np.abs(got - oracle.gguf.dequant_k(blocks, fmt, K)) <= bound)
 
 
-# rows 1..300; the int8 group-16 layout has no few-row kernel (tiled at every M); K >= 1024 takes the LDS-DMA kernel
+# rows 1..300: 1 and 7 rows take the few-row kernel, the others the tiled path (16 x 4096 is past the
+# few-row kernel's 64 KB of activations); K >= 1024 takes the LDS-DMA kernel
 KSHAPES = [(1, 256, 512), (7, 384, 512), (40, 1024, 1024), (300, 384, 1536), (16, 512, 4096)]
+
+
+def _few_rows(M, K):
+    return 1 <= M <= 16 and K % 128 == 0 and M * K * 2 <= 64 * 1024
+
+
+def _kq_tolerance(x, w, ref, fmt, s, m, few_rows, pre=None):
+    """fp32 accumulation and bf16 output (gemm_tolerance), the tiled path's
+    bf16 rounding of each weight (2^-9 |W|), the scaled fp32 group sums
+    (4 x 2^-24 |y|) and, for Q4_K's int4-min layout on the few-row path, the
+    offset arithmetic 2^-9 sum_k |x_k| (|s| + |m|) of test_gpu_gemv.py's
+    derivation."""
+    tol = gemm_tolerance(x, w, ref, out_bf16=True, weight_rel=2.0 ** -9, pre=pre) + 2.0 ** -24 * 4 * np.abs(ref)
+    if few_rows and m is not None:
+        sm = np.repeat(np.abs(s.astype(np.float64)) + np.abs(m.astype(np.float64)), 32, axis=1)
+        tol = tol + 2.0 ** -9 * (np.abs(x.astype(np.float64)) @ sm.T)
+    return tol
 
 
 @pytest.mark.parametrize("fmt", KFMTS)
@@ -160,10 +179,32 @@ def test_kquant_matmul_parity(rlx, fmt, M, N, K):
     y = rlx.dequant_matmul(_dev(x, torch.bfloat16), codes, scheme=scheme, scales=scales, zeros=zeros,
                            group_size=16 if fmt == "q6_k" else 32, N=N, bias=_dev(b, torch.float32), epi=code)
     torch.cuda.synchronize()
-    w = _kq_internal_w(blocks, fmt, K)[-1]
+    _, _, s, m, w = _kq_internal_w(blocks, fmt, K)
     ref = oracle.linear(x, w, None if epi == "none" else b)
     pre = None
     if epi == "gelu":
         pre, ref = ref, oracle.gelu(ref)
-    tol = gemm_tolerance(x, w, ref, out_bf16=True, weight_rel=2.0 ** -9, pre=pre) + 2.0 ** -24 * 4 * np.abs(ref)
+    tol = _kq_tolerance(x, w, ref, fmt, s, m, _few_rows(M, K), pre=pre)
     assert_within(y.float().cpu().numpy(), ref, tol, f"gguf {fmt} {epi} {M}x{N}x{K}")
+
+
+@pytest.mark.parametrize("fmt", KFMTS)
+@pytest.mark.parametrize("M", [1, 8])
+def test_kquant_decode_shape_sampled_columns(rlx, fmt, M):
+    """The decode-sized product of the dequantising GEMV benchmark (N 14336,
+    K 4096) on the few-row kernel, 96 sampled output columns against the
+    oracle (which dequantises only those weight rows)."""
+    N, K = 14336, 4096
+    rng = np.random.default_rng(7300 + M + len(fmt))
+    x = to_bf16_exact(rng.normal(0, 1, (M, K)))
+    blocks = wg.random_kquant_blocks(rng, N, K, fmt)
+    b = rng.normal(0, 0.5, N).astype(np.float32)
+    cols = np.sort(np.concatenate([rng.choice(N, 94, replace=False), [0, N - 1]]))
+    scheme, codes, scales, zeros = rlx.gguf_repack(_dev(blocks), fmt, N=N, K=K)
+    y = rlx.dequant_matmul(_dev(x, torch.bfloat16), codes, scheme=scheme, scales=scales, zeros=zeros,
+                           group_size=16 if fmt == "q6_k" else 32, N=N, bias=_dev(b, torch.float32), epi=rlx.EPI_BIAS)
+    torch.cuda.synchronize()
+    _, _, s, m, w = _kq_internal_w(blocks[cols], fmt, K)
+    ref = oracle.linear(x, w, b[cols])
+    tol = _kq_tolerance(x, w, ref, fmt, s, m, few_rows=True)
+    assert_within(y.float().cpu().numpy()[:, cols], ref, tol, f"decode shape {fmt} M={M}")
