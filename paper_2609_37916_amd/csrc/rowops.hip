@@ -20,47 +20,61 @@
 namespace rlx {
 namespace {
 
-constexpr int kScanSeqs = 4;    // sequences per wave whose mask loads are in flight together
-constexpr int kScanChunks = 8;  // 64-position loads per sequence (S <= 512)
+// The mask scan keeps kScanLoads mask loads per lane in flight: a wave takes
+// kScanLoads / NCH sequences at a time, NCH 64-position loads each (NCH the
+// row length in 64s rounded up to a power of two, S <= 64 * kScanMaxChunks).
+constexpr int kScanLoads = 32;
+constexpr int kScanMaxChunks = 8;
 
-// Mask bytes of sequences b0 .. b0 + kScanSeqs - 1 at positions 64 c + lane,
-// 0 past the batch or the row.  Every load is issued unconditionally at an
+// Mask bytes of sequences b0 .. b0 + SEQS - 1 at positions 64 c + lane, 0
+// past the batch or the row.  Every load is issued unconditionally at an
 // in-bounds (clamped) address and selected afterwards: a load under a
 // per-lane condition gets its own wait for the data, which serialises them.
-// Needs B >= 1 and 1 <= S <= 64 * kScanChunks.
+// Needs B >= 1 and 1 <= S <= 64 * NCH.
+template <int SEQS, int NCH>
 __device__ __forceinline__ void load_mask_group(const uint8_t* mask, int B, int S, int b0, int lane,
-                                                uint8_t (&mb)[kScanSeqs][kScanChunks]) {
-  uint8_t raw[kScanSeqs][kScanChunks];
+                                                uint8_t (&mb)[SEQS][NCH]) {
+  uint8_t raw[SEQS][NCH];
 #pragma unroll
-  for (int g = 0; g < kScanSeqs; ++g)
+  for (int g = 0; g < SEQS; ++g)
 #pragma unroll
-    for (int c = 0; c < kScanChunks; ++c)
-      raw[g][c] = mask[(size_t)min(b0 + g, B - 1) * S + min(64 * c + lane, S - 1)];
+    for (int c = 0; c < NCH; ++c) raw[g][c] = mask[(size_t)min(b0 + g, B - 1) * S + min(64 * c + lane, S - 1)];
 #pragma unroll
-  for (int g = 0; g < kScanSeqs; ++g)
+  for (int g = 0; g < SEQS; ++g)
 #pragma unroll
-    for (int c = 0; c < kScanChunks; ++c) mb[g][c] = (b0 + g < B && 64 * c + lane < S) ? raw[g][c] : 0;
+    for (int c = 0; c < NCH; ++c) mb[g][c] = (b0 + g < B && 64 * c + lane < S) ? raw[g][c] : 0;
 }
 
+template <int NCH>
 __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, int B, int S, int* cu, int* tok_src,
                                                          int* tok_dst, int* order) {
+  constexpr int SEQS = kScanLoads / NCH;
   extern __shared__ int offs[];  // [B+1]: token counts, then their exclusive prefix; then [B] ranks
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-  // each wave takes kScanSeqs sequences at a time and requests all their mask
-  // bytes (64 positions per load, up to 8 per sequence) before the first
-  // ballot: one memory round trip per group instead of one per 64 positions
-  const int nch = (S + 63) / 64;
-  for (int b0 = wave * kScanSeqs; b0 < B; b0 += nw * kScanSeqs) {
-    uint8_t mb[kScanSeqs][kScanChunks];
-    load_mask_group(mask, B, S, b0, lane, mb);
+  // Each wave takes SEQS sequences at a time and requests all their mask
+  // bytes before the first ballot: one memory round trip per group.  The
+  // wave's first group stays in registers for the second pass (the only
+  // group when B <= 16 * SEQS, e.g. 256 sequences of <= 128 positions).
+  const int first = wave * SEQS, stride = nw * SEQS;
+  uint8_t mb0[SEQS][NCH];
+  auto count = [&](int b0, const uint8_t (&mb)[SEQS][NCH]) {
 #pragma unroll
-    for (int g = 0; g < kScanSeqs; ++g) {
+    for (int g = 0; g < SEQS; ++g) {
       int cnt = 0;
 #pragma unroll
-      for (int c = 0; c < kScanChunks; ++c) cnt += __popcll(__ballot(mb[g][c] != 0));
+      for (int c = 0; c < NCH; ++c) cnt += __popcll(__ballot(mb[g][c] != 0));
       if (lane == 0 && b0 + g < B) offs[b0 + g] = cnt;
     }
+  };
+  if (first < B) {
+    load_mask_group<SEQS, NCH>(mask, B, S, first, lane, mb0);
+    count(first, mb0);
+  }
+  for (int b0 = first + stride; b0 < B; b0 += stride) {
+    uint8_t mb[SEQS][NCH];
+    load_mask_group<SEQS, NCH>(mask, B, S, b0, lane, mb);
+    count(b0, mb);
   }
   __syncthreads();
   // Sequences by token count, longest first (ties by index), for kernels that
@@ -103,17 +117,14 @@ __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, in
   }
   __syncthreads();
   for (int i = threadIdx.x; i <= B; i += blockDim.x) cu[i] = offs[i];
-  for (int b0 = wave * kScanSeqs; b0 < B; b0 += nw * kScanSeqs) {
-    uint8_t mb[kScanSeqs][kScanChunks];
-    load_mask_group(mask, B, S, b0, lane, mb);
+  auto emit = [&](int b0, const uint8_t (&mb)[SEQS][NCH]) {
 #pragma unroll
-    for (int g = 0; g < kScanSeqs; ++g) {
+    for (int g = 0; g < SEQS; ++g) {
       const int b = b0 + g;
       if (b >= B) break;  // wave-uniform
       int base = offs[b];
 #pragma unroll
-      for (int c = 0; c < kScanChunks; ++c) {
-        if (c >= nch) break;
+      for (int c = 0; c < NCH; ++c) {
         const int s = 64 * c + lane;
         const bool v = mb[g][c] != 0;
         const uint64_t bal = __ballot(v);
@@ -126,6 +137,12 @@ __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, in
         base += __popcll(bal);
       }
     }
+  };
+  if (first < B) emit(first, mb0);
+  for (int b0 = first + stride; b0 < B; b0 += stride) {
+    uint8_t mb[SEQS][NCH];
+    load_mask_group<SEQS, NCH>(mask, B, S, b0, lane, mb);
+    emit(b0, mb);
   }
 }
 
@@ -526,10 +543,17 @@ inline int blocks_for_rows(int rows) { return (rows + 3) / 4; }
 
 hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, int* order,
                             hipStream_t s) {
-  if (B < 1 || S < 1 || S > 64 * kScanChunks) return hipErrorInvalidValue;
-  RLX_LOG_LAUNCH("mask_scan_kernel", dim3(1), dim3(1024), (size_t)(2 * B + 1) * sizeof(int), "B=%d S=%d", B, S);
-  hipLaunchKernelGGL(mask_scan_kernel, dim3(1), dim3(1024), (size_t)(2 * B + 1) * sizeof(int), s, mask, B, S, cu,
-                     tok_src, tok_dst, B <= kMaxOrderedBatch ? order : nullptr);
+  if (B < 1 || S < 1 || S > 64 * kScanMaxChunks) return hipErrorInvalidValue;
+  const int nch = S <= 64 ? 1 : S <= 128 ? 2 : S <= 256 ? 4 : 8;
+  const size_t lds = (size_t)(2 * B + 1) * sizeof(int);
+  int* ord = B <= kMaxOrderedBatch ? order : nullptr;
+  RLX_LOG_LAUNCH("mask_scan_kernel", dim3(1), dim3(1024), lds, "B=%d S=%d chunks=%d", B, S, nch);
+  switch (nch) {
+    case 1: hipLaunchKernelGGL(mask_scan_kernel<1>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;
+    case 2: hipLaunchKernelGGL(mask_scan_kernel<2>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;
+    case 4: hipLaunchKernelGGL(mask_scan_kernel<4>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;
+    default: hipLaunchKernelGGL(mask_scan_kernel<8>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;
+  }
   return hipGetLastError();
 }
 

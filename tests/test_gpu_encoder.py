@@ -141,17 +141,22 @@ def test_encoder_mask_with_holes_and_empty_row(rlx):
     _compare(got, ref, wl, TOL["bf16"], "mask with holes")
 
 
-def test_encoder_hidden_input_large_ragged_mask_f32(rlx):
+# (batch, seq, hidden): the scan's four row-length classes (<= 64, 128, 256, 512
+# positions), each with more sequences than one pass of its waves covers (512, 256,
+# 128, 64); a narrow layer (2 heads, FFN 128) keeps the oracle quick on the big masks
+@pytest.mark.parametrize("batch,seq,hidden", [(136, 136, 384), (520, 9, 64), (260, 66, 64), (70, 260, 64)])
+def test_encoder_hidden_input_large_ragged_mask_f32(rlx, batch, seq, hidden):
     """Hidden-state input always takes the separate mask scan (counts, prefix,
-    compaction maps): 136 sequences of up to 136 positions (more than 128
-    sequences, a length that is not a multiple of 64), holes, empty sequences
-    at both ends and in the middle, full-length ones; one fp32 layer."""
-    sp = workloads.spec("layer_f32_b2_s16", batch=136, seq=136, layers=1, len_lo=1, len_hi=136)
+    compaction maps): many sequences, lengths that are not multiples of 64,
+    holes, empty sequences at both ends and in the middle, full-length ones;
+    one fp32 layer."""
+    narrow = {} if hidden == 384 else dict(hidden=hidden, heads=hidden // 32, ffn=2 * hidden)
+    sp = workloads.spec("layer_f32_b2_s16", batch=batch, seq=seq, layers=1, len_lo=1, len_hi=seq, **narrow)
     wl = workloads.make(sp, affine=True)
-    rng = np.random.default_rng(21)
+    rng = np.random.default_rng(21 + batch)
     wl.mask = (wl.mask & (rng.random(wl.mask.shape) < 0.7)).astype(np.uint8)
-    wl.mask[[0, 77, 135]] = 0
-    wl.mask[[5, 100]] = 1
+    wl.mask[[0, batch // 2 + 9, batch - 1]] = 0
+    wl.mask[[5, batch // 2 + 32]] = 1
     wl.lengths = wl.mask.sum(axis=1)
     got = _run(rlx, wl)
     ref = oracle.encoder_forward(wl)
