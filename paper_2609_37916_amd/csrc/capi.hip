@@ -516,11 +516,16 @@ rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* m
   }
   const rlx_layer_weights& last = E.layers[c.layers - 1];
   if (c.output_kind == RLX_OUTPUT_POOLED) {
+    // G (the last FFN-up output, consumed by now) holds the partial sums of long sequences
+    float* pool_scratch = static_cast<float*>(E.G);
+    const size_t pool_scratch_bytes = (size_t)T * F * (E.dt == DType::BF16 ? 2 : 4);
     if (E.deferred) {
       STEP(K_POOL, launch_pool_l2(E.X, H, E.cu, B, static_cast<float*>(output), E.dt, ss, E.S2,
-                                  last.ln2_gamma, last.ln2_beta, c.ln_eps, c.quant != RLX_Q_NONE));
+                                  last.ln2_gamma, last.ln2_beta, c.ln_eps, c.quant != RLX_Q_NONE, S, pool_scratch,
+                                  pool_scratch_bytes));
     } else {
-      STEP(K_POOL, launch_pool_l2(E.X, H, E.cu, B, static_cast<float*>(output), E.dt, ss));
+      STEP(K_POOL, launch_pool_l2(E.X, H, E.cu, B, static_cast<float*>(output), E.dt, ss, nullptr, nullptr, nullptr,
+                                  0.0f, false, S, pool_scratch, pool_scratch_bytes));
     }
   } else {
     const void* hid = E.X;

@@ -252,10 +252,15 @@ hipError_t launch_layer_norm(const void* a, const float* gamma, const float* bet
 // out[b] = normalize(mean over the sequence's compact rows) (f32 [B,H]).
 // With x_stats (bf16), x is a deferred-LayerNorm activation (see GemmParams)
 // and the rows are normalised with gamma, beta and eps first; gamma_scaled:
-// the rows are stored gamma-scaled (quantised-weight encoders).
+// the rows are stored gamma-scaled (quantised-weight encoders).  S bounds the
+// sequence lengths (<= 512); with S > 128 each sequence is summed by
+// ceil(S / 64) blocks of 64 rows and combined by a second kernel when
+// `scratch` holds B * ceil(S / 64) * H floats (scratch_bytes), else by one
+// block per sequence.
 hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s,
                           const float2* x_stats = nullptr, const float* gamma = nullptr,
-                          const float* beta = nullptr, float eps = 0.0f, bool gamma_scaled = false);
+                          const float* beta = nullptr, float eps = 0.0f, bool gamma_scaled = false, int S = 0,
+                          float* scratch = nullptr, size_t scratch_bytes = 0);
 
 // out[b,s,:] = x[tok_dst[b*S+s]] or 0 (f32 [B,S,H]).
 hipError_t launch_scatter_hidden(const void* x, int H, const int* tok_dst, int n_tok, float* out, DType dt,

@@ -272,6 +272,7 @@ __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, co
   __shared__ __attribute__((aligned(16))) uint8_t mlds[kEmbedScanMaxMask];  // the whole mask
   __shared__ int cnt[kMaxOrderedBatch];
   __shared__ int posl[kEmbedScanMaxSeq];  // positions of sequence b's real tokens
+  __shared__ int idl[kEmbedScanMaxSeq];   // token ids of sequence b
   const int b = blockIdx.x, p = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
@@ -291,6 +292,9 @@ __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, co
       if (i < nm) mlds[i] = mask[i];
     }
   }
+  // sequence b's ids in the same round trip (the rows' gather needs them
+  // only after the scan has placed the tokens)
+  for (int i = threadIdx.x; i < S; i += 256) idl[i] = ids[(size_t)b * S + i];
   __syncthreads();
   // real tokens of every sequence
   if ((S & 15) == 0) {
@@ -354,9 +358,9 @@ __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, co
     __syncthreads();  // the real positions overwrite the -1s after them
     for (int i = threadIdx.x; i < L; i += 256) tok_dst[(size_t)b * S + posl[i]] = off + i;
   }
-  // embedding rows of this block's tokens: ids first, then every row of the
-  // wave's tokens requested before any is used (tokens past the sequence end
-  // read row 0 and are not stored)
+  // embedding rows of this block's tokens: every row of the wave's tokens
+  // requested before any is used (tokens past the sequence end read row 0
+  // and are not stored)
   const int nch = H / EPC;
   constexpr int TPW = kEmbedScanTokens / 4;  // tokens per wave
   int sp[TPW], id[TPW];
@@ -364,7 +368,7 @@ __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, co
   for (int j = 0; j < TPW; ++j) {
     const int i = p * kEmbedScanTokens + wave + 4 * j;
     sp[j] = i < L ? posl[i] : -1;
-    id[j] = sp[j] >= 0 ? min(max(ids[(size_t)b * S + sp[j]], 0), vocab - 1) : 0;
+    id[j] = sp[j] >= 0 ? min(max(idl[sp[j]], 0), vocab - 1) : 0;
   }
   uint4 rw[TPW][CPL], rp[TPW][CPL], rt[CPL];
 #pragma unroll
@@ -430,21 +434,51 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const T* hidden, int H
 // so their loads are in flight while the rows' LayerNorm statistics (deferred
 // input) are merged, one thread per row: the two round trips overlap.  A batch
 // is 16 chunks per lane (8 rows of bf16: a 128-token sequence at once).
-constexpr int kMaxPoolRows = 512;  // the longest sequence
+constexpr int kMaxPoolRows = 512;    // the longest sequence
+constexpr int kPoolSplitRows = 64;   // rows per block when sequences are split
+constexpr int kPoolSplitAbove = 128;  // split when sequences may be longer than this
 // With x_stats the rows are pre-LayerNorm values with their partial
 // statistics (deferred LayerNorm): the block averages (x - mean) * rstd and
 // applies gamma and beta to the average.
+// Finishes a pooled row: thread c < H holds column c's sum over the
+// sequence's L rows (normalised rows when deferred); the mean, the LayerNorm's
+// gamma and beta of a deferred input, then the L2 normalisation over the
+// block (16 waves).
+__device__ __forceinline__ void pool_finish(float sum, int L, int H, bool deferred, bool gamma_scaled,
+                                            const float* gamma, const float* beta, float* out_row, float* red) {
+  const int c = threadIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float mean = 0.0f;
+  if (c < H) {
+    mean = sum / fmaxf((float)L, 1e-9f);
+    if (deferred) mean = L > 0 ? (gamma_scaled ? mean + beta[c] : fmaf(gamma[c], mean, beta[c])) : 0.0f;
+  }
+  const float ss = wave_sum(mean * mean);
+  if (lane == 0) red[wave] = ss;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) tot += red[w];
+  const float inv = 1.0f / fmaxf(sqrtf(tot), 1e-12f);
+  if (c < H) out_row[c] = mean * inv;
+}
+
+// Block (b, q) sums rows q R .. q R + R - 1 of sequence b (all its rows when
+// R == 0).  With partial == nullptr the block finishes the pooled row itself;
+// otherwise it stores its column sums to partial[(b gridDim.y + q) H + c] for
+// pool_combine_kernel.
 template <typename T>
 __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const int* cu, float* out,
                                                        const float2* x_stats, const float* gamma, const float* beta,
-                                                       float eps, bool gamma_scaled) {
+                                                       float eps, bool gamma_scaled, int R, float* partial) {
   constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
   constexpr int kPoolBatch = 16 / CPL;  // rows per wave in flight
   extern __shared__ float part[];  // [16][H]
   __shared__ float red[16];
   __shared__ float2 row_st[kMaxPoolRows];  // (mean, rstd) per row of a deferred-LayerNorm input
   const int b = blockIdx.x;
-  const int r0 = cu[b], L = cu[b + 1] - r0;
+  const int len = cu[b + 1] - cu[b];  // the sequence's rows
+  const int r0 = cu[b] + (R ? (int)blockIdx.y * R : 0);
+  const int L = R ? max(0, min(R, len - (int)blockIdx.y * R)) : len;  // this block's rows
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nch = H / EPC;
   float acc[CPL][EPC];
@@ -506,24 +540,30 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
       for (int e = 0; e < EPC; ++e) part[wave * H + ch * EPC + e] = acc[i][e];
   }
   __syncthreads();
-  const float denom = fmaxf((float)L, 1e-9f);
   const int c = threadIdx.x;
-  float mean = 0.0f;
+  float sum = 0.0f;
   if (c < H) {
-    float sum = 0.0f;
 #pragma unroll
     for (int w = 0; w < 16; ++w) sum += part[w * H + c];
-    mean = sum / denom;
-    if (x_stats) mean = L > 0 ? (gamma_scaled ? mean + beta[c] : fmaf(gamma[c], mean, beta[c])) : 0.0f;
   }
-  const float ss = wave_sum(mean * mean);
-  if (lane == 0) red[wave] = ss;
-  __syncthreads();
-  float tot = 0.0f;
-#pragma unroll
-  for (int w = 0; w < 16; ++w) tot += red[w];
-  const float inv = 1.0f / fmaxf(sqrtf(tot), 1e-12f);
-  if (c < H) out[(size_t)b * H + c] = mean * inv;
+  if (partial) {
+    if (c < H) partial[((size_t)b * gridDim.y + blockIdx.y) * H + c] = sum;
+    return;
+  }
+  pool_finish(sum, len, H, x_stats != nullptr, gamma_scaled, gamma, beta, out + (size_t)b * H, red);
+}
+
+// Adds the Q partial column sums of sequence b (in block order, so the
+// result does not depend on timing) and finishes the pooled row.
+__global__ __launch_bounds__(1024) void pool_combine_kernel(const float* partial, int Q, int H, const int* cu,
+                                                            float* out, bool deferred, const float* gamma,
+                                                            const float* beta, bool gamma_scaled) {
+  __shared__ float red[16];
+  const int b = blockIdx.x, c = threadIdx.x;
+  float sum = 0.0f;
+  if (c < H)
+    for (int q = 0; q < Q; ++q) sum += partial[((size_t)b * Q + q) * H + c];
+  pool_finish(sum, cu[b + 1] - cu[b], H, deferred, gamma_scaled, gamma, beta, out + (size_t)b * H, red);
 }
 
 template <typename T>
@@ -618,20 +658,37 @@ hipError_t launch_layer_norm(const void* a, const float* gamma, const float* bet
 }
 
 hipError_t launch_pool_l2(const void* x, int H, const int* cu, int B, float* out, DType dt, hipStream_t s,
-                          const float2* x_stats, const float* gamma, const float* beta, float eps, bool gamma_scaled) {
+                          const float2* x_stats, const float* gamma, const float* beta, float eps, bool gamma_scaled,
+                          int S, float* scratch, size_t scratch_bytes) {
   if (B <= 0) return hipSuccess;
   if (gamma_scaled && !x_stats) return hipErrorInvalidValue;
+  if (dt != DType::BF16 && x_stats) return hipErrorInvalidValue;
+  if (H > 1024 || S > kMaxPoolRows) return hipErrorInvalidValue;
   const size_t lds = (size_t)16 * H * sizeof(float);
-  RLX_LOG_LAUNCH("pool_l2_kernel", dim3(B), dim3(1024), lds, "%s B=%d H=%d%s", dt == DType::BF16 ? "bf16" : "f32", B, H,
-                 x_stats ? (gamma_scaled ? " deferred-LN input (gamma-scaled)" : " deferred-LN input") : "");
+  // Sequences of up to S > kPoolSplitAbove rows are summed by
+  // ceil(S / kPoolSplitRows) blocks each, then combined, when the scratch
+  // holds the partial sums (one block per sequence takes about as long as the
+  // second launch up to 128 rows, whose loads are all in flight at once).
+  const int Q = (S + kPoolSplitRows - 1) / kPoolSplitRows;
+  const bool split = S > kPoolSplitAbove && scratch && (size_t)B * Q * H * sizeof(float) <= scratch_bytes;
+  const dim3 grid(B, split ? Q : 1);
+  const int R = split ? kPoolSplitRows : 0;
+  float* partial = split ? scratch : nullptr;
+  RLX_LOG_LAUNCH("pool_l2_kernel", grid, dim3(1024), lds, "%s B=%d H=%d%s%s", dt == DType::BF16 ? "bf16" : "f32", B, H,
+                 x_stats ? (gamma_scaled ? " deferred-LN input (gamma-scaled)" : " deferred-LN input") : "",
+                 split ? " partial sums" : "");
   if (dt == DType::BF16)
-    hipLaunchKernelGGL(pool_l2_kernel<bf16_t>, dim3(B), dim3(1024), lds, s, (const bf16_t*)x, H, cu, out, x_stats,
-                       gamma, beta, eps, gamma_scaled);
-  else if (x_stats)
-    return hipErrorInvalidValue;
+    hipLaunchKernelGGL(pool_l2_kernel<bf16_t>, grid, dim3(1024), lds, s, (const bf16_t*)x, H, cu, out, x_stats,
+                       gamma, beta, eps, gamma_scaled, R, partial);
   else
-    hipLaunchKernelGGL(pool_l2_kernel<float>, dim3(B), dim3(1024), lds, s, (const float*)x, H, cu, out, nullptr,
-                       nullptr, nullptr, 0.0f, false);
+    hipLaunchKernelGGL(pool_l2_kernel<float>, grid, dim3(1024), lds, s, (const float*)x, H, cu, out, nullptr,
+                       nullptr, nullptr, 0.0f, false, R, partial);
+  if (!split) return hipGetLastError();
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  RLX_LOG_LAUNCH("pool_combine_kernel", dim3(B), dim3(1024), 0, "B=%d H=%d partial sums per sequence=%d", B, H, Q);
+  hipLaunchKernelGGL(pool_combine_kernel, dim3(B), dim3(1024), 0, s, partial, Q, H, cu, out, x_stats != nullptr,
+                     gamma, beta, gamma_scaled);
   return hipGetLastError();
 }
 

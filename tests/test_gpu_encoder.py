@@ -127,6 +127,25 @@ def test_encoder_parity_quant_small_batch(rlx, quant, batch, mode):
     _compare(got, oracle.encoder_forward(wl), wl, _tol(sp), f"{sp.name} b{batch}, {mode}")
 
 
+@pytest.mark.parametrize("kind", ["f32", "bf16", "int8_in_gemm", "int4_prologue"])
+def test_encoder_long_sequences_pooled(rlx, kind):
+    """Pooling of sequences longer than 128 tokens (summed 64 rows per block,
+    then combined): lengths U[1, 300] with one full-length and one empty
+    sequence, affine LayerNorms; plain rows (f32), deferred-LayerNorm rows
+    (bf16, the prologue) and gamma-scaled ones (the dequantising GEMMs)."""
+    dtype, quant = ("f32", "none") if kind == "f32" else ("bf16", kind.split("_")[0] if "_" in kind else "none")
+    name = f"minilm_b32_s128_{quant}" if quant != "none" else f"minilm_b4_s128_{dtype}"
+    sp = workloads.spec(name, batch=5, seq=300, layers=2, len_lo=1, len_hi=300)
+    wl = workloads.make(sp, affine=True)
+    wl.mask[1] = 1
+    wl.mask[3] = 0
+    wl.lengths = wl.mask.sum(axis=1)
+    with _dequant_mode("in_gemm" if kind.endswith("in_gemm") else "prologue"):
+        got = _run(rlx, wl)
+    assert np.all(got[3] == 0), "an empty sequence pools to zero"
+    _compare(got, oracle.encoder_forward(wl), wl, _tol(sp), f"long sequences pooled, {kind}")
+
+
 def test_encoder_mask_with_holes_and_empty_row(rlx):
     """A custom key mask that is not right-padded, and a sequence with no token."""
     sp = workloads.spec("minilm_b4_s128_bf16", batch=5, seq=64, len_lo=30, len_hi=64)
