@@ -15,12 +15,18 @@
 // four codes per three bytes (little-endian bit stream), FP4 two per byte
 // (lower k in the low nibble); scales [rows][K/32] bytes.
 //
-// Design (256 threads = 4 waves in a 2 x 2 grid, tile 128 x 128, each wave
+// Design (512 threads = 8 waves in a 4 x 2 grid, tile 256 x 128, each wave
 // 64 x 64 = 2 x 2 instructions):
 //  * A stage is 128 k: the rows' 128 / 96 / 64 bytes (FP8 / FP6 / FP4) go
 //    global -> LDS by DMA into a 128-byte row pitch with the 16-byte chunks
 //    XOR-swizzled by (row / 2) mod 8; the rows' four scale bytes per stage go
-//    by a dword DMA.  Two stages, two blocks per CU.
+//    by a dword DMA.  Three stages (150 KB, one block per CU): two stages are
+//    in flight while one is multiplied, which is what hides the memory
+//    latency -- with two 128 x 128 stages per block and two blocks per CU
+//    only one stage per block was in flight and every stage waited for it.
+//    The tall tile keeps the tile count at or below the CU count at the
+//    benchmark shape (71 x 3 tiles for M = 18048, N = 384), so no CU runs a
+//    second tile after the others have finished.
 //  * Operand layout of the instruction (lane l: row l % 32, half h = l / 32),
 //    checked on the GPU against the oracle: FP6 / FP4 lanes hold the 32 codes
 //    of block h contiguously; FP8 lanes hold bytes 16h .. 16h+15 of block 0 in
@@ -35,15 +41,21 @@
 namespace rlx {
 namespace {
 
-constexpr int kMxBM = 128, kMxBN = 128;
+constexpr int kMxBM = 256, kMxBN = 128;
+constexpr int kMxWaves = 8;
 constexpr int kMxStageK = 128;     // k per stage
 constexpr int kMxPitch = 128;      // LDS bytes per staged row
-constexpr int kMxStages = 2;
+constexpr int kMxStages = 3;
 constexpr int kMxOpBytes = (kMxBM + kMxBN) * kMxPitch;
-constexpr int kMxScaleBytes = (kMxBM + kMxBN) * 4;
+// one 256-byte scale DMA per wave and stage: x rows, then w rows, then (the
+// waves left over) a copy that is never read, so every wave issues as many
+// loads per stage
+constexpr int kMxScaleBytes = kMxWaves * 256;
 constexpr int kMxStageBytes = kMxOpBytes + kMxScaleBytes;
-// per wave per stage: (BM + BN) rows * 128 B / (4 waves * 1 KB) chunk DMAs + 1 scale DMA
-constexpr int kMxLps = (kMxBM + kMxBN) * kMxPitch / (4 * 1024) + 1;
+// per wave per stage: (BM + BN) rows * 128 B / (8 waves * 1 KB) chunk DMAs + 1 scale DMA
+constexpr int kMxLps = (kMxBM + kMxBN) * kMxPitch / (kMxWaves * 1024) + 1;
+static_assert((kMxBM + kMxBN) * 4 <= kMxScaleBytes && kMxBM % 64 == 0 && kMxBN % 64 == 0, "scale DMA layout");
+static_assert(kMxStages * kMxStageBytes <= 160 * 1024, "LDS");
 
 __host__ __device__ constexpr int mx_bits(int fmt) { return fmt <= 1 ? 8 : (fmt <= 3 ? 6 : 4); }
 
@@ -78,7 +90,7 @@ __device__ __forceinline__ mx_v8i mx_fragment(const uint8_t* rows, int r, int s,
 }
 
 template <int FX, int FW>
-__global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
+__global__ __launch_bounds__(kMxWaves * 64) void mx_gemm_kernel(MxGemmParams p) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kMxStages * kMxStageBytes];
   const int M = p.M, N = p.N, K = p.K;
   const int n_tiles = N / kMxBN;
@@ -92,13 +104,13 @@ __global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
   const int m0 = (tile / n_tiles) * kMxBM, n0 = (tile % n_tiles) * kMxBN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;
+  const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, h = lane >> 5;  // 4 x 2 waves of 64 x 64
   const int KT = K / kMxStageK;
   constexpr int RBX = kMxStageK * mx_bits(FX) / 8, RBW = kMxStageK * mx_bits(FW) / 8;  // bytes per stage row
   const size_t pitch_x = (size_t)K * mx_bits(FX) / 8, pitch_w = (size_t)K * mx_bits(FW) / 8;
   const int sb_row = K / 32;  // scale bytes per row
 
-  // Chunk DMA: instruction i of wave w fills staged rows 8(w + 4i) .. +7; lane
+  // Chunk DMA: instruction i of wave w fills staged rows 8(w + 8i) .. +7; lane
   // lands at row (lane >> 3), physical chunk (lane & 7).  Chunks past the
   // format's row bytes are never read; their lanes fetch chunk 0 again.
   constexpr int CL = kMxLps - 1;
@@ -106,7 +118,7 @@ __global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
   int step_bytes[CL];
 #pragma unroll
   for (int i = 0; i < CL; ++i) {
-    const int row = (wave + 4 * i) * 8 + (lane >> 3);
+    const int row = (wave + kMxWaves * i) * 8 + (lane >> 3);
     const int c = mx_swz(row, lane & 7);
     if (row < kMxBM) {
       const int m = min(m0 + row, M - 1);
@@ -117,19 +129,22 @@ __global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
       step_bytes[i] = RBW;
     }
   }
-  // Scale DMA: wave 0/1 -> x rows 0-63 / 64-127, wave 2/3 -> w rows; one dword per row and stage
+  // Scale DMA, one dword per row and stage: waves 0-3 -> x rows 64w .. 64w+63,
+  // waves 4-5 -> w rows 64(w-4) .. +63, waves 6-7 -> w rows again (unread)
   const uint8_t* ssrc;
   {
-    const int row = (wave & 1) * 64 + lane;
-    ssrc = wave < 2 ? p.x_scales + (size_t)min(m0 + row, M - 1) * sb_row
-                    : p.w_scales + (size_t)(n0 + row) * sb_row;
+    constexpr int XW = kMxBM / 64, WW = kMxBN / 64;
+    const int row = (wave < XW ? wave : (wave - XW) % WW) * 64 + lane;
+    ssrc = wave < XW ? p.x_scales + (size_t)min(m0 + row, M - 1) * sb_row
+                     : p.w_scales + (size_t)(n0 + row) * sb_row;
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)smem;
   auto issue = [&](int kt, int buf) {
     const uint32_t sbase = lds0 + buf * kMxStageBytes;
 #pragma unroll
     for (int i = 0; i < CL; ++i)
-      lds_dma16(src[i] + (size_t)kt * step_bytes[i], __builtin_amdgcn_readfirstlane(sbase + (wave + 4 * i) * 8 * kMxPitch));
+      lds_dma16(src[i] + (size_t)kt * step_bytes[i],
+                __builtin_amdgcn_readfirstlane(sbase + (wave + kMxWaves * i) * 8 * kMxPitch));
     lds_dma4(ssrc + kt * 4, __builtin_amdgcn_readfirstlane(sbase + kMxOpBytes + wave * 256));
   };
 
@@ -142,19 +157,23 @@ __global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
 
+  // Stages kt and kt + 1 are in flight when stage kt's wait begins; stage
+  // kt + 2 is issued after the barrier that follows it, into the buffer of
+  // stage kt - 1, which every wave has finished multiplying by then.
+  static_assert(kMxStages == 3, "the ring below keeps two stages ahead");
   issue(0, 0);
+  if (KT > 1) issue(1, 1);
   for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) {
-      issue(kt + 1, buf ^ 1);
+    const int buf = kt % kMxStages;
+    if (kt + 1 < KT)
       wait_vmcnt<kMxLps>();  // stage kt landed; kt + 1 in flight
-    } else {
+    else
       wait_vmcnt<0>();
-    }
     __syncthreads();
+    if (kt + 2 < KT) issue(kt + 2, (kt + 2) % kMxStages);
     const uint8_t* xs = smem + buf * kMxStageBytes;
     const uint8_t* ws = xs + kMxBM * kMxPitch;
-    const uint32_t* sx = reinterpret_cast<const uint32_t*>(xs + kMxOpBytes);  // [128] x rows, then [128] w rows
+    const uint32_t* sx = reinterpret_cast<const uint32_t*>(xs + kMxOpBytes);  // [BM] x rows, then [BN] w rows
     const uint32_t* sw = sx + kMxBM;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
@@ -175,32 +194,45 @@ __global__ __launch_bounds__(256) void mx_gemm_kernel(MxGemmParams p) {
           acc[tm][tn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wf[tn], xf[tm], acc[tm][tn], FW, FX, 0,
                                                                          wsc[tn], 0, xsc[tm]);
     }
-    __syncthreads();  // the buffer of stage kt is free for stage kt + 2
   }
 
-  // lane: output row m = m0 + wm*64 + tm*32 + l32; register v: column
-  // n = n0 + wn*64 + tn*32 + 8(v/4) + 4h + v%4
+  // Epilogue through LDS (the stage ring is free once every wave is past the
+  // loop): lane holds output row wm*64 + tm*32 + l32 of the tile and, per
+  // register quad i, columns wn*64 + tn*32 + 8i + 4h .. +3.  The tile goes to
+  // LDS row-major, then every wave stores whole 512-byte rows: written from
+  // the instruction layout, each store touched 32 rows with 32 bytes apiece.
+  constexpr int kOutPitch = kMxBN + 4;  // floats per LDS row (16-byte aligned, rows 4 banks apart)
+  static_assert(kMxBM * kOutPitch * 4 <= kMxStages * kMxStageBytes, "output tile in the stage ring");
+  float* out_lds = reinterpret_cast<float*>(smem);
+  __syncthreads();
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm) {
-    const int m = m0 + wm * 64 + tm * 32 + l32;
-    if (m >= M) continue;
+  for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
     for (int tn = 0; tn < 2; ++tn)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int n = n0 + wn * 64 + tn * 32 + 8 * i + 4 * h;
-        *reinterpret_cast<float4*>(p.y + (size_t)m * N + n) =
+        const int r = wm * 64 + tm * 32 + l32, c = wn * 64 + tn * 32 + 8 * i + 4 * h;
+        *reinterpret_cast<float4*>(out_lds + r * kOutPitch + c) =
             make_float4(acc[tm][tn][4 * i], acc[tm][tn][4 * i + 1], acc[tm][tn][4 * i + 2], acc[tm][tn][4 * i + 3]);
       }
+  __syncthreads();
+  constexpr int kRowThreads = kMxBN / 4;                       // float4 per row
+  constexpr int kRowsPerPass = kMxWaves * 64 / kRowThreads;    // rows stored per pass
+  const int rr = tid / kRowThreads, c4 = (tid % kRowThreads) * 4;
+#pragma unroll 4
+  for (int r = rr; r < kMxBM; r += kRowsPerPass) {
+    const int m = m0 + r;
+    if (m < M)
+      *reinterpret_cast<float4*>(p.y + (size_t)m * N + n0 + c4) = *reinterpret_cast<const float4*>(out_lds + r * kOutPitch + c4);
   }
 }
 
 template <int FX, int FW>
 hipError_t launch_mx_typed(const MxGemmParams& p, hipStream_t s) {
   const int tiles = (p.N / kMxBN) * ((p.M + kMxBM - 1) / kMxBM);
-  RLX_LOG_LAUNCH("mx_gemm_kernel", dim3(tiles), dim3(256), 0, "formats=%d,%d M=%d N=%d K=%d", (int)FX, (int)FW, p.M,
-                 p.N, p.K);
-  hipLaunchKernelGGL((mx_gemm_kernel<FX, FW>), dim3(tiles), dim3(256), 0, s, p);
+  RLX_LOG_LAUNCH("mx_gemm_kernel", dim3(tiles), dim3(kMxWaves * 64), 0, "formats=%d,%d M=%d N=%d K=%d", (int)FX,
+                 (int)FW, p.M, p.N, p.K);
+  hipLaunchKernelGGL((mx_gemm_kernel<FX, FW>), dim3(tiles), dim3(kMxWaves * 64), 0, s, p);
   return hipGetLastError();
 }
 
