@@ -401,6 +401,35 @@ rlx_status rlx_encoder_set_profiling(rlx_encoder* enc, int enable);
 rlx_status rlx_encoder_profile_read(rlx_encoder* enc, int max_entries, const char** names, int* launches,
                                     double* total_ms, int* n_entries);
 
+/* Test support for token compaction, the index work a forward starts with
+ * (Section VIII-B's inputs are padded batches; every later kernel of a
+ * forward runs on the real tokens only).  This is the kernel a forward runs
+ * for hidden-state input and for masks of more than 16384 entries; the
+ * embedding kernel computes the same maps itself for smaller masks.
+ * From attention_mask u8 [B,S] (nonzero = real token) it writes, to int32
+ * device arrays owned by the caller:
+ *   cu [B+1]       cu[b] = the number of real tokens of sequences 0 .. b-1;
+ *   tok_src [B*S]  entries 0 .. cu[B]-1: b*S + s of every real token,
+ *                  sequences in order, positions ascending (the entries after
+ *                  them are not written);
+ *   tok_dst [B*S]  the index of token (b,s) in tok_src, or -1 when masked;
+ *   order [B]      (NULL skips it; requires B <= 256) the sequences by
+ *                  real-token count, longest first, ties by sequence index.
+ * Requires 1 <= B <= 4096 and 1 <= S <= 512 (RLX_ERR_UNSUPPORTED beyond),
+ * non-null mask, cu, tok_src and tok_dst (RLX_ERR_INVALID_ARG). */
+rlx_status rlx_mask_compaction(const uint8_t* attention_mask, int B, int S, int32_t* cu, int32_t* tok_src,
+                               int32_t* tok_dst, int32_t* order, void* stream);
+
+/* Test support: copies the token compaction maps that the handle's most
+ * recent forward computed (layouts as for rlx_mask_compaction, for that
+ * forward's B and S, which must be the ones passed: RLX_ERR_INVALID_ARG
+ * otherwise) into caller-owned int32 device arrays.  The copies are enqueued
+ * on `stream`; order them after the forward.  order (NULL skips it) requires
+ * B <= 256.  Handles that take the persistent forward keep no maps
+ * (RLX_ERR_UNSUPPORTED). */
+rlx_status rlx_encoder_token_maps(const rlx_encoder* enc, int B, int S, int32_t* cu, int32_t* tok_src,
+                                  int32_t* tok_dst, int32_t* order, void* stream);
+
 /* Message describing the last error on the calling thread ("" if none).
  * Valid until the next rlx_* call on this thread. */
 const char* rlx_last_error(void);

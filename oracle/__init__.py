@@ -30,6 +30,9 @@ definitions and multiplied in float64.
 ``oracle.gguf`` reads the GGUF Q4_0 / Q4_1 / Q8_0 weight blocks (and the int8
 group and int4 min layouts they map onto) into float64 weights.
 
+``oracle.compaction`` lists a padded batch's real tokens (the index maps every
+forward computes before its row-local steps).
+
 Pins (tests/test_oracle_*.py) tie each function to something other than
 itself: brute force on tiny inputs, closed forms, invariants, library special
 cases (torch SDPA, nn.TransformerEncoderLayer, transformers.BertModel in
@@ -43,3 +46,4 @@ from .encoder import (  # noqa: F401
 from .quant import unpack_int4, dequant_int8, dequant_int4  # noqa: F401
 from . import mx  # noqa: F401
 from . import gguf  # noqa: F401
+from . import compaction  # noqa: F401

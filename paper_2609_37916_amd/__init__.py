@@ -38,8 +38,8 @@ STATUS_NAMES = {0: "RLX_OK", 1: "RLX_ERR_INVALID_ARG", 2: "RLX_ERR_UNSUPPORTED",
 EXPORTS = ("rlx_masked_attention", "rlx_dequant_matmul", "rlx_dequant_unpack", "rlx_gguf_repack", "rlx_scaled_matmul",
            "rlx_encoder_create",
            "rlx_encoder_forward", "rlx_encoder_forward_noalloc", "rlx_encoder_destroy", "rlx_encoder_set_profiling",
-           "rlx_encoder_profile_read", "rlx_encoder_check", "rlx_encoder_uses_persistent_forward", "rlx_last_error",
-           "rlx_version")
+           "rlx_encoder_profile_read", "rlx_encoder_check", "rlx_encoder_uses_persistent_forward",
+           "rlx_mask_compaction", "rlx_encoder_token_maps", "rlx_last_error", "rlx_version")
 
 
 class RlxError(RuntimeError):
@@ -100,6 +100,8 @@ def lib() -> ctypes.CDLL:
     L.rlx_encoder_forward.argtypes = [_vp, _vp, _vp, i32, i32, _vp, _vp]
     L.rlx_encoder_forward_noalloc.argtypes = [ctypes.POINTER(EncoderConfig), ctypes.POINTER(EncoderWeights), _vp, _vp,
                                               i32, i32, _vp, _vp]
+    L.rlx_mask_compaction.argtypes = [_vp, i32, i32, _vp, _vp, _vp, _vp, _vp]
+    L.rlx_encoder_token_maps.argtypes = [_vp, i32, i32, _vp, _vp, _vp, _vp, _vp]
     L.rlx_encoder_check.argtypes = [_vp]
     L.rlx_encoder_uses_persistent_forward.argtypes = [_vp]
     L.rlx_encoder_uses_persistent_forward.restype = ctypes.c_int
@@ -233,6 +235,28 @@ def dequant_unpack(w, *, scheme: int, scales, zeros=None, group_size: int = 32, 
     return out
 
 
+def _token_map_tensors(B: int, S: int, device, with_order: bool):
+    torch = _torch()
+    cu = torch.empty(B + 1, dtype=torch.int32, device=device)
+    src = torch.full((B * S,), -2, dtype=torch.int32, device=device)
+    dst = torch.empty(B * S, dtype=torch.int32, device=device)
+    order = torch.empty(B, dtype=torch.int32, device=device) if with_order else None
+    return cu, src, dst, order
+
+
+def mask_compaction(mask, *, with_order: bool = True, stream=None):
+    """Token compaction maps of a u8 mask [B, S] (see rlx_mask_compaction):
+    (cu [B+1], tok_src [cu[B]], tok_dst [B*S], order [B] or None), int32."""
+    torch = _torch()
+    if mask.dtype != torch.uint8 or mask.dim() != 2 or not mask.is_contiguous():
+        raise ValueError("mask: expected a contiguous uint8 [B, S] tensor")
+    B, S = mask.shape
+    cu, src, dst, order = _token_map_tensors(B, S, mask.device, with_order)
+    check(lib().rlx_mask_compaction(_ptr(mask), B, S, _ptr(cu), _ptr(src), _ptr(dst), _ptr(order), _stream(stream)))
+    (stream or torch.cuda.current_stream()).synchronize()  # the slice below reads cu[B]
+    return cu, src[:int(cu[-1].item())], dst, order
+
+
 def gguf_repack(blocks, gguf_type, *, N: int, K: int, stream=None):
     """GGUF blocks (uint8 device tensor of N * K/32 blocks, or N * K/256 for the
     K-quants) -> (scheme, codes, scales, zeros) for dequant_matmul (see
@@ -352,6 +376,16 @@ class Encoder:
     def persistent(self) -> bool:
         """True when supported forwards run as one persistent launch."""
         return bool(lib().rlx_encoder_uses_persistent_forward(self._h))
+
+    def token_maps(self, B: int, S: int, *, with_order: bool = True, stream=None):
+        """The token compaction maps of this handle's most recent forward of
+        B x S (see rlx_encoder_token_maps), as for mask_compaction."""
+        torch = _torch()
+        cu, src, dst, order = _token_map_tensors(B, S, torch.device("cuda", torch.cuda.current_device()), with_order)
+        check(lib().rlx_encoder_token_maps(self._h, B, S, _ptr(cu), _ptr(src), _ptr(dst), _ptr(order),
+                                           _stream(stream)))
+        (stream or torch.cuda.current_stream()).synchronize()  # the slice below reads cu[B]
+        return cu, src[:int(cu[-1].item())], dst, order
 
     def check(self) -> None:
         """Waits for the last forward; raises if a wait of the persistent launch gave up."""

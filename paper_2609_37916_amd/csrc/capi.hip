@@ -180,6 +180,7 @@ struct rlx_encoder {
   int* tok_src = nullptr;
   int* tok_dst = nullptr;
   int* order = nullptr;  // sequences by token count, longest first (mask scan, B <= kMaxOrderedBatch)
+  int last_B = 0, last_S = 0;  // shape of the most recent forward (its token maps are in the workspace)
   void *X = nullptr, *X1 = nullptr, *A = nullptr, *CTX = nullptr, *QKV = nullptr, *G = nullptr;
   // Deferred LayerNorm (dense bf16 weights): no kernel writes a LayerNorm
   // output.  The output projection and FFN-down store their pre-norm sums (A,
@@ -1142,6 +1143,8 @@ rlx_status rlx_encoder_forward(rlx_encoder* e, const void* input, const uint8_t*
     st = run_graph_forward(e, input, attention_mask, B, S, output, s);
   if (st != RLX_OK) return st;
   RLX_HIP(hipEventRecord(e->done_ev, s), "hipEventRecord");
+  e->last_B = B;
+  e->last_S = S;
   return ok();
 }
 
@@ -1227,6 +1230,43 @@ rlx_status rlx_encoder_check(rlx_encoder* e) {
 }
 
 int rlx_encoder_uses_persistent_forward(const rlx_encoder* e) { return e && e->pipe ? 1 : 0; }
+
+rlx_status rlx_mask_compaction(const uint8_t* attention_mask, int B, int S, int32_t* cu, int32_t* tok_src,
+                               int32_t* tok_dst, int32_t* order, void* stream) {
+  log_refresh();
+  if (!attention_mask || !cu || !tok_src || !tok_dst)
+    return fail(RLX_ERR_INVALID_ARG, "mask_compaction: attention_mask, cu, tok_src and tok_dst must be non-null");
+  if (B < 1 || S < 1) return fail(RLX_ERR_INVALID_ARG, "mask_compaction: B=%d and S=%d must be >= 1", B, S);
+  if (B > 4096 || S > 512)
+    return fail(RLX_ERR_UNSUPPORTED, "mask_compaction: B=%d, S=%d beyond B <= 4096, S <= 512", B, S);
+  if (order && B > kMaxOrderedBatch)
+    return fail(RLX_ERR_UNSUPPORTED, "mask_compaction: the order is computed for B <= %d, not %d", kMaxOrderedBatch, B);
+  RLX_HIP(launch_mask_scan(attention_mask, B, S, cu, tok_src, tok_dst, order, static_cast<hipStream_t>(stream)),
+          "mask compaction launch");
+  return ok();
+}
+
+rlx_status rlx_encoder_token_maps(const rlx_encoder* e, int B, int S, int32_t* cu, int32_t* tok_src,
+                                  int32_t* tok_dst, int32_t* order, void* stream) {
+  log_refresh();
+  if (!e) return fail(RLX_ERR_INVALID_ARG, "encoder_token_maps: null handle");
+  if (!cu || !tok_src || !tok_dst)
+    return fail(RLX_ERR_INVALID_ARG, "encoder_token_maps: cu, tok_src and tok_dst must be non-null");
+  if (e->pipe) return fail(RLX_ERR_UNSUPPORTED, "encoder_token_maps: the persistent forward keeps no maps");
+  if (e->last_B < 1 || B != e->last_B || S != e->last_S)
+    return fail(RLX_ERR_INVALID_ARG, "encoder_token_maps: B=%d, S=%d differ from the most recent forward's %d, %d", B,
+                S, e->last_B, e->last_S);
+  if (order && B > kMaxOrderedBatch)
+    return fail(RLX_ERR_UNSUPPORTED, "encoder_token_maps: the order is kept for B <= %d, not %d", kMaxOrderedBatch, B);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t n = (size_t)B * S * sizeof(int32_t);
+  RLX_HIP(hipMemcpyAsync(cu, e->cu, (size_t)(B + 1) * sizeof(int32_t), hipMemcpyDeviceToDevice, s), "copy cu");
+  RLX_HIP(hipMemcpyAsync(tok_src, e->tok_src, n, hipMemcpyDeviceToDevice, s), "copy tok_src");
+  RLX_HIP(hipMemcpyAsync(tok_dst, e->tok_dst, n, hipMemcpyDeviceToDevice, s), "copy tok_dst");
+  if (order)
+    RLX_HIP(hipMemcpyAsync(order, e->order, (size_t)B * sizeof(int32_t), hipMemcpyDeviceToDevice, s), "copy order");
+  return ok();
+}
 
 rlx_status rlx_encoder_set_profiling(rlx_encoder* e, int enable) {
   if (!e) return fail(RLX_ERR_INVALID_ARG, "encoder_set_profiling: null handle");

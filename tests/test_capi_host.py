@@ -33,6 +33,22 @@ def test_every_declared_function_is_exported(L):
         assert getattr(L, name) is not None
 
 
+def test_token_compaction_argument_errors(L):
+    P = 4096  # an aligned stand-in address: validation rejects before any use
+    f = L.rlx_mask_compaction
+    assert f(None, 2, 8, P, P, P, None, None) == rlx.ERR_INVALID_ARG
+    assert f(P, 2, 8, P, None, P, None, None) == rlx.ERR_INVALID_ARG
+    assert f(P, 0, 8, P, P, P, None, None) == rlx.ERR_INVALID_ARG
+    assert f(P, 2, 0, P, P, P, None, None) == rlx.ERR_INVALID_ARG
+    assert f(P, 2, 513, P, P, P, None, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, 4097, 8, P, P, P, None, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, 257, 8, P, P, P, P, None) == rlx.ERR_UNSUPPORTED
+    assert b"order" in L.rlx_last_error()
+    g = L.rlx_encoder_token_maps
+    assert g(None, 2, 8, P, P, P, None, None) == rlx.ERR_INVALID_ARG
+    assert b"null handle" in L.rlx_last_error()
+
+
 def test_version_string(L):
     assert "gfx950" in rlx.version()
 

@@ -475,3 +475,65 @@ def test_planted_kquant_mistake_fails_a_pin(name, monkeypatch):
         except Exception as e:
             failed.append(type(e).__name__)
     assert failed, f"no pin caught the planted mistake '{name}'"
+
+
+# --- token compaction ------------------------------------------------------------
+
+import oracle.compaction as ocp  # noqa: E402
+import test_oracle_compaction as cpins  # noqa: E402
+
+_ORIG_MAPS = ocp.token_maps
+
+
+def cp_order_ties_reversed(mask):
+    cu, src, dst, _ = _ORIG_MAPS(mask)
+    lengths = np.diff(cu)
+    return cu, src, dst, np.lexsort((-np.arange(len(lengths)), -lengths))
+
+
+def cp_order_shortest_first(mask):
+    cu, src, dst, _ = _ORIG_MAPS(mask)
+    lengths = np.diff(cu)
+    return cu, src, dst, np.lexsort((np.arange(len(lengths)), lengths))
+
+
+def cp_cu_inclusive(mask):
+    cu, src, dst, order = _ORIG_MAPS(mask)
+    return np.concatenate([cu[1:], cu[-1:]]), src, dst, order
+
+
+def cp_src_column_major(mask):
+    m = np.asarray(mask) != 0
+    cu, _, _, order = _ORIG_MAPS(mask)
+    B, S = m.shape
+    flat = np.flatnonzero(m.T.reshape(-1))
+    src = (flat % B) * S + flat // B  # the same tokens, position-major
+    dst = np.full(B * S, -1)
+    dst[src] = np.arange(src.size)
+    return cu, src, dst, order
+
+
+def cp_dst_masked_zero(mask):
+    cu, src, dst, order = _ORIG_MAPS(mask)
+    return cu, src, np.maximum(dst, 0), order
+
+
+CP_MUTANTS = {
+    "order: equal counts by descending index": cp_order_ties_reversed,
+    "order: shortest first": cp_order_shortest_first,
+    "cu: inclusive prefix": cp_cu_inclusive,
+    "tok_src: positions before sequences": cp_src_column_major,
+    "tok_dst: masked tokens map to 0": cp_dst_masked_zero,
+}
+
+
+@pytest.mark.parametrize("name", list(CP_MUTANTS))
+def test_planted_compaction_mistake_fails_a_pin(name, monkeypatch):
+    monkeypatch.setattr(ocp, "token_maps", CP_MUTANTS[name])
+    failed = []
+    for call in (cpins.test_hand_worked_mask, cpins.test_against_position_loops):
+        try:
+            call()
+        except Exception as e:
+            failed.append(type(e).__name__)
+    assert failed, f"no pin caught the planted mistake '{name}'"
