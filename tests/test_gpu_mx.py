@@ -54,7 +54,7 @@ def _abs_bound(x, w, K):
 
 @pytest.mark.parametrize("fx,fw", PAIRS)
 def test_bit_exact_on_exact_inputs(rlx, fx, fw):
-    M, N, K = 200, 256, 512  # a ragged second row tile, two column tiles, four stages
+    M, N, K = 300, 256, 640  # a ragged second row tile of 256, two column tiles, five stages in a ring of three
     x, w = wmx.matmul_inputs(1000 + 7 * FORMATS.index(fx) + FORMATS.index(fw), M, N, K, fx, fw, exact=True)
     got = _run(rlx, x, w, K)
     ref = oracle.mx.scaled_matmul(x.packed, x.scales, fx, w.packed, w.scales, fw, K)
