@@ -612,11 +612,23 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   store_tile<BM, BN, T, Q, E, TM, TN, NRB, KS, LN, STAGED>(acc, smem, p, m0, n0, M, epi_lds);
 }
 
+// LDS a workgroup can hold on gfx950.
+constexpr size_t kMaxLdsBytes = 160 * 1024;
+
+// Static LDS of gemm_dma_kernel<BM, BN, STAGES, T, ..., Q>: its operand ring.
+template <int BM, int BN, int STAGES, typename T, Quant Q>
+constexpr size_t dma_ring_bytes() {
+  return (size_t)STAGES * (BM * kRowBytes + BN * (Q == Quant::None ? kRowBytes : (quant_int8(Q) ? 64 : 32)));
+}
+
 template <int BM, int BN, int STAGES, typename T, Epi E, int KS, int LN, Quant Q = Quant::None>
 hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
   const dim3 grid((p.N / BN) * ((p.M + BM - 1) / BM));
   const size_t epi = (sizeof(T) == 2 ? (size_t)epi_layout_of<BM, BN, E, LN>(p.K, p.N).bytes : 0) +
                      (size_t)gq_lds_bytes(Q, BN, p.K);
+  // the ring (static) and the epilogue operands (dynamic) share the CU's LDS:
+  // a launch asking for more than there is must never be enqueued
+  if (dma_ring_bytes<BM, BN, STAGES, T, Q>() + epi > kMaxLdsBytes) return hipErrorInvalidValue;
   RLX_LOG_LAUNCH("gemm_dma_kernel", grid, dim3(kThreads * KS), epi,
                  "tile=%dx%d stages=%d %s %s ksplit=%d ln=%d epi=%s M=%d%s N=%d K=%d", BM, BN, STAGES,
                  sizeof(T) == 2 ? "bf16" : "f32", quant_name(Q), KS, LN, epi_name(E), p.M, p.m_dev ? "(device)" : "",
