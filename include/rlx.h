@@ -415,7 +415,7 @@ rlx_status rlx_encoder_profile_read(rlx_encoder* enc, int max_entries, const cha
  *   tok_dst [B*S]  the index of token (b,s) in tok_src, or -1 when masked;
  *   order [B]      (NULL skips it; requires B <= 256) the sequences by
  *                  real-token count, longest first, ties by sequence index.
- * Requires 1 <= B <= 4096 and 1 <= S <= 512 (RLX_ERR_UNSUPPORTED beyond),
+ * Requires 1 <= B <= 8192 and 1 <= S <= 512 (RLX_ERR_UNSUPPORTED beyond),
  * non-null mask, cu, tok_src and tok_dst (RLX_ERR_INVALID_ARG). */
 rlx_status rlx_mask_compaction(const uint8_t* attention_mask, int B, int S, int32_t* cu, int32_t* tok_src,
                                int32_t* tok_dst, int32_t* order, void* stream);

@@ -1237,8 +1237,8 @@ rlx_status rlx_mask_compaction(const uint8_t* attention_mask, int B, int S, int3
   if (!attention_mask || !cu || !tok_src || !tok_dst)
     return fail(RLX_ERR_INVALID_ARG, "mask_compaction: attention_mask, cu, tok_src and tok_dst must be non-null");
   if (B < 1 || S < 1) return fail(RLX_ERR_INVALID_ARG, "mask_compaction: B=%d and S=%d must be >= 1", B, S);
-  if (B > 4096 || S > 512)
-    return fail(RLX_ERR_UNSUPPORTED, "mask_compaction: B=%d, S=%d beyond B <= 4096, S <= 512", B, S);
+  if (B > 8192 || S > 512)
+    return fail(RLX_ERR_UNSUPPORTED, "mask_compaction: B=%d, S=%d beyond B <= 8192, S <= 512", B, S);
   if (order && B > kMaxOrderedBatch)
     return fail(RLX_ERR_UNSUPPORTED, "mask_compaction: the order is computed for B <= %d, not %d", kMaxOrderedBatch, B);
   RLX_HIP(launch_mask_scan(attention_mask, B, S, cu, tok_src, tok_dst, order, static_cast<hipStream_t>(stream)),

@@ -49,7 +49,7 @@ template <int NCH>
 __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, int B, int S, int* cu, int* tok_src,
                                                          int* tok_dst, int* order) {
   constexpr int SEQS = kScanLoads / NCH;
-  extern __shared__ int offs[];  // [B+1]: token counts, then their exclusive prefix; then [B] ranks
+  extern __shared__ int offs[];  // [B+1]: token counts, then their exclusive prefix; then [B] ranks (with order)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
   // Each wave takes SEQS sequences at a time and requests all their mask
@@ -585,8 +585,10 @@ hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok
                             hipStream_t s) {
   if (B < 1 || S < 1 || S > 64 * kScanMaxChunks) return hipErrorInvalidValue;
   const int nch = S <= 64 ? 1 : S <= 128 ? 2 : S <= 256 ? 4 : 8;
-  const size_t lds = (size_t)(2 * B + 1) * sizeof(int);
   int* ord = B <= kMaxOrderedBatch ? order : nullptr;
+  // counts / prefix [B+1], then the ranks [B] only when the order is written
+  // (B <= 8192 sequences stay within the default 64 KB of dynamic LDS)
+  const size_t lds = (size_t)(B + 1 + (ord ? B : 0)) * sizeof(int);
   RLX_LOG_LAUNCH("mask_scan_kernel", dim3(1), dim3(1024), lds, "B=%d S=%d chunks=%d", B, S, nch);
   switch (nch) {
     case 1: hipLaunchKernelGGL(mask_scan_kernel<1>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;

@@ -41,7 +41,7 @@ def test_token_compaction_argument_errors(L):
     assert f(P, 0, 8, P, P, P, None, None) == rlx.ERR_INVALID_ARG
     assert f(P, 2, 0, P, P, P, None, None) == rlx.ERR_INVALID_ARG
     assert f(P, 2, 513, P, P, P, None, None) == rlx.ERR_UNSUPPORTED
-    assert f(P, 4097, 8, P, P, P, None, None) == rlx.ERR_UNSUPPORTED
+    assert f(P, 8193, 8, P, P, P, None, None) == rlx.ERR_UNSUPPORTED
     assert f(P, 257, 8, P, P, P, P, None) == rlx.ERR_UNSUPPORTED
     assert b"order" in L.rlx_last_error()
     g = L.rlx_encoder_token_maps

@@ -59,7 +59,7 @@ def _check(got, mask, what):
 # (B, S): each row-length class, one and several passes of the scan's waves
 # (32 / 16 / 8 / 4 sequences per wave, 16 waves), batches past the ordered limit
 SCAN_SHAPES = [(1, 1), (3, 7), (1, 64), (520, 64), (32, 128), (256, 128), (300, 66), (130, 256), (70, 260),
-               (8, 512), (65, 512), (4096, 3)]
+               (8, 512), (65, 512), (4096, 3), (8192, 2)]
 
 
 @pytest.mark.parametrize("B,S", SCAN_SHAPES)

@@ -162,8 +162,10 @@ def test_encoder_mask_with_holes_and_empty_row(rlx):
 
 # (batch, seq, hidden): the scan's four row-length classes (<= 64, 128, 256, 512
 # positions), each with more sequences than one pass of its waves covers (512, 256,
-# 128, 64); a narrow layer (2 heads, FFN 128) keeps the oracle quick on the big masks
-@pytest.mark.parametrize("batch,seq,hidden", [(136, 136, 384), (520, 9, 64), (260, 66, 64), (70, 260, 64)])
+# 128, 64), and the largest batch a handle accepts (8192); a narrow layer (2 heads,
+# FFN 128) keeps the oracle quick on the big masks
+@pytest.mark.parametrize("batch,seq,hidden", [(136, 136, 384), (520, 9, 64), (260, 66, 64), (70, 260, 64),
+                                              (8192, 3, 64)])
 def test_encoder_hidden_input_large_ragged_mask_f32(rlx, batch, seq, hidden):
     """Hidden-state input always takes the separate mask scan (counts, prefix,
     compaction maps): many sequences, lengths that are not multiples of 64,
