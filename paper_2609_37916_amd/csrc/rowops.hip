@@ -183,11 +183,38 @@ template <> struct Chunk<float> {
 // Chunks per lane: H <= 1024 gives at most 2 (bf16) or 4 (f32).
 template <typename T> constexpr int kMaxCpl = 8 / Chunk<T>::EPC * 2;
 
-// LayerNorm of the wave's row held in v (fp32), written as T.
-template <typename T>
-__device__ __forceinline__ void ln_row_store(float (&v)[kMaxCpl<T>][Chunk<T>::EPC], int H, const float* gamma,
-                                             const float* beta, float eps, T* out) {
-  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
+// gamma and beta of the columns a lane's chunks hold (chunk lane + 64 i),
+// loaded with the row they scale instead of after its reductions: one
+// memory round trip less per row.  Every lane loads NC chunks, clamped to
+// the last one (lanes past the row's end load a copy they never use), so the
+// loads cannot be sunk into the branches that use them.
+template <typename T, int NC = kMaxCpl<T>>
+struct LnAffine {
+  float g[NC][Chunk<T>::EPC], b[NC][Chunk<T>::EPC];
+  __device__ __forceinline__ void load(const float* gamma, const float* beta, int H) {
+    constexpr int EPC = Chunk<T>::EPC;
+    const int lane = threadIdx.x & 63;
+    const int nch = H / EPC;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int ch = min(lane + 64 * i, nch - 1);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        g[i][e] = gamma[ch * EPC + e];
+        b[i][e] = beta[ch * EPC + e];
+      }
+    }
+  }
+};
+
+// LayerNorm of the wave's row held in v (fp32), written as T when `keep`,
+// with the lane's gamma and beta already in registers.  The norm is computed
+// either way, so that a caller's loads of the row are never sunk into the
+// branch of the store (the reductions are cross-lane and stay outside it).
+template <typename T, int NC = kMaxCpl<T>>
+__device__ __forceinline__ void ln_row_store(float (&v)[NC][Chunk<T>::EPC], int H, const LnAffine<T, NC>& aff,
+                                             float eps, T* out, bool keep = true) {
+  constexpr int EPC = Chunk<T>::EPC, CPL = NC;
   const int lane = threadIdx.x & 63;
   const int nch = H / EPC;
   float sum = 0.0f;
@@ -213,43 +240,43 @@ __device__ __forceinline__ void ln_row_store(float (&v)[kMaxCpl<T>][Chunk<T>::EP
     if (ch < nch) {
       float o[EPC];
 #pragma unroll
-      for (int e = 0; e < EPC; ++e) {
-        const int c = ch * EPC + e;
-        o[e] = (v[i][e] - mean) * rstd * gamma[c] + beta[c];
-      }
-      Chunk<T>::store(out + ch * EPC, o);
+      for (int e = 0; e < EPC; ++e) o[e] = (v[i][e] - mean) * rstd * aff.g[i][e] + aff.b[i][e];
+      if (keep) Chunk<T>::store(out + ch * EPC, o);
     }
   }
 }
 
-template <typename T>
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void embed_ln_kernel(const int* ids, const T* word, const T* pos, const T* type,
                                                        const float* gamma, const float* beta, float eps, int vocab,
                                                        int S, int H, const int* tok_src, const int* n_dev, int n_max,
                                                        T* x) {
-  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
+  constexpr int EPC = Chunk<T>::EPC;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_max) return;
+  // the token count, the token's source and the LayerNorm affine in one
+  // round trip (tok_src holds n_max entries; past the count it is unused)
+  LnAffine<T, NC> aff;
+  aff.load(gamma, beta, H);
+  const int src = tok_src[t];
   const int n = min(n_max, *n_dev);
   if (t >= n) return;
   const int lane = threadIdx.x & 63;
-  const int src = tok_src[t];
   const int s = src % S;
   const int id = min(max(ids[src], 0), vocab - 1);
   const int nch = H / EPC;
-  float v[CPL][EPC];
+  float v[NC][EPC];
 #pragma unroll
-  for (int i = 0; i < CPL; ++i) {
-    const int ch = lane + 64 * i;
-    if (ch < nch) {
-      float a[EPC], b[EPC], c[EPC];
-      Chunk<T>::load(word + (size_t)id * H + ch * EPC, a);
-      Chunk<T>::load(pos + (size_t)s * H + ch * EPC, b);
-      Chunk<T>::load(type + ch * EPC, c);
+  for (int i = 0; i < NC; ++i) {
+    const int ch = min(lane + 64 * i, nch - 1);
+    float a[EPC], b[EPC], c[EPC];
+    Chunk<T>::load(word + (size_t)id * H + ch * EPC, a);
+    Chunk<T>::load(pos + (size_t)s * H + ch * EPC, b);
+    Chunk<T>::load(type + ch * EPC, c);
 #pragma unroll
-      for (int e = 0; e < EPC; ++e) v[i][e] = a[e] + b[e] + c[e];
-    }
+    for (int e = 0; e < EPC; ++e) v[i][e] = a[e] + b[e] + c[e];
   }
-  ln_row_store<T>(v, H, gamma, beta, eps, x + (size_t)t * H);
+  ln_row_store<T, NC>(v, H, aff, eps, x + (size_t)t * H);
 }
 
 // Mask scan fused with the embedding gather + LayerNorm, for small masks
@@ -262,13 +289,13 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int* ids, const T* 
 // sequence's place in the longest-first order.  One launch and one memory
 // round trip less than the mask scan followed by the embedding kernel.
 constexpr int kEmbedScanTokens = 16;  // real tokens per block
-template <typename T>
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, const int* ids, int B, int S,
                                                          const T* word, const T* pos, const T* type,
                                                          const float* gamma, const float* beta, float eps, int vocab,
                                                          int H, int* cu, int* tok_src, int* tok_dst, int* order,
                                                          T* x) {
-  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
+  constexpr int EPC = Chunk<T>::EPC, CPL = NC;  // chunks per lane: NC * 64 * EPC >= H
   __shared__ __attribute__((aligned(16))) uint8_t mlds[kEmbedScanMaxMask];  // the whole mask
   __shared__ int cnt[kMaxOrderedBatch];
   __shared__ int posl[kEmbedScanMaxSeq];  // positions of sequence b's real tokens
@@ -276,25 +303,41 @@ __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, co
   const int b = blockIdx.x, p = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t below = (lane == 0) ? 0ull : ((~0ull) >> (64 - lane));
-  // the mask into LDS, every load of a thread issued at once: 16-byte loads
-  // when the mask allows them, bytes otherwise
+  // One round trip for the mask (16-byte loads when it allows them), sequence
+  // b's ids (the rows' gather needs them only after the scan has placed the
+  // tokens) and the LayerNorm affine: every load issued before any is
+  // waited for, then the mask and ids go to LDS.  Loads and LDS stores are
+  // unconditional, at indexes clamped into the arrays (lanes past the end
+  // copy the last element again, to the same place): a load used only under
+  // a condition is sunk into that branch and waited for there, one at a time.
   const int nm = B * S;
-  if ((reinterpret_cast<uintptr_t>(mask) & 15) == 0 && (nm & 15) == 0) {
+  constexpr int MJ = kEmbedScanMaxMask / (16 * 256), IJ = kEmbedScanMaxSeq / 256;
+  int ir[IJ];
+  LnAffine<T, NC> aff;
+  auto load_ids_affine = [&] {
 #pragma unroll
-    for (int j = 0; j < kEmbedScanMaxMask / (16 * 256); ++j) {
-      const int i = (threadIdx.x + 256 * j) * 16;
-      if (i < nm) *reinterpret_cast<uint4*>(mlds + i) = *reinterpret_cast<const uint4*>(mask + i);
-    }
+    for (int j = 0; j < IJ; ++j) ir[j] = ids[(size_t)b * S + min((int)threadIdx.x + 256 * j, S - 1)];
+    aff.load(gamma, beta, H);
+  };
+  if ((reinterpret_cast<uintptr_t>(mask) & 15) == 0 && (nm & 15) == 0) {
+    uint4 mr[MJ];
+#pragma unroll
+    for (int j = 0; j < MJ; ++j)
+      mr[j] = *reinterpret_cast<const uint4*>(mask + min((int)(threadIdx.x + 256 * j) * 16, nm - 16));
+    load_ids_affine();
+#pragma unroll
+    for (int j = 0; j < MJ; ++j)
+      *reinterpret_cast<uint4*>(mlds + min((int)(threadIdx.x + 256 * j) * 16, nm - 16)) = mr[j];
   } else {
+    load_ids_affine();
 #pragma unroll 16
     for (int j = 0; j < kEmbedScanMaxMask / 256; ++j) {
       const int i = threadIdx.x + 256 * j;
       if (i < nm) mlds[i] = mask[i];
     }
   }
-  // sequence b's ids in the same round trip (the rows' gather needs them
-  // only after the scan has placed the tokens)
-  for (int i = threadIdx.x; i < S; i += 256) idl[i] = ids[(size_t)b * S + i];
+#pragma unroll
+  for (int j = 0; j < IJ; ++j) idl[min((int)threadIdx.x + 256 * j, S - 1)] = ir[j];
   __syncthreads();
   // real tokens of every sequence
   if ((S & 15) == 0) {
@@ -395,25 +438,26 @@ __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, co
     }
 #pragma unroll
   for (int j = 0; j < TPW; ++j)
-    if (sp[j] >= 0) ln_row_store<T>(v[j], H, gamma, beta, eps, x + (size_t)(off + p * kEmbedScanTokens + wave + 4 * j) * H);
+    ln_row_store<T, NC>(v[j], H, aff, eps, x + (size_t)(off + p * kEmbedScanTokens + wave + 4 * j) * H, sp[j] >= 0);
 }
 
-template <typename T>
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void layer_norm_kernel(const T* a, const float* gamma, const float* beta, float eps,
                                                          int H, const int* n_dev, int n_max, T* y) {
-  constexpr int EPC = Chunk<T>::EPC, CPL = kMaxCpl<T>;
+  constexpr int EPC = Chunk<T>::EPC;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int n = n_dev ? min(n_max, *n_dev) : n_max;
-  if (t >= n) return;
+  if (t >= n_max) return;
+  // the affine in the round trip of the row count, then the row
   const int lane = threadIdx.x & 63;
   const int nch = H / EPC;
-  float v[CPL][EPC];
+  LnAffine<T, NC> aff;
+  aff.load(gamma, beta, H);
+  const int n = n_dev ? min(n_max, *n_dev) : n_max;
+  if (t >= n) return;
+  float v[NC][EPC];
 #pragma unroll
-  for (int i = 0; i < CPL; ++i) {
-    const int ch = lane + 64 * i;
-    if (ch < nch) Chunk<T>::load(a + (size_t)t * H + ch * EPC, v[i]);
-  }
-  ln_row_store<T>(v, H, gamma, beta, eps, y + (size_t)t * H);
+  for (int i = 0; i < NC; ++i) Chunk<T>::load(a + (size_t)t * H + min(lane + 64 * i, nch - 1) * EPC, v[i]);
+  ln_row_store<T, NC>(v, H, aff, eps, y + (size_t)t * H);
 }
 
 template <typename T>
@@ -578,6 +622,11 @@ __global__ __launch_bounds__(256) void scatter_hidden_kernel(const T* x, int H, 
 }
 
 inline int blocks_for_rows(int rows) { return (rows + 3) / 4; }
+// 16-byte chunks per lane that a row of H elements needs (H <= 1024): 1, 2 or 4
+template <typename T> inline int row_chunks(int H) {
+  const int per = 64 * Chunk<T>::EPC;  // elements one chunk per lane covers
+  return H <= per ? 1 : H <= 2 * per ? 2 : 4;
+}
 
 }  // namespace
 
@@ -604,14 +653,18 @@ hipError_t launch_embed_ln(const int* ids, const void* word, const void* pos, co
                            const int* n_dev, int n_max, void* x, DType dt, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
   RLX_LOG_LAUNCH("embed_ln_kernel", dim3(blocks_for_rows(n_max)), dim3(256), 0, "%s rows<=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", n_max, H);
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(embed_ln_kernel<bf16_t>, dim3(blocks_for_rows(n_max)), dim3(256), 0, s, ids,
-                       (const bf16_t*)word, (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, S, H,
-                       tok_src, n_dev, n_max, (bf16_t*)x);
-  else
-    hipLaunchKernelGGL(embed_ln_kernel<float>, dim3(blocks_for_rows(n_max)), dim3(256), 0, s, ids, (const float*)word,
-                       (const float*)pos, (const float*)type, gamma, beta, eps, vocab, S, H, tok_src, n_dev, n_max,
-                       (float*)x);
+  const dim3 grid(blocks_for_rows(n_max));
+#define RLX_EMBED_LN(TT, NC)                                                                                 \
+  hipLaunchKernelGGL((embed_ln_kernel<TT, NC>), grid, dim3(256), 0, s, ids, (const TT*)word, (const TT*)pos,    \
+                     (const TT*)type, gamma, beta, eps, vocab, S, H, tok_src, n_dev, n_max, (TT*)x)
+  switch (dt == DType::BF16 ? 10 + row_chunks<bf16_t>(H) : row_chunks<float>(H)) {
+    case 11: RLX_EMBED_LN(bf16_t, 1); break;
+    case 12: RLX_EMBED_LN(bf16_t, 2); break;
+    case 1: RLX_EMBED_LN(float, 1); break;
+    case 2: RLX_EMBED_LN(float, 2); break;
+    default: RLX_EMBED_LN(float, 4); break;
+  }
+#undef RLX_EMBED_LN
   return hipGetLastError();
 }
 
@@ -622,14 +675,26 @@ hipError_t launch_embed_scan(const uint8_t* mask, const int* ids, int B, int S, 
   if (!embed_scan_supported(B, S)) return hipErrorInvalidValue;
   const dim3 grid(B, (S + kEmbedScanTokens - 1) / kEmbedScanTokens);
   RLX_LOG_LAUNCH("embed_scan_kernel", grid, dim3(256), 0, "mask scan + embedding %s B=%d S=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", B, S, H);
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(embed_scan_kernel<bf16_t>, grid, dim3(256), 0, s, mask, ids, B, S, (const bf16_t*)word,
-                       (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
-                       order, (bf16_t*)x);
-  else
-    hipLaunchKernelGGL(embed_scan_kernel<float>, grid, dim3(256), 0, s, mask, ids, B, S, (const float*)word,
-                       (const float*)pos, (const float*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst, order,
-                       (float*)x);
+  // chunks of 16 bytes per lane that a row needs: bf16 1 (H <= 512) or 2, f32 2 (H <= 512) or 4
+  if (dt == DType::BF16) {
+    if (H <= 64 * Chunk<bf16_t>::EPC)
+      hipLaunchKernelGGL((embed_scan_kernel<bf16_t, 1>), grid, dim3(256), 0, s, mask, ids, B, S, (const bf16_t*)word,
+                         (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
+                         order, (bf16_t*)x);
+    else
+      hipLaunchKernelGGL((embed_scan_kernel<bf16_t, 2>), grid, dim3(256), 0, s, mask, ids, B, S, (const bf16_t*)word,
+                         (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
+                         order, (bf16_t*)x);
+  } else {
+    if (H <= 128 * Chunk<float>::EPC)
+      hipLaunchKernelGGL((embed_scan_kernel<float, 2>), grid, dim3(256), 0, s, mask, ids, B, S, (const float*)word,
+                         (const float*)pos, (const float*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
+                         order, (float*)x);
+    else
+      hipLaunchKernelGGL((embed_scan_kernel<float, 4>), grid, dim3(256), 0, s, mask, ids, B, S, (const float*)word,
+                         (const float*)pos, (const float*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
+                         order, (float*)x);
+  }
   return hipGetLastError();
 }
 
@@ -650,12 +715,29 @@ hipError_t launch_layer_norm(const void* a, const float* gamma, const float* bet
                              const int* n_dev, int n_max, void* y, DType dt, hipStream_t s) {
   if (n_max <= 0) return hipSuccess;
   RLX_LOG_LAUNCH("layer_norm_kernel", dim3(blocks_for_rows(n_max)), dim3(256), 0, "%s rows<=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", n_max, H);
-  if (dt == DType::BF16)
-    hipLaunchKernelGGL(layer_norm_kernel<bf16_t>, dim3(blocks_for_rows(n_max)), dim3(256), 0, s, (const bf16_t*)a,
-                       gamma, beta, eps, H, n_dev, n_max, (bf16_t*)y);
-  else
-    hipLaunchKernelGGL(layer_norm_kernel<float>, dim3(blocks_for_rows(n_max)), dim3(256), 0, s, (const float*)a, gamma,
-                       beta, eps, H, n_dev, n_max, (float*)y);
+  const dim3 grid(blocks_for_rows(n_max));
+  switch (dt == DType::BF16 ? 10 + row_chunks<bf16_t>(H) : row_chunks<float>(H)) {
+    case 11:
+      hipLaunchKernelGGL((layer_norm_kernel<bf16_t, 1>), grid, dim3(256), 0, s, (const bf16_t*)a, gamma, beta, eps, H,
+                         n_dev, n_max, (bf16_t*)y);
+      break;
+    case 12:
+      hipLaunchKernelGGL((layer_norm_kernel<bf16_t, 2>), grid, dim3(256), 0, s, (const bf16_t*)a, gamma, beta, eps, H,
+                         n_dev, n_max, (bf16_t*)y);
+      break;
+    case 1:
+      hipLaunchKernelGGL((layer_norm_kernel<float, 1>), grid, dim3(256), 0, s, (const float*)a, gamma, beta, eps, H,
+                         n_dev, n_max, (float*)y);
+      break;
+    case 2:
+      hipLaunchKernelGGL((layer_norm_kernel<float, 2>), grid, dim3(256), 0, s, (const float*)a, gamma, beta, eps, H,
+                         n_dev, n_max, (float*)y);
+      break;
+    default:
+      hipLaunchKernelGGL((layer_norm_kernel<float, 4>), grid, dim3(256), 0, s, (const float*)a, gamma, beta, eps, H,
+                         n_dev, n_max, (float*)y);
+      break;
+  }
   return hipGetLastError();
 }
 
