@@ -488,13 +488,15 @@ constexpr int kPoolSplitAbove = 128;  // split when sequences may be longer than
 // sequence's L rows (normalised rows when deferred); the mean, the LayerNorm's
 // gamma and beta of a deferred input, then the L2 normalisation over the
 // block (16 waves).
-__device__ __forceinline__ void pool_finish(float sum, int L, int H, bool deferred, bool gamma_scaled,
-                                            const float* gamma, const float* beta, float* out_row, float* red) {
+// g and bt are column c's gamma and beta (used when deferred), loaded by the
+// caller when its block starts so that they are not a round trip of their own.
+__device__ __forceinline__ void pool_finish(float sum, int L, int H, bool deferred, bool gamma_scaled, float g,
+                                            float bt, float* out_row, float* red) {
   const int c = threadIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float mean = 0.0f;
   if (c < H) {
     mean = sum / fmaxf((float)L, 1e-9f);
-    if (deferred) mean = L > 0 ? (gamma_scaled ? mean + beta[c] : fmaf(gamma[c], mean, beta[c])) : 0.0f;
+    if (deferred) mean = L > 0 ? (gamma_scaled ? mean + bt : fmaf(g, mean, bt)) : 0.0f;
   }
   const float ss = wave_sum(mean * mean);
   if (lane == 0) red[wave] = ss;
@@ -520,6 +522,14 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
   __shared__ float red[16];
   __shared__ float2 row_st[kMaxPoolRows];  // (mean, rstd) per row of a deferred-LayerNorm input
   const int b = blockIdx.x;
+  // column threadIdx.x's gamma and beta for the finish, requested with the
+  // sequence's bounds (clamped: threads past H load a copy they never use)
+  float g = 1.0f, bt = 0.0f;
+  if (x_stats && !partial) {
+    const int cc = min((int)threadIdx.x, H - 1);
+    g = gamma[cc];
+    bt = beta[cc];
+  }
   const int len = cu[b + 1] - cu[b];  // the sequence's rows
   const int r0 = cu[b] + (R ? (int)blockIdx.y * R : 0);
   const int L = R ? max(0, min(R, len - (int)blockIdx.y * R)) : len;  // this block's rows
@@ -594,7 +604,7 @@ __global__ __launch_bounds__(1024) void pool_l2_kernel(const T* x, int H, const 
     if (c < H) partial[((size_t)b * gridDim.y + blockIdx.y) * H + c] = sum;
     return;
   }
-  pool_finish(sum, len, H, x_stats != nullptr, gamma_scaled, gamma, beta, out + (size_t)b * H, red);
+  pool_finish(sum, len, H, x_stats != nullptr, gamma_scaled, g, bt, out + (size_t)b * H, red);
 }
 
 // Adds the Q partial column sums of sequence b (in block order, so the
@@ -604,10 +614,16 @@ __global__ __launch_bounds__(1024) void pool_combine_kernel(const float* partial
                                                             const float* beta, bool gamma_scaled) {
   __shared__ float red[16];
   const int b = blockIdx.x, c = threadIdx.x;
+  float g = 1.0f, bt = 0.0f;
+  if (deferred) {
+    const int cc = min(c, H - 1);
+    g = gamma[cc];
+    bt = beta[cc];
+  }
   float sum = 0.0f;
   if (c < H)
     for (int q = 0; q < Q; ++q) sum += partial[((size_t)b * Q + q) * H + c];
-  pool_finish(sum, cu[b + 1] - cu[b], H, deferred, gamma_scaled, gamma, beta, out + (size_t)b * H, red);
+  pool_finish(sum, cu[b + 1] - cu[b], H, deferred, gamma_scaled, g, bt, out + (size_t)b * H, red);
 }
 
 template <typename T>
