@@ -504,9 +504,16 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   const int grp = slot / p.heads, h = slot - grp * p.heads;
   const int rank = 8 * grp + ((grp & 1) ? 7 - xcd : xcd);
   if (rank >= p.B) return;
-  const int b = p.seq_order ? p.seq_order[rank] : rank;
-  const int row0 = p.cu_seqlens[b];
-  const int L = p.cu_seqlens[b + 1] - row0;
+  int row0, L;
+  if (p.rank_rows) {  // one load: the scan wrote (first row, length) by rank
+    const int2 rl = p.rank_rows[rank];
+    row0 = rl.x;
+    L = rl.y;
+  } else {
+    const int b = p.seq_order ? p.seq_order[rank] : rank;
+    row0 = p.cu_seqlens[b];
+    L = p.cu_seqlens[b + 1] - row0;
+  }
   if (L <= 0) return;
   qkv_attention_block<STAGES>(p, row0, L, h, smem, vec_lds, st_lds, [] {});
 }

@@ -180,6 +180,7 @@ struct rlx_encoder {
   int* tok_src = nullptr;
   int* tok_dst = nullptr;
   int* order = nullptr;  // sequences by token count, longest first (mask scan, B <= kMaxOrderedBatch)
+  int2* rank_rows = nullptr;  // (first row, real tokens) of order[r] at entry r (written with the order)
   int last_B = 0, last_S = 0;  // shape of the most recent forward (its token maps are in the workspace)
   void *X = nullptr, *X1 = nullptr, *A = nullptr, *CTX = nullptr, *QKV = nullptr, *G = nullptr;
   // Deferred LayerNorm (dense bf16 weights): no kernel writes a LayerNorm
@@ -257,6 +258,7 @@ struct FwdCtx {
   // the weight dequantisation that starts the forward (dq_njobs == 0: none)
   const DequantJob* dq_jobs;
   int dq_njobs, dq_max_elems;
+  int2* rank_rows = nullptr;  // [B]: (first row, real tokens) by launch rank, beside the order
 };
 
 // The forward of B sequences of S positions: with the dequantisation prologue
@@ -266,12 +268,13 @@ FwdCtx ctx_of(const rlx_encoder* e, int B, int S) {
   return FwdCtx{dq ? &e->dq_cfg : &e->cfg, &e->w, dq ? e->dq_layers.data() : e->layers.data(), e->dt, e->cu,
                 e->tok_src, e->tok_dst, e->order, e->X, e->X1, e->A, e->CTX, e->QKV, e->G, e->deferred, e->S1,
                 e->S2, dq ? e->dq_folded.data() : e->folded.data(), e->pipe ? e->pipe_grid : 0, e->pipe_layers,
-                e->pipe_sync, dq ? e->dq_jobs : nullptr, dq ? e->dq_njobs : 0, dq ? e->dq_max_elems : 0};
+                e->pipe_sync, dq ? e->dq_jobs : nullptr, dq ? e->dq_njobs : 0, dq ? e->dq_max_elems : 0,
+                e->rank_rows};
 }
 
 // Workspace layout for max_batch sequences of max_seq tokens (256-byte aligned regions).
 struct WsPlan {
-  size_t cu, src, dst, ord, X, X1, A, C, Q, G, S1, S2, bytes;
+  size_t cu, src, dst, ord, rr, X, X1, A, C, Q, G, S1, S2, bytes;
 };
 WsPlan plan_workspace(size_t max_batch, size_t max_seq, size_t H, size_t F, size_t es, bool deferred) {
   const size_t T = max_batch * max_seq;
@@ -282,6 +285,7 @@ WsPlan plan_workspace(size_t max_batch, size_t max_seq, size_t H, size_t F, size
   p.src = take(T * sizeof(int));
   p.dst = take(T * sizeof(int));
   p.ord = take(max_batch * sizeof(int));
+  p.rr = take(max_batch * sizeof(int2));
   p.X = take(T * H * es); p.X1 = take(T * H * es); p.A = take(T * H * es); p.C = take(T * H * es);
   p.Q = take(T * 3 * H * es); p.G = take(T * F * es);
   const size_t stats_bytes = deferred ? T * (H / 64) * sizeof(float2) : 0;
@@ -295,6 +299,7 @@ void bind_workspace(FwdCtx& c, uint8_t* base, const WsPlan& p) {
   c.tok_src = reinterpret_cast<int*>(base + p.src);
   c.tok_dst = reinterpret_cast<int*>(base + p.dst);
   c.order = reinterpret_cast<int*>(base + p.ord);
+  c.rank_rows = reinterpret_cast<int2*>(base + p.rr);
   c.X = base + p.X; c.X1 = base + p.X1; c.A = base + p.A; c.CTX = base + p.C; c.QKV = base + p.Q; c.G = base + p.G;
   c.S1 = c.deferred ? reinterpret_cast<float2*>(base + p.S1) : nullptr;
   c.S2 = c.deferred ? reinterpret_cast<float2*>(base + p.S2) : nullptr;
@@ -409,9 +414,9 @@ rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* m
     // small masks: the scan runs inside the embedding kernel
     STEP(K_EMBED_LN, launch_embed_scan(mask, static_cast<const int*>(input), B, S, E.w->word_emb, E.w->pos_emb,
                                        E.w->type_emb, E.w->emb_ln_gamma, E.w->emb_ln_beta, c.ln_eps, c.vocab, H,
-                                       E.cu, E.tok_src, E.tok_dst, E.order, E.X, E.dt, ss));
+                                       E.cu, E.tok_src, E.tok_dst, E.order, E.X, E.dt, ss, E.rank_rows));
   } else {
-    STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, E.cu, E.tok_src, E.tok_dst, E.order, ss));
+    STEP(K_MASK_SCAN, launch_mask_scan(mask, B, S, E.cu, E.tok_src, E.tok_dst, E.order, ss, E.rank_rows));
     if (c.input_kind == RLX_INPUT_IDS) {
       STEP(K_EMBED_LN, launch_embed_ln(static_cast<const int*>(input), E.w->word_emb, E.w->pos_emb, E.w->type_emb,
                                        E.w->emb_ln_gamma, E.w->emb_ln_beta, c.ln_eps, c.vocab, S, H, E.tok_src,
@@ -445,6 +450,7 @@ rlx_status enqueue_forward(const FwdCtx& fc, const void* input, const uint8_t* m
       fa.x = E.X; fa.wqkv = wqkv; fa.bqkv = bqkv; fa.cu_seqlens = E.cu; fa.out = E.CTX; fa.out_rows = T;
       fa.B = B; fa.H = H; fa.heads = c.heads; fa.scale = 1.0f / std::sqrt((float)c.head_dim);
       fa.seq_order = B <= kMaxOrderedBatch ? E.order : nullptr;  // written by the mask scan
+      fa.rank_rows = B <= kMaxOrderedBatch ? E.rank_rows : nullptr;  // (with the order)
       fa.x_stats = x_def ? E.S2 : nullptr; fa.fold_u = uqkv; fa.ln_eps = c.ln_eps;
       STEP(K_QKV_ATTENTION, launch_qkv_attention(fa, ss));
     } else {
@@ -1089,6 +1095,7 @@ rlx_status rlx_encoder_create(const rlx_encoder_config* cfg, const rlx_encoder_w
     view.deferred = e->deferred;
     bind_workspace(view, static_cast<uint8_t*>(e->ws), plan);
     e->cu = view.cu; e->tok_src = view.tok_src; e->tok_dst = view.tok_dst; e->order = view.order;
+    e->rank_rows = view.rank_rows;
     e->X = view.X; e->X1 = view.X1; e->A = view.A; e->CTX = view.CTX; e->QKV = view.QKV; e->G = view.G;
     e->S1 = view.S1; e->S2 = view.S2;
   }

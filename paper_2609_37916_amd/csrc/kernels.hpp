@@ -143,6 +143,10 @@ struct FusedAttnParams {
   int B, H, heads;
   float scale;
   const int* seq_order;  // optional [B]: the sequences in launch order (longest first)
+  // optional [B]: (first row, real tokens) of the sequence at each launch rank,
+  // written by the scan that wrote seq_order; read instead of seq_order and
+  // cu_seqlens, one dependent load less before a block's first row request
+  const int2* rank_rows;
   // optional deferred LayerNorm of x (as GemmParams::x_stats): wqkv holds
   // gamma-scaled weights, bqkv the folded bias, fold_u [3H] the row sums
   const float2* x_stats;
@@ -221,9 +225,11 @@ hipError_t init_kernel_attributes();
 //   tok_dst[i]  = compact index of padded token i, or -1 (i < B*S)
 // order (optional, [B]): the sequences sorted by token count, longest first;
 // written only for B <= kMaxOrderedBatch (consumers must then also check B).
+// rank_rows (optional, [B], with order): (cu[b], count of b) of b = order[r]
+// at entry r, for consumers that walk the sequences in that order.
 constexpr int kMaxOrderedBatch = 256;
 hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, int* order,
-                            hipStream_t s);
+                            hipStream_t s, int2* rank_rows = nullptr);
 
 // x[t] = LN(word[id] + pos[s] + type[0]) for compact tokens t < cu[B].
 hipError_t launch_embed_ln(const int* ids, const void* word, const void* pos, const void* type, const float* gamma,
@@ -239,7 +245,8 @@ inline bool embed_scan_supported(int B, int S) {
 }
 hipError_t launch_embed_scan(const uint8_t* mask, const int* ids, int B, int S, const void* word, const void* pos,
                              const void* type, const float* gamma, const float* beta, float eps, int vocab, int H,
-                             int* cu, int* tok_src, int* tok_dst, int* order, void* x, DType dt, hipStream_t s);
+                             int* cu, int* tok_src, int* tok_dst, int* order, void* x, DType dt, hipStream_t s,
+                             int2* rank_rows = nullptr);
 
 // x[t] = hidden[tok_src[t]] (row copy) for t < *n_dev.
 hipError_t launch_gather_rows(const void* hidden, int H, const int* tok_src, const int* n_dev, int n_max, void* x,

@@ -47,7 +47,7 @@ __device__ __forceinline__ void load_mask_group(const uint8_t* mask, int B, int 
 
 template <int NCH>
 __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, int B, int S, int* cu, int* tok_src,
-                                                         int* tok_dst, int* order) {
+                                                         int* tok_dst, int* order, int2* rank_rows) {
   constexpr int SEQS = kScanLoads / NCH;
   extern __shared__ int offs[];  // [B+1]: token counts, then their exclusive prefix; then [B] ranks (with order)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
@@ -117,6 +117,10 @@ __global__ __launch_bounds__(1024) void mask_scan_kernel(const uint8_t* mask, in
   }
   __syncthreads();
   for (int i = threadIdx.x; i <= B; i += blockDim.x) cu[i] = offs[i];
+  if (order && rank_rows) {  // the ranks are still in LDS after the prefix
+    const int* rank = offs + B + 1;
+    for (int i = threadIdx.x; i < B; i += blockDim.x) rank_rows[rank[i]] = make_int2(offs[i], offs[i + 1] - offs[i]);
+  }
   auto emit = [&](int b0, const uint8_t (&mb)[SEQS][NCH]) {
 #pragma unroll
     for (int g = 0; g < SEQS; ++g) {
@@ -294,7 +298,7 @@ __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, co
                                                          const T* word, const T* pos, const T* type,
                                                          const float* gamma, const float* beta, float eps, int vocab,
                                                          int H, int* cu, int* tok_src, int* tok_dst, int* order,
-                                                         T* x) {
+                                                         T* x, int2* rank_rows) {
   constexpr int EPC = Chunk<T>::EPC, CPL = NC;  // chunks per lane: NC * 64 * EPC >= H
   __shared__ __attribute__((aligned(16))) uint8_t mlds[kEmbedScanMaxMask];  // the whole mask
   __shared__ int cnt[kMaxOrderedBatch];
@@ -395,6 +399,7 @@ __global__ __launch_bounds__(256) void embed_scan_kernel(const uint8_t* mask, co
       cu[b] = off;
       if (b == B - 1) cu[B] = off + L;
       if (order) order[ahead] = b;
+      if (rank_rows) rank_rows[ahead] = make_int2(off, L);
     }
     for (int i = threadIdx.x; i < L; i += 256) tok_src[off + i] = b * S + posl[i];
     for (int s = threadIdx.x; s < S; s += 256) tok_dst[(size_t)b * S + s] = -1;
@@ -647,19 +652,20 @@ template <typename T> inline int row_chunks(int H) {
 }  // namespace
 
 hipError_t launch_mask_scan(const uint8_t* mask, int B, int S, int* cu, int* tok_src, int* tok_dst, int* order,
-                            hipStream_t s) {
+                            hipStream_t s, int2* rank_rows) {
   if (B < 1 || S < 1 || S > 64 * kScanMaxChunks) return hipErrorInvalidValue;
   const int nch = S <= 64 ? 1 : S <= 128 ? 2 : S <= 256 ? 4 : 8;
   int* ord = B <= kMaxOrderedBatch ? order : nullptr;
+  int2* rr = ord ? rank_rows : nullptr;
   // counts / prefix [B+1], then the ranks [B] only when the order is written
   // (B <= 8192 sequences stay within the default 64 KB of dynamic LDS)
   const size_t lds = (size_t)(B + 1 + (ord ? B : 0)) * sizeof(int);
   RLX_LOG_LAUNCH("mask_scan_kernel", dim3(1), dim3(1024), lds, "B=%d S=%d chunks=%d", B, S, nch);
   switch (nch) {
-    case 1: hipLaunchKernelGGL(mask_scan_kernel<1>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;
-    case 2: hipLaunchKernelGGL(mask_scan_kernel<2>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;
-    case 4: hipLaunchKernelGGL(mask_scan_kernel<4>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;
-    default: hipLaunchKernelGGL(mask_scan_kernel<8>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord); break;
+    case 1: hipLaunchKernelGGL(mask_scan_kernel<1>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord, rr); break;
+    case 2: hipLaunchKernelGGL(mask_scan_kernel<2>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord, rr); break;
+    case 4: hipLaunchKernelGGL(mask_scan_kernel<4>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord, rr); break;
+    default: hipLaunchKernelGGL(mask_scan_kernel<8>, dim3(1), dim3(1024), lds, s, mask, B, S, cu, tok_src, tok_dst, ord, rr); break;
   }
   return hipGetLastError();
 }
@@ -686,9 +692,11 @@ hipError_t launch_embed_ln(const int* ids, const void* word, const void* pos, co
 
 hipError_t launch_embed_scan(const uint8_t* mask, const int* ids, int B, int S, const void* word, const void* pos,
                              const void* type, const float* gamma, const float* beta, float eps, int vocab, int H,
-                             int* cu, int* tok_src, int* tok_dst, int* order, void* x, DType dt, hipStream_t s) {
+                             int* cu, int* tok_src, int* tok_dst, int* order, void* x, DType dt, hipStream_t s,
+                             int2* rank_rows) {
   if (B <= 0 || S <= 0) return hipSuccess;
   if (!embed_scan_supported(B, S)) return hipErrorInvalidValue;
+  if (!order) rank_rows = nullptr;  // (the table follows the order)
   const dim3 grid(B, (S + kEmbedScanTokens - 1) / kEmbedScanTokens);
   RLX_LOG_LAUNCH("embed_scan_kernel", grid, dim3(256), 0, "mask scan + embedding %s B=%d S=%d H=%d", dt == DType::BF16 ? "bf16" : "f32", B, S, H);
   // chunks of 16 bytes per lane that a row needs: bf16 1 (H <= 512) or 2, f32 2 (H <= 512) or 4
@@ -696,20 +704,20 @@ hipError_t launch_embed_scan(const uint8_t* mask, const int* ids, int B, int S, 
     if (H <= 64 * Chunk<bf16_t>::EPC)
       hipLaunchKernelGGL((embed_scan_kernel<bf16_t, 1>), grid, dim3(256), 0, s, mask, ids, B, S, (const bf16_t*)word,
                          (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
-                         order, (bf16_t*)x);
+                         order, (bf16_t*)x, rank_rows);
     else
       hipLaunchKernelGGL((embed_scan_kernel<bf16_t, 2>), grid, dim3(256), 0, s, mask, ids, B, S, (const bf16_t*)word,
                          (const bf16_t*)pos, (const bf16_t*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
-                         order, (bf16_t*)x);
+                         order, (bf16_t*)x, rank_rows);
   } else {
     if (H <= 128 * Chunk<float>::EPC)
       hipLaunchKernelGGL((embed_scan_kernel<float, 2>), grid, dim3(256), 0, s, mask, ids, B, S, (const float*)word,
                          (const float*)pos, (const float*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
-                         order, (float*)x);
+                         order, (float*)x, rank_rows);
     else
       hipLaunchKernelGGL((embed_scan_kernel<float, 4>), grid, dim3(256), 0, s, mask, ids, B, S, (const float*)word,
                          (const float*)pos, (const float*)type, gamma, beta, eps, vocab, H, cu, tok_src, tok_dst,
-                         order, (float*)x);
+                         order, (float*)x, rank_rows);
   }
   return hipGetLastError();
 }
