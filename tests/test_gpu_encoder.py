@@ -146,6 +146,21 @@ def test_encoder_long_sequences_pooled(rlx, kind):
     _compare(got, oracle.encoder_forward(wl), wl, _tol(sp), f"long sequences pooled, {kind}")
 
 
+@pytest.mark.parametrize("batch", [256, 300])
+def test_encoder_bf16_at_and_beyond_the_ordered_batch(rlx, batch):
+    """bf16 ids of S = 40 positions.  At B = 256 the scan keeps the launch order
+    and the (first row, length) table the fused projection + attention kernel
+    reads; at B = 300 it keeps neither, and the kernel takes the sequences in
+    index order from cu_seqlens.  Sampled rows against the oracle."""
+    wl = workloads.make(workloads.spec("minilm_b32_s128_bf16", batch=batch, seq=40, layers=2, len_lo=1, len_hi=40))
+    got = _run(rlx, wl)
+    rows = np.random.default_rng(11 + batch).choice(batch, 24, replace=False)
+    rows.sort()
+    sub = workloads.select_rows(wl, rows)
+    _compare(got[rows], oracle.encoder_forward(sub), sub, _tol(wl.spec), f"B={batch} S=40 bf16 (sampled rows)")
+    assert np.max(np.abs(np.linalg.norm(got, axis=1) - 1)) < 1e-3
+
+
 def test_encoder_mask_with_holes_and_empty_row(rlx):
     """A custom key mask that is not right-padded, and a sequence with no token."""
     sp = workloads.spec("minilm_b4_s128_bf16", batch=5, seq=64, len_lo=30, len_hi=64)
