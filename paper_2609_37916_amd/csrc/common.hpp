@@ -125,10 +125,41 @@ __device__ __forceinline__ float2 row_ln_stats(const float2* part, int np, float
   load_ln_parts(part, np, v);
   return merge_ln_parts(v, np, eps);
 }
-// The same from statistics staged in LDS.  All kLnMaxParts entries are read
-// at once (16-byte aligned, 128 readable bytes: the caller pads) and the ones
-// past np are masked, so the merge costs one LDS round trip.
-__device__ __forceinline__ float2 merge_ln_lds(const float2* part, int np, float eps) {
+// The same from statistics staged in LDS, for np parts known at compile
+// time (np even: rows of an even number of 64-column parts): the np / 2
+// 16-byte pairs are read at once (one LDS round trip), the sums are taken as
+// trees rather than one serial chain, and the reciprocal square root is the
+// hardware one (its argument is at least eps, never denormal).
+template <int NP>
+__device__ __forceinline__ float2 merge_ln_lds_n(const float2* part, float eps) {
+  static_assert(NP % 2 == 0 && NP >= 2 && NP <= kLnMaxParts, "even part count");
+  constexpr int NQ = NP / 2;
+  const float4* q = reinterpret_cast<const float4*>(part);
+  float4 v[NQ];
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) v[j] = q[j];
+  float a[NQ];
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) a[j] = v[j].x + v[j].z;
+#pragma unroll
+  for (int w = 1; w < NQ; w *= 2)
+#pragma unroll
+    for (int j = 0; j + w < NQ; j += 2 * w) a[j] += a[j + w];
+  const float mean = a[0] * (1.0f / NP);
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    const float d0 = v[j].x - mean, d1 = v[j].z - mean;
+    a[j] = fmaf(64.0f * d0, d0, fmaf(64.0f * d1, d1, v[j].y + v[j].w));
+  }
+#pragma unroll
+  for (int w = 1; w < NQ; w *= 2)
+#pragma unroll
+    for (int j = 0; j + w < NQ; j += 2 * w) a[j] += a[j + w];
+  return make_float2(mean, __builtin_amdgcn_rsqf(fmaf(a[0], 1.0f / (64.0f * NP), eps)));
+}
+// Any part count: all kLnMaxParts entries are read at once (16-byte aligned,
+// 128 readable bytes: the caller pads) and the ones past np are masked.
+__device__ __forceinline__ float2 merge_ln_lds_any(const float2* part, int np, float eps) {
   const float4* q = reinterpret_cast<const float4*>(part);
   float4 v[kLnMaxParts / 2];
 #pragma unroll
@@ -146,6 +177,18 @@ __device__ __forceinline__ float2 merge_ln_lds(const float2* part, int np, float
     m2 += 2 * j < np ? t : 0.0f;
   }
   return make_float2(mean, rsqrtf(fmaf(m2, inv_np * (1.0f / 64.0f), eps)));
+}
+// np is the same across the wave, so the switch is a scalar branch.
+__device__ __forceinline__ float2 merge_ln_lds(const float2* part, int np, float eps) {
+  switch (np) {
+    case 2: return merge_ln_lds_n<2>(part, eps);
+    case 4: return merge_ln_lds_n<4>(part, eps);
+    case 6: return merge_ln_lds_n<6>(part, eps);
+    case 8: return merge_ln_lds_n<8>(part, eps);
+    case 12: return merge_ln_lds_n<12>(part, eps);
+    case 16: return merge_ln_lds_n<16>(part, eps);
+    default: return merge_ln_lds_any(part, np, eps);
+  }
 }
 
 // Sum over each group of 8 consecutive lanes, by DPP lane swaps (no LDS):

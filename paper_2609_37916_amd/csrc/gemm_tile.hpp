@@ -120,13 +120,13 @@ __host__ __device__ constexpr EpiLayout epi_layout_of(int K, int N) {
 
 // Merges the partial statistics staged at `epi` into each row's (mean, rstd)
 // at the EpiLayout's mrg region: x rows at [0, BM), residual rows at [BM, 2BM).
-// One thread per row.
+// One thread per row: thread `tid` of 0 .. BM-1 merges row tid, others none.
 template <int BM, int BN, Epi E, int LN>
 __device__ __forceinline__ void merge_row_stats(const GemmParams& p, uint8_t* epi, int tid) {
   if constexpr ((LN & (kLnX | kLnRes)) != 0) {
     const EpiLayout lay = epi_layout_of<BM, BN, E, LN>(p.K, p.N);
     float2* mrg = reinterpret_cast<float2*>(epi + lay.mrg_off);
-    if (tid < BM) {
+    if (tid >= 0 && tid < BM) {
       if constexpr ((LN & kLnX) != 0)
         mrg[tid] = merge_ln_lds(reinterpret_cast<const float2*>(epi + lay.xst_off) + tid * (p.K >> 6), p.K >> 6,
                                 p.ln_eps);
@@ -168,12 +168,13 @@ __device__ __forceinline__ void store_tile(const f32x16_t (&acc)[TM][TN], uint8_
   const EpiLayout lay = epi_layout_of<BM, BN, E, LN>(p.K, N);
   const float* vec = reinterpret_cast<const float*>(epi);  // [4 or 5][BN]: bias, fold_u, res_gamma, res_beta, y_gamma
   float2* mrg = reinterpret_cast<float2*>(epi + lay.mrg_off);  // [2][BM]: (mean, rstd) of x rows, residual rows
-  // one thread per row merges the rows' statistics while the others stage
-  // their accumulators; the barrier after the staging publishes them
-  merge_row_stats<BM, BN, E, LN>(p, epi, tid);
 #pragma unroll
   for (int rb = 0; rb < NRB; ++rb) {
     __syncthreads();  // the operand stages (or the previous row block) are no longer read
+    // the block's last BM threads merge the rows' statistics (one row each)
+    // while the other waves stage their accumulators; the barrier after the
+    // staging publishes them
+    if (rb == 0) merge_row_stats<BM, BN, E, LN>(p, epi, tid - (NT - BM));
 #pragma unroll
     for (int g = 0; g < KS; ++g) {
       if (g > 0) __syncthreads();  // the previous group's partial is in place
