@@ -248,6 +248,35 @@ __device__ __forceinline__ void wait_stage(int ahead) {
   }
 }
 
+// wait_stage, with `extra` (0 .. 7) younger loads issued after the later
+// stages also allowed to stay in flight (more: waits for everything).
+template <int LPS, int MAXA, int E>
+__device__ __forceinline__ void wait_stage_e(int ahead) {
+  if constexpr (MAXA > 0) {
+    if (ahead >= MAXA) {
+      wait_vmcnt<MAXA * LPS + E>();
+      return;
+    }
+    wait_stage_e<LPS, MAXA - 1, E>(ahead);
+  } else {
+    wait_vmcnt<E>();
+  }
+}
+template <int LPS, int MAXA>
+__device__ __forceinline__ void wait_stage_plus(int ahead, int extra) {
+  switch (extra) {
+    case 0: wait_stage_e<LPS, MAXA, 0>(ahead); break;
+    case 1: wait_stage_e<LPS, MAXA, 1>(ahead); break;
+    case 2: wait_stage_e<LPS, MAXA, 2>(ahead); break;
+    case 3: wait_stage_e<LPS, MAXA, 3>(ahead); break;
+    case 4: wait_stage_e<LPS, MAXA, 4>(ahead); break;
+    case 5: wait_stage_e<LPS, MAXA, 5>(ahead); break;
+    case 6: wait_stage_e<LPS, MAXA, 6>(ahead); break;
+    case 7: wait_stage_e<LPS, MAXA, 7>(ahead); break;
+    default: wait_vmcnt<0>(); break;
+  }
+}
+
 // LDS byte address of a __shared__ pointer (for m0).
 __device__ __forceinline__ uint32_t lds_addr_of(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;

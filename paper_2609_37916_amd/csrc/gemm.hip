@@ -378,7 +378,12 @@ __host__ __device__ inline int gq_lds_bytes(Quant q, int BN, int K) {
                           : 0;
 }
 
-template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1, int LN = 0, Quant Q = Quant::None>
+// EL: the epilogue operands are requested after the first operand stage
+// instead of before it (launch_dma picks it: 128-column tiles, or calls of at
+// least kGemmLateEpiRows rows, where there are more tiles than CUs).
+constexpr int kGemmLateEpiRows = 8192;
+
+template <int BM, int BN, int STAGES, typename T, Epi E, int KS = 1, int LN = 0, Quant Q = Quant::None, bool EL = false>
 __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   static_assert(BM % 64 == 0 && BN % 64 == 0 && STAGES >= 2 && STAGES <= 6, "tile");
   static_assert(KS == 1 || (sizeof(T) == 2 && (BK_BF16 / 16) % KS == 0), "K split over bf16 chunks");
@@ -417,8 +422,6 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  // oldest in every wave's memory queue: landed before the first stage is waited for
-  if constexpr (STAGED) issue_epilogue_operands<BM, BN, E, LN, NW>(p, m0, n0, M, epi_lds, wave, lane);
   const int kg = wave >> 2;  // K group (KS > 1)
   const int wm = (wave & 3) >> 1, wn = wave & 1;
   const int l32 = lane & 31, half = lane >> 5;
@@ -503,8 +506,21 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
 
+  // The epilogue operands are needed only at the end.  Early (!EL): oldest in
+  // every wave's memory queue, landed before the first stage is waited for.
+  // Late (EL): after stage 0, so they do not delay the first stage; the first
+  // wait lets this wave's epi_loads epilogue loads stay in flight, and from
+  // stage 1 on they are older than the stage waited for.
+  constexpr bool LATE = STAGED && EL;
+  if constexpr (STAGED && !LATE) issue_epilogue_operands<BM, BN, E, LN, NW>(p, m0, n0, M, epi_lds, wave, lane);
+  if (KT > 0) issue(0, 0);
+  int epi_loads = 0;
+  if constexpr (LATE) {
+    issue_epilogue_operands<BM, BN, E, LN, NW, true>(p, m0, n0, M, epi_lds, wave, lane);
+    epi_loads = epilogue_dma_count<BM, BN, E, LN, NW>(p, wave);
+  }
 #pragma unroll
-  for (int st = 0; st < STAGES - 1; ++st)
+  for (int st = 1; st < STAGES - 1; ++st)
     if (st < KT) issue(st, st);
 
   for (int kt0 = 0; kt0 < KT; kt0 += STAGES) {
@@ -512,10 +528,18 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
     for (int u = 0; u < STAGES; ++u) {
       const int kt = kt0 + u;
       if (kt < KT) {
-        if (NI % NW == 0 || wave < NI % NW)
-          wait_stage<LPS, STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
-        else
-          wait_stage<(NI % NW == 0 ? LPS : LPS - 1), STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
+        const int extra = LATE && kt == 0 ? epi_loads : 0;
+        if constexpr (LATE) {
+          if (NI % NW == 0 || wave < NI % NW)
+            wait_stage_plus<LPS, STAGES - 2>(min(STAGES - 2, KT - 1 - kt), extra);
+          else
+            wait_stage_plus<(NI % NW == 0 ? LPS : LPS - 1), STAGES - 2>(min(STAGES - 2, KT - 1 - kt), extra);
+        } else {
+          if (NI % NW == 0 || wave < NI % NW)
+            wait_stage<LPS, STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
+          else
+            wait_stage<(NI % NW == 0 ? LPS : LPS - 1), STAGES - 2>(min(STAGES - 2, KT - 1 - kt));
+        }
         __syncthreads();  // stage kt visible to all waves; buffer of stage kt-1 is free
         const bool prefetch = kt + STAGES - 1 < KT;
         const uint8_t* xs = smem + u * kStage;
@@ -609,6 +633,10 @@ __global__ __launch_bounds__(kThreads * KS) void gemm_dma_kernel(GemmParams p) {
 
   constexpr int NRB = BM * (BN * 4 + 16) <= (int)sizeof(smem) ? 1 : 2;
   static_assert(BM / NRB * (BN * 4 + 16) <= (int)sizeof(smem), "epilogue row block fits the stage memory");
+  // late epilogue operands have all landed (with a single K stage the only
+  // wait let them stay in flight); the epilogue's first barrier then covers
+  // all waves
+  if constexpr (LATE) wait_vmcnt<0>();
   store_tile<BM, BN, T, Q, E, TM, TN, NRB, KS, LN, STAGED>(acc, smem, p, m0, n0, M, epi_lds);
 }
 
@@ -633,7 +661,16 @@ hipError_t launch_dma(const GemmParams& p, hipStream_t s) {
                  "tile=%dx%d stages=%d %s %s ksplit=%d ln=%d epi=%s M=%d%s N=%d K=%d", BM, BN, STAGES,
                  sizeof(T) == 2 ? "bf16" : "f32", quant_name(Q), KS, LN, epi_name(E), p.M, p.m_dev ? "(device)" : "",
                  p.N, p.K);
-  hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, E, KS, LN, Q>), grid, dim3(kThreads * KS), epi, s, p);
+  bool late = false;  // (only bf16 activations stage epilogue operands)
+  if constexpr (sizeof(T) == 2) late = BN >= 128 || p.M >= kGemmLateEpiRows;
+  if constexpr (sizeof(T) == 2) {
+    if (late) {
+      hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, E, KS, LN, Q, true>), grid, dim3(kThreads * KS), epi, s,
+                         p);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, STAGES, T, E, KS, LN, Q, false>), grid, dim3(kThreads * KS), epi, s, p);
   return hipGetLastError();
 }
 

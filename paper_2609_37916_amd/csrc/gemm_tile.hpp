@@ -328,7 +328,16 @@ __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >>
 // 1 KB DMA block at a time, spread over the block's NW waves.  Rows at or past
 // M read row M-1 (as the operand stages do); statistics are read as one
 // contiguous run per block, clamped to the last whole 16 bytes of row M-1.
+// With EXACT, every block is one DMA instruction of the wave, also where some
+// or all of its lanes have no operand (they fetch 16 bytes of the weights
+// into a slot nothing reads), so the wave's count of loads is exactly
+// epilogue_dma_count(): callers may wait for older loads with it.
 template <int BM, int BN, Epi E, int LN, int NW>
+__device__ __forceinline__ int epilogue_dma_count(const GemmParams& p, int wave) {
+  const int nb = epi_layout_of<BM, BN, E, LN>(p.K, p.N).mrg_off / 1024;
+  return wave < nb ? (nb - wave + NW - 1) / NW : 0;
+}
+template <int BM, int BN, Epi E, int LN, int NW, bool EXACT = false>
 __device__ __forceinline__ void issue_epilogue_operands(const GemmParams& p, int m0, int n0, int M, uint8_t* epi,
                                                         int wave, int lane) {
   const EpiLayout lay = epi_layout_of<BM, BN, E, LN>(p.K, p.N);
@@ -356,7 +365,10 @@ __device__ __forceinline__ void issue_epilogue_operands(const GemmParams& p, int
       const size_t b = (size_t)m0 * np * 8 + (o - (xs ? lay.xst_off : lay.rst_off));
       src = reinterpret_cast<const uint8_t*>(xs ? p.x_stats : p.res_stats) + min(b, (size_t)M * np * 8 - 16);
     }
-    if (src) lds_dma16(src, __builtin_amdgcn_readfirstlane(e0 + j * 1024));
+    if constexpr (EXACT)
+      lds_dma16(src ? src : reinterpret_cast<const uint8_t*>(p.w), __builtin_amdgcn_readfirstlane(e0 + j * 1024));
+    else if (src)
+      lds_dma16(src, __builtin_amdgcn_readfirstlane(e0 + j * 1024));
   }
 }
 
