@@ -243,19 +243,27 @@ __device__ __forceinline__ void qkv_attention_block(const FusedAttnParams& p, in
       sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(make_uint4(k10.x, k10.y, k11.x, k11.y)), qf1, sc[t], 0,
                                                       0, 0);
     }
-    float m_all = -INFINITY;
+    // The maximum is taken over the raw scores and scaled once (the scale
+    // 1/sqrt(d) is positive, so scaling keeps the order): each probability is
+    // then one fma and one exp2.  Only the last key tile can be partial, so
+    // only it is masked.
+    float m_raw = -INFINITY;
 #pragma unroll
     for (int t = 0; t < kFxRows / 32; ++t) {
       if (t >= ntiles) break;
       const int kb = t * 32;
+      if (kb + 32 > L) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = kb + 8 * (v >> 2) + 4 * half + (v & 3);
-        sc[t][v] = (kb + 32 <= L || key < L) ? sc[t][v] * sl2 : -INFINITY;  // only the last tile is partial
-        m_all = fmaxf(m_all, sc[t][v]);
+        for (int v = 0; v < 16; ++v) {
+          const int key = kb + 8 * (v >> 2) + 4 * half + (v & 3);
+          if (key >= L) sc[t][v] = -INFINITY;
+        }
       }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) m_raw = fmaxf(m_raw, sc[t][v]);
     }
-    m_all = fmaxf(m_all, __shfl_xor(m_all, 32, 64));  // finite: the sequence has a real key
+    m_raw = fmaxf(m_raw, __shfl_xor(m_raw, 32, 64));  // finite: the sequence has a real key
+    const float m_neg = -(m_raw * sl2);
 #pragma unroll
     for (int t = 0; t < kFxRows / 32; ++t) {
       if (t >= ntiles) break;
@@ -264,10 +272,11 @@ __device__ __forceinline__ void qkv_attention_block(const FusedAttnParams& p, in
       // (flushed to 0) are far under the bf16 rounding of P
       float pv[16];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        pv[v] = __builtin_amdgcn_exp2f(sc[t][v] - m_all);
-        l_run += pv[v];
-      }
+      for (int v = 0; v < 16; ++v) pv[v] = __builtin_amdgcn_exp2f(fmaf(sc[t][v], sl2, m_neg));
+      float ps[8];
+#pragma unroll
+      for (int v = 0; v < 8; ++v) ps[v] = pv[2 * v] + pv[2 * v + 1];
+      l_run += ((ps[0] + ps[1]) + (ps[2] + ps[3])) + ((ps[4] + ps[5]) + (ps[6] + ps[7]));
       const uint4 pb0 = make_uint4(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]), pack_bf16x2(pv[4], pv[5]),
                                    pack_bf16x2(pv[6], pv[7]));
       const uint4 pb1 = make_uint4(pack_bf16x2(pv[8], pv[9]), pack_bf16x2(pv[10], pv[11]),
