@@ -498,10 +498,21 @@ __global__ __launch_bounds__(256) void qkv_attn_bf16_kernel(FusedAttnParams p) {
   // sequence are given to one XCD, so its L2 fetches the sequence's token rows
   // once instead of once per XCD.  Sequences are taken in groups of 8 by rank
   // (longest first when an order is given), one per XCD, the direction
-  // alternating between groups to balance the XCDs' work; within an XCD the
-  // blocks follow the ranks, so long sequences are placed first.
+  // alternating between groups to balance the XCDs' work.  Within an XCD the
+  // items (group, head) are ranked longest first.  When an XCD has more
+  // blocks than CUs but at most twice as many, its slots c and c + C (C CUs
+  // per XCD) land on the same CU: all CUs are free at launch and each takes a
+  // second block in the same round-robin order.  The longest items then get a
+  // CU of their own, and the rest are paired longest with shortest, which
+  // lowers the busiest CU's load.  Otherwise slots follow the ranks.
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-  const int grp = slot / p.heads, h = slot - grp * p.heads;
+  const int n = gridDim.x >> 3, C = p.cu_per_xcd;
+  int item = slot;
+  if (C > 0 && n > C && n <= 2 * C) {
+    const int P = n - C;  // CUs with two blocks
+    item = slot < P ? 2 * C - n + slot : (slot < C ? slot - P : n - 1 - (slot - C));
+  }
+  const int grp = item / p.heads, h = item - grp * p.heads;
   const int rank = 8 * grp + ((grp & 1) ? 7 - xcd : xcd);
   if (rank >= p.B) return;
   int row0, L;
@@ -525,7 +536,16 @@ hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s) {
   RLX_LOG_LAUNCH("qkv_attn_bf16_kernel", dim3(((p.B + 7) / 8) * 8 * p.heads), dim3(256), 0,
                  "fused QKV projection + attention, stages=2 B=%d heads=%d H=%d%s", p.B, p.heads, p.H,
                  p.x_stats ? " deferred-LN input" : "");
-  hipLaunchKernelGGL(qkv_attn_bf16_kernel<2>, dim3(((p.B + 7) / 8) * 8 * p.heads), dim3(256), 0, s, p);
+  static const int cu_per_xcd = [] {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    return cus % 8 == 0 ? cus / 8 : 0;
+  }();
+  FusedAttnParams q = p;
+  q.cu_per_xcd = cu_per_xcd;
+  hipLaunchKernelGGL(qkv_attn_bf16_kernel<2>, dim3(((p.B + 7) / 8) * 8 * p.heads), dim3(256), 0, s, q);
   return hipGetLastError();
 }
 

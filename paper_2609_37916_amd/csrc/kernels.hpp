@@ -152,6 +152,8 @@ struct FusedAttnParams {
   const float2* x_stats;
   const float* fold_u;
   float ln_eps;
+  // compute units per XCD; set by launch_qkv_attention (0: slots in rank order)
+  int cu_per_xcd;
 };
 hipError_t launch_qkv_attention(const FusedAttnParams& p, hipStream_t s);
 
